@@ -1,0 +1,172 @@
+/*
+ * specgen.h -- C ABI of the MI355X (gfx950) fork-decode attention and
+ * KV-block import library behind SpecGen's speculative generation
+ * (arXiv 2606.17518).
+ *
+ * The paper forks non-reasoning generations off a long reasoning trace; every
+ * fork is conditioned on the trace's prefix and reuses its cached KV state,
+ * then continues with a short private suffix (Sec. 1; Sec. 4.2 "Insight:
+ * Speculative Generation"; Sec. 8.7, prefix caching paragraph).  A fork event
+ * launches K forks (Algorithm 1, the line that sets K from the resource
+ * capacity), and idle-triggered forking adds more forks on the same prefix
+ * (Sec. 6.1.1), so one trace's prefix is shared by F forks.  Suspended
+ * prefixes are kept in spare GPU memory and restored into the serving cache
+ * instead of being recomputed (Sec. 6.2.3 "Remote Cache of Reasoning
+ * Prefixes").
+ *
+ * Conventions fixed here (the paper states none of them):
+ *  - Attention is single-query softmax attention with scale sm_scale > 0.
+ *    For fork f of trace t and query head h the keys are, in logical order,
+ *    the P_t prefix tokens of t followed by the S_f suffix tokens of f; the
+ *    current decode token's own K/V is expected to be in the suffix already.
+ *  - Grouped-query heads: q head h reads kv head h / (Hq / Hkv).
+ *  - KV pools are paged: [num_blocks][block_size=16][Hkv][D], row-major.  A
+ *    block table lists physical block ids in logical order; the last block of
+ *    a prefix or suffix may be partly filled, and its unused slots are never
+ *    read.  A fork's suffix starts at slot 0 of its own first block.
+ *  - out is bf16 (round to nearest even from fp32); out_lse is the natural-log
+ *    log-sum-exp of the scaled scores, fp32.
+ *  - E4M3 KV is the OCP 8-bit "E4M3FN" format (bias 7, max 448, no inf,
+ *    0x7F/0xFF NaN) with one fp32 scale per physical block and tensor: the
+ *    value of a stored code c in block b is decode(c) * scale[b].
+ *
+ * Ownership: the caller allocates every buffer and keeps it alive until the
+ * work queued on `stream` has finished.  The library keeps no pointer after a
+ * call returns; host-side index mirrors are read only during the call.
+ * Errors: every entry point returns a status; argument checks all run before
+ * anything is queued, so a non-OK status means nothing was launched and no
+ * output was written.  specgen_last_error() gives a message for the calling
+ * thread's most recent non-OK status.
+ * Streams: all work is asynchronous on `stream` (0 = the null stream) of the
+ * current HIP device.  Results are deterministic: the work split depends only
+ * on the lengths, and no floating-point atomics are used.
+ */
+#ifndef SPECGEN_H
+#define SPECGEN_H
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPECGEN_OK = 0,
+  SPECGEN_ERR_INVALID_ARG = 1, /* a null pointer, size or shape out of range */
+  SPECGEN_ERR_UNSUPPORTED = 2, /* a valid request this build does not serve */
+  SPECGEN_ERR_WORKSPACE = 3,   /* workspace missing or too small            */
+  SPECGEN_ERR_DEVICE = 4       /* a HIP call or kernel launch failed        */
+} specgen_status_t;
+
+typedef enum { SPECGEN_BF16 = 0, SPECGEN_FP8_E4M3 = 1, SPECGEN_FP32 = 2 } specgen_dtype_t;
+
+/* Which kernel serves each work item.  AUTO: a prefix item uses the bf16 MFMA
+ * kernel when its row count F_t * (Hq/Hkv) is at least 16, else the
+ * wavefront dot kernel; suffix items use the MFMA kernel.  DOT / MFMA force
+ * one kernel for every item (used by tests to cover both paths). */
+typedef enum { SPECGEN_PATH_AUTO = 0, SPECGEN_PATH_DOT = 1, SPECGEN_PATH_MFMA = 2 } specgen_path_t;
+
+/* One decode step for every fork of T traces. */
+typedef struct {
+  int32_t num_traces;        /* T >= 1                                           */
+  int32_t num_forks;         /* N = sum_t F_t >= 1; forks are grouped by trace   */
+  int32_t num_q_heads;       /* Hq >= 1                                          */
+  int32_t num_kv_heads;      /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 128         */
+  int32_t head_dim;          /* D: 64 or 128                                     */
+  int32_t block_size;        /* must be 16                                       */
+  int64_t num_blocks;        /* pool capacity in blocks (>= 1)                   */
+  float sm_scale;            /* > 0 and finite, e.g. 1/sqrt(D)                   */
+  int32_t kv_dtype;          /* specgen_dtype_t: SPECGEN_BF16 or SPECGEN_FP8_E4M3 */
+  int32_t path;              /* specgen_path_t                                   */
+  int32_t reserved;          /* must be 0                                        */
+  /* device memory, caller-owned */
+  const void *q;             /* [N][Hq][D] bf16                                  */
+  const void *k_pool;        /* [num_blocks][16][Hkv][D] kv_dtype                */
+  const void *v_pool;        /* same layout as k_pool                           */
+  const float *k_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
+  const float *v_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
+  const int32_t *fork_off;   /* [T+1], fork_off[0] = 0, nondecreasing, [T] = N;
+                                forks of trace t are [fork_off[t], fork_off[t+1]),
+                                each trace has at least one fork                */
+  const int32_t *prefix_len; /* [T], P_t >= 1                                    */
+  const int32_t *prefix_table_off; /* [T+1]; trace t's ids are
+                                prefix_table[prefix_table_off[t] ..], at least
+                                ceil(P_t/16) of them                            */
+  const int32_t *prefix_table;
+  const int32_t *suffix_len; /* [N], S_f >= 0                                    */
+  const int32_t *suffix_table_off; /* [N+1], at least ceil(S_f/16) ids per fork  */
+  const int32_t *suffix_table;
+  /* host mirrors of the index arrays above (same contents), read only during
+     the call to size the work split and the workspace; the device copies are
+     what the kernels read, so the two must agree */
+  const int32_t *fork_off_h;
+  const int32_t *prefix_len_h;
+  const int32_t *suffix_len_h;
+} specgen_fork_batch_t;
+
+/* Workspace bytes that specgen_fork_decode_attn needs for this batch (partial
+ * outputs of the split key axis).  Validates the batch like the call itself. */
+specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batch_t *b,
+                                                         size_t *bytes);
+
+/* Fork-decode attention, one decode token per fork:
+ *   out[f][h][:] = softmax(sm_scale * q[f][h] . K_seq^T) V_seq,
+ *   out_lse[f][h] = ln sum_i exp(sm_scale * q[f][h] . K_seq[i])
+ * where K_seq/V_seq are the prefix tokens of fork f's trace followed by f's
+ * suffix tokens (kv head h / (Hq/Hkv)).  The shared prefix of each trace is
+ * streamed from HBM once per kv head for all of the trace's forks and query
+ * heads of a GQA group; each fork's suffix is streamed once.  The key axis is
+ * split across workgroups and the partial results are merged with the
+ * log-sum-exp rule (specgen_lse_merge computes the same merge standalone).
+ *   out: [N][Hq][D] bf16, device.  out_lse: [N][Hq] fp32 device, or NULL.
+ *   workspace: device, at least specgen_fork_decode_attn_workspace_size bytes,
+ *   256-byte aligned; its contents on entry do not matter.
+ * Block ids must lie in [0, num_blocks); an out-of-range id is undefined
+ * behaviour (the kernels do not check it). */
+specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t *b, void *out, float *out_lse,
+                                          void *workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
+
+/* One tensor of a KV-block import: dst_pool is [num_dst_blocks][block_bytes],
+ * src_staging is [n][block_bytes] contiguous (the restored remote copy). */
+typedef struct {
+  void *dst_pool;
+  const void *src_staging;
+  int64_t block_bytes;       /* > 0 and a multiple of 4; multiples of 16 take the
+                                16-byte vector path                             */
+} specgen_kv_tensor_t;
+
+/* KV-block import (restore of a cached prefix, Sec. 6.2.3): for every tensor
+ * and every i < n, copy staging block i to pool block dst_block_ids[i], byte
+ * for byte.  Ids outside [0, num_dst_blocks) are skipped and, if
+ * bad_id_count is not NULL, counted there (device int32, incremented, not
+ * reset).  Destinations must be distinct; with duplicates the winner is
+ * unspecified.  Staging and pool must not overlap.
+ *   tensors: host array of 1..4 descriptors (e.g. K, V, K scales, V scales).
+ *   dst_block_ids: device int32 [n].  n >= 0 (0 queues nothing). */
+specgen_status_t specgen_kv_import(const specgen_kv_tensor_t *tensors, int32_t num_tensors,
+                                   const int32_t *dst_block_ids, int64_t n,
+                                   int64_t num_dst_blocks, int32_t *bad_id_count,
+                                   hipStream_t stream);
+
+/* Log-sum-exp merge of S partial attention results over disjoint key sets:
+ *   M = max_s lse[s][r]; w_s = exp(lse[s][r] - M);
+ *   out[r] = sum_s w_s o[s][r] / sum_s w_s; out_lse[r] = M + ln sum_s w_s.
+ * A part with lse = -inf is empty and its o is ignored; a row with only empty
+ * parts gives out = 0 and out_lse = -inf.
+ *   o_parts: device fp32 [S][R][D]; lse_parts: device fp32 [S][R] (natural log).
+ *   out: device [R][D] of out_dtype (SPECGEN_BF16 or SPECGEN_FP32).
+ *   out_lse: device fp32 [R] or NULL.  1 <= S, 0 <= R, 1 <= D <= 1024. */
+specgen_status_t specgen_lse_merge(const float *o_parts, const float *lse_parts, int32_t num_parts,
+                                   int64_t rows, int32_t head_dim, void *out, int32_t out_dtype,
+                                   float *out_lse, hipStream_t stream);
+
+/* Message for the calling thread's most recent non-OK status ("" if none). */
+const char *specgen_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECGEN_H */

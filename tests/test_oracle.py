@@ -1,0 +1,324 @@
+"""Pins of the fp64 oracle against things it does not compute itself:
+library routines (torch SDPA / logsumexp in float64, torch's E4M3 and bf16
+decoders, numpy slicing), closed forms, hand-derived cases and invariants.
+
+The oracle follows the fork semantics of SpecGen (arXiv 2606.17518): forks
+reuse the reasoning prefix's KV (Sec. 4.2; Sec. 8.7), the restore path copies
+cached KV blocks instead of recomputing them (Sec. 6.2.3).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---- element decoding -------------------------------------------------------
+
+def test_e4m3_spot_values_from_format_definition():
+    v = oracle.e4m3_to_f64(np.array([0x00, 0x38, 0x7E, 0x08, 0x01, 0x07, 0x80, 0xB8, 0xFE], np.uint8))
+    assert v[0] == 0.0
+    assert v[1] == 1.0
+    assert v[2] == 448.0
+    assert v[3] == 2.0 ** -6           # smallest normal
+    assert v[4] == 2.0 ** -9           # smallest subnormal
+    assert v[5] == 7 * 2.0 ** -9       # largest subnormal
+    assert v[6] == 0.0 and math.copysign(1.0, v[6]) == -1.0
+    assert v[7] == -1.0
+    assert v[8] == -448.0
+    nan = oracle.e4m3_to_f64(np.array([0x7F, 0xFF], np.uint8))
+    assert np.isnan(nan).all()
+
+
+def test_e4m3_all_codes_match_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = oracle.e4m3_to_f64(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(np.isnan(ours), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(ours[ok], ref[ok])
+    assert np.array_equal(np.signbit(ours[ok]), np.signbit(ref[ok]))
+
+
+def test_bf16_decode_matches_torch():
+    rng = np.random.default_rng(0)
+    bits = rng.integers(0, 1 << 16, size=4096, dtype=np.uint16)
+    ours = oracle.bf16_to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(np.isnan(ours), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(ours[ok], ref[ok])
+
+
+# ---- dense single-query attention ---------------------------------------------
+
+def _sdpa(q, K, V, scale):
+    qt = torch.from_numpy(np.asarray(q, np.float64))[None, None, None, :]
+    kt = torch.from_numpy(np.asarray(K, np.float64))[None, None]
+    vt = torch.from_numpy(np.asarray(V, np.float64))[None, None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)
+    s = (kt[0, 0] @ qt[0, 0, 0]) * scale
+    return o[0, 0, 0].numpy(), float(torch.logsumexp(s, dim=0))
+
+
+@pytest.mark.parametrize("n,D", [(1, 4), (7, 4), (100, 64), (333, 128)])
+def test_dense_matches_torch_sdpa(n, D):
+    rng = np.random.default_rng(n * 1000 + D)
+    q, K, V = rng.standard_normal(D), rng.standard_normal((n, D)), rng.standard_normal((n, D))
+    scale = 1.0 / math.sqrt(D)
+    o, lse = oracle.attend_dense(q, K, V, scale)
+    o_ref, lse_ref = _sdpa(q, K, V, scale)
+    np.testing.assert_allclose(o, o_ref, rtol=0, atol=1e-12)
+    assert abs(lse - lse_ref) < 1e-12
+
+
+def test_dense_constant_keys_give_mean_of_v():
+    rng = np.random.default_rng(1)
+    n, D = 37, 16
+    q = rng.standard_normal(D)
+    k = rng.standard_normal(D)
+    K = np.tile(k, (n, 1))
+    V = rng.standard_normal((n, D))
+    scale = 0.3
+    o, lse = oracle.attend_dense(q, K, V, scale)
+    np.testing.assert_allclose(o, V.mean(axis=0), rtol=0, atol=1e-13)
+    assert abs(lse - (scale * float(q @ k) + math.log(n))) < 1e-12
+
+
+def test_dense_hand_derived_two_key_cases():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "two_key_cases.txt")) if l.strip() and not l.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        scale, q, k1, k2, v1, v2, out, lse = map(float, r)
+        o, l = oracle.attend_dense([q], [[k1], [k2]], [[v1], [v2]], scale)
+        assert abs(o[0] - out) < 1e-12
+        assert abs(l - lse) < 1e-12
+
+
+def test_dense_empty_is_an_empty_part():
+    o, lse = oracle.attend_dense(np.ones(8), np.zeros((0, 8)), np.zeros((0, 8)), 1.0)
+    assert np.all(o == 0) and lse == -math.inf
+
+
+def test_dense_key_shift_invariance():
+    rng = np.random.default_rng(2)
+    n, D = 200, 32
+    q, K, V = rng.standard_normal(D), rng.standard_normal((n, D)), rng.standard_normal((n, D))
+    b = rng.normal(0, 0.5, D)
+    scale = 1 / math.sqrt(D)
+    o1, l1 = oracle.attend_dense(q, K, V, scale)
+    o2, l2 = oracle.attend_dense(q, K + b[None, :], V, scale)
+    np.testing.assert_allclose(o1, o2, rtol=0, atol=1e-12)
+    assert abs((l2 - l1) - scale * float(q @ b)) < 1e-11
+
+
+def test_split_then_merge_equals_unsplit():
+    rng = np.random.default_rng(3)
+    n, D = 500, 64
+    q, K, V = rng.standard_normal(D), rng.standard_normal((n, D)), rng.standard_normal((n, D))
+    scale = 1 / math.sqrt(D)
+    o_full, l_full = oracle.attend_dense(q, K, V, scale)
+    cuts = [0, 0, 17, 17, 200, 499, 500]          # includes empty parts
+    o_parts, l_parts = [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        o, l = oracle.attend_dense(q, K[a:b], V[a:b], scale)
+        o_parts.append(o)
+        l_parts.append(l)
+    o_m, l_m = oracle.lse_merge(np.array(o_parts, np.float32)[:, None, :], np.array(l_parts, np.float32)[:, None])
+    # partials pass through fp32 (the merge's input type), hence 1e-6
+    np.testing.assert_allclose(o_m[0], o_full, rtol=0, atol=2e-6)
+    assert abs(l_m[0] - l_full) < 2e-6
+
+
+# ---- LSE merge -----------------------------------------------------------------
+
+def test_merge_single_part_is_identity():
+    rng = np.random.default_rng(4)
+    o = rng.standard_normal((1, 5, 8)).astype(np.float32)
+    l = rng.standard_normal((1, 5)).astype(np.float32)
+    out, lse = oracle.lse_merge(o, l)
+    np.testing.assert_array_equal(out, o[0].astype(np.float64))
+    np.testing.assert_array_equal(lse, l[0].astype(np.float64))
+
+
+def test_merge_closed_form_two_parts_and_empty_parts():
+    # lse values ln 1 and ln 3 -> weights 1/4 and 3/4; a -inf part is ignored even if its o is NaN
+    o = np.array([[[4.0, 0.0]], [[0.0, 8.0]], [[np.nan, np.nan]]], np.float32)
+    l = np.array([[0.0], [math.log(3.0)], [-np.inf]], np.float32)
+    out, lse = oracle.lse_merge(o, l)
+    np.testing.assert_allclose(out[0], [1.0, 6.0], rtol=0, atol=1e-6)
+    assert abs(lse[0] - math.log(4.0)) < 1e-6
+    # all parts empty -> zero output, -inf lse
+    out, lse = oracle.lse_merge(np.full((2, 1, 3), np.nan, np.float32), np.full((2, 1), -np.inf, np.float32))
+    assert np.all(out == 0) and lse[0] == -math.inf
+
+
+def test_merge_order_independent():
+    rng = np.random.default_rng(5)
+    o = rng.standard_normal((6, 4, 16)).astype(np.float32)
+    l = (3 * rng.standard_normal((6, 4))).astype(np.float32)
+    a, la = oracle.lse_merge(o, l)
+    p = rng.permutation(6)
+    b, lb = oracle.lse_merge(o[p], l[p])
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(la, lb, rtol=0, atol=1e-13)
+
+
+# ---- fork-decode attention over the paged shared-prefix cache ------------------
+
+def _logical_dense(batch, f):
+    """fp64 K/V [n][Hkv][D] of fork f in logical order, decoded by torch from the
+    generator's pre-paging copies (not via the oracle or the pool)."""
+    t = batch.trace_of_fork(f)
+    segs = [(batch.k_logical[t], batch.v_logical[t], batch.k_logical_scale[t], batch.v_logical_scale[t]),
+            (batch.k_logical[batch.num_traces + f], batch.v_logical[batch.num_traces + f],
+             batch.k_logical_scale[batch.num_traces + f], batch.v_logical_scale[batch.num_traces + f])]
+    Ks, Vs = [], []
+    for k, v, ks, vs in segs:
+        if batch.kv_dtype == "bf16":
+            dec = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+            Ks.append(dec(k))
+            Vs.append(dec(v))
+        else:
+            dec = lambda a: torch.from_numpy(a).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+            Ks.append(dec(k) * ks.astype(np.float64)[:, None, None])
+            Vs.append(dec(v) * vs.astype(np.float64)[:, None, None])
+    return np.concatenate(Ks), np.concatenate(Vs)
+
+
+def _check_batch_against_sdpa(batch, atol=1e-12):
+    out, lse = oracle.fork_decode_attn(batch)
+    g = batch.group
+    qd = torch.from_numpy(batch.q.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    for f in range(batch.num_forks):
+        K, V = _logical_dense(batch, f)
+        for h in range(batch.num_q_heads):
+            j = h // g
+            o_ref, l_ref = _sdpa(qd[f, h], K[:, j], V[:, j], batch.sm_scale)
+            np.testing.assert_allclose(out[f, h], o_ref, rtol=0, atol=atol)
+            assert abs(lse[f, h] - l_ref) < atol
+
+
+@pytest.mark.parametrize("P", [1, 2, 15, 16, 17, 33])
+def test_fork_batch_matches_sdpa_on_logical_kv(P):
+    b = synth.make_fork_batch(prefix_lens=[P], forks_per_trace=3, suffix_lens=[0, 1, 17], num_q_heads=4,
+                              num_kv_heads=2, head_dim=8, seed=10 + P, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_batch_multi_trace_ragged_matches_sdpa():
+    b = synth.make_fork_batch(prefix_lens=[5, 40, 16], forks_per_trace=[1, 3, 2],
+                              suffix_lens=[15, 0, 16, 31, 2, 9], num_q_heads=6, num_kv_heads=3, head_dim=16,
+                              seed=21, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_batch_mha_group_one_matches_sdpa():
+    b = synth.make_fork_batch(prefix_lens=[50], forks_per_trace=2, suffix_lens=[3, 20], num_q_heads=3,
+                              num_kv_heads=3, head_dim=8, seed=22, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_batch_fp8_matches_sdpa_on_dequantised_kv():
+    b = synth.make_fork_batch(prefix_lens=[45], forks_per_trace=2, suffix_lens=[0, 19], num_q_heads=4,
+                              num_kv_heads=1, head_dim=16, kv_dtype="fp8_e4m3", seed=23, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_batch_tiny_workload_matches_sdpa():
+    b = synth.workload("tiny_p256_f4", keep_logical=True)
+    _check_batch_against_sdpa(b, atol=1e-11)
+
+
+def test_paging_invariance():
+    kw = dict(prefix_lens=[70], forks_per_trace=3, suffix_lens=[5, 0, 33], num_q_heads=4, num_kv_heads=2,
+              head_dim=16, seed=30)
+    a = synth.make_fork_batch(identity_table=True, **kw)
+    b = synth.make_fork_batch(**kw)
+    assert not np.array_equal(a.prefix_table, b.prefix_table)
+    oa, la = oracle.fork_decode_attn(a)
+    ob, lb = oracle.fork_decode_attn(b)
+    # the identity table draws no permutation, so the random streams differ; the
+    # logical contents are compared through the SDPA pin instead.  Here, re-place
+    # a's logical tokens under b's tables and require identical results.
+    c = _replace_tables(a, b)
+    oc, lc = oracle.fork_decode_attn(c)
+    np.testing.assert_array_equal(oa, oc)
+    np.testing.assert_array_equal(la, lc)
+
+
+def _replace_tables(src, dst_layout):
+    """Copy src's logical KV into the physical placement of dst_layout's tables."""
+    import copy
+    c = copy.deepcopy(src)
+    c.prefix_table = dst_layout.prefix_table.copy()
+    c.suffix_table = dst_layout.suffix_table.copy()
+    c.k_pool = np.full_like(src.k_pool, synth.fork_batch.BF16_NAN)
+    c.v_pool = np.full_like(src.v_pool, synth.fork_batch.BF16_NAN)
+    for old_tab, new_tab in ((src.prefix_table, c.prefix_table), (src.suffix_table, c.suffix_table)):
+        c.k_pool[new_tab] = src.k_pool[old_tab]
+        c.v_pool[new_tab] = src.v_pool[old_tab]
+    return c
+
+
+def test_fork_independence():
+    kw = dict(prefix_lens=[40], forks_per_trace=4, suffix_lens=[5, 9, 16, 1], num_q_heads=4, num_kv_heads=2,
+              head_dim=16, seed=31)
+    a = synth.make_fork_batch(**kw)
+    o1, l1 = oracle.fork_decode_attn(a)
+    b = synth.make_fork_batch(**kw)
+    # perturb fork 2's suffix values (its own blocks only)
+    ids = b.suffix_table[b.suffix_table_off[2]:b.suffix_table_off[3]]
+    rng = np.random.default_rng(99)
+    b.v_pool[ids, :16] = synth.fork_batch._to_bf16_bits(rng.standard_normal(b.v_pool[ids, :16].shape).astype(np.float32))
+    o2, l2 = oracle.fork_decode_attn(b)
+    for f in range(4):
+        if f == 2:
+            assert not np.array_equal(o1[f], o2[f])
+        else:
+            np.testing.assert_array_equal(o1[f], o2[f])
+            np.testing.assert_array_equal(l1[f], l2[f])
+
+
+def test_gqa_group_members_with_equal_queries_agree():
+    b = synth.make_fork_batch(prefix_lens=[30], forks_per_trace=2, suffix_lens=[4, 7], num_q_heads=8,
+                              num_kv_heads=2, head_dim=16, seed=32)
+    b.q[:, 1] = b.q[:, 0]      # heads 0 and 1 share kv head 0
+    b.q[:, 5] = b.q[:, 0]      # head 5 reads kv head 1: same query, different keys
+    o, l = oracle.fork_decode_attn(b)
+    np.testing.assert_array_equal(o[:, 0], o[:, 1])
+    assert not np.allclose(o[:, 0], o[:, 5])
+
+
+def test_row_subset_matches_full():
+    b = synth.make_fork_batch(prefix_lens=[64], forks_per_trace=3, suffix_lens=[1, 2, 3], num_q_heads=4,
+                              num_kv_heads=2, head_dim=16, seed=33)
+    o, l = oracle.fork_decode_attn(b)
+    rows = np.array([[2, 3], [0, 0], [1, 2]], np.int32)
+    os_, ls = oracle.fork_decode_attn(b, rows=rows)
+    for i, (f, h) in enumerate(rows):
+        np.testing.assert_array_equal(os_[i], o[f, h])
+        assert ls[i] == l[f, h]
+
+
+# ---- KV-block import -------------------------------------------------------------
+
+def test_import_is_blockwise_memcpy_with_bad_ids_skipped():
+    case = synth.make_import_case(n=12, num_dst_blocks=40, block_bytes=96, num_tensors=2, seed=5, bad_ids=[3, 7])
+    for t in range(2):
+        pool = case.pool[t].copy()
+        bad = oracle.kv_import(pool, case.staging[t], case.block_bytes, case.dst_ids, case.num_dst_blocks)
+        assert bad == 2
+        ref = case.pool[t].copy().reshape(case.num_dst_blocks, case.block_bytes)
+        st = case.staging[t].reshape(case.n, case.block_bytes)
+        ok = (case.dst_ids >= 0) & (case.dst_ids < case.num_dst_blocks)
+        ref[case.dst_ids[ok]] = st[ok]
+        assert np.array_equal(pool, ref.reshape(-1))
+        untouched = np.setdiff1d(np.arange(case.num_dst_blocks), case.dst_ids[ok])
+        assert np.all(pool.reshape(case.num_dst_blocks, -1)[untouched] == synth.SENTINEL)
