@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Fork-decode attention + prefix KV import on one MI355X.
+
+One step = restore a trace's prefix KV blocks from a contiguous staging copy
+into the paged pool (specgen_kv_import), then one decode step of fork-decode
+attention for all forks (specgen_fork_decode_attn: split partial kernel, then
+the log-sum-exp merge).  Inputs are seeded synthetic tensors already resident
+in HBM.  R replicas of the pool/q rotate so that every step reads data no
+cache level still holds (a replica is far larger than the 256 MB MALL): step k
+imports into replica k % R and attends over replica (k+1) % R, whose prefix
+was restored R-1 steps earlier.
+
+Prints one JSON line.  `value` is the attention call's achieved HBM rate in
+GB/s: algorithmic bytes (each valid prefix token's K/V once per kv head, each
+suffix token's K/V once, q in, out/lse out, index arrays) over the average
+attention time measured with HIP events on the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "fork-decode attention achieved HBM GB/s (% of peak) + fork-tokens/s at P=32k,F=16"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("attn_mfma.hip", "worker.h", "common.h", "plan.h"):
+        with open(os.path.join(ROOT, "paper_2606_17518_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str):
+    """HBM traffic of the partial kernel from committed rocprofv3 counter runs,
+    only if they were taken on the current kernel source."""
+    p = os.path.join(ROOT, "profiles", f"traffic_attn_mfma_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as fh:
+        d = json.load(fh)
+    if d.get("source_hash") != source_hash():
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(batch, target_s: float):
+    """The fp64 oracle on whole forks of the same workload, on this host's cores."""
+    import oracle
+    Hq = batch.num_q_heads
+    one = np.array([[0, h] for h in range(Hq)], np.int32)
+    t0 = time.perf_counter()
+    oracle.fork_decode_attn(batch, rows=one)
+    t1 = time.perf_counter() - t0
+    nf = int(max(1, min(batch.num_forks - 1, target_s / max(t1, 1e-3))))
+    rows = np.array([[f, h] for f in range(1, 1 + nf) for h in range(Hq)], np.int32)
+    t0 = time.perf_counter()
+    oracle.fork_decode_attn(batch, rows=rows)
+    dt = time.perf_counter() - t0
+    forks_per_s = nf / dt
+    step_s = batch.num_forks / forks_per_s
+    return {"value": round(batch.algorithmic_bytes() / step_s / 1e9, 4), "unit": "GB/s",
+            "fork_tokens_per_s": round(forks_per_s, 3), "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"forks 1..{nf} of {batch.num_forks} (all {Hq} q heads each, {nf * Hq} rows) of the same "
+                      f"workload, fp64 C oracle, {dt:.1f} s; GB/s = step algorithmic bytes / extrapolated step time"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="trace_p32k_f16")
+    ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--path", default="auto", choices=["auto", "mfma", "dot"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the fork-decode path has no multi-GPU part in this build "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_17518_amd as sg
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    spec = synth.WORKLOADS[args.workload]
+    log(f"generating {args.workload}")
+    b = synth.workload(args.workload)
+    do_import = spec.get("import_prefix", False)
+    R = max(2, args.replicas)
+    log(f"uploading {R} replicas")
+    reps = []
+    for r in range(R):
+        fb = sg.ForkBatchTensors.from_numpy(b, dev, args.path)
+        if r > 0:   # index arrays are shared; only q and the pools are replicated
+            for name in ("fork_off", "prefix_len", "prefix_table_off", "prefix_table", "suffix_len",
+                         "suffix_table_off", "suffix_table"):
+                setattr(fb, name, getattr(reps[0], name))
+        reps.append(fb)
+    N, Hq, D = b.num_forks, b.num_q_heads, b.head_dim
+    out = torch.empty((N, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((N, Hq), dtype=torch.float32, device=dev)
+    ws = sg.alloc_workspace(reps[0])
+    stream = torch.cuda.current_stream()
+
+    imp = None
+    if do_import:
+        ks, vs, ids, kss, vss = synth.prefix_import_from_batch(b, 0)
+        bb = b.block_bytes()
+        ids_d = torch.from_numpy(ids).to(dev)
+        imp = []
+        for fb in reps:
+            tensors = [(fb.k_pool, torch.from_numpy(ks.reshape(-1).view(np.uint8)).to(dev), bb),
+                       (fb.v_pool, torch.from_numpy(vs.reshape(-1).view(np.uint8)).to(dev), bb)]
+            if kss is not None:
+                tensors += [(fb.k_scale, torch.from_numpy(kss).to(dev), 4), (fb.v_scale, torch.from_numpy(vss).to(dev), 4)]
+            imp.append(tensors)
+            # poison the destination blocks, restore them, and check the restore once
+            fb.k_pool.view(b.num_blocks, -1)[ids_d.long()] = -1
+            fb.v_pool.view(b.num_blocks, -1)[ids_d.long()] = -1
+            sg.specgen_kv_import(tensors, ids_d, b.num_blocks)
+        torch.cuda.synchronize()
+        ref_k = torch.from_numpy(b.k_pool.reshape(b.num_blocks, -1).view(np.uint8)[ids]).to(dev)
+        assert torch.equal(reps[-1].k_pool.view(b.num_blocks, -1).view(torch.uint8)[ids_d.long()], ref_k), \
+            "prefix restore mismatch"
+        import_bytes = (len(imp[0]) and sum(2 * t[2] for t in imp[0])) * len(ids) + 4 * len(ids)
+
+    def step(k, evs):
+        r_imp, r_att = k % R, (k + 1) % R
+        evs[0].record(stream)
+        if imp is not None:
+            sg.specgen_kv_import(imp[r_imp], ids_d, b.num_blocks, stream=stream)
+        evs[1].record(stream)
+        sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_PARTIALS, None, None, ws, stream=stream)
+        evs[2].record(stream)
+        sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_MERGE, out, lse, ws, stream=stream)
+        evs[3].record(stream)
+
+    total = args.warmup + args.steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
+    log(f"warmup {args.warmup}")
+    for k in range(args.warmup):
+        step(k, events[k])
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for k in range(args.warmup, total):
+        step(k, events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    timed = events[args.warmup:]
+    imp_ms = np.array([e[0].elapsed_time(e[1]) for e in timed])
+    part_ms = np.array([e[1].elapsed_time(e[2]) for e in timed])
+    merge_ms = np.array([e[2].elapsed_time(e[3]) for e in timed])
+    attn_ms = part_ms + merge_ms
+    assert torch.isfinite(out.float()).all(), "non-finite attention output"
+
+    attn_bytes = b.algorithmic_bytes()
+    out_bytes = N * Hq * (D * 2 + 4)
+    kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
+    attn_s = float(attn_ms.mean()) / 1e3
+    part_s = float(part_ms.mean()) / 1e3
+    value = attn_bytes / attn_s / 1e9
+    achieved = kern_bytes / part_s / 1e9
+    res = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "traces": b.num_traces, "forks": N,
+                   "prefix_len": [int(x) for x in b.prefix_len[:4]], "suffix_tokens": int(b.suffix_len.sum()),
+                   "q_heads": Hq, "kv_heads": b.num_kv_heads, "head_dim": D, "kv_dtype": b.kv_dtype,
+                   "path": args.path, "replicas": R, "import_blocks": int(len(ids)) if imp is not None else 0},
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "fork_tokens_per_s": round(N / attn_s, 1),
+        "attn_us": {"mean": round(float(attn_ms.mean()) * 1e3, 2), "p10": round(float(np.percentile(attn_ms, 10)) * 1e3, 2),
+                    "p50": round(float(np.median(attn_ms)) * 1e3, 2), "p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
+                    "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2)},
+        "attn_algorithmic_bytes": int(attn_bytes),
+        "roofline": {"kernel": "attn_mfma_kernel (partials phase)", "bound": "hbm", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic_from_profile(args.workload), "algorithmic_bytes_per_launch": int(kern_bytes)},
+    }
+    if imp is not None:
+        res["import"] = {"blocks": int(len(ids)), "bytes": int(import_bytes), "us": round(float(imp_ms.mean()) * 1e3, 2),
+                         "gbps": round(import_bytes / (float(imp_ms.mean()) / 1e3) / 1e9, 2)}
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

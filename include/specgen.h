@@ -97,7 +97,7 @@ typedef struct {
   const int32_t *prefix_table;
   const int32_t *suffix_len; /* [N], S_f >= 0                                    */
   const int32_t *suffix_table_off; /* [N+1], at least ceil(S_f/16) ids per fork  */
-  const int32_t *suffix_table;
+  const int32_t *suffix_table;     /* may be NULL only if every S_f is 0         */
   /* host mirrors of the index arrays above (same contents), read only during
      the call to size the work split and the workspace; the device copies are
      what the kernels read, so the two must agree */
@@ -128,6 +128,19 @@ specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batc
 specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t *b, void *out, float *out_lse,
                                           void *workspace, size_t workspace_bytes,
                                           hipStream_t stream);
+
+/* The two phases of specgen_fork_decode_attn, for callers that want to place
+ * work or timing events between them.  SPECGEN_PHASE_PARTIALS runs the split
+ * attention kernels, which leave one partial (o, lse) per worker and item in
+ * the workspace; SPECGEN_PHASE_MERGE combines those partials into out and
+ * out_lse.  PARTIALS followed by MERGE on the same stream, with the same batch
+ * and workspace, gives exactly the result of one specgen_fork_decode_attn
+ * call (SPECGEN_PHASE_ALL).  Arguments as for specgen_fork_decode_attn; `out`
+ * may be NULL for PARTIALS. */
+typedef enum { SPECGEN_PHASE_ALL = 0, SPECGEN_PHASE_PARTIALS = 1, SPECGEN_PHASE_MERGE = 2 } specgen_phase_t;
+specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t *b, int32_t phase, void *out,
+                                                float *out_lse, void *workspace, size_t workspace_bytes,
+                                                hipStream_t stream);
 
 /* One tensor of a KV-block import: dst_pool is [num_dst_blocks][block_bytes],
  * src_staging is [n][block_bytes] contiguous (the restored remote copy). */

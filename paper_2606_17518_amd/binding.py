@@ -1,0 +1,222 @@
+"""ctypes binding of libspecgen.so (include/specgen.h), argument marshalling only.
+
+Every function here forwards to the C entry point of the same name; all the
+work happens in the HIP kernels.  Device buffers are torch tensors on the
+current HIP device; the stream defaults to torch's current stream.  If the
+library has not been built this module raises on first use -- there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from .build import LIB_PATH
+
+SPECGEN_OK, SPECGEN_ERR_INVALID_ARG, SPECGEN_ERR_UNSUPPORTED, SPECGEN_ERR_WORKSPACE, SPECGEN_ERR_DEVICE = range(5)
+SPECGEN_BF16, SPECGEN_FP8_E4M3, SPECGEN_FP32 = 0, 1, 2
+SPECGEN_PATH_AUTO, SPECGEN_PATH_DOT, SPECGEN_PATH_MFMA = 0, 1, 2
+PATHS = {"auto": SPECGEN_PATH_AUTO, "dot": SPECGEN_PATH_DOT, "mfma": SPECGEN_PATH_MFMA}
+
+SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
+
+EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
+            "specgen_kv_import", "specgen_lse_merge", "specgen_last_error")
+
+
+class SpecgenError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"specgen status {status}: {message}")
+        self.status = status
+
+
+class ForkBatchC(C.Structure):
+    _fields_ = [
+        ("num_traces", C.c_int32), ("num_forks", C.c_int32), ("num_q_heads", C.c_int32),
+        ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("block_size", C.c_int32),
+        ("num_blocks", C.c_int64), ("sm_scale", C.c_float), ("kv_dtype", C.c_int32),
+        ("path", C.c_int32), ("reserved", C.c_int32),
+        ("q", C.c_void_p), ("k_pool", C.c_void_p), ("v_pool", C.c_void_p),
+        ("k_scale", C.c_void_p), ("v_scale", C.c_void_p),
+        ("fork_off", C.c_void_p), ("prefix_len", C.c_void_p), ("prefix_table_off", C.c_void_p),
+        ("prefix_table", C.c_void_p), ("suffix_len", C.c_void_p), ("suffix_table_off", C.c_void_p),
+        ("suffix_table", C.c_void_p),
+        ("fork_off_h", C.c_void_p), ("prefix_len_h", C.c_void_p), ("suffix_len_h", C.c_void_p),
+    ]
+
+
+class KvTensorC(C.Structure):
+    _fields_ = [("dst_pool", C.c_void_p), ("src_staging", C.c_void_p), ("block_bytes", C.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it was never built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2606_17518_amd.build.build()")
+        L = C.CDLL(LIB_PATH)
+        P = C.c_void_p
+        L.specgen_fork_decode_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), C.POINTER(C.c_size_t)]
+        L.specgen_fork_decode_attn_workspace_size.restype = C.c_int
+        L.specgen_fork_decode_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, C.c_size_t, P]
+        L.specgen_fork_decode_attn.restype = C.c_int
+        L.specgen_fork_decode_attn_phase.argtypes = [C.POINTER(ForkBatchC), C.c_int32, P, P, P, C.c_size_t, P]
+        L.specgen_fork_decode_attn_phase.restype = C.c_int
+        L.specgen_kv_import.argtypes = [C.POINTER(KvTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
+        L.specgen_kv_import.restype = C.c_int
+        L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
+        L.specgen_lse_merge.restype = C.c_int
+        L.specgen_last_error.argtypes = []
+        L.specgen_last_error.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != SPECGEN_OK:
+        raise SpecgenError(status, lib().specgen_last_error().decode())
+
+
+def _dptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return C.c_void_p(stream.cuda_stream)
+    return C.c_void_p(int(stream))
+
+
+@dataclasses.dataclass
+class ForkBatchTensors:
+    """Device tensors + host mirrors of one fork batch (see specgen_fork_batch_t)."""
+    num_traces: int
+    num_forks: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    num_blocks: int
+    sm_scale: float
+    kv_dtype: int
+    q: torch.Tensor
+    k_pool: torch.Tensor
+    v_pool: torch.Tensor
+    k_scale: Optional[torch.Tensor]
+    v_scale: Optional[torch.Tensor]
+    fork_off: torch.Tensor
+    prefix_len: torch.Tensor
+    prefix_table_off: torch.Tensor
+    prefix_table: torch.Tensor
+    suffix_len: torch.Tensor
+    suffix_table_off: torch.Tensor
+    suffix_table: torch.Tensor
+    fork_off_h: np.ndarray
+    prefix_len_h: np.ndarray
+    suffix_len_h: np.ndarray
+    path: int = SPECGEN_PATH_AUTO
+    block_size: int = 16
+
+    @staticmethod
+    def from_numpy(b, device="cuda", path: str | int = "auto") -> "ForkBatchTensors":
+        """Upload an object with the numpy fields of a fork batch (q, pools,
+        scales, index arrays) and keep int32 host mirrors of the lengths."""
+        def dev(a, dt):
+            return torch.from_numpy(np.ascontiguousarray(a).view(dt)).to(device)
+        fp8 = b.kv_dtype != "bf16"
+        kv_np = np.uint8 if fp8 else np.int16
+        return ForkBatchTensors(
+            num_traces=b.num_traces, num_forks=b.num_forks, num_q_heads=b.num_q_heads,
+            num_kv_heads=b.num_kv_heads, head_dim=b.head_dim, num_blocks=b.num_blocks,
+            sm_scale=float(b.sm_scale), kv_dtype=SPECGEN_FP8_E4M3 if fp8 else SPECGEN_BF16,
+            q=dev(b.q, np.int16), k_pool=dev(b.k_pool, kv_np), v_pool=dev(b.v_pool, kv_np),
+            k_scale=dev(b.k_scale, np.float32) if fp8 else None,
+            v_scale=dev(b.v_scale, np.float32) if fp8 else None,
+            fork_off=dev(b.fork_off, np.int32), prefix_len=dev(b.prefix_len, np.int32),
+            prefix_table_off=dev(b.prefix_table_off, np.int32), prefix_table=dev(b.prefix_table, np.int32),
+            suffix_len=dev(b.suffix_len, np.int32), suffix_table_off=dev(b.suffix_table_off, np.int32),
+            suffix_table=dev(b.suffix_table, np.int32),
+            fork_off_h=np.ascontiguousarray(b.fork_off, np.int32),
+            prefix_len_h=np.ascontiguousarray(b.prefix_len, np.int32),
+            suffix_len_h=np.ascontiguousarray(b.suffix_len, np.int32),
+            path=PATHS[path] if isinstance(path, str) else int(path))
+
+    def c_struct(self, **overrides) -> ForkBatchC:
+        s = ForkBatchC()
+        s.num_traces = self.num_traces
+        s.num_forks = self.num_forks
+        s.num_q_heads = self.num_q_heads
+        s.num_kv_heads = self.num_kv_heads
+        s.head_dim = self.head_dim
+        s.block_size = self.block_size
+        s.num_blocks = self.num_blocks
+        s.sm_scale = self.sm_scale
+        s.kv_dtype = self.kv_dtype
+        s.path = self.path
+        s.reserved = 0
+        for name in ("q", "k_pool", "v_pool", "k_scale", "v_scale", "fork_off", "prefix_len", "prefix_table_off",
+                     "prefix_table", "suffix_len", "suffix_table_off", "suffix_table"):
+            t = getattr(self, name)
+            setattr(s, name, None if t is None else t.data_ptr())
+        for name in ("fork_off_h", "prefix_len_h", "suffix_len_h"):
+            setattr(s, name, getattr(self, name).ctypes.data)
+        for k, v in overrides.items():
+            setattr(s, k, v)
+        return s
+
+
+def specgen_fork_decode_attn_workspace_size(batch) -> int:
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    n = C.c_size_t(0)
+    _check(lib().specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)))
+    return int(n.value)
+
+
+def alloc_workspace(batch, device="cuda") -> torch.Tensor:
+    n = specgen_fork_decode_attn_workspace_size(batch)
+    return torch.empty(max(n, 256) // 4 + 64, dtype=torch.float32, device=device)
+
+
+def specgen_fork_decode_attn(batch, out: torch.Tensor, out_lse: Optional[torch.Tensor], workspace: torch.Tensor,
+                             stream=None) -> None:
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _check(lib().specgen_fork_decode_attn(C.byref(s), _dptr(out), _dptr(out_lse), _dptr(workspace),
+                                          workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def specgen_fork_decode_attn_phase(batch, phase: int, out: Optional[torch.Tensor], out_lse: Optional[torch.Tensor],
+                                   workspace: torch.Tensor, stream=None) -> None:
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _check(lib().specgen_fork_decode_attn_phase(C.byref(s), int(phase), _dptr(out), _dptr(out_lse), _dptr(workspace),
+                                                workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def specgen_kv_import(tensors: Sequence[tuple], dst_block_ids: torch.Tensor, num_dst_blocks: int,
+                      bad_id_count: Optional[torch.Tensor] = None, stream=None) -> None:
+    """tensors: sequence of (dst_pool tensor, src_staging tensor, block_bytes)."""
+    arr = (KvTensorC * max(1, len(tensors)))()
+    for i, (dst, src, bb) in enumerate(tensors):
+        arr[i].dst_pool = dst.data_ptr()
+        arr[i].src_staging = src.data_ptr()
+        arr[i].block_bytes = int(bb)
+    _check(lib().specgen_kv_import(arr, len(tensors), _dptr(dst_block_ids), int(dst_block_ids.numel()),
+                                   int(num_dst_blocks), _dptr(bad_id_count), _stream(stream)))
+
+
+def specgen_lse_merge(o_parts: torch.Tensor, lse_parts: torch.Tensor, out: torch.Tensor,
+                      out_lse: Optional[torch.Tensor] = None, stream=None) -> None:
+    """o_parts [S][R][D] f32, lse_parts [S][R] f32, out [R][D] bf16 or f32."""
+    S, R, D = o_parts.shape
+    dt = SPECGEN_BF16 if out.dtype == torch.bfloat16 else SPECGEN_FP32
+    _check(lib().specgen_lse_merge(_dptr(o_parts), _dptr(lse_parts), S, R, D, _dptr(out), dt, _dptr(out_lse),
+                                   _stream(stream)))

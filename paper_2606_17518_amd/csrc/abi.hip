@@ -1,0 +1,208 @@
+// abi.hip -- the extern "C" entry points declared in include/specgen.h:
+// argument checks (all before any launch), the host planner that turns the
+// host length mirrors into the work split of plan.h, and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/specgen.h"
+#include "kernels.h"
+#include "planner.h"
+
+
+using namespace specgen;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+specgen_status_t fail(specgen_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+specgen_status_t ok() { return SPECGEN_OK; }
+
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  static int cached[64] = {0};
+  if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+  if (dev >= 0 && dev < 64) cached[dev] = cus;
+  return cus;
+}
+
+// Checks the batch and builds the plan; `ws_floats` receives the workspace size.
+specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* ws_floats) {
+  if (!b) return fail(SPECGEN_ERR_INVALID_ARG, "batch is NULL");
+  if (b->reserved != 0) return fail(SPECGEN_ERR_INVALID_ARG, "reserved field must be 0");
+  if (b->num_traces < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_traces must be >= 1 (got %d)", b->num_traces);
+  if (b->num_forks < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_forks must be >= 1 (got %d)", b->num_forks);
+  if (b->block_size != 16) return fail(SPECGEN_ERR_UNSUPPORTED, "block_size %d must be 16", b->block_size);
+  if (b->num_blocks < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_blocks must be >= 1");
+  if (!(b->sm_scale > 0.f) || !std::isfinite(b->sm_scale))
+    return fail(SPECGEN_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  if (b->kv_dtype != SPECGEN_BF16 && b->kv_dtype != SPECGEN_FP8_E4M3)
+    return fail(SPECGEN_ERR_UNSUPPORTED, "kv_dtype %d not supported", b->kv_dtype);
+  if (b->path != SPECGEN_PATH_AUTO && b->path != SPECGEN_PATH_DOT && b->path != SPECGEN_PATH_MFMA)
+    return fail(SPECGEN_ERR_INVALID_ARG, "path %d unknown", b->path);
+  if (!b->q || !b->k_pool || !b->v_pool || !b->fork_off || !b->prefix_len || !b->prefix_table_off ||
+      !b->prefix_table || !b->suffix_len || !b->suffix_table_off)
+    return fail(SPECGEN_ERR_INVALID_ARG, "a device pointer of the batch is NULL");
+  if (b->kv_dtype == SPECGEN_FP8_E4M3 && (!b->k_scale || !b->v_scale))
+    return fail(SPECGEN_ERR_INVALID_ARG, "E4M3 KV needs k_scale and v_scale");
+  if (!b->fork_off_h || !b->prefix_len_h || !b->suffix_len_h)
+    return fail(SPECGEN_ERR_INVALID_ARG, "a host mirror of the batch is NULL");
+  if (!b->suffix_table) {   // only a batch without suffix tokens may omit the suffix table
+    for (int f = 0; f < b->num_forks; ++f)
+      if (b->suffix_len_h[f] > 0) return fail(SPECGEN_ERR_INVALID_ARG, "suffix_table is NULL but fork %d has suffix tokens", f);
+  }
+  const bool fp8 = b->kv_dtype == SPECGEN_FP8_E4M3;
+  PlanInputs in;
+  in.T = b->num_traces;
+  in.N = b->num_forks;
+  in.Hq = b->num_q_heads;
+  in.Hkv = b->num_kv_heads;
+  in.D = b->head_dim;
+  in.policy = b->path;
+  in.fork_off = b->fork_off_h;
+  in.prefix_len = b->prefix_len_h;
+  in.suffix_len = b->suffix_len_h;
+  in.tt[0] = mfma_tile_tokens(in.D == 64 ? 64 : 128, fp8);
+  in.tt[1] = dot_tile_tokens(in.D);
+  in.rbs[0] = 128;
+  in.rbs[1] = dot_rows();
+  in.item_cap[0] = mfma_item_cap();
+  in.item_cap[1] = dot_item_cap();
+  in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128);
+  in.tile_cap[1] = dot_tile_cap(in.D);
+  char err[256];
+  const int rc = plan_build(in, [] { return device_cus(); }, plan, ws_floats, err, sizeof err);
+  if (rc == kPlanInvalid) return fail(SPECGEN_ERR_INVALID_ARG, "%s", err);
+  if (rc == kPlanUnsupported) return fail(SPECGEN_ERR_UNSUPPORTED, "%s", err);
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batch_t* b, size_t* bytes) {
+  if (!bytes) return fail(SPECGEN_ERR_INVALID_ARG, "bytes is NULL");
+  Plan plan;
+  int64_t wsf = 0;
+  const specgen_status_t st = build_plan(b, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  *bytes = (size_t)(wsf * 4);
+  return ok();
+}
+
+specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, int32_t phase, void* out,
+                                                float* out_lse, void* workspace, size_t workspace_bytes,
+                                                hipStream_t stream) {
+  if (phase != SPECGEN_PHASE_ALL && phase != SPECGEN_PHASE_PARTIALS && phase != SPECGEN_PHASE_MERGE)
+    return fail(SPECGEN_ERR_INVALID_ARG, "phase %d unknown", phase);
+  Plan plan;
+  int64_t wsf = 0;
+  specgen_status_t st = build_plan(b, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  if (!out && phase != SPECGEN_PHASE_PARTIALS) return fail(SPECGEN_ERR_INVALID_ARG, "out is NULL");
+  if ((size_t)(wsf * 4) > workspace_bytes || (wsf > 0 && !workspace))
+    return fail(SPECGEN_ERR_WORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes, (long long)(wsf * 4));
+  if (((uintptr_t)workspace & 255) != 0) return fail(SPECGEN_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (((uintptr_t)b->q & 15) || ((uintptr_t)b->k_pool & 15) || ((uintptr_t)b->v_pool & 15))
+    return fail(SPECGEN_ERR_INVALID_ARG, "q, k_pool and v_pool must be 16-byte aligned");
+  AttnArgs a;
+  a.q = static_cast<const uint16_t*>(b->q);
+  a.k_pool = static_cast<const uint8_t*>(b->k_pool);
+  a.v_pool = static_cast<const uint8_t*>(b->v_pool);
+  a.k_scale = b->k_scale;
+  a.v_scale = b->v_scale;
+  a.prefix_table_off = b->prefix_table_off;
+  a.prefix_table = b->prefix_table;
+  a.suffix_len = b->suffix_len;
+  a.suffix_table_off = b->suffix_table_off;
+  a.suffix_table = b->suffix_table;
+  a.ws = static_cast<float*>(workspace);
+  a.sm_scale = b->sm_scale;
+  a.c_log2 = b->sm_scale * kLog2e;
+  const bool fp8 = b->kv_dtype == SPECGEN_FP8_E4M3;
+  hipError_t e = hipSuccess;
+  if (phase != SPECGEN_PHASE_MERGE) {
+    if (plan.part[kPartMfma].workers > 0) e = launch_attn_mfma_any(a, plan, fp8, stream);
+    if (e == hipSuccess && plan.part[kPartDot].workers > 0) e = launch_attn_dot_any(a, plan, fp8, stream);
+  }
+  if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t* b, void* out, float* out_lse,
+                                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return specgen_fork_decode_attn_phase(b, SPECGEN_PHASE_ALL, out, out_lse, workspace, workspace_bytes, stream);
+}
+
+specgen_status_t specgen_kv_import(const specgen_kv_tensor_t* tensors, int32_t num_tensors,
+                                   const int32_t* dst_block_ids, int64_t n, int64_t num_dst_blocks,
+                                   int32_t* bad_id_count, hipStream_t stream) {
+  if (!tensors) return fail(SPECGEN_ERR_INVALID_ARG, "tensors is NULL");
+  if (num_tensors < 1 || num_tensors > 4) return fail(SPECGEN_ERR_INVALID_ARG, "num_tensors %d not in 1..4", num_tensors);
+  if (n < 0 || n > INT32_MAX) return fail(SPECGEN_ERR_INVALID_ARG, "n %lld out of range", (long long)n);
+  if (num_dst_blocks < 0) return fail(SPECGEN_ERR_INVALID_ARG, "num_dst_blocks must be >= 0");
+  if (n > 0 && !dst_block_ids) return fail(SPECGEN_ERR_INVALID_ARG, "dst_block_ids is NULL");
+  ImportArgs a;
+  std::memset(&a, 0, sizeof a);
+  for (int i = 0; i < num_tensors; ++i) {
+    const specgen_kv_tensor_t& t = tensors[i];
+    if (t.block_bytes <= 0 || (t.block_bytes & 3))
+      return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: block_bytes %lld must be > 0 and a multiple of 4", i,
+                  (long long)t.block_bytes);
+    if (n > 0 && (!t.dst_pool || !t.src_staging)) return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: NULL pointer", i);
+    const uintptr_t al = (t.block_bytes & 15) ? 3 : 15;
+    if (((uintptr_t)t.dst_pool & al) || ((uintptr_t)t.src_staging & al))
+      return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: pointers must be aligned to the copy vector", i);
+    a.t[i].dst = static_cast<uint8_t*>(t.dst_pool);
+    a.t[i].src = static_cast<const uint8_t*>(t.src_staging);
+    a.t[i].block_bytes = t.block_bytes;
+  }
+  a.num_tensors = num_tensors;
+  a.dst_ids = dst_block_ids;
+  a.n = n;
+  a.num_dst_blocks = num_dst_blocks;
+  a.bad_id_count = bad_id_count;
+  const hipError_t e = launch_kv_import(a, stream);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+specgen_status_t specgen_lse_merge(const float* o_parts, const float* lse_parts, int32_t num_parts, int64_t rows,
+                                   int32_t head_dim, void* out, int32_t out_dtype, float* out_lse,
+                                   hipStream_t stream) {
+  if (num_parts < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_parts must be >= 1");
+  if (rows < 0) return fail(SPECGEN_ERR_INVALID_ARG, "rows must be >= 0");
+  if (head_dim < 1 || head_dim > 1024) return fail(SPECGEN_ERR_INVALID_ARG, "head_dim %d not in 1..1024", head_dim);
+  if (out_dtype != SPECGEN_BF16 && out_dtype != SPECGEN_FP32)
+    return fail(SPECGEN_ERR_INVALID_ARG, "out_dtype must be BF16 or FP32");
+  if (rows > 0 && (!o_parts || !lse_parts || !out)) return fail(SPECGEN_ERR_INVALID_ARG, "NULL pointer");
+  if (rows > (int64_t)UINT32_MAX * 4) return fail(SPECGEN_ERR_UNSUPPORTED, "too many rows");
+  const hipError_t e = launch_lse_merge(o_parts, lse_parts, num_parts, rows, head_dim, out,
+                                        out_dtype == SPECGEN_BF16, out_lse, stream);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+const char* specgen_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,396 @@
+// attn_mfma.hip -- the shared-prefix (and suffix) partial-attention kernel on
+// gfx950 bf16 matrix cores.
+//
+// One workgroup = one worker of the MFMA partition (plan.h): it walks a
+// contiguous range of tiles, each tile being TT consecutive tokens of one work
+// item.  For a prefix item the rows are every (fork, q head) pair of a GQA
+// group of one trace, so the tile's K/V is read from HBM once and used by all
+// forks -- the shared reasoning prefix is read once per step instead of once
+// per fork (forks reuse the prefix cache, Sec. 4.2 / Sec. 8.7).  For a suffix
+// item the rows are one fork's g query heads (padded to 32 rows per wave).
+//
+// Data path per tile (D=128 bf16: 64 tokens, 16 KiB of K + 16 KiB of V):
+//   HBM --global_load_dwordx4--> VGPRs (two tiles in flight) --ds_write_b128-->
+//   XOR-swizzled LDS --ds_read_b128 (K) / ds_read_b64_tr_b16 (V)--> MFMA.
+// Per 32-token slab and 16-row N-tile, S^T = K Q^T on v_mfma_f32_16x16x32_bf16
+// (A = 16 keys x 32 dims, B = Q^T 32 dims x 16 rows); the keys of the two S^T
+// tiles are taken in the order that makes each lane's scores the 8
+// consecutive tokens PV consumes, so the scores feed O^T = V^T P^T (A = V^T 16
+// dims x 32 tokens from the transposing LDS read, B = P^T) without a shuffle.
+// Online softmax in fp32 per row; each worker writes one normalised partial
+// (o, lse) per item it touched, merged later by the log-sum-exp rule.
+#include "worker.h"
+
+namespace specgen {
+
+template <int D, bool FP8>
+struct MfmaCfg {
+  static constexpr int kThreads = 256;
+  static constexpr int kWaves = 4;
+  static constexpr int kTT = (D == 128) ? 64 : 128;   // tokens per tile
+  static constexpr int kRowB = D * 2;                 // LDS bytes per token row (bf16)
+  static constexpr int kCPR = kRowB / 16;             // 16-byte chunks per LDS row
+  static constexpr int kTileB = kTT * kRowB;          // LDS bytes of one K or V tile
+  static constexpr int kLoads = kTileB / 16 / kThreads;  // chunks per thread per tensor
+  static constexpr int kGElem = FP8 ? 1 : 2;          // pool bytes per element
+  static constexpr int kGChunk = 8 * kGElem;          // pool bytes per LDS chunk
+  static constexpr int kIdsPerTile = kTT / 16;
+  static constexpr int kStageB = 2 * kTileB;
+  static constexpr int kItemCap = 64;
+  static constexpr int kIdCap = 2048;
+  static constexpr int kTileCap = kIdCap / kIdsPerTile;
+  // LDS layout
+  static constexpr int kOffStage0 = 0;
+  static constexpr int kOffStage1 = kStageB;
+  static constexpr int kOffComb = 2 * kStageB;                 // [2 rg][32 rows][D] f32
+  static constexpr int kOffCombML = kOffComb + 2 * 32 * D * 4; // [2 rg][32] m, then l
+  static constexpr int kOffItems = kOffCombML + 2 * 2 * 32 * 4;
+  static constexpr int kOffIds = kOffItems + kItemCap * kItemInts * 4;
+  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
+  static_assert(kLoads * 16 * kThreads == kTileB, "tile must split evenly over threads");
+  static_assert(kLdsBytes <= 163840, "LDS budget");
+};
+
+// LDS swizzles: K chunks are XOR-ed so a 16-key MFMA operand read hits
+// distinct banks; V chunks are XOR-ed by even values (8-byte halves stay
+// together) so the 4 keys of a transposing read hit distinct 32-byte groups.
+template <int CPR>
+__device__ __forceinline__ int swz_k(int tok) { return ((tok & 3) | ((tok >> 1) & 12)) & (CPR - 1); }
+template <int CPR>
+__device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >> 1) & 4))) & (CPR - 1); }
+
+template <int D, bool FP8>
+__global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const Plan plan) {
+  using C = MfmaCfg<D, FP8>;
+  constexpr int TT = C::kTT;
+  constexpr int KS = D / 32;   // k-steps of S^T
+  constexpr int DT = D / 16;   // d-tiles of O^T
+  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
+  int32_t* ids = reinterpret_cast<int32_t*>(lds + C::kOffIds);
+
+  const PartPlan& pp = plan.part[kPartMfma];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int w = blockIdx.x;
+  const WorkerRange wr =
+      worker_prepass<C::kThreads, C::kItemCap, C::kIdsPerTile, C::kTileCap>(a, plan, kPartMfma, w, items, ids);
+  const int R = wr.R;
+  const int nitems = wr.nitems;
+  const int first_ord = wr.first_ord;
+  if (R <= 0) return;
+
+  // ---- loads: tile r of the range into registers ------------------------------
+  typedef typename std::conditional<FP8, u32x2, u32x4>::type chunk_t;
+  const int64_t head_stride = (int64_t)D * C::kGElem;               // bytes between kv heads
+  const int64_t tok_stride = (int64_t)plan.Hkv * head_stride;       // bytes between tokens
+  auto tile_item = [&](int r) { return item_of_tile(items, nitems, r); };
+  auto issue = [&](chunk_t (&rk)[C::kLoads], chunk_t (&rv)[C::kLoads], int r) {
+    if (r >= R) return;
+    const int ii = uniform(tile_item(r));
+    const int32_t* d = items + ii * kItemInts;
+    const int j = uniform(d[IT_J]);
+    const int nv = uniform(d[IT_NVALID]);
+    const int tbase = (uniform(d[IT_TILE0]) + (r - uniform(d[IT_RTILE0]))) * TT;
+#pragma unroll
+    for (int it = 0; it < C::kLoads; ++it) {
+      const int c = it * C::kThreads + tid;
+      const int tok = c / C::kCPR;
+      const int part = c % C::kCPR;
+      int ti = tbase + tok;
+      if (ti >= nv) ti = nv - 1;
+      const int blk = ids[r * C::kIdsPerTile + tok / 16];
+      const int64_t off = ((int64_t)blk * 16 + (ti & 15)) * tok_stride + j * head_stride + part * C::kGChunk;
+      rk[it] = *reinterpret_cast<const chunk_t*>(a.k_pool + off);
+      rv[it] = *reinterpret_cast<const chunk_t*>(a.v_pool + off);
+    }
+  };
+  auto to_lds_chunk = [&](const chunk_t& v) -> u32x4 {
+    if constexpr (FP8) {
+      // exact E4M3 -> bf16: the hardware fp8 -> f32 conversion, then the upper half
+      u32x4 o;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t wv = v[h];
+        f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(wv, false);
+        f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(wv, true);
+        o[2 * h] = (__float_as_uint(lo[0]) >> 16) | (__float_as_uint(lo[1]) & 0xFFFF0000u);
+        o[2 * h + 1] = (__float_as_uint(hi[0]) >> 16) | (__float_as_uint(hi[1]) & 0xFFFF0000u);
+      }
+      return o;
+    } else {
+      return v;
+    }
+  };
+  auto store = [&](const chunk_t (&rk)[C::kLoads], const chunk_t (&rv)[C::kLoads], int stage_off) {
+#pragma unroll
+    for (int it = 0; it < C::kLoads; ++it) {
+      const int c = it * C::kThreads + tid;
+      const int tok = c / C::kCPR;
+      const int part = c % C::kCPR;
+      const int kpos = tok * C::kRowB + ((part ^ swz_k<C::kCPR>(tok)) << 4);
+      const int vpos = tok * C::kRowB + ((part ^ swz_v<C::kCPR>(tok)) << 4);
+      *reinterpret_cast<SG_LDS u32x4*>((SG_LDS uint8_t*)lds + stage_off + kpos) = to_lds_chunk(rk[it]);
+      *reinterpret_cast<SG_LDS u32x4*>((SG_LDS uint8_t*)lds + stage_off + C::kTileB + vpos) = to_lds_chunk(rv[it]);
+    }
+  };
+
+  // ---- per-wave compute state -----------------------------------------------------
+  const int G = lane >> 4;     // 16-lane group
+  const int ln = lane & 15;    // row within an N-tile / key within an S^T tile
+  bf16x8 qop[2][KS];
+  f32x4 acc[2][DT];
+  float m_run[2], l_run[2];
+  int rg = 0, tg = 0, ntg = 1, active = 0, nrows = 0;
+  float ks_scale = 1.f;        // E4M3: K block scale folded into the scores
+  (void)ks_scale;
+
+  auto begin_item = [&](const int32_t* d) {
+    nrows = uniform(d[IT_NROWS]);
+    if (nrows > 64) { ntg = 1; rg = wave; tg = 0; }
+    else { ntg = 2; rg = wave & 1; tg = wave >> 1; }
+    active = rg * 32 < nrows;
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int rr = rg * 32 + nt * 16 + ln;
+      int fork = 0, h = 0;
+      item_row(plan, d, rr, &fork, &h);
+      const bool ok = active && rr < nrows;
+      const uint16_t* qrow = a.q + ((int64_t)fork * plan.Hq + h) * D;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (ok) v = *reinterpret_cast<const u32x4*>(qrow + ks * 32 + G * 8);
+        qop[nt][ks] = __builtin_bit_cast(bf16x8, v);
+      }
+      m_run[nt] = -INFINITY;
+      l_run[nt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+
+  auto compute_tile = [&](int stage_off, const int32_t* d, int r) {
+    if (!active) return;
+    const int tile_in_item = uniform(d[IT_TILE0]) + (r - uniform(d[IT_RTILE0]));
+    const int nv = uniform(d[IT_NVALID]);
+    const int valid = (nv - tile_in_item * TT) < TT ? (nv - tile_in_item * TT) : TT;
+    const int ntok = TT / ntg;
+    const int tok0 = tg * ntok;
+    const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage_off;
+    const SG_LDS uint8_t* vb = kb + C::kTileB;
+    for (int sb = tok0; sb < tok0 + ntok; sb += 32) {
+      if (sb >= valid) break;
+      f32x4 s[2][2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int ta = sb + 8 * (ln >> 2) + (ln & 3);   // key of S^T tile a held by this lane as A row
+      const int tb = ta + 4;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int ch = 4 * ks + G;
+        const u32x4 ka = *reinterpret_cast<const SG_LDS u32x4*>(kb + ta * C::kRowB + ((ch ^ swz_k<C::kCPR>(ta)) << 4));
+        const u32x4 kbv = *reinterpret_cast<const SG_LDS u32x4*>(kb + tb * C::kRowB + ((ch ^ swz_k<C::kCPR>(tb)) << 4));
+        const bf16x8 A0 = __builtin_bit_cast(bf16x8, ka);
+        const bf16x8 A1 = __builtin_bit_cast(bf16x8, kbv);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, qop[nt][ks], s[0][nt], 0, 0, 0);
+          s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, qop[nt][ks], s[1][nt], 0, 0, 0);
+        }
+      }
+      // lane (G, ln) now holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
+      if constexpr (FP8) {
+        const int kb0 = ids[r * C::kIdsPerTile + (sb + 8 * G) / 16];
+        const float ksc = a.k_scale[kb0];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt) s[u][nt] *= ksc;
+      }
+      if (sb + 32 > valid) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (sb + 8 * G + 4 * u + e >= valid) {
+              s[u][0][e] = -INFINITY;
+              s[u][1][e] = -INFINITY;
+            }
+      }
+      bf16x8 pop[2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                         fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+        mx = wave_max_xor(mx, 16);
+        mx = wave_max_xor(mx, 32);
+        const float m_new = fmaxf(m_run[nt], mx);
+        const float mc = (m_new == -INFINITY) ? 0.f : m_new * a.c_log2;
+        const float alpha = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
+        m_run[nt] = m_new;
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(fmaf(s[0][nt][e], a.c_log2, -mc));
+          p[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][nt][e], a.c_log2, -mc));
+        }
+        float ps = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+        l_run[nt] = l_run[nt] * alpha + ps;
+        if (alpha != 1.f) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
+        }
+        if constexpr (FP8) {
+          const int vb0 = ids[r * C::kIdsPerTile + (sb + 8 * G) / 16];
+          const float vsc = a.v_scale[vb0];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) p[e] *= vsc;
+        }
+        u32x4 pk;
+        pk[0] = pack_bf16x2(p[0], p[1]);
+        pk[1] = pack_bf16x2(p[2], p[3]);
+        pk[2] = pack_bf16x2(p[4], p[5]);
+        pk[3] = pack_bf16x2(p[6], p[7]);
+        pop[nt] = __builtin_bit_cast(bf16x8, pk);
+      }
+      // O^T += V^T P^T ; the transposing read gives lane (G, ln) V[sb+8G+4h+e][16dt+ln]
+      const int vt = sb + 8 * G + (ln >> 2);
+      const int vsub = ln & 3;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int ch = 2 * dt + (vsub >> 1);
+        const int off0 = vt * C::kRowB + ((ch ^ swz_v<C::kCPR>(vt)) << 4) + ((vsub & 1) << 3);
+        const int off1 = (vt + 4) * C::kRowB + ((ch ^ swz_v<C::kCPR>(vt + 4)) << 4) + ((vsub & 1) << 3);
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(vb + off0));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(vb + off1));
+        const bf16x8 A = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
+      }
+    }
+  };
+
+  float* comb = reinterpret_cast<float*>(lds + C::kOffComb);
+  float* comb_m = reinterpret_cast<float*>(lds + C::kOffCombML);
+  float* comb_l = comb_m + 2 * 32;
+  auto finish_item = [&](const int32_t* d) {
+    float lrow[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      float v = l_run[nt] + __shfl_xor(l_run[nt], 16, 64);
+      lrow[nt] = v + __shfl_xor(v, 32, 64);
+    }
+    if (ntg == 2) {
+      if (tg == 1 && active) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int row = nt * 16 + ln;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            *reinterpret_cast<f32x4*>(comb + (rg * 32 + row) * D + dt * 16 + 4 * G) = acc[nt][dt];
+          if (G == 0) {
+            comb_m[rg * 32 + row] = m_run[nt];
+            comb_l[rg * 32 + row] = lrow[nt];
+          }
+        }
+      }
+      __syncthreads();
+      if (tg == 0 && active) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int row = nt * 16 + ln;
+          const float m1 = comb_m[rg * 32 + row];
+          const float l1 = comb_l[rg * 32 + row];
+          const float m = fmaxf(m_run[nt], m1);
+          const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
+          const float a0 = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
+          const float a1 = __builtin_amdgcn_exp2f(m1 * a.c_log2 - mc);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const f32x4 o1 = *reinterpret_cast<const f32x4*>(comb + (rg * 32 + row) * D + dt * 16 + 4 * G);
+            acc[nt][dt] = acc[nt][dt] * a0 + o1 * a1;
+          }
+          lrow[nt] = lrow[nt] * a0 + l1 * a1;
+          m_run[nt] = m;
+        }
+      }
+      __syncthreads();
+    }
+    if (tg == 0 && active) {
+      const int k = uniform(d[IT_ORD]) - first_ord;
+      const int64_t slot = slot_of(pp, w, k);
+      if (slot >= 0) {
+        float* o = a.ws + pp.o_base + slot * pp.slot_rows * D;
+        float* ls = a.ws + pp.lse_base + slot * pp.slot_rows;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int rr = rg * 32 + nt * 16 + ln;
+          if (rr < nrows) {
+            const float inv = 1.f / lrow[nt];
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+              *reinterpret_cast<f32x4*>(o + rr * D + dt * 16 + 4 * G) = acc[nt][dt] * inv;
+            if (G == 0) ls[rr] = m_run[nt] * a.sm_scale + __logf(lrow[nt]);
+          }
+        }
+      }
+    }
+  };
+
+  // ---- pipeline: tiles r, r+1 in LDS stages 0/1; two tiles in flight in registers
+  chunk_t kA[C::kLoads], vA[C::kLoads], kB[C::kLoads], vB[C::kLoads];
+  issue(kA, vA, 0);
+  issue(kB, vB, 1);
+  store(kA, vA, C::kOffStage0);
+  issue(kA, vA, 2);
+  __syncthreads();
+
+  int cur = -1;   // item index being accumulated
+  auto step = [&](int r, int stage_off) {
+    const int ii = uniform(tile_item(r));
+    const int32_t* d = items + ii * kItemInts;
+    if (ii != cur) {
+      begin_item(d);
+      cur = ii;
+    }
+    compute_tile(stage_off, d, r);
+    if (r - uniform(d[IT_RTILE0]) == uniform(d[IT_NTILE]) - 1) finish_item(d);
+  };
+  for (int r = 0; r < R; r += 2) {
+    step(r, C::kOffStage0);
+    if (r + 1 < R) store(kB, vB, C::kOffStage1);
+    issue(kB, vB, r + 3);
+    __syncthreads();
+    if (r + 1 >= R) break;
+    step(r + 1, C::kOffStage1);
+    if (r + 2 < R) store(kA, vA, C::kOffStage0);
+    issue(kA, vA, r + 4);
+    __syncthreads();
+  }
+}
+
+template <int D, bool FP8>
+hipError_t launch_attn_mfma_t(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
+  const int W = plan.part[kPartMfma].workers;
+  if (W <= 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_mfma_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, plan);
+  return hipGetLastError();
+}
+
+int mfma_tile_tokens(int D, bool fp8) {
+  (void)fp8;
+  return D == 128 ? MfmaCfg<128, false>::kTT : MfmaCfg<64, false>::kTT;
+}
+int mfma_item_cap() { return MfmaCfg<128, false>::kItemCap; }
+int mfma_tile_cap(int D) { return D == 128 ? MfmaCfg<128, false>::kTileCap : MfmaCfg<64, false>::kTileCap; }
+
+hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream) {
+  if (plan.D == 128) return fp8 ? launch_attn_mfma_t<128, true>(a, plan, stream) : launch_attn_mfma_t<128, false>(a, plan, stream);
+  return fp8 ? launch_attn_mfma_t<64, true>(a, plan, stream) : launch_attn_mfma_t<64, false>(a, plan, stream);
+}
+
+}  // namespace specgen

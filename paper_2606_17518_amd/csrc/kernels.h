@@ -1,0 +1,42 @@
+// kernels.h -- host-side launchers of the device kernels (one per .hip file).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+#include "plan.h"
+
+namespace specgen {
+
+// attn_mfma.hip
+hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
+int mfma_tile_tokens(int D, bool fp8);
+int mfma_item_cap();
+int mfma_tile_cap(int D);
+// attn_dot.hip
+hipError_t launch_attn_dot_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
+int dot_tile_tokens(int D);
+int dot_rows();
+int dot_item_cap();
+int dot_tile_cap(int D);
+// merge.hip
+hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream);
+hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S, int64_t R, int D, void* out,
+                            bool out_bf16, float* out_lse, hipStream_t stream);
+// kv_import.hip
+struct ImportTensor {
+  uint8_t* dst;
+  const uint8_t* src;
+  int64_t block_bytes;
+};
+struct ImportArgs {
+  ImportTensor t[4];
+  int32_t num_tensors;
+  const int32_t* dst_ids;
+  int64_t n;
+  int64_t num_dst_blocks;
+  int32_t* bad_id_count;
+};
+hipError_t launch_kv_import(const ImportArgs& a, hipStream_t stream);
+
+}  // namespace specgen

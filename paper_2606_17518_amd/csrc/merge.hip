@@ -1,0 +1,132 @@
+// merge.hip -- log-sum-exp merge of partial attention results.
+//
+// Partials over disjoint key sets combine exactly: with M = max_s lse_s and
+// w_s = exp(lse_s - M), out = sum_s w_s o_s / sum_s w_s and
+// lse = M + ln sum_s w_s (a part with lse = -inf is empty and is skipped).
+// One wavefront merges one output row: lane p first takes part p's lse to
+// find the running max and weights (chunks of 64 parts, rescaled between
+// chunks), then all lanes sweep the parts over the head dimension.
+#include "common.h"
+#include "plan.h"
+
+namespace specgen {
+
+// Merge `nparts` parts of one row.  part_o(p) -> const float* (row vector of
+// D floats), part_lse(p) -> float.  Writes out (bf16 or fp32) and lse.
+template <int VEC, typename PO, typename PL>
+__device__ __forceinline__ void merge_row(int nparts, int D, PO part_o, PL part_lse, void* out_row,
+                                          bool out_bf16, float* out_lse_p) {
+  const int lane = threadIdx.x & 63;
+  float M = -INFINITY, z = 0.f;
+  float acc[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+  for (int p0 = 0; p0 < nparts; p0 += 64) {
+    const int p = p0 + lane;
+    const float l = p < nparts ? part_lse(p) : -INFINITY;
+    float cm = l;
+    for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
+    const float Mn = fmaxf(M, cm);
+    if (Mn == -INFINITY) continue;   // every part so far empty
+    const float rescale = __expf(M - Mn);   // M = -inf -> 0
+    z *= rescale;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] *= rescale;
+    M = Mn;
+    const float wl = (l == -INFINITY) ? 0.f : __expf(l - M);
+    float zs = wl;
+    for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
+    z += zs;
+    const int cnt = (nparts - p0) < 64 ? (nparts - p0) : 64;
+    for (int q = 0; q < cnt; ++q) {
+      const float wq = __shfl(wl, q, 64);
+      if (wq == 0.f) continue;   // wave-uniform
+      const float* o = part_o(p0 + q);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) {
+        const int d = lane + 64 * v;
+        if (d < D) acc[v] = fmaf(wq, o[d], acc[v]);
+      }
+    }
+  }
+  const bool empty = (M == -INFINITY);
+  const float inv = empty ? 0.f : 1.f / z;
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) {
+    const int d = lane + 64 * v;
+    if (d < D) {
+      const float r = empty ? 0.f : acc[v] * inv;
+      if (out_bf16) reinterpret_cast<uint16_t*>(out_row)[d] = f32_to_bf16(r);
+      else reinterpret_cast<float*>(out_row)[d] = r;
+    }
+  }
+  if (out_lse_p && lane == 0) *out_lse_p = empty ? -INFINITY : M + __logf(z);
+}
+
+// ---- standalone merge: o_parts [S][R][D], lse_parts [S][R] -------------------
+template <int VEC>
+__global__ void __launch_bounds__(256) lse_merge_kernel(const float* __restrict__ o_parts,
+                                                        const float* __restrict__ lse_parts, int S,
+                                                        int64_t R, int D, void* __restrict__ out,
+                                                        int out_bf16, float* __restrict__ out_lse) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= R) return;
+  auto po = [&](int p) { return o_parts + ((int64_t)p * R + r) * D; };
+  auto pl = [&](int p) { return lse_parts[(int64_t)p * R + r]; };
+  void* orow = out_bf16 ? (void*)(reinterpret_cast<uint16_t*>(out) + r * D)
+                        : (void*)(reinterpret_cast<float*>(out) + r * D);
+  merge_row<VEC>(S, D, po, pl, orow, out_bf16 != 0, out_lse ? out_lse + r : nullptr);
+}
+
+hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S, int64_t R, int D,
+                            void* out, bool out_bf16, float* out_lse, hipStream_t stream) {
+  if (R == 0) return hipSuccess;
+  const dim3 grid((unsigned)((R + 3) / 4)), block(256);
+  const int vec = (D + 63) / 64;
+  switch (vec) {
+#define SG_CASE(V) case V: hipLaunchKernelGGL(lse_merge_kernel<V>, grid, block, 0, stream, o_parts, lse_parts, S, R, D, out, (int)out_bf16, out_lse); break;
+    SG_CASE(1) SG_CASE(2) SG_CASE(3) SG_CASE(4) SG_CASE(5) SG_CASE(6) SG_CASE(7) SG_CASE(8)
+    SG_CASE(9) SG_CASE(10) SG_CASE(11) SG_CASE(12) SG_CASE(13) SG_CASE(14) SG_CASE(15) SG_CASE(16)
+#undef SG_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ---- fork merge: the parts of row (f, h) are the partials of the workers that
+// covered its prefix item and its suffix item ---------------------------------
+
+template <int D>
+__global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan, const float* __restrict__ ws,
+                                                         uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= (int64_t)plan.N * plan.Hq) return;
+  const int f = (int)(row / plan.Hq);
+  const int h = (int)(row % plan.Hq);
+  const ItemParts P = prefix_parts_of_row(plan, f, h);
+  const int np = P.w_hi - P.w_lo + 1;
+  ItemParts S;
+  const int ns = suffix_parts_of_row(plan, f, h, &S) ? S.w_hi - S.w_lo + 1 : 0;
+  auto slot_ptr = [&](const ItemParts& ip, int i, bool lse) -> int64_t {
+    const PartPlan& q = plan.part[ip.part];
+    const int w = ip.w_lo + i;
+    const int k = (i == 0) ? ip.k_lo : 0;
+    const int64_t slot = (int64_t)w * q.kmax + k;
+    return lse ? q.lse_base + slot * q.slot_rows + ip.row : q.o_base + (slot * q.slot_rows + ip.row) * D;
+  };
+  auto po = [&](int p) { return p < np ? ws + slot_ptr(P, p, false) : ws + slot_ptr(S, p - np, false); };
+  auto pl = [&](int p) { return p < np ? ws[slot_ptr(P, p, true)] : ws[slot_ptr(S, p - np, true)]; };
+  merge_row<D / 64>(np + ns, D, po, pl, out + row * D, true, out_lse ? out_lse + row : nullptr);
+}
+
+hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
+  const int64_t rows = (int64_t)plan.N * plan.Hq;
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (plan.D == 128)
+    hipLaunchKernelGGL(fork_merge_kernel<128>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  else
+    hipLaunchKernelGGL(fork_merge_kernel<64>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  return hipGetLastError();
+}
+
+}  // namespace specgen

@@ -1,0 +1,231 @@
+// plan.h -- the work split of fork-decode attention, shared by the host
+// planner and the kernels (all functions are __host__ __device__).
+//
+// Work items.  A prefix item is (trace t, kv head j, row block rb): the rows
+// are every (fork of t, q head of j's group) pair, F_t * g of them, cut into
+// blocks of `rbs` rows; it streams the trace's P_t prefix tokens of head j
+// once for all those rows, which is the point of forking off a shared prefix
+// (the forks reuse the reasoning prefix's KV, Sec. 4.2 and Sec. 8.7).  A
+// suffix item is (fork f, kv head j, row block rb) over the fork's own S_f
+// tokens with the g query heads of the group as rows.
+//
+// Partitions.  Each item is served by one of two kernels (0 = MFMA, 1 = dot),
+// chosen by the path policy.  Within a partition the items are laid out in a
+// fixed order -- prefix items (trace-major, then j, then rb), then suffix
+// items (fork-major, then j, then rb) -- and each item is cut into tiles of
+// `tt` tokens.  The partition's tile sequence is split evenly over W workers
+// (workgroups): worker w takes tiles [start(w), start(w+1)).  A worker emits
+// one partial (o, lse) per item it touches, into slot w * kmax + k where k is
+// the item's ordinal minus the ordinal of the worker's first item.  The merge
+// finds the workers covering an item from its tile range alone.
+#pragma once
+#include <stdint.h>
+
+#ifdef __HIPCC__
+#define SG_HD __host__ __device__ __forceinline__
+#else
+#define SG_HD inline
+#endif
+
+namespace specgen {
+
+constexpr int kMaxTraces = 32;   // traces per call
+constexpr int kMaxForks = 512;   // forks per call
+constexpr int kBlock = 16;       // tokens per KV block
+
+enum { kPartMfma = 0, kPartDot = 1 };
+enum { kPolicyAuto = 0, kPolicyDot = 1, kPolicyMfma = 2 };
+
+struct PartPlan {
+  int64_t tiles;          // total tiles of the partition
+  int64_t prefix_tiles;   // tiles of its prefix items (they come first)
+  int64_t o_base;         // float offset of slot 0's o in the workspace
+  int64_t lse_base;       // float offset of slot 0's lse
+  int32_t workers;        // W (0: partition unused)
+  int32_t kmax;           // max items touched by one worker
+  int32_t tt;             // tokens per tile
+  int32_t rbs;            // rows per row block
+  int32_t slot_rows;      // rows reserved per partial slot (== rbs)
+  int32_t n_prefix_items; // prefix items in the partition
+  int32_t has_suffix;     // suffix items belong to this partition
+  int32_t suffix_rb;      // row blocks per suffix (fork, head): ceil(g / rbs)
+  int32_t n_traces;       // traces whose prefix items are in the partition
+  int32_t trace_begin;    // their positions in Plan::ptrace: [trace_begin, +n_traces)
+};
+
+struct Plan {
+  int32_t T, N, Hq, Hkv, g, D;
+  int32_t policy, pad_;
+  PartPlan part[2];
+  int32_t fork_off[kMaxTraces + 1];
+  int32_t prefix_len[kMaxTraces];
+  int32_t trace_part[kMaxTraces];   // partition of trace t's prefix items
+  int32_t trace_pos[kMaxTraces];    // index of t in ptrace
+  int32_t ptrace[kMaxTraces];       // traces grouped by partition, ascending within each
+  int32_t tileP[kMaxTraces];        // (by ptrace position) first tile of the trace's prefix items
+  int32_t ordP[kMaxTraces];         // (by ptrace position) ordinal of its first prefix item
+  int32_t tileS[kMaxForks + 1];     // first tile of fork f's suffix items, relative to prefix_tiles
+};
+
+SG_HD int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+
+SG_HD int32_t trace_rows(const Plan& p, int t) { return (p.fork_off[t + 1] - p.fork_off[t]) * p.g; }
+
+SG_HD int part_of_trace(int policy, int rows) {
+  if (policy == kPolicyDot) return kPartDot;
+  if (policy == kPolicyMfma) return kPartMfma;
+  return rows >= 16 ? kPartMfma : kPartDot;
+}
+
+SG_HD int part_of_suffix(int policy) { return policy == kPolicyDot ? kPartDot : kPartMfma; }
+
+SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) { return (w * pp.tiles) / pp.workers; }
+
+// Worker owning tile x: the largest w with worker_start(w) <= x.
+SG_HD int32_t worker_of_tile(const PartPlan& pp, int64_t x) {
+  return (int32_t)(((x + 1) * (int64_t)pp.workers - 1) / pp.tiles);
+}
+
+struct ItemRef {
+  int32_t kind;      // 0 prefix, 1 suffix, -1 past the end
+  int32_t t, f, j, rb;
+  int32_t tiles;     // tiles of the item
+  int32_t tile;      // tile of x within the item
+  int64_t first;     // partition tile index of the item's first tile
+  int32_t ord;       // ordinal of the item in the partition
+};
+
+// The item containing partition tile x.  Suffix items need ceil(S_f/tt),
+// which equals (tileS[f+1]-tileS[f]) / (Hkv * suffix_rb).
+SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
+  const PartPlan& pp = p.part[part];
+  ItemRef r;
+  r.kind = -1;
+  r.t = r.f = r.j = r.rb = r.tiles = r.tile = r.ord = 0;
+  r.first = 0;
+  if (x < 0 || x >= pp.tiles) return r;
+  if (x < pp.prefix_tiles) {
+    // largest position i in the partition's trace list with tileP[i] <= x
+    int lo = pp.trace_begin, hi = pp.trace_begin + pp.n_traces - 1;
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (p.tileP[mid] <= x) lo = mid; else hi = mid - 1;
+    }
+    const int t = p.ptrace[lo];
+    const int rb_count = cdiv(trace_rows(p, t), pp.rbs);
+    const int tiles = cdiv(p.prefix_len[t], pp.tt);
+    const int64_t local = x - p.tileP[lo];
+    const int item = (int)(local / tiles);
+    r.kind = 0;
+    r.t = t;
+    r.j = item / rb_count;
+    r.rb = item % rb_count;
+    r.tiles = tiles;
+    r.tile = (int)(local % tiles);
+    r.first = x - r.tile;
+    r.ord = p.ordP[lo] + item;
+    return r;
+  }
+  const int64_t xs = x - pp.prefix_tiles;
+  int lo = 0, hi = p.N - 1;   // largest f with tileS[f] <= xs
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (p.tileS[mid] <= xs) lo = mid; else hi = mid - 1;
+  }
+  const int f = lo;
+  const int per_fork = p.Hkv * pp.suffix_rb;
+  const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
+  const int64_t local = xs - p.tileS[f];
+  const int item = (int)(local / tiles);
+  r.kind = 1;
+  r.f = f;
+  r.j = item / pp.suffix_rb;
+  r.rb = item % pp.suffix_rb;
+  r.tiles = tiles;
+  r.tile = (int)(local % tiles);
+  r.first = x - r.tile;
+  r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
+  return r;
+}
+
+// Trace of fork f (fork_off is nondecreasing; empty traces are rejected).
+SG_HD int trace_of_fork(const Plan& p, int f) {
+  int lo = 0, hi = p.T - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (p.fork_off[mid] <= f) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// (fork, q head) of row rr of an item whose first row is row0.
+SG_HD void item_row_fork_head(const Plan& p, int kind, int t, int f, int j, int row0, int rr, int* fork, int* head) {
+  if (kind == 0) {
+    const int ri = row0 + rr;
+    *fork = p.fork_off[t] + ri / p.g;
+    *head = j * p.g + ri % p.g;
+  } else {
+    *fork = f;
+    *head = j * p.g + row0 + rr;
+  }
+}
+
+// The partial results of one item: workers w_lo..w_hi of partition `part`
+// covered its tiles; in w_lo it is segment k_lo, in every later one segment 0
+// (their ranges start inside the item).
+struct ItemParts {
+  int part;
+  int w_lo, w_hi;
+  int k_lo;
+  int row;         // row inside the item
+};
+
+SG_HD ItemParts item_parts(const Plan& p, int part, int64_t first_tile, int tiles, int ord, int row) {
+  const PartPlan& pp = p.part[part];
+  ItemParts ip;
+  ip.part = part;
+  ip.row = row;
+  ip.w_lo = worker_of_tile(pp, first_tile);
+  ip.w_hi = worker_of_tile(pp, first_tile + tiles - 1);
+  const ItemRef f0 = locate(p, part, worker_start(pp, ip.w_lo));
+  ip.k_lo = ord - f0.ord;
+  return ip;
+}
+
+// The prefix item of row (f, h) and its row inside the item.
+SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h) {
+  const int g = p.g, j = h / g, hh = h - j * g;
+  const int t = trace_of_fork(p, f);
+  const int ri = (f - p.fork_off[t]) * g + hh;
+  const int X = p.trace_part[t];
+  const PartPlan& pp = p.part[X];
+  const int rbc = cdiv(trace_rows(p, t), pp.rbs);
+  const int rb = ri / pp.rbs;
+  const int tiles = cdiv(p.prefix_len[t], pp.tt);
+  const int pos = p.trace_pos[t];
+  const int item = j * rbc + rb;
+  return item_parts(p, X, (int64_t)p.tileP[pos] + (int64_t)item * tiles, tiles, p.ordP[pos] + item, ri - rb * pp.rbs);
+}
+
+// The suffix item of row (f, h); returns false if the fork has no suffix tokens.
+SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
+  const int g = p.g, j = h / g, hh = h - j * g;
+  const int X = part_of_suffix(p.policy);
+  const PartPlan& pp = p.part[X];
+  const int per_fork = p.Hkv * pp.suffix_rb;
+  const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
+  if (tiles <= 0) return false;
+  const int rb = hh / pp.rbs;
+  const int item = j * pp.suffix_rb + rb;
+  *out = item_parts(p, X, pp.prefix_tiles + p.tileS[f] + (int64_t)item * tiles, tiles,
+                    pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
+  return true;
+}
+
+// Partial-slot index of (worker w, item of ordinal ord), or -1 if out of range.
+SG_HD int64_t slot_of(const PartPlan& pp, int32_t w, int32_t k) {
+  if (k < 0 || k >= pp.kmax || w < 0 || w >= pp.workers) return -1;
+  return (int64_t)w * pp.kmax + k;
+}
+
+}  // namespace specgen

@@ -1,0 +1,153 @@
+// planner.h -- host-only construction of the work split (plan.h) from the
+// host mirrors of the lengths.  Plain C++ with no HIP dependency, so it is
+// also compiled by a g++ test harness that replays every worker walk and
+// every merge lookup on the CPU.
+#pragma once
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "plan.h"
+
+namespace specgen {
+
+enum { kPlanOk = 0, kPlanInvalid = 1, kPlanUnsupported = 2 };
+
+struct PlanInputs {
+  int T, N, Hq, Hkv, D, policy;
+  const int32_t* fork_off;    // [T+1]
+  const int32_t* prefix_len;  // [T]
+  const int32_t* suffix_len;  // [N]
+  int tt[2];                  // tokens per tile, per partition
+  int rbs[2];                 // rows per row block
+  int item_cap[2];            // max items per worker
+  int tile_cap[2];            // max tiles per worker
+};
+
+constexpr int64_t kAlignFloats = 64;   // 256-byte alignment of workspace regions
+
+inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+// Validates shapes and lengths, fills `plan` and the workspace size in floats.
+// `cus` returns the number of compute units (workers per partition start at it).
+template <typename CusFn>
+int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_floats, char* err, size_t errlen) {
+#define SG_FAIL(code, ...)                 \
+  do {                                     \
+    snprintf(err, errlen, __VA_ARGS__);    \
+    return code;                           \
+  } while (0)
+  const int T = in.T, N = in.N, Hq = in.Hq, Hkv = in.Hkv, D = in.D;
+  if (T < 1) SG_FAIL(kPlanInvalid, "num_traces must be >= 1 (got %d)", T);
+  if (N < 1) SG_FAIL(kPlanInvalid, "num_forks must be >= 1 (got %d)", N);
+  if (T > kMaxTraces) SG_FAIL(kPlanUnsupported, "num_traces %d exceeds %d per call", T, kMaxTraces);
+  if (N > kMaxForks) SG_FAIL(kPlanUnsupported, "num_forks %d exceeds %d per call", N, kMaxForks);
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0)
+    SG_FAIL(kPlanInvalid, "num_q_heads %d must be a positive multiple of num_kv_heads %d", Hq, Hkv);
+  if (Hq / Hkv > 128) SG_FAIL(kPlanUnsupported, "GQA group size %d exceeds 128", Hq / Hkv);
+  if (D != 64 && D != 128) SG_FAIL(kPlanUnsupported, "head_dim %d not in {64, 128}", D);
+  const int32_t* fo = in.fork_off;
+  if (fo[0] != 0 || fo[T] != N) SG_FAIL(kPlanInvalid, "fork_off must start at 0 and end at num_forks");
+  for (int t = 0; t < T; ++t) {
+    if (fo[t + 1] <= fo[t]) SG_FAIL(kPlanInvalid, "trace %d has no forks", t);
+    if (in.prefix_len[t] < 1) SG_FAIL(kPlanInvalid, "prefix_len[%d] must be >= 1", t);
+  }
+  for (int f = 0; f < N; ++f)
+    if (in.suffix_len[f] < 0) SG_FAIL(kPlanInvalid, "suffix_len[%d] must be >= 0", f);
+
+  const int g = Hq / Hkv;
+  memset(plan, 0, sizeof(Plan));
+  plan->T = T;
+  plan->N = N;
+  plan->Hq = Hq;
+  plan->Hkv = Hkv;
+  plan->g = g;
+  plan->D = D;
+  plan->policy = in.policy;
+  for (int t = 0; t <= T; ++t) plan->fork_off[t] = fo[t];
+  for (int t = 0; t < T; ++t) plan->prefix_len[t] = in.prefix_len[t];
+  const int xs = part_of_suffix(in.policy);
+
+  // prefix items, traces grouped by partition
+  int pos = 0;
+  for (int X = 0; X < 2; ++X) {
+    PartPlan& pp = plan->part[X];
+    pp.tt = in.tt[X];
+    pp.rbs = in.rbs[X];
+    pp.slot_rows = in.rbs[X];
+    pp.trace_begin = pos;
+    int64_t tiles = 0, items = 0;
+    for (int t = 0; t < T; ++t) {
+      const int rows = (fo[t + 1] - fo[t]) * g;
+      if (part_of_trace(in.policy, rows) != X) continue;
+      plan->trace_part[t] = X;
+      plan->trace_pos[t] = pos;
+      plan->ptrace[pos] = t;
+      plan->tileP[pos] = (int32_t)tiles;
+      plan->ordP[pos] = (int32_t)items;
+      const int rb = cdiv(rows, pp.rbs);
+      tiles += (int64_t)Hkv * rb * cdiv(in.prefix_len[t], pp.tt);
+      items += (int64_t)Hkv * rb;
+      if (tiles > INT32_MAX || items > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
+      ++pos;
+    }
+    pp.n_traces = pos - pp.trace_begin;
+    pp.prefix_tiles = tiles;
+    pp.n_prefix_items = (int32_t)items;
+    pp.tiles = tiles;
+    pp.has_suffix = (X == xs);
+    pp.suffix_rb = cdiv(g, pp.rbs);
+  }
+  // suffix items, all in one partition
+  {
+    PartPlan& pp = plan->part[xs];
+    int64_t acc = 0;
+    for (int f = 0; f < N; ++f) {
+      plan->tileS[f] = (int32_t)acc;
+      acc += (int64_t)Hkv * pp.suffix_rb * cdiv(in.suffix_len[f], pp.tt);
+      if (acc > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
+    }
+    plan->tileS[N] = (int32_t)acc;
+    pp.tiles += acc;
+    if ((int64_t)pp.n_prefix_items + (int64_t)N * Hkv * pp.suffix_rb > INT32_MAX)
+      SG_FAIL(kPlanUnsupported, "batch too large");
+  }
+  // workers: one per compute unit, more while a worker's range would exceed
+  // the kernel's per-worker capacity (items it can describe, tiles it can hold)
+  int64_t off = 0;
+  for (int X = 0; X < 2; ++X) {
+    PartPlan& pp = plan->part[X];
+    pp.workers = 0;
+    pp.kmax = 0;
+    if (pp.tiles == 0) continue;
+    int64_t W = std::min<int64_t>(pp.tiles, (int64_t)cus_fn());
+    for (;;) {
+      pp.workers = (int32_t)W;
+      const int64_t per = (pp.tiles + W - 1) / W;
+      int kmax = 0;
+      for (int64_t w = 0; w < W; ++w) {
+        const int64_t a = worker_start(pp, w), e = worker_start(pp, w + 1);
+        if (e <= a) continue;
+        const int k = locate(*plan, X, e - 1).ord - locate(*plan, X, a).ord + 1;
+        if (k > kmax) kmax = k;
+      }
+      pp.kmax = kmax;
+      if ((per <= in.tile_cap[X] && kmax <= in.item_cap[X]) || W == pp.tiles) break;
+      W = std::min<int64_t>(pp.tiles, W * 2);
+    }
+    if (pp.kmax > in.item_cap[X] || (pp.tiles + pp.workers - 1) / pp.workers > in.tile_cap[X])
+      SG_FAIL(kPlanUnsupported, "work split exceeds the kernel's per-worker capacity");
+    const int64_t slots = (int64_t)pp.workers * pp.kmax;
+    pp.o_base = off;
+    off = align_up(off + slots * pp.slot_rows * D, kAlignFloats);
+    pp.lse_base = off;
+    off = align_up(off + slots * pp.slot_rows, kAlignFloats);
+  }
+  *ws_floats = off;
+  return kPlanOk;
+#undef SG_FAIL
+}
+
+}  // namespace specgen

@@ -1,0 +1,114 @@
+// worker.h -- the part of a worker (workgroup) that both attention kernels
+// share: list the items its tile range touches, fetch their lengths and table
+// offsets, and gather the block id of every 16-token block the range reads.
+// Everything lands in LDS so the tile loop never waits on a dependent load.
+#pragma once
+#include "common.h"
+#include "plan.h"
+
+namespace specgen {
+
+// item descriptor fields (ints in LDS)
+enum {
+  IT_KIND, IT_T, IT_F, IT_J, IT_RB, IT_ORD, IT_TILE0, IT_NTILE, IT_NVALID, IT_TABOFF,
+  IT_NROWS, IT_ROW0, IT_RTILE0, IT_TILES, IT_LASTBLK, IT_COUNT
+};
+constexpr int kItemInts = 16;
+static_assert(IT_COUNT <= kItemInts, "item descriptor size");
+
+struct WorkerRange {
+  int nitems;     // items touched (non-empty)
+  int first_ord;  // ordinal of the first one
+  int R;          // tiles in the range
+};
+
+// All threads of the block call this; `items` holds item_cap descriptors and
+// `ids` holds tile_cap * ids_per_tile block ids.
+template <int kThreads, int kItemCap, int kIdsPerTile, int kTileCap>
+__device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
+                                      int32_t* ids) {
+  const PartPlan& pp = plan.part[part];
+  const int tid = threadIdx.x;
+  const int64_t x0 = worker_start(pp, w);
+  const int64_t x1 = worker_start(pp, w + 1);
+  WorkerRange wr;
+  wr.nitems = 0;
+  wr.first_ord = 0;
+  wr.R = 0;
+  if (x1 <= x0) return wr;
+  // 1. walk the range item by item (identical in every thread)
+  int64_t x = x0;
+  int rt = 0;
+  while (x < x1 && wr.nitems < kItemCap) {
+    const ItemRef it = locate(plan, part, x);
+    const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
+    if (wr.nitems == 0) wr.first_ord = it.ord;
+    if (tid == 0) {
+      int32_t* d = items + wr.nitems * kItemInts;
+      d[IT_KIND] = it.kind;
+      d[IT_T] = it.t;
+      d[IT_F] = it.f;
+      d[IT_J] = it.j;
+      d[IT_RB] = it.rb;
+      d[IT_ORD] = it.ord;
+      d[IT_TILE0] = it.tile;
+      d[IT_NTILE] = n;
+      d[IT_RTILE0] = rt;
+      d[IT_TILES] = it.tiles;
+      const int r0 = it.rb * pp.rbs;
+      const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
+      d[IT_NROWS] = (rows - r0) < pp.rbs ? (rows - r0) : pp.rbs;
+      d[IT_ROW0] = r0;
+    }
+    x += n;
+    rt += n;
+    ++wr.nitems;
+  }
+  // the host sizes workers so the caps hold; never index past them
+  wr.R = rt < kTileCap ? rt : kTileCap;
+  __syncthreads();
+  // 2. lengths and table offsets
+  if (tid < wr.nitems) {
+    int32_t* d = items + tid * kItemInts;
+    int nv, off;
+    if (d[IT_KIND] == 0) {
+      nv = plan.prefix_len[d[IT_T]];
+      off = a.prefix_table_off[d[IT_T]];
+    } else {
+      nv = a.suffix_len[d[IT_F]];
+      off = a.suffix_table_off[d[IT_F]];
+    }
+    d[IT_NVALID] = nv;
+    d[IT_TABOFF] = off;
+    d[IT_LASTBLK] = (nv - 1) / 16;
+  }
+  __syncthreads();
+  // 3. block ids of every tile of the range, clamped to the item's last valid block
+  for (int e = tid; e < wr.R * kIdsPerTile; e += kThreads) {
+    const int r = e / kIdsPerTile;
+    const int b = e % kIdsPerTile;
+    int ii = 0;
+    while (ii + 1 < wr.nitems && items[(ii + 1) * kItemInts + IT_RTILE0] <= r) ++ii;
+    const int32_t* d = items + ii * kItemInts;
+    int bi = (d[IT_TILE0] + (r - d[IT_RTILE0])) * kIdsPerTile + b;
+    if (bi > d[IT_LASTBLK]) bi = d[IT_LASTBLK];
+    const int32_t* tab = d[IT_KIND] == 0 ? a.prefix_table : a.suffix_table;
+    ids[e] = tab[d[IT_TABOFF] + bi];
+  }
+  __syncthreads();
+  return wr;
+}
+
+// Index of the item that range tile r belongs to.
+__device__ __forceinline__ int item_of_tile(const int32_t* items, int nitems, int r) {
+  int ii = 0;
+  while (ii + 1 < nitems && items[(ii + 1) * kItemInts + IT_RTILE0] <= r) ++ii;
+  return ii;
+}
+
+// (fork, q head) of row rr of the item described by d.
+__device__ __forceinline__ void item_row(const Plan& plan, const int32_t* d, int rr, int* fork, int* head) {
+  item_row_fork_head(plan, d[IT_KIND], d[IT_T], d[IT_F], d[IT_J], d[IT_ROW0], rr, fork, head);
+}
+
+}  // namespace specgen

@@ -1,0 +1,219 @@
+// plan_check.cpp -- CPU replay of the fork-decode work split.
+//
+// Builds plans for random batch shapes with the host planner, then replays
+// every worker's walk the way the attention kernels do (locate, segment
+// lengths, segment index k) and every output row's merge lookup the way the
+// merge kernel does, and checks:
+//   - every tile of every work item is processed exactly once;
+//   - per-worker item count and tile count stay within the kernels' caps;
+//   - each row's merge finds exactly the (worker, segment) pairs that
+//     processed its prefix item and its suffix item, with in-range slots;
+//   - each item row maps back to the (fork, q head) it belongs to.
+// Built and run by tests/test_plan.py with g++ (no GPU involved).
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <random>
+#include <set>
+#include <tuple>
+#include <vector>
+
+#include "../paper_2606_17518_amd/csrc/planner.h"
+
+using namespace specgen;
+
+#define CHECK(cond, ...)                                             \
+  do {                                                               \
+    if (!(cond)) {                                                   \
+      fprintf(stderr, "FAIL %s:%d: %s | ", __FILE__, __LINE__, #cond); \
+      fprintf(stderr, __VA_ARGS__);                                  \
+      fprintf(stderr, "\n");                                         \
+      return false;                                                  \
+    }                                                                \
+  } while (0)
+
+struct Seg {
+  int w, k;
+  int64_t first;  // partition tile index of the segment's first tile
+  int n;          // tiles
+};
+
+static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
+  Plan plan;
+  int64_t wsf = 0;
+  char err[256];
+  const int rc = plan_build(in, [&] { return cus; }, &plan, &wsf, err, sizeof err);
+  CHECK(rc == kPlanOk, "case %llu: plan_build failed: %s", (unsigned long long)case_id, err);
+  // segments per (partition, item ordinal)
+  std::map<std::pair<int, int>, std::vector<Seg>> segs;
+  for (int X = 0; X < 2; ++X) {
+    const PartPlan& pp = plan.part[X];
+    if (pp.workers == 0) {
+      CHECK(pp.tiles == 0, "partition %d has tiles but no workers", X);
+      continue;
+    }
+    for (int w = 0; w < pp.workers; ++w) {
+      const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
+      CHECK(x1 - x0 <= in.tile_cap[X], "worker %d has %lld tiles > cap", w, (long long)(x1 - x0));
+      int64_t x = x0;
+      int nitems = 0, first_ord = -1;
+      while (x < x1) {
+        const ItemRef it = locate(plan, X, x);
+        CHECK(it.kind >= 0, "tile %lld not located", (long long)x);
+        CHECK(it.tile >= 0 && it.tile < it.tiles, "tile index");
+        const int n = (int)std::min<int64_t>(it.tiles - it.tile, x1 - x);
+        if (first_ord < 0) first_ord = it.ord;
+        const int k = it.ord - first_ord;
+        CHECK(k >= 0 && k < pp.kmax, "k %d kmax %d", k, pp.kmax);
+        segs[{X, it.ord}].push_back(Seg{w, k, x, n});
+        x += n;
+        ++nitems;
+      }
+      CHECK(nitems <= in.item_cap[X], "worker %d touches %d items > cap", w, nitems);
+    }
+  }
+  // enumerate items independently of locate() and check coverage
+  const int g = in.Hq / in.Hkv;
+  int64_t ptile[2] = {0, 0};
+  int pord[2] = {0, 0};
+  auto cover = [&](int X, int ord, int tiles) -> bool {
+    auto itv = segs.find({X, ord});
+    if (tiles == 0) {
+      CHECK(itv == segs.end(), "empty item has segments");
+      return true;
+    }
+    CHECK(itv != segs.end(), "item (%d, %d) never processed", X, ord);
+    int64_t expect = ptile[X];
+    int total = 0;
+    for (const Seg& s : itv->second) {
+      CHECK(s.first == expect, "item tiles not contiguous");
+      expect += s.n;
+      total += s.n;
+    }
+    CHECK(total == tiles, "item covered %d of %d tiles", total, tiles);
+    ptile[X] += tiles;
+    return true;
+  };
+  for (int X = 0; X < 2; ++X) {
+    for (int t = 0; t < in.T; ++t) {
+      const int rows = (in.fork_off[t + 1] - in.fork_off[t]) * g;
+      if (part_of_trace(in.policy, rows) != X) continue;
+      const int rb = (rows + in.rbs[X] - 1) / in.rbs[X];
+      const int tiles = (in.prefix_len[t] + in.tt[X] - 1) / in.tt[X];
+      for (int i = 0; i < in.Hkv * rb; ++i)
+        if (!cover(X, pord[X]++, tiles)) return false;
+    }
+  }
+  {
+    const int X = part_of_suffix(in.policy);
+    const int rb = (g + in.rbs[X] - 1) / in.rbs[X];
+    for (int f = 0; f < in.N; ++f) {
+      const int tiles = (in.suffix_len[f] + in.tt[X] - 1) / in.tt[X];
+      for (int i = 0; i < in.Hkv * rb; ++i)
+        if (!cover(X, pord[X]++, tiles)) return false;
+    }
+  }
+  for (int X = 0; X < 2; ++X) CHECK(ptile[X] == plan.part[X].tiles, "partition %d tile total", X);
+  // merge lookups
+  auto same = [&](const ItemParts& ip, int ord) -> bool {
+    const auto& v = segs.at({ip.part, ord});
+    CHECK((int)v.size() == ip.w_hi - ip.w_lo + 1, "merge finds %d parts, %zu processed",
+          ip.w_hi - ip.w_lo + 1, v.size());
+    for (size_t i = 0; i < v.size(); ++i) {
+      CHECK(v[i].w == ip.w_lo + (int)i, "worker mismatch");
+      CHECK(v[i].k == (i == 0 ? ip.k_lo : 0), "segment index mismatch");
+      const PartPlan& pp = plan.part[ip.part];
+      const int64_t slot = slot_of(pp, v[i].w, v[i].k);
+      CHECK(slot >= 0, "slot out of range");
+      CHECK(pp.o_base + (slot * pp.slot_rows + ip.row + 1) * in.D <= wsf, "o slot past workspace");
+      CHECK(pp.lse_base + slot * pp.slot_rows + ip.row < wsf, "lse slot past workspace");
+      CHECK(ip.row >= 0 && ip.row < pp.slot_rows, "row in item");
+    }
+    return true;
+  };
+  for (int f = 0; f < in.N; ++f) {
+    int t = 0;
+    while (in.fork_off[t + 1] <= f) ++t;
+    CHECK(trace_of_fork(plan, f) == t, "trace_of_fork");
+    for (int h = 0; h < in.Hq; ++h) {
+      const int j = h / g, hh = h % g;
+      const int ri = (f - in.fork_off[t]) * g + hh;
+      const int X = plan.trace_part[t];
+      const int rbs = in.rbs[X];
+      const int rows = (in.fork_off[t + 1] - in.fork_off[t]) * g;
+      const int rbc = (rows + rbs - 1) / rbs;
+      // prefix item ordinal, counted directly
+      int ord = 0;
+      for (int t2 = 0; t2 < t; ++t2) {
+        const int r2 = (in.fork_off[t2 + 1] - in.fork_off[t2]) * g;
+        if (part_of_trace(in.policy, r2) == X) ord += in.Hkv * ((r2 + rbs - 1) / rbs);
+      }
+      ord += j * rbc + ri / rbs;
+      const ItemParts P = prefix_parts_of_row(plan, f, h);
+      CHECK(P.part == X, "prefix partition");
+      if (!same(P, ord)) return false;
+      int ff, hh2;
+      item_row_fork_head(plan, 0, t, -1, j, (ri / rbs) * rbs, P.row, &ff, &hh2);
+      CHECK(ff == f && hh2 == h, "prefix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
+      ItemParts S;
+      const bool has = suffix_parts_of_row(plan, f, h, &S);
+      CHECK(has == (in.suffix_len[f] > 0), "suffix presence");
+      if (has) {
+        const int Xs = part_of_suffix(in.policy);
+        const int rbss = in.rbs[Xs];
+        const int srb = (g + rbss - 1) / rbss;
+        const int sord = plan.part[Xs].n_prefix_items + (f * in.Hkv + j) * srb + hh / rbss;
+        if (!same(S, sord)) return false;
+        item_row_fork_head(plan, 1, t, f, j, (hh / rbss) * rbss, S.row, &ff, &hh2);
+        CHECK(ff == f && hh2 == h, "suffix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
+      }
+    }
+  }
+  return true;
+}
+
+int main(int argc, char** argv) {
+  const int cases = argc > 1 ? atoi(argv[1]) : 300;
+  const uint64_t seed = argc > 2 ? strtoull(argv[2], nullptr, 10) : 1;
+  std::mt19937_64 rng(seed);
+  auto U = [&](int lo, int hi) { return (int)(lo + rng() % (uint64_t)(hi - lo + 1)); };
+  int done = 0;
+  for (int c = 0; c < cases; ++c) {
+    PlanInputs in;
+    in.D = U(0, 1) ? 128 : 64;
+    in.policy = U(0, 2);
+    const int gs[] = {1, 2, 4, 8, 16, 24, 128};
+    const int g = gs[U(0, 6)];
+    in.Hkv = U(1, 3) == 1 ? 8 : U(1, 4);
+    in.Hq = g * in.Hkv;
+    in.T = U(1, 12);
+    std::vector<int32_t> fo(in.T + 1, 0), P(in.T);
+    for (int t = 0; t < in.T; ++t) fo[t + 1] = fo[t] + U(1, U(0, 3) == 0 ? 40 : 6);
+    in.N = fo[in.T];
+    if (in.N > kMaxForks) continue;
+    const int pmax = U(0, 4) == 0 ? 140000 : (U(0, 1) ? 3000 : 300);
+    for (int t = 0; t < in.T; ++t) P[t] = U(1, pmax);
+    std::vector<int32_t> S(in.N);
+    const int smax = U(0, 1) ? 2100 : 40;
+    for (int f = 0; f < in.N; ++f) S[f] = U(0, 3) == 0 ? 0 : U(0, smax);
+    in.fork_off = fo.data();
+    in.prefix_len = P.data();
+    in.suffix_len = S.data();
+    in.tt[0] = in.D == 128 ? 64 : 128;
+    in.tt[1] = 64;
+    in.rbs[0] = 128;
+    in.rbs[1] = 16;
+    in.item_cap[0] = in.item_cap[1] = 64;
+    in.tile_cap[0] = 2048 / (in.tt[0] / 16);
+    in.tile_cap[1] = 2048 / 4;
+    const int cus = U(0, 2) == 0 ? U(1, 16) : 256;
+    if (!check_plan(in, cus, (uint64_t)c)) {
+      fprintf(stderr, "case %d: D=%d policy=%d g=%d Hkv=%d T=%d N=%d cus=%d\n", c, in.D, in.policy, g, in.Hkv,
+              in.T, in.N, cus);
+      return 1;
+    }
+    ++done;
+  }
+  printf("OK %d plans\n", done);
+  return 0;
+}

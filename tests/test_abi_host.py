@@ -1,0 +1,100 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every entry
+point include/specgen.h declares, and rejects bad arguments before touching
+the device (these calls return during argument checking)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "specgen.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(specgen_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2606_17518_amd as sg
+    lib_path = os.path.join(ROOT, "paper_2606_17518_amd", "libspecgen.so")
+    if not os.path.exists(lib_path):
+        sg.build.build()
+    return sg.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert set(names) == {"specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn",
+                          "specgen_fork_decode_attn_phase", "specgen_kv_import", "specgen_lse_merge",
+                          "specgen_last_error"}
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _host_batch(**kw):
+    import paper_2606_17518_amd.binding as B
+    s = B.ForkBatchC()
+    s.num_traces, s.num_forks, s.num_q_heads, s.num_kv_heads, s.head_dim, s.block_size = 1, 2, 8, 2, 64, 16
+    s.num_blocks, s.sm_scale, s.kv_dtype, s.path, s.reserved = 8, 0.125, 0, 0, 0
+    fake = 0x10000   # never dereferenced: every call below fails argument checks first
+    for f in ("q", "k_pool", "v_pool", "fork_off", "prefix_len", "prefix_table_off", "prefix_table",
+              "suffix_len", "suffix_table_off", "suffix_table"):
+        setattr(s, f, fake)
+    keep = [np.array([0, 2], np.int32), np.array([20], np.int32), np.array([3, 0], np.int32)]
+    s.fork_off_h, s.prefix_len_h, s.suffix_len_h = (a.ctypes.data for a in keep)
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s, keep
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("num_traces", 0, 1), ("num_forks", 0, 1), ("num_q_heads", 7, 1), ("head_dim", 96, 2),
+    ("block_size", 32, 2), ("sm_scale", 0.0, 1), ("sm_scale", float("nan"), 1), ("kv_dtype", 5, 2),
+    ("path", 9, 1), ("reserved", 1, 1), ("q", None, 1), ("suffix_len_h", None, 1), ("num_blocks", 0, 1),
+])
+def test_bad_batch_rejected_without_launch(L, field, value, status):
+    s, keep = _host_batch(**{field: value})
+    n = C.c_size_t(123)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status
+    assert n.value == 123
+    assert L.specgen_last_error().decode() != ""
+    assert L.specgen_fork_decode_attn(C.byref(s), C.c_void_p(0x10000), None, None, 0, None) == status
+    for phase in (0, 1, 2):
+        assert L.specgen_fork_decode_attn_phase(C.byref(s), phase, C.c_void_p(0x10000), None, None, 0, None) == status
+
+
+def test_bad_lengths_rejected(L):
+    import paper_2606_17518_amd.binding as B
+    s, keep = _host_batch()
+    bad = np.array([0, 3], np.int32)          # fork_off must end at N = 2
+    s.fork_off_h = bad.ctypes.data
+    n = C.c_size_t(0)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
+    s, keep = _host_batch()
+    neg = np.array([-1, 0], np.int32)
+    s.suffix_len_h = neg.ctypes.data
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
+    zero_prefix = np.array([0], np.int32)
+    s, keep = _host_batch()
+    s.prefix_len_h = zero_prefix.ctypes.data
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
+
+
+def test_import_and_merge_argument_errors(L):
+    import paper_2606_17518_amd.binding as B
+    t = (B.KvTensorC * 1)()
+    t[0].dst_pool, t[0].src_staging, t[0].block_bytes = 0x10000, 0x20000, 6
+    assert L.specgen_kv_import(t, 1, C.c_void_p(0x30000), 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    t[0].block_bytes = 64
+    assert L.specgen_kv_import(t, 0, C.c_void_p(0x30000), 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_import(t, 5, C.c_void_p(0x30000), 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_import(t, 1, None, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_import(t, 1, C.c_void_p(0x30000), -1, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    P = C.c_void_p(0x10000)
+    assert L.specgen_lse_merge(P, P, 0, 4, 64, P, 0, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_lse_merge(P, P, 2, 4, 2000, P, 0, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_lse_merge(P, P, 2, 4, 64, P, 7, None, None) == B.SPECGEN_ERR_INVALID_ARG
