@@ -99,11 +99,14 @@ typedef struct {
   const int32_t *suffix_table_off; /* [N+1], at least ceil(S_f/16) ids per fork  */
   const int32_t *suffix_table;     /* may be NULL only if every S_f is 0         */
   /* host mirrors of the index arrays above (same contents), read only during
-     the call to size the work split and the workspace; the device copies are
-     what the kernels read, so the two must agree */
+     the call: they size the work split and the workspace and travel to the
+     kernels with the launch; the block tables themselves are read on the
+     device.  Mirrors and device arrays must agree. */
   const int32_t *fork_off_h;
   const int32_t *prefix_len_h;
   const int32_t *suffix_len_h;
+  const int32_t *prefix_table_off_h;
+  const int32_t *suffix_table_off_h;
 } specgen_fork_batch_t;
 
 /* Workspace bytes that specgen_fork_decode_attn needs for this batch (partial

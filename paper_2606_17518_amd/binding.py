@@ -47,6 +47,7 @@ class ForkBatchC(C.Structure):
         ("prefix_table", C.c_void_p), ("suffix_len", C.c_void_p), ("suffix_table_off", C.c_void_p),
         ("suffix_table", C.c_void_p),
         ("fork_off_h", C.c_void_p), ("prefix_len_h", C.c_void_p), ("suffix_len_h", C.c_void_p),
+        ("prefix_table_off_h", C.c_void_p), ("suffix_table_off_h", C.c_void_p),
     ]
 
 
@@ -124,13 +125,16 @@ class ForkBatchTensors:
     fork_off_h: np.ndarray
     prefix_len_h: np.ndarray
     suffix_len_h: np.ndarray
+    prefix_table_off_h: np.ndarray
+    suffix_table_off_h: np.ndarray
     path: int = SPECGEN_PATH_AUTO
     block_size: int = 16
 
     @staticmethod
     def from_numpy(b, device="cuda", path: str | int = "auto") -> "ForkBatchTensors":
         """Upload an object with the numpy fields of a fork batch (q, pools,
-        scales, index arrays) and keep int32 host mirrors of the lengths."""
+        scales, index arrays) and keep int32 host mirrors of the lengths and
+        table offsets."""
         def dev(a, dt):
             return torch.from_numpy(np.ascontiguousarray(a).view(dt)).to(device)
         fp8 = b.kv_dtype != "bf16"
@@ -149,6 +153,8 @@ class ForkBatchTensors:
             fork_off_h=np.ascontiguousarray(b.fork_off, np.int32),
             prefix_len_h=np.ascontiguousarray(b.prefix_len, np.int32),
             suffix_len_h=np.ascontiguousarray(b.suffix_len, np.int32),
+            prefix_table_off_h=np.ascontiguousarray(b.prefix_table_off, np.int32),
+            suffix_table_off_h=np.ascontiguousarray(b.suffix_table_off, np.int32),
             path=PATHS[path] if isinstance(path, str) else int(path))
 
     def c_struct(self, **overrides) -> ForkBatchC:
@@ -168,7 +174,7 @@ class ForkBatchTensors:
                      "prefix_table", "suffix_len", "suffix_table_off", "suffix_table"):
             t = getattr(self, name)
             setattr(s, name, None if t is None else t.data_ptr())
-        for name in ("fork_off_h", "prefix_len_h", "suffix_len_h"):
+        for name in ("fork_off_h", "prefix_len_h", "suffix_len_h", "prefix_table_off_h", "suffix_table_off_h"):
             setattr(s, name, getattr(self, name).ctypes.data)
         for k, v in overrides.items():
             setattr(s, k, v)

@@ -63,7 +63,7 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
     return fail(SPECGEN_ERR_INVALID_ARG, "a device pointer of the batch is NULL");
   if (b->kv_dtype == SPECGEN_FP8_E4M3 && (!b->k_scale || !b->v_scale))
     return fail(SPECGEN_ERR_INVALID_ARG, "E4M3 KV needs k_scale and v_scale");
-  if (!b->fork_off_h || !b->prefix_len_h || !b->suffix_len_h)
+  if (!b->fork_off_h || !b->prefix_len_h || !b->suffix_len_h || !b->prefix_table_off_h || !b->suffix_table_off_h)
     return fail(SPECGEN_ERR_INVALID_ARG, "a host mirror of the batch is NULL");
   if (!b->suffix_table) {   // only a batch without suffix tokens may omit the suffix table
     for (int f = 0; f < b->num_forks; ++f)
@@ -80,6 +80,8 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.fork_off = b->fork_off_h;
   in.prefix_len = b->prefix_len_h;
   in.suffix_len = b->suffix_len_h;
+  in.prefix_table_off = b->prefix_table_off_h;
+  in.suffix_table_off = b->suffix_table_off_h;
   in.tt[0] = mfma_tile_tokens(in.D == 64 ? 64 : 128, fp8);
   in.tt[1] = dot_tile_tokens(in.D);
   in.rbs[0] = 128;
@@ -130,10 +132,12 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, i
   a.v_pool = static_cast<const uint8_t*>(b->v_pool);
   a.k_scale = b->k_scale;
   a.v_scale = b->v_scale;
-  a.prefix_table_off = b->prefix_table_off;
+  a.ix.fork_off = b->fork_off;
+  a.ix.prefix_len = b->prefix_len;
+  a.ix.prefix_table_off = b->prefix_table_off;
+  a.ix.suffix_len = b->suffix_len;
+  a.ix.suffix_table_off = b->suffix_table_off;
   a.prefix_table = b->prefix_table;
-  a.suffix_len = b->suffix_len;
-  a.suffix_table_off = b->suffix_table_off;
   a.suffix_table = b->suffix_table;
   a.ws = static_cast<float*>(workspace);
   a.sm_scale = b->sm_scale;
@@ -144,7 +148,7 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, i
     if (plan.part[kPartMfma].workers > 0) e = launch_attn_mfma_any(a, plan, fp8, stream);
     if (e == hipSuccess && plan.part[kPartDot].workers > 0) e = launch_attn_dot_any(a, plan, fp8, stream);
   }
-  if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);
+  if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ix, a.ws, out, out_lse, stream);
   if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -30,7 +30,8 @@ struct DotCfg {
   static constexpr int kOffML = kOffComb + 4 * kRows * D * 4;   // [4 waves][16] m, then l
   static constexpr int kOffItems = kOffML + 2 * 4 * kRows * 4;
   static constexpr int kOffIds = kOffItems + kItemCap * kItemInts * 4;
-  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
+  static constexpr int kOffScales = kOffIds + kIdCap * 4;      // E4M3: k then v scale per id
+  static constexpr int kLdsBytes = kOffScales + (FP8 ? 2 * kIdCap * 4 : 0);
 };
 
 // kDPL pool elements of one token as packed bf16 pairs (E4M3 decoded exactly).
@@ -40,13 +41,17 @@ struct TokVec {
 };
 
 template <int D, bool FP8>
-__global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, const Plan plan) {
+__global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, const PlanHead head) {
   using C = DotCfg<D, FP8>;
   constexpr int DPL = C::kDPL;
   constexpr int NP = DPL / 2;     // bf16 pairs per lane
   constexpr int RWS = C::kRows;
   constexpr int TB = C::kTB;
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  __shared__ Plan splan;
+  plan_build_lds(head, a.ix, splan);
+  const Plan& plan = splan;
+  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   int32_t* ids = reinterpret_cast<int32_t*>(lds + C::kOffIds);
   const PartPlan& pp = plan.part[kPartDot];
@@ -56,8 +61,9 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
   const int grp = lane >> 4;      // token stream within the wave
   const int sub = lane & 15;      // dims [sub*DPL, +DPL)
   const int w = blockIdx.x;
-  const WorkerRange wr =
-      worker_prepass<C::kThreads, C::kItemCap, C::kIdsPerTile, C::kTileCap>(a, plan, kPartDot, w, items, ids);
+  float* scales = FP8 ? reinterpret_cast<float*>(lds + C::kOffScales) : nullptr;
+  const WorkerRange wr = worker_prepass<C::kThreads, C::kItemCap, C::kIdsPerTile, C::kTileCap>(
+      a, plan, kPartDot, w, items, ids, scales);
   const int R = wr.R;
   if (R <= 0) return;
   const int nitems = wr.nitems;
@@ -136,14 +142,19 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
       int fork = 0, h = 0;
       item_row(plan, d, row, &fork, &h);
       const bool ok = row < nrows;
-      const uint16_t* qrow = a.q + ((int64_t)fork * plan.Hq + h) * D + sub * DPL;
+      // unconditional loads (padded rows read row 0 and are zeroed)
+      const uint16_t* qrow = a.q + (ok ? ((int64_t)fork * plan.Hq + h) * D : 0) + sub * DPL;
 #pragma unroll
-      for (int q = 0; q < NP; ++q) qp[row][q] = ok ? *reinterpret_cast<const uint32_t*>(qrow + 2 * q) : 0u;
+      for (int q = 0; q < NP; ++q) {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(qrow + 2 * q);
+        qp[row][q] = ok ? v : 0u;
+      }
       m_run[row] = -INFINITY;
       l_run[row] = 0.f;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) o[row][e] = 0.f;
     }
+    wait_vmem();
   };
 
   auto compute_tile = [&](const Raw& raw, const int32_t* d, int r) {
@@ -165,9 +176,8 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
     }
     float ksc = 1.f, vsc = 1.f;
     if constexpr (FP8) {
-      const int blk = ids[r * C::kIdsPerTile + wave];
-      ksc = a.k_scale[blk];
-      vsc = a.v_scale[blk];
+      ksc = scales[r * C::kIdsPerTile + wave];
+      vsc = scales[C::kIdCap + r * C::kIdsPerTile + wave];
     }
 #pragma unroll
     for (int row = 0; row < RWS; ++row) {
@@ -243,7 +253,7 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
     // combine the four waves: thread -> (row, 8 or 4 dims)
     {
       constexpr int PER = RWS * D / C::kThreads;   // 8 (D=128) or 4 (D=64)
@@ -275,7 +285,7 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
   };
 
   Raw cur, nxt;
@@ -299,7 +309,7 @@ template <int D, bool FP8>
 hipError_t launch_attn_dot_t(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
   const int W = plan.part[kPartDot].workers;
   if (W <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_dot_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, plan);
+  hipLaunchKernelGGL((attn_dot_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, static_cast<const PlanHead&>(plan));
   return hipGetLastError();
 }
 

@@ -23,6 +23,10 @@
 
 namespace specgen {
 
+// The running max moves only when a new score would give a probability above
+// 2^kRescaleLog2 relative to it.
+constexpr float kRescaleLog2 = 8.f;
+
 template <int D, bool FP8>
 struct MfmaCfg {
   static constexpr int kThreads = 256;
@@ -46,7 +50,8 @@ struct MfmaCfg {
   static constexpr int kOffCombML = kOffComb + 2 * 32 * D * 4; // [2 rg][32] m, then l
   static constexpr int kOffItems = kOffCombML + 2 * 2 * 32 * 4;
   static constexpr int kOffIds = kOffItems + kItemCap * kItemInts * 4;
-  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
+  static constexpr int kOffScales = kOffIds + kIdCap * 4;      // E4M3: k then v scale per id
+  static constexpr int kLdsBytes = kOffScales + (FP8 ? 2 * kIdCap * 4 : 0);
   static_assert(kLoads * 16 * kThreads == kTileB, "tile must split evenly over threads");
   static_assert(kLdsBytes <= 163840, "LDS budget");
 };
@@ -60,12 +65,16 @@ template <int CPR>
 __device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >> 1) & 4))) & (CPR - 1); }
 
 template <int D, bool FP8>
-__global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const Plan plan) {
+__global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const PlanHead head) {
   using C = MfmaCfg<D, FP8>;
   constexpr int TT = C::kTT;
   constexpr int KS = D / 32;   // k-steps of S^T
   constexpr int DT = D / 16;   // d-tiles of O^T
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  __shared__ Plan splan;
+  plan_build_lds(head, a.ix, splan);
+  const Plan& plan = splan;
+  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   int32_t* ids = reinterpret_cast<int32_t*>(lds + C::kOffIds);
 
@@ -74,8 +83,9 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int w = blockIdx.x;
-  const WorkerRange wr =
-      worker_prepass<C::kThreads, C::kItemCap, C::kIdsPerTile, C::kTileCap>(a, plan, kPartMfma, w, items, ids);
+  float* scales = FP8 ? reinterpret_cast<float*>(lds + C::kOffScales) : nullptr;
+  const WorkerRange wr = worker_prepass<C::kThreads, C::kItemCap, C::kIdsPerTile, C::kTileCap>(
+      a, plan, kPartMfma, w, items, ids, scales);
   const int R = wr.R;
   const int nitems = wr.nitems;
   const int first_ord = wr.first_ord;
@@ -86,13 +96,19 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   const int64_t head_stride = (int64_t)D * C::kGElem;               // bytes between kv heads
   const int64_t tok_stride = (int64_t)plan.Hkv * head_stride;       // bytes between tokens
   auto tile_item = [&](int r) { return item_of_tile(items, nitems, r); };
+  // Loads are issued unconditionally so the compiler can count outstanding
+  // vector loads exactly across the pipeline; past the range end every lane
+  // re-reads the first 16 bytes of q (one cached line, no HBM traffic).
   auto issue = [&](chunk_t (&rk)[C::kLoads], chunk_t (&rv)[C::kLoads], int r) {
-    if (r >= R) return;
-    const int ii = uniform(tile_item(r));
+    const bool real = r < R;
+    const int rr = real ? r : R - 1;
+    const int ii = uniform(tile_item(rr));
     const int32_t* d = items + ii * kItemInts;
     const int j = uniform(d[IT_J]);
     const int nv = uniform(d[IT_NVALID]);
-    const int tbase = (uniform(d[IT_TILE0]) + (r - uniform(d[IT_RTILE0]))) * TT;
+    const int tbase = (uniform(d[IT_TILE0]) + (rr - uniform(d[IT_RTILE0]))) * TT;
+    const uint8_t* kp = real ? a.k_pool : reinterpret_cast<const uint8_t*>(a.q);
+    const uint8_t* vp = real ? a.v_pool : reinterpret_cast<const uint8_t*>(a.q);
 #pragma unroll
     for (int it = 0; it < C::kLoads; ++it) {
       const int c = it * C::kThreads + tid;
@@ -100,10 +116,11 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       const int part = c % C::kCPR;
       int ti = tbase + tok;
       if (ti >= nv) ti = nv - 1;
-      const int blk = ids[r * C::kIdsPerTile + tok / 16];
-      const int64_t off = ((int64_t)blk * 16 + (ti & 15)) * tok_stride + j * head_stride + part * C::kGChunk;
-      rk[it] = *reinterpret_cast<const chunk_t*>(a.k_pool + off);
-      rv[it] = *reinterpret_cast<const chunk_t*>(a.v_pool + off);
+      const int blk = ids[rr * C::kIdsPerTile + tok / 16];
+      int64_t off = ((int64_t)blk * 16 + (ti & 15)) * tok_stride + j * head_stride + part * C::kGChunk;
+      off = real ? off : 0;
+      rk[it] = *reinterpret_cast<const chunk_t*>(kp + off);
+      rv[it] = *reinterpret_cast<const chunk_t*>(vp + off);
     }
   };
   auto to_lds_chunk = [&](const chunk_t& v) -> u32x4 {
@@ -139,6 +156,15 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   // ---- per-wave compute state -----------------------------------------------------
   const int G = lane >> 4;     // 16-lane group
   const int ln = lane & 15;    // row within an N-tile / key within an S^T tile
+  // Lane-constant parts of the LDS addresses (slab bases are multiples of 32):
+  // the key this lane feeds to S^T tile a (tile b is 4 keys later) and its
+  // swizzle, and the keys / swizzles of this lane's two transposing V reads.
+  const int k_lane_tok = 8 * (ln >> 2) + (ln & 3);
+  const int k_lane_swz = swz_k<C::kCPR>(k_lane_tok);
+  const int v_lane_tok = 8 * G + (ln >> 2);
+  const int v_lane_swz0 = swz_v<C::kCPR>(v_lane_tok);
+  const int v_lane_swz1 = swz_v<C::kCPR>(v_lane_tok + 4);
+  const int vsub = ln & 3;
   bf16x8 qop[2][KS];
   f32x4 acc[2][DT];
   float m_run[2], l_run[2];
@@ -157,11 +183,13 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       int fork = 0, h = 0;
       item_row(plan, d, rr, &fork, &h);
       const bool ok = active && rr < nrows;
-      const uint16_t* qrow = a.q + ((int64_t)fork * plan.Hq + h) * D;
+      // unconditional loads (padded rows read row 0 and are zeroed) keep the
+      // number of outstanding loads the same on every path
+      const uint16_t* qrow = a.q + (ok ? ((int64_t)fork * plan.Hq + h) * D : 0);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (ok) v = *reinterpret_cast<const u32x4*>(qrow + ks * 32 + G * 8);
+        u32x4 v = *reinterpret_cast<const u32x4*>(qrow + ks * 32 + G * 8);
+        if (!ok) v = u32x4{0u, 0u, 0u, 0u};
         qop[nt][ks] = __builtin_bit_cast(bf16x8, v);
       }
       m_run[nt] = -INFINITY;
@@ -169,6 +197,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    wait_vmem();
   };
 
   auto compute_tile = [&](int stage_off, const int32_t* d, int r) {
@@ -187,13 +216,14 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int ta = sb + 8 * (ln >> 2) + (ln & 3);   // key of S^T tile a held by this lane as A row
-      const int tb = ta + 4;
+      // slab bases are multiples of 32, so the swizzles depend on the lane only
+      const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
+      const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int ch = 4 * ks + G;
-        const u32x4 ka = *reinterpret_cast<const SG_LDS u32x4*>(kb + ta * C::kRowB + ((ch ^ swz_k<C::kCPR>(ta)) << 4));
-        const u32x4 kbv = *reinterpret_cast<const SG_LDS u32x4*>(kb + tb * C::kRowB + ((ch ^ swz_k<C::kCPR>(tb)) << 4));
+        const int cho = (((4 * ks + G) ^ k_lane_swz) << 4);
+        const u32x4 ka = *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho);
+        const u32x4 kbv = *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho);
         const bf16x8 A0 = __builtin_bit_cast(bf16x8, ka);
         const bf16x8 A1 = __builtin_bit_cast(bf16x8, kbv);
 #pragma unroll
@@ -204,8 +234,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       }
       // lane (G, ln) now holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
       if constexpr (FP8) {
-        const int kb0 = ids[r * C::kIdsPerTile + (sb + 8 * G) / 16];
-        const float ksc = a.k_scale[kb0];
+        const float ksc = scales[r * C::kIdsPerTile + (sb + 8 * G) / 16];
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -226,27 +255,28 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       for (int nt = 0; nt < 2; ++nt) {
         float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
                          fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
-        mx = wave_max_xor(mx, 16);
-        mx = wave_max_xor(mx, 32);
-        const float m_new = fmaxf(m_run[nt], mx);
-        const float mc = (m_new == -INFINITY) ? 0.f : m_new * a.c_log2;
-        const float alpha = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
-        m_run[nt] = m_new;
+        mx = rows4_max(mx);
+        // Lazy rescaling: the reference max only moves when a score exceeds it
+        // by more than 2^kRescaleLog2 in probability, so P <= 2^8 stays exact
+        // enough in bf16 and fp32 and the accumulator is rarely touched.
+        if (__builtin_amdgcn_ballot_w64(mx * a.c_log2 > m_run[nt] * a.c_log2 + kRescaleLog2)) {
+          const float m_new = fmaxf(m_run[nt], mx);
+          const float alpha = __builtin_amdgcn_exp2f((m_run[nt] - m_new) * a.c_log2);
+          m_run[nt] = m_new;
+          l_run[nt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) scale_acc(acc[nt][dt], alpha);
+        }
+        const float mc = m_run[nt] * a.c_log2;
         float p[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           p[e] = __builtin_amdgcn_exp2f(fmaf(s[0][nt][e], a.c_log2, -mc));
           p[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][nt][e], a.c_log2, -mc));
         }
-        float ps = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-        l_run[nt] = l_run[nt] * alpha + ps;
-        if (alpha != 1.f) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
-        }
+        l_run[nt] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
         if constexpr (FP8) {
-          const int vb0 = ids[r * C::kIdsPerTile + (sb + 8 * G) / 16];
-          const float vsc = a.v_scale[vb0];
+          const float vsc = scales[C::kIdCap + r * C::kIdsPerTile + (sb + 8 * G) / 16];
 #pragma unroll
           for (int e = 0; e < 8; ++e) p[e] *= vsc;
         }
@@ -258,15 +288,15 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
         pop[nt] = __builtin_bit_cast(bf16x8, pk);
       }
       // O^T += V^T P^T ; the transposing read gives lane (G, ln) V[sb+8G+4h+e][16dt+ln]
-      const int vt = sb + 8 * G + (ln >> 2);
-      const int vsub = ln & 3;
+      const SG_LDS uint8_t* v_row0 = vb + (sb + v_lane_tok) * C::kRowB;
+      const SG_LDS uint8_t* v_row1 = v_row0 + 4 * C::kRowB;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int ch = 2 * dt + (vsub >> 1);
-        const int off0 = vt * C::kRowB + ((ch ^ swz_v<C::kCPR>(vt)) << 4) + ((vsub & 1) << 3);
-        const int off1 = (vt + 4) * C::kRowB + ((ch ^ swz_v<C::kCPR>(vt + 4)) << 4) + ((vsub & 1) << 3);
-        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(vb + off0));
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(vb + off1));
+        const int off0 = ((ch ^ v_lane_swz0) << 4) + ((vsub & 1) << 3);
+        const int off1 = ((ch ^ v_lane_swz1) << 4) + ((vsub & 1) << 3);
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row0 + off0));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row1 + off1));
         const bf16x8 A = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
@@ -280,10 +310,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   auto finish_item = [&](const int32_t* d) {
     float lrow[2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      float v = l_run[nt] + __shfl_xor(l_run[nt], 16, 64);
-      lrow[nt] = v + __shfl_xor(v, 32, 64);
-    }
+    for (int nt = 0; nt < 2; ++nt) lrow[nt] = rows4_sum(l_run[nt]);
     if (ntg == 2) {
       if (tg == 1 && active) {
 #pragma unroll
@@ -298,7 +325,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
           }
         }
       }
-      __syncthreads();
+      lds_barrier();
       if (tg == 0 && active) {
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
@@ -318,7 +345,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
           m_run[nt] = m;
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
     if (tg == 0 && active) {
       const int k = uniform(d[IT_ORD]) - first_ord;
@@ -341,16 +368,20 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
     }
   };
 
-  // ---- pipeline: tiles r, r+1 in LDS stages 0/1; two tiles in flight in registers
-  chunk_t kA[C::kLoads], vA[C::kLoads], kB[C::kLoads], vB[C::kLoads];
+  // ---- pipeline: tile t is staged through LDS stage t % 2 and register set
+  // t % 3, so three tiles are in flight while one is computed
+  chunk_t kA[C::kLoads], vA[C::kLoads], kB[C::kLoads], vB[C::kLoads], kC[C::kLoads], vC[C::kLoads];
+  auto stage_of = [&](int t) { return (t & 1) ? C::kOffStage1 : C::kOffStage0; };
   issue(kA, vA, 0);
   issue(kB, vB, 1);
-  store(kA, vA, C::kOffStage0);
-  issue(kA, vA, 2);
-  __syncthreads();
+  issue(kC, vC, 2);
+  store(kA, vA, stage_of(0));
+  issue(kA, vA, 3);
+  lds_barrier();
 
   int cur = -1;   // item index being accumulated
   auto step = [&](int r, int stage_off) {
+    if (r >= R) return;
     const int ii = uniform(tile_item(r));
     const int32_t* d = items + ii * kItemInts;
     if (ii != cur) {
@@ -360,16 +391,22 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
     compute_tile(stage_off, d, r);
     if (r - uniform(d[IT_RTILE0]) == uniform(d[IT_NTILE]) - 1) finish_item(d);
   };
-  for (int r = 0; r < R; r += 2) {
-    step(r, C::kOffStage0);
-    if (r + 1 < R) store(kB, vB, C::kOffStage1);
-    issue(kB, vB, r + 3);
-    __syncthreads();
-    if (r + 1 >= R) break;
-    step(r + 1, C::kOffStage1);
-    if (r + 2 < R) store(kA, vA, C::kOffStage0);
-    issue(kA, vA, r + 4);
-    __syncthreads();
+  // Stores are unconditional too: a stage written past the range end is never read.
+  // Single-exit loop over tile triples; step() ignores tiles past the range and
+  // the loads behind them are harmless re-reads of q.
+  for (int r = 0; r < R; r += 3) {
+    step(r, stage_of(r));
+    store(kB, vB, stage_of(r + 1));
+    issue(kB, vB, r + 4);
+    lds_barrier();
+    step(r + 1, stage_of(r + 1));
+    store(kC, vC, stage_of(r + 2));
+    issue(kC, vC, r + 5);
+    lds_barrier();
+    step(r + 2, stage_of(r + 2));
+    store(kA, vA, stage_of(r + 3));
+    issue(kA, vA, r + 6);
+    lds_barrier();
   }
 }
 
@@ -377,7 +414,7 @@ template <int D, bool FP8>
 hipError_t launch_attn_mfma_t(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_mfma_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, plan);
+  hipLaunchKernelGGL((attn_mfma_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, static_cast<const PlanHead&>(plan));
   return hipGetLastError();
 }
 

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace specgen {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -27,15 +29,61 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, h);
 }
 
+// Two fp32 -> packed bf16 pair (round to nearest even), one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 __device__ __forceinline__ float wave_max_xor(float v, int mask) {
   return fmaxf(v, __shfl_xor(v, mask, 64));
 }
 
+// acc *= alpha for an MFMA accumulator that lives in AGPRs: read, scale and
+// write back inside one asm block so the compiler keeps the accumulator in
+// AGPRs instead of shuttling every accumulator through VGPRs around the
+// (rare) rescale branch.
+__device__ __forceinline__ void scale_acc(f32x4& acc, float alpha) {
+  float x0 = acc[0], x1 = acc[1], x2 = acc[2], x3 = acc[3];
+  float t;
+  asm volatile(
+      "v_accvgpr_read_b32 %4, %0\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %0, %4\n\t"
+      "v_accvgpr_read_b32 %4, %1\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %1, %4\n\t"
+      "v_accvgpr_read_b32 %4, %2\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %2, %4\n\t"
+      "v_accvgpr_read_b32 %4, %3\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %3, %4"
+      : "+a"(x0), "+a"(x1), "+a"(x2), "+a"(x3), "=&v"(t)
+      : "v"(alpha));
+  acc = f32x4{x0, x1, x2, x3};
+}
+
+// Max / sum over the four 16-lane rows of a wave (lanes l, l^16, l^32, l^48)
+// with the gfx950 row-swap permutes (no LDS round trip).
+__device__ __forceinline__ float rows4_max(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
+// operations, then s_barrier.  Unlike __syncthreads() it does not wait for
+// outstanding global loads (vector loads and stores share one counter on
+// gfx950, so a workgroup release fence would drain the prefetched tiles).
+// The memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Wait for every outstanding vector-memory operation of this wave.  Used at
+// the end of rarely taken paths that load registers the hot loop later reads,
+// so the compiler does not place that wait inside the hot loop instead.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Partial-result and plan arguments shared by the attention kernels.
 struct AttnArgs {
@@ -44,10 +92,8 @@ struct AttnArgs {
   const uint8_t* __restrict__ v_pool;
   const float* __restrict__ k_scale;       // [blocks] (E4M3 only)
   const float* __restrict__ v_scale;
-  const int32_t* __restrict__ prefix_table_off;
+  IndexArrays ix;                          // lengths and table offsets (device)
   const int32_t* __restrict__ prefix_table;
-  const int32_t* __restrict__ suffix_len;
-  const int32_t* __restrict__ suffix_table_off;
   const int32_t* __restrict__ suffix_table;
   float* __restrict__ ws;                  // workspace (partials)
   float sm_scale;

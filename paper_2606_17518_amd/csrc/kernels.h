@@ -20,7 +20,8 @@ int dot_rows();
 int dot_item_cap();
 int dot_tile_cap(int D);
 // merge.hip
-hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream);
+hipError_t launch_fork_merge(const Plan& plan, const IndexArrays& ix, const float* ws, void* out, float* out_lse,
+                             hipStream_t stream);
 hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S, int64_t R, int D, void* out,
                             bool out_bf16, float* out_lse, hipStream_t stream);
 // kv_import.hip

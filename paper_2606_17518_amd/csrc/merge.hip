@@ -96,11 +96,87 @@ hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S,
 // ---- fork merge: the parts of row (f, h) are the partials of the workers that
 // covered its prefix item and its suffix item ---------------------------------
 
+// Row merge for D in {64, 128}: lanes read 16 bytes each, so one load
+// instruction covers 64 / (D/4) parts; loads for up to 8 instructions' worth
+// of parts are issued before any is consumed, so a row costs a few memory
+// latencies rather than one per part.
+template <int D, typename PO, typename PL>
+__device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse, uint16_t* out_row,
+                                             float* out_lse_p) {
+  constexpr int LPP = D / 4;       // lanes per part
+  constexpr int PPI = 64 / LPP;    // parts per load instruction
+  constexpr int U = 8;             // load instructions in flight
+  const int lane = threadIdx.x & 63;
+  const int gsl = lane / LPP;      // part slot of this lane within an instruction
+  const int c4 = (lane % LPP) * 4; // first of the 4 dims this lane owns
+  float M = -INFINITY, z = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int p0 = 0; p0 < nparts; p0 += 64) {
+    const int p = p0 + lane;
+    const float l = p < nparts ? part_lse(p) : -INFINITY;
+    float cm = l;
+    for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
+    const float Mn = fmaxf(M, cm);
+    if (Mn == -INFINITY) continue;          // every part so far empty (wave-uniform)
+    const float rescale = __expf(M - Mn);   // M = -inf -> 0
+    z *= rescale;
+    acc *= rescale;
+    M = Mn;
+    const float wl = (l == -INFINITY) ? 0.f : __expf(l - M);
+    float zs = wl;
+    for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
+    z += zs;
+    const int cnt = (nparts - p0) < 64 ? (nparts - p0) : 64;
+    for (int q0 = 0; q0 < cnt; q0 += PPI * U) {
+      f32x4 v[U];
+      float wq[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + u * PPI + gsl;
+        const int qc = q < cnt ? q : cnt - 1;
+        wq[u] = __shfl(wl, qc, 64);
+        if (q >= cnt) wq[u] = 0.f;
+        v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (wq[u] != 0.f) acc += wq[u] * v[u];   // an empty part's o may be garbage
+    }
+  }
+  // sum the PPI lane groups
+#pragma unroll
+  for (int o = LPP; o < 64; o <<= 1) {
+    acc[0] += __shfl_xor(acc[0], o, 64);
+    acc[1] += __shfl_xor(acc[1], o, 64);
+    acc[2] += __shfl_xor(acc[2], o, 64);
+    acc[3] += __shfl_xor(acc[3], o, 64);
+  }
+  const bool empty = (M == -INFINITY);
+  if (gsl == 0) {
+    const float inv = empty ? 0.f : 1.f / z;
+    u32x2 pk;
+    pk[0] = pack_bf16x2(empty ? 0.f : acc[0] * inv, empty ? 0.f : acc[1] * inv);
+    pk[1] = pack_bf16x2(empty ? 0.f : acc[2] * inv, empty ? 0.f : acc[3] * inv);
+    *reinterpret_cast<u32x2*>(out_row + c4) = pk;
+  }
+  if (out_lse_p && lane == 0) *out_lse_p = empty ? -INFINITY : M + __logf(z);
+}
+
 template <int D>
-__global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan, const float* __restrict__ ws,
-                                                         uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+__global__ void __launch_bounds__(256) fork_merge_kernel(const PlanHead head, const IndexArrays ix,
+                                                         const float* __restrict__ ws, uint16_t* __restrict__ out,
+                                                         float* __restrict__ out_lse) {
+  __shared__ Plan splan;
+  plan_build_lds(head, ix, splan);
+  const Plan& plan = splan;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= (int64_t)plan.N * plan.Hq) return;
+  if (!plan.consistent) {   // host mirrors disagree with the device arrays: fail loudly
+    const int lane = threadIdx.x & 63;
+    for (int d = lane; d < D; d += 64) out[row * D + d] = 0x7FC0;   // bf16 NaN
+    if (out_lse && lane == 0) out_lse[row] = __builtin_nanf("");
+    return;
+  }
   const int f = (int)(row / plan.Hq);
   const int h = (int)(row % plan.Hq);
   const ItemParts P = prefix_parts_of_row(plan, f, h);
@@ -116,16 +192,18 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan, const 
   };
   auto po = [&](int p) { return p < np ? ws + slot_ptr(P, p, false) : ws + slot_ptr(S, p - np, false); };
   auto pl = [&](int p) { return p < np ? ws[slot_ptr(P, p, true)] : ws[slot_ptr(S, p - np, true)]; };
-  merge_row<D / 64>(np + ns, D, po, pl, out + row * D, true, out_lse ? out_lse + row : nullptr);
+  merge_row_v4<D>(np + ns, po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
-hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
+hipError_t launch_fork_merge(const Plan& plan, const IndexArrays& ix, const float* ws, void* out, float* out_lse,
+                             hipStream_t stream) {
   const int64_t rows = (int64_t)plan.N * plan.Hq;
   const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  const PlanHead& h = plan;
   if (plan.D == 128)
-    hipLaunchKernelGGL(fork_merge_kernel<128>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    hipLaunchKernelGGL(fork_merge_kernel<128>, grid, block, 0, stream, h, ix, ws, (uint16_t*)out, out_lse);
   else
-    hipLaunchKernelGGL(fork_merge_kernel<64>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    hipLaunchKernelGGL(fork_merge_kernel<64>, grid, block, 0, stream, h, ix, ws, (uint16_t*)out, out_lse);
   return hipGetLastError();
 }
 

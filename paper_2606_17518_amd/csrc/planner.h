@@ -20,6 +20,8 @@ struct PlanInputs {
   const int32_t* fork_off;    // [T+1]
   const int32_t* prefix_len;  // [T]
   const int32_t* suffix_len;  // [N]
+  const int32_t* prefix_table_off;  // [T+1]
+  const int32_t* suffix_table_off;  // [N+1]
   int tt[2];                  // tokens per tile, per partition
   int rbs[2];                 // rows per row block
   int item_cap[2];            // max items per worker
@@ -68,6 +70,9 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   plan->policy = in.policy;
   for (int t = 0; t <= T; ++t) plan->fork_off[t] = fo[t];
   for (int t = 0; t < T; ++t) plan->prefix_len[t] = in.prefix_len[t];
+  for (int t = 0; t <= T; ++t) plan->prefix_table_off[t] = in.prefix_table_off[t];
+  for (int f = 0; f < N; ++f) plan->suffix_len[f] = in.suffix_len[f];
+  for (int f = 0; f <= N; ++f) plan->suffix_table_off[f] = in.suffix_table_off[f];
   const int xs = part_of_suffix(in.policy);
 
   // prefix items, traces grouped by partition

@@ -1,7 +1,8 @@
 // worker.h -- the part of a worker (workgroup) that both attention kernels
-// share: list the items its tile range touches, fetch their lengths and table
-// offsets, and gather the block id of every 16-token block the range reads.
-// Everything lands in LDS so the tile loop never waits on a dependent load.
+// share: list the items its tile range touches (with their lengths and table
+// offsets, from the plan in LDS), and gather the block id of every 16-token
+// block the range reads.  Everything lands in LDS so the tile loop never
+// waits on a dependent load.
 #pragma once
 #include "common.h"
 #include "plan.h"
@@ -24,9 +25,11 @@ struct WorkerRange {
 
 // All threads of the block call this; `items` holds item_cap descriptors and
 // `ids` holds tile_cap * ids_per_tile block ids.
+// If `scales` is not null (E4M3 KV), scales[e] / scales[cap + e] receive the
+// k / v block scale of ids[e], where cap = tile_cap * ids_per_tile.
 template <int kThreads, int kItemCap, int kIdsPerTile, int kTileCap>
 __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
-                                      int32_t* ids) {
+                                      int32_t* ids, float* scales = nullptr) {
   const PartPlan& pp = plan.part[part];
   const int tid = threadIdx.x;
   const int64_t x0 = worker_start(pp, w);
@@ -36,7 +39,7 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
   wr.first_ord = 0;
   wr.R = 0;
   if (x1 <= x0) return wr;
-  // 1. walk the range item by item (identical in every thread)
+  // 1. walk the range item by item (identical in every thread; `plan` is in LDS)
   int64_t x = x0;
   int rt = 0;
   while (x < x1 && wr.nitems < kItemCap) {
@@ -59,6 +62,10 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
       const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
       d[IT_NROWS] = (rows - r0) < pp.rbs ? (rows - r0) : pp.rbs;
       d[IT_ROW0] = r0;
+      const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+      d[IT_NVALID] = nv;
+      d[IT_TABOFF] = it.kind == 0 ? plan.prefix_table_off[it.t] : plan.suffix_table_off[it.f];
+      d[IT_LASTBLK] = (nv - 1) / 16;
     }
     x += n;
     rt += n;
@@ -67,23 +74,7 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
   // the host sizes workers so the caps hold; never index past them
   wr.R = rt < kTileCap ? rt : kTileCap;
   __syncthreads();
-  // 2. lengths and table offsets
-  if (tid < wr.nitems) {
-    int32_t* d = items + tid * kItemInts;
-    int nv, off;
-    if (d[IT_KIND] == 0) {
-      nv = plan.prefix_len[d[IT_T]];
-      off = a.prefix_table_off[d[IT_T]];
-    } else {
-      nv = a.suffix_len[d[IT_F]];
-      off = a.suffix_table_off[d[IT_F]];
-    }
-    d[IT_NVALID] = nv;
-    d[IT_TABOFF] = off;
-    d[IT_LASTBLK] = (nv - 1) / 16;
-  }
-  __syncthreads();
-  // 3. block ids of every tile of the range, clamped to the item's last valid block
+  // 2. block ids of every tile of the range, clamped to the item's last valid block
   for (int e = tid; e < wr.R * kIdsPerTile; e += kThreads) {
     const int r = e / kIdsPerTile;
     const int b = e % kIdsPerTile;
@@ -93,7 +84,12 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
     int bi = (d[IT_TILE0] + (r - d[IT_RTILE0])) * kIdsPerTile + b;
     if (bi > d[IT_LASTBLK]) bi = d[IT_LASTBLK];
     const int32_t* tab = d[IT_KIND] == 0 ? a.prefix_table : a.suffix_table;
-    ids[e] = tab[d[IT_TABOFF] + bi];
+    const int id = tab[d[IT_TABOFF] + bi];
+    ids[e] = id;
+    if (scales) {
+      scales[e] = a.k_scale[id];
+      scales[kTileCap * kIdsPerTile + e] = a.v_scale[id];
+    }
   }
   __syncthreads();
   return wr;

@@ -196,9 +196,14 @@ int main(int argc, char** argv) {
     std::vector<int32_t> S(in.N);
     const int smax = U(0, 1) ? 2100 : 40;
     for (int f = 0; f < in.N; ++f) S[f] = U(0, 3) == 0 ? 0 : U(0, smax);
+    std::vector<int32_t> pto(in.T + 1, 0), sto(in.N + 1, 0);
+    for (int t = 0; t < in.T; ++t) pto[t + 1] = pto[t] + (P[t] + 15) / 16;
+    for (int f = 0; f < in.N; ++f) sto[f + 1] = sto[f] + (S[f] + 15) / 16;
     in.fork_off = fo.data();
     in.prefix_len = P.data();
     in.suffix_len = S.data();
+    in.prefix_table_off = pto.data();
+    in.suffix_table_off = sto.data();
     in.tt[0] = in.D == 128 ? 64 : 128;
     in.tt[1] = 64;
     in.rbs[0] = 128;

@@ -44,8 +44,10 @@ def _host_batch(**kw):
     for f in ("q", "k_pool", "v_pool", "fork_off", "prefix_len", "prefix_table_off", "prefix_table",
               "suffix_len", "suffix_table_off", "suffix_table"):
         setattr(s, f, fake)
-    keep = [np.array([0, 2], np.int32), np.array([20], np.int32), np.array([3, 0], np.int32)]
-    s.fork_off_h, s.prefix_len_h, s.suffix_len_h = (a.ctypes.data for a in keep)
+    keep = [np.array([0, 2], np.int32), np.array([20], np.int32), np.array([3, 0], np.int32),
+            np.array([0, 2], np.int32), np.array([0, 1, 1], np.int32)]
+    s.fork_off_h, s.prefix_len_h, s.suffix_len_h, s.prefix_table_off_h, s.suffix_table_off_h = \
+        (a.ctypes.data for a in keep)
     for k, v in kw.items():
         setattr(s, k, v)
     return s, keep
@@ -55,6 +57,7 @@ def _host_batch(**kw):
     ("num_traces", 0, 1), ("num_forks", 0, 1), ("num_q_heads", 7, 1), ("head_dim", 96, 2),
     ("block_size", 32, 2), ("sm_scale", 0.0, 1), ("sm_scale", float("nan"), 1), ("kv_dtype", 5, 2),
     ("path", 9, 1), ("reserved", 1, 1), ("q", None, 1), ("suffix_len_h", None, 1), ("num_blocks", 0, 1),
+    ("suffix_table_off_h", None, 1), ("prefix_table_off_h", None, 1),
 ])
 def test_bad_batch_rejected_without_launch(L, field, value, status):
     s, keep = _host_batch(**{field: value})
