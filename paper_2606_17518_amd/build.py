@@ -16,7 +16,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
-SOURCES = ["abi.hip", "attn_mfma.hip", "attn_dot.hip", "merge.hip", "kv_import.hip"]
+SOURCES = ["abi.hip", "attn_mfma.hip", "attn_mfma2.hip", "attn_dot.hip", "merge.hip", "kv_import.hip"]
+# Per-source device flags: the eight-wave kernel keeps MFMA accumulators in VGPRs.
+EXTRA_FLAGS = {"attn_mfma2.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _hipcc() -> str:
@@ -40,7 +42,7 @@ def build(verbose: bool = False) -> str:
 
     def one(src: str) -> str:
         obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
-        cmd = [hipcc, *flags, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc, *flags, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

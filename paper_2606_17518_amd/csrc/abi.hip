@@ -88,7 +88,7 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.rbs[1] = dot_rows();
   in.item_cap[0] = mfma_item_cap();
   in.item_cap[1] = dot_item_cap();
-  in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128);
+  in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128, fp8);
   in.tile_cap[1] = dot_tile_cap(in.D);
   char err[256];
   const int rc = plan_build(in, [] { return device_cus(); }, plan, ws_floats, err, sizeof err);

@@ -19,6 +19,7 @@
 // dims x 32 tokens from the transposing LDS read, B = P^T) without a shuffle.
 // Online softmax in fp32 per row; each worker writes one normalised partial
 // (o, lse) per item it touched, merged later by the log-sum-exp rule.
+#include "kernels.h"
 #include "worker.h"
 
 namespace specgen {
@@ -55,14 +56,6 @@ struct MfmaCfg {
   static_assert(kLoads * 16 * kThreads == kTileB, "tile must split evenly over threads");
   static_assert(kLdsBytes <= 163840, "LDS budget");
 };
-
-// LDS swizzles: K chunks are XOR-ed so a 16-key MFMA operand read hits
-// distinct banks; V chunks are XOR-ed by even values (8-byte halves stay
-// together) so the 4 keys of a transposing read hit distinct 32-byte groups.
-template <int CPR>
-__device__ __forceinline__ int swz_k(int tok) { return ((tok & 3) | ((tok >> 1) & 12)) & (CPR - 1); }
-template <int CPR>
-__device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >> 1) & 4))) & (CPR - 1); }
 
 template <int D, bool FP8>
 __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const PlanHead head) {
@@ -423,11 +416,15 @@ int mfma_tile_tokens(int D, bool fp8) {
   return D == 128 ? MfmaCfg<128, false>::kTT : MfmaCfg<64, false>::kTT;
 }
 int mfma_item_cap() { return MfmaCfg<128, false>::kItemCap; }
-int mfma_tile_cap(int D) { return D == 128 ? MfmaCfg<128, false>::kTileCap : MfmaCfg<64, false>::kTileCap; }
+// bf16 KV runs on the eight-wave kernel (attn_mfma2.hip), which has no per-worker tile cap.
+int mfma_tile_cap(int D, bool fp8) {
+  if (!fp8) return 1 << 24;
+  return D == 128 ? MfmaCfg<128, true>::kTileCap : MfmaCfg<64, true>::kTileCap;
+}
 
 hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream) {
-  if (plan.D == 128) return fp8 ? launch_attn_mfma_t<128, true>(a, plan, stream) : launch_attn_mfma_t<128, false>(a, plan, stream);
-  return fp8 ? launch_attn_mfma_t<64, true>(a, plan, stream) : launch_attn_mfma_t<64, false>(a, plan, stream);
+  if (!fp8) return launch_attn_mfma2(a, plan, stream);
+  return plan.D == 128 ? launch_attn_mfma_t<128, true>(a, plan, stream) : launch_attn_mfma_t<64, true>(a, plan, stream);
 }
 
 }  // namespace specgen

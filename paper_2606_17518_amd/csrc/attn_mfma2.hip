@@ -1,0 +1,477 @@
+// attn_mfma2.hip -- the bf16 shared-prefix (and suffix) partial-attention
+// kernel on gfx950 matrix cores: eight waves per workgroup, tiles streamed
+// from HBM straight into LDS.
+//
+// One workgroup = one worker of the MFMA partition (plan.h).  It walks its
+// range of work items; an item's rows are every (fork, q head) pair of a GQA
+// group of one trace (prefix item: the trace's shared prefix is read from HBM
+// once for all its forks, Sec. 4.2 / Sec. 8.7) or the g heads of one fork
+// (suffix item).
+//
+// Slots.  The worker's range is a sequence of 32 KiB slots: for each item one
+// "q slot" (the item's query rows, up to 128 x D bf16) followed by its tiles
+// (TT tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
+// stages with three slots in flight.  Every wave moves exactly four 1 KiB
+// pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no VGPR
+// staging), so the number of vector-memory operations a wave has in flight
+// is known exactly and the wait for slot s is "vmcnt <= 4 x (slots issued
+// after s) + partial stores issued since".  These loads are issued from
+// inline asm: the compiler does not see them, so it neither drains them
+// (vmcnt(0)) before LDS reads nor reorders them across the LDS barriers.
+//
+// Rows and tokens.  An item with r rows uses row groups of 16 (r <= 64) or 32
+// (r > 64) rows, RG = ceil(r / rows per group) <= 4 of them, and splits each
+// tile's tokens over TG = min(TT/32, 8/RG) token groups: wave w computes row
+// group w % RG over token group w / RG (two waves per SIMD for the 128-row
+// prefix items, so one wave's softmax overlaps the other's MFMAs).  At the
+// item's end the token groups are combined through the stage that was just
+// consumed, and token group 0 writes the normalised partial (o, lse).
+//
+// The accumulators live in VGPRs: this file is compiled with MFMA operands and
+// results in VGPRs (-amdgpu-mfma-vgpr-form), which leaves the whole 256-register
+// budget of a two-waves-per-SIMD kernel to one register file.
+//
+// Math per 32-token slab and 16-row tile (as in the four-wave kernel):
+// S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with keys taken so that each lane's
+// scores are the 8 consecutive tokens the PV operand needs, online softmax in
+// base 2 with lazy rescaling, O^T += V^T P^T with V^T from ds_read_b64_tr_b16.
+#include "worker.h"
+
+namespace specgen {
+namespace mfma2 {
+
+// The running max moves only when a new score would give a probability above
+// 2^kRescaleLog2 relative to it.
+constexpr float kRescaleLog2 = 8.f;
+
+template <int D>
+struct Cfg {
+  static constexpr int kThreads = 512;
+  static constexpr int kWaves = 8;
+  static constexpr int kTT = (D == 128) ? 64 : 128;   // tokens per tile
+  static constexpr int kRowB = D * 2;                 // bytes per token (or q) row
+  static constexpr int kCPR = kRowB / 16;             // 16-byte chunks per row
+  static constexpr int kTileB = kTT * kRowB;          // K (or V) bytes of a tile
+  static constexpr int kStageB = 2 * kTileB;          // one slot
+  static constexpr int kStages = 4;
+  static constexpr int kRPI = 1024 / kRowB;           // rows moved by one wave instruction
+  static constexpr int kDmaT = kTileB / 1024 / kWaves;  // instructions per wave per tensor
+  static constexpr int kDmaSlot = 4;                  // instructions per wave per slot
+  static constexpr int kItemCap = 64;
+  static constexpr int kMaxRows = 128;                // rows per item (row block)
+  static constexpr int kOffItems = kStages * kStageB;
+  static constexpr int kOffML = kOffItems + kItemCap * kItemInts * 4;
+  static constexpr int kMLBytes = kWaves * 2 * 64 * 2 * 4;   // [wave][nt][lane] (m, l)
+  static constexpr int kLdsBytes = kOffML + kMLBytes;
+  static_assert(kDmaT * 2 == kDmaSlot, "a tile slot is four instructions per wave");
+  static_assert(kDmaT * kWaves * 1024 == kTileB, "tile split over the waves");
+  static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
+  static_assert(kMaxRows / kRPI <= kDmaSlot * kWaves, "q slot split over the waves");
+};
+
+// Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
+// touches land in distinct banks.
+template <int D>
+__device__ __forceinline__ int swz_q(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
+
+// One wave instruction: 64 lanes x 16 bytes from gbase + voff (per lane) into
+// LDS at lds_addr + 16 * lane.  gbase and lds_addr must be wave-uniform.
+__device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gbase), "s"(lds_addr) : "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Wait until at most n vector-memory operations of this wave are outstanding;
+// n is rounded down to an available immediate, which only waits longer.
+__device__ __forceinline__ void vm_wait_le(int n) {
+  if (n == 8) vm_wait<8>();
+  else if (n >= 32) {
+    if (n >= 63) vm_wait<63>();
+    else if (n >= 48) vm_wait<48>();
+    else if (n >= 40) vm_wait<40>();
+    else vm_wait<32>();
+  } else if (n >= 16) {
+    if (n >= 28) vm_wait<28>();
+    else if (n >= 24) vm_wait<24>();
+    else if (n >= 20) vm_wait<20>();
+    else vm_wait<16>();
+  } else if (n >= 12) vm_wait<12>();
+  else if (n >= 8) vm_wait<8>();
+  else if (n >= 4) vm_wait<4>();
+  else vm_wait<0>();
+}
+
+}  // namespace mfma2
+
+template <int D>
+__global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, const PlanHead head) {
+  using namespace mfma2;
+  using C = Cfg<D>;
+  constexpr int TT = C::kTT;
+  constexpr int CPR = C::kCPR;
+  constexpr int KS = D / 32;   // k-steps of S^T
+  constexpr int DT = D / 16;   // d-tiles of O^T
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLdsBytes];
+  __shared__ Plan splan;
+  plan_build_lds<512>(head, a.ix, splan);
+  const Plan& plan = splan;
+  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
+  int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
+  float* ml = reinterpret_cast<float*>(lds + C::kOffML);
+
+  const PartPlan& pp = plan.part[kPartMfma];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = uniform(tid >> 6);
+  const int w = blockIdx.x;
+  const WorkerRange wr = worker_items<C::kItemCap>(plan, kPartMfma, w, items);
+  const int R = wr.R;
+  const int first_ord = wr.first_ord;
+  if (R <= 0) return;
+  const int S = R + wr.nitems;   // slots: a q slot per item, then its tiles
+  const uint32_t lds_base = (uint32_t)(size_t)((SG_LDS uint8_t*)lds);
+
+  auto field = [&](int ii, int f) { return uniform(items[ii * kItemInts + f]); };
+
+  // ---- issue side ------------------------------------------------------------
+  const int64_t head_stride = (int64_t)D * 2;                  // bytes between kv heads of a token
+  const uint32_t tok_stride = (uint32_t)(plan.Hkv * head_stride);  // bytes between tokens of a block
+  const int64_t blk_stride = 16 * (int64_t)tok_stride;
+  // this wave's blocks within a tile: tokens [16 * wblk, +16) of the tile hold
+  // both of its K (and V) instructions
+  const int wblk = (D == 128) ? (wave >> 1) : wave;
+  int tit[2], kch[2], vch[2];   // lane constants: token within the tile, swizzled source chunk
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int n = wave * 2 + i;
+    tit[i] = n * C::kRPI + lane / CPR;
+    const int p = lane % CPR;
+    kch[i] = p ^ swz_k<CPR>(tit[i]);
+    vch[i] = p ^ swz_v<CPR>(tit[i]);
+  }
+  typedef const __attribute__((address_space(4))) int32_t* cint_ptr;
+  // block index (within the item) and physical id of this wave's block of tile k of item ii
+  auto wave_block = [&](int ii, int k) {
+    const int bi = (field(ii, IT_TILE0) + k) * (TT / 16) + wblk;
+    const int last = field(ii, IT_LASTBLK);
+    return bi < last ? bi : last;
+  };
+  auto block_id = [&](int ii, int k) -> int {
+    const cint_ptr tab = (cint_ptr)(field(ii, IT_KIND) == 0 ? a.prefix_table : a.suffix_table);
+    return tab[field(ii, IT_TABOFF) + wave_block(ii, k)];
+  };
+  auto issue_slot = [&](int ii, int k, int id, int stage) {
+    const uint32_t st = lds_base + (uint32_t)(stage * C::kStageB);
+    if (k < 0) {
+      // q rows of the item (rows past its end repeat its last row)
+      const int32_t* d = items + ii * kItemInts;
+      const int nrows = field(ii, IT_NROWS);
+#pragma unroll
+      for (int i = 0; i < C::kDmaSlot; ++i) {
+        const int n = wave * C::kDmaSlot + i;
+        const int row = (n * C::kRPI + lane / CPR) & (C::kMaxRows - 1);
+        const int rr = row < nrows ? row : nrows - 1;
+        int fork = 0, hq = 0;
+        item_row(plan, d, rr, &fork, &hq);
+        const int chunk = (lane % CPR) ^ swz_q<D>(row);
+        const uint32_t voff = (uint32_t)(((int64_t)fork * plan.Hq + hq) * head_stride) + (uint32_t)(chunk * 16);
+        dma16(a.q, voff, st + (uint32_t)(n * 1024));
+      }
+    } else {
+      const int j = field(ii, IT_J);
+      const int nv = field(ii, IT_NVALID);
+      const int tile = field(ii, IT_TILE0) + k;
+      const int bi = wave_block(ii, k);
+      const uint8_t* kb = a.k_pool + (int64_t)id * blk_stride + j * head_stride;
+      const uint8_t* vb = a.v_pool + (int64_t)id * blk_stride + j * head_stride;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        int tok = tile * TT + tit[i];
+        tok = tok < nv ? tok : nv - 1;   // tokens past the end re-read the last valid one
+        const uint32_t row_off = (uint32_t)(tok - bi * 16) * tok_stride;
+        const int n = wave * 2 + i;
+        dma16(kb, row_off + (uint32_t)(kch[i] * 16), st + (uint32_t)(n * 1024));
+        dma16(vb, row_off + (uint32_t)(vch[i] * 16), st + (uint32_t)(C::kTileB + n * 1024));
+      }
+    }
+  };
+
+  // ---- compute side ------------------------------------------------------------
+  const int G = lane >> 4;     // 16-lane group
+  const int ln = lane & 15;    // row within an N-tile / key within an S^T tile
+  const int k_lane_tok = 8 * (ln >> 2) + (ln & 3);
+  const int k_lane_swz = swz_k<CPR>(k_lane_tok);
+  const int v_lane_tok = 8 * G + (ln >> 2);
+  const int v_lane_swz0 = swz_v<CPR>(v_lane_tok);
+  const int v_lane_swz1 = swz_v<CPR>(v_lane_tok + 4);
+  const int vsub = ln & 3;
+  bf16x8 qop[2][KS];
+  f32x4 acc[2][DT];
+  float m_run[2], l_run[2];
+  int NT = 1, RG = 1, TG = 1, rg = 0, tg = 0;
+  bool active = false;
+
+  auto begin_item = [&](int ii, int stage) {
+    const int nrows = field(ii, IT_NROWS);
+    NT = nrows > 64 ? 2 : 1;
+    const int RS = 16 * NT;
+    RG = (nrows + RS - 1) / RS;
+    TG = (TT / 32) < (C::kWaves / RG) ? (TT / 32) : (C::kWaves / RG);
+    rg = wave % RG;
+    tg = wave / RG;
+    active = wave < RG * TG;
+    const SG_LDS uint8_t* qb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      if (nt < NT) {
+        const int row = rg * RS + nt * 16 + ln;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int slot = (ks * 4 + G) ^ swz_q<D>(row);
+          qop[nt][ks] = *reinterpret_cast<const SG_LDS bf16x8*>(qb + row * C::kRowB + slot * 16);
+        }
+      }
+      m_run[nt] = -INFINITY;
+      l_run[nt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+
+  // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
+  auto slab = [&](auto nt_c, int stage, int sb, int valid) {
+    constexpr int NTc = decltype(nt_c)::value;
+    const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
+    const SG_LDS uint8_t* vb = kb + C::kTileB;
+    f32x4 s[2][NTc];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int nt = 0; nt < NTc; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
+    const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cho = (((4 * ks + G) ^ k_lane_swz) << 4);
+      const bf16x8 A0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
+      const bf16x8 A1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
+#pragma unroll
+      for (int nt = 0; nt < NTc; ++nt) {
+        s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, qop[nt][ks], s[0][nt], 0, 0, 0);
+        s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, qop[nt][ks], s[1][nt], 0, 0, 0);
+      }
+    }
+    // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
+    if (sb + 32 > valid) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (sb + 8 * G + 4 * u + e >= valid) {
+#pragma unroll
+            for (int nt = 0; nt < NTc; ++nt) s[u][nt][e] = -INFINITY;
+          }
+    }
+    bf16x8 pop[NTc];
+#pragma unroll
+    for (int nt = 0; nt < NTc; ++nt) {
+      float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                       fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+      mx = rows4_max(mx);
+      // lazy rescaling: the reference max only moves when a score exceeds it
+      // by more than 2^kRescaleLog2 in probability (wave-uniform decision)
+      if (__builtin_amdgcn_ballot_w64(mx * a.c_log2 > m_run[nt] * a.c_log2 + kRescaleLog2)) {
+        const float m_new = fmaxf(m_run[nt], mx);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[nt] - m_new) * a.c_log2);
+        m_run[nt] = m_new;
+        l_run[nt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
+      }
+      const float mc = m_run[nt] * a.c_log2;
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(fmaf(s[0][nt][e], a.c_log2, -mc));
+        p[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][nt][e], a.c_log2, -mc));
+      }
+      l_run[nt] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+      u32x4 pk;
+      pk[0] = pack_bf16x2(p[0], p[1]);
+      pk[1] = pack_bf16x2(p[2], p[3]);
+      pk[2] = pack_bf16x2(p[4], p[5]);
+      pk[3] = pack_bf16x2(p[6], p[7]);
+      pop[nt] = __builtin_bit_cast(bf16x8, pk);
+    }
+    // O^T += V^T P^T ; the transposing read gives lane (G, ln) V[sb+8G+4h+e][16dt+ln]
+    const SG_LDS uint8_t* v_row0 = vb + (sb + v_lane_tok) * C::kRowB;
+    const SG_LDS uint8_t* v_row1 = v_row0 + 4 * C::kRowB;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int ch = 2 * dt + (vsub >> 1);
+      const int off0 = ((ch ^ v_lane_swz0) << 4) + ((vsub & 1) << 3);
+      const int off1 = ((ch ^ v_lane_swz1) << 4) + ((vsub & 1) << 3);
+      const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row0 + off0));
+      const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row1 + off1));
+      const bf16x8 A = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+      for (int nt = 0; nt < NTc; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
+    }
+  };
+
+  auto compute_tile = [&](int ii, int k, int stage) {
+    if (!active) return;
+    const int tile = field(ii, IT_TILE0) + k;
+    const int rem = field(ii, IT_NVALID) - tile * TT;
+    const int valid = rem < TT ? rem : TT;
+    const int ntok = TT / TG;
+    const int tok0 = tg * ntok;
+    for (int sb = tok0; sb < tok0 + ntok && sb < valid; sb += 32) {
+      if (NT == 2) slab(std::integral_constant<int, 2>(), stage, sb, valid);
+      else slab(std::integral_constant<int, 1>(), stage, sb, valid);
+    }
+  };
+
+  // Combine the token groups of the item through the stage just consumed and
+  // write token group 0's normalised partial.  Every wave calls this (it has
+  // barriers); returns the number of vector-memory stores this wave issued.
+  auto finish_item = [&](int ii, int stage) -> int {
+    float lrow[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) lrow[nt] = rows4_sum(l_run[nt]);
+    if (TG > 1) {
+      float* cb = reinterpret_cast<float*>(lds + stage * C::kStageB);
+      const int wave_bytes = NT * DT * 64 * 16;
+      const int per_round = C::kStageB / wave_bytes;      // writers whose accumulators fit at once
+      const int writers = (TG - 1) * RG;
+      const int rounds = (writers + per_round - 1) / per_round;
+      const int windex = (tg - 1) * RG + rg;              // this wave as a writer (tg >= 1)
+      for (int r = 0; r < rounds; ++r) {
+        lds_barrier();
+        if (active && tg >= 1 && windex / per_round == r) {
+          float* dst = cb + (windex % per_round) * (wave_bytes / 4);
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt)
+            if (nt < NT) {
+#pragma unroll
+              for (int dt = 0; dt < DT; ++dt)
+                *reinterpret_cast<f32x4*>(dst + ((nt * DT + dt) * 64 + lane) * 4) = acc[nt][dt];
+              ml[((wave * 2 + nt) * 64 + lane) * 2 + 0] = m_run[nt];
+              ml[((wave * 2 + nt) * 64 + lane) * 2 + 1] = lrow[nt];
+            }
+        }
+        lds_barrier();
+        if (active && tg == 0) {
+          for (int t2 = 1; t2 < TG; ++t2) {
+            const int wi = (t2 - 1) * RG + rg;
+            if (wi / per_round != r) continue;
+            const int pw = t2 * RG + rg;   // the partner wave
+            const float* src = cb + (wi % per_round) * (wave_bytes / 4);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+              if (nt < NT) {
+                const float m1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 0];
+                const float l1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 1];
+                const float m = fmaxf(m_run[nt], m1);
+                const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
+                const float a0 = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
+                const float a1 = __builtin_amdgcn_exp2f(m1 * a.c_log2 - mc);
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                  const f32x4 o1 = *reinterpret_cast<const f32x4*>(src + ((nt * DT + dt) * 64 + lane) * 4);
+                  acc[nt][dt] = acc[nt][dt] * a0 + o1 * a1;
+                }
+                lrow[nt] = lrow[nt] * a0 + l1 * a1;
+                m_run[nt] = m;
+              }
+          }
+        }
+      }
+    }
+    if (!(active && tg == 0)) return 0;
+    const int kseg = field(ii, IT_ORD) - first_ord;
+    const int64_t slot = slot_of(pp, w, kseg);
+    if (slot < 0) return 0;
+    float* o = a.ws + pp.o_base + slot * pp.slot_rows * D;
+    float* ls = a.ws + pp.lse_base + slot * pp.slot_rows;
+    const int RS = 16 * NT;
+    int stores = 0;
+    // every lane stores (rows past the item's end land in unused rows of the
+    // slot), so the number of stores is the same on every path
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+      if (nt < NT) {
+        const int row = rg * RS + nt * 16 + ln;
+        const float inv = 1.f / lrow[nt];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G) = acc[nt][dt] * inv;
+        ls[row] = m_run[nt] * a.sm_scale + __logf(lrow[nt]);
+        stores += DT + 1;
+      }
+    return stores;
+  };
+
+  // ---- the slot loop -------------------------------------------------------------
+  auto advance = [&](int& ii, int& k) {
+    if (k + 1 < field(ii, IT_NTILE)) {
+      ++k;
+    } else {
+      ++ii;
+      k = -1;
+    }
+  };
+  int is_ii = 0, is_k = -1, is_id = 0, issued = 0;   // next slot to issue and its block id
+  for (int p = 0; p < 3; ++p) {
+    if (issued < S) {
+      if (is_k >= 0) is_id = block_id(is_ii, is_k);
+      issue_slot(is_ii, is_k, is_id, issued & 3);
+      advance(is_ii, is_k);
+      ++issued;
+    }
+  }
+  if (issued < S && is_k >= 0) is_id = block_id(is_ii, is_k);
+  int st1 = 0, st2 = 0, st3 = 0;   // stores issued one, two and three iterations ago
+  int cp_ii = 0, cp_k = -1;
+  for (int s = 0; s < S; ++s) {
+    // slot s has landed once at most the operations issued after it are
+    // outstanding: the later slots' loads and the stores of the last three
+    // iterations (slot s was issued three iterations ago)
+    vm_wait_le(C::kDmaSlot * (issued - 1 - s) + st1 + st2 + st3);
+    lds_barrier();
+    if (issued < S) {
+      issue_slot(is_ii, is_k, is_id, issued & 3);   // into the stage consumed last iteration
+      advance(is_ii, is_k);
+      ++issued;
+      if (issued < S && is_k >= 0) is_id = block_id(is_ii, is_k);   // used next iteration
+    }
+    const int stage = s & 3;
+    int st0 = 0;
+    if (cp_k < 0) {
+      begin_item(cp_ii, stage);
+    } else {
+      compute_tile(cp_ii, cp_k, stage);
+      if (cp_k == field(cp_ii, IT_NTILE) - 1) st0 = finish_item(cp_ii, stage);
+    }
+    st3 = st2;
+    st2 = st1;
+    st1 = st0;
+    advance(cp_ii, cp_k);
+  }
+}
+
+hipError_t launch_attn_mfma2(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
+  const int W = plan.part[kPartMfma].workers;
+  if (W <= 0) return hipSuccess;
+  if (plan.D == 128)
+    hipLaunchKernelGGL((attn_mfma2_kernel<128>), dim3(W), dim3(512), 0, stream, a, static_cast<const PlanHead&>(plan));
+  else
+    hipLaunchKernelGGL((attn_mfma2_kernel<64>), dim3(W), dim3(512), 0, stream, a, static_cast<const PlanHead&>(plan));
+  return hipGetLastError();
+}
+
+int mfma2_item_cap() { return mfma2::Cfg<128>::kItemCap; }
+
+}  // namespace specgen

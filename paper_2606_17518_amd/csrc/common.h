@@ -85,6 +85,14 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // so the compiler does not place that wait inside the hot loop instead.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// LDS swizzles: K chunks are XOR-ed so a 16-key MFMA operand read hits
+// distinct banks; V chunks are XOR-ed by even values (8-byte halves stay
+// together) so the 4 keys of a transposing read hit distinct 32-byte groups.
+template <int CPR>
+__device__ __forceinline__ int swz_k(int tok) { return ((tok & 3) | ((tok >> 1) & 12)) & (CPR - 1); }
+template <int CPR>
+__device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >> 1) & 4))) & (CPR - 1); }
+
 // Partial-result and plan arguments shared by the attention kernels.
 struct AttnArgs {
   const uint16_t* __restrict__ q;          // [N][Hq][D] bf16 bits

@@ -106,24 +106,26 @@ SG_HD int part_of_suffix(int policy) { return policy == kPolicyDot ? kPartDot : 
 SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) { return (w * pp.tiles) / pp.workers; }
 
 #ifdef __HIPCC__
-// Rebuild the plan's arrays in LDS (all threads of the block call this; the
-// block has 256 threads).  Mirrors the host planner: traces are grouped by
+// Rebuild the plan's arrays in LDS (all kThreads threads of the block call
+// this; kThreads is 256 or 512).  Mirrors the host planner: traces are grouped by
 // partition with running tile / item counts, suffix tiles are an exclusive
 // scan over forks.  Sets p.consistent = 0 if the totals disagree with the
 // host header (host mirrors and device arrays differ).  Ends with a barrier.
+template <int kThreads = 256>
 __device__ __forceinline__ void plan_build_lds(const PlanHead& h, const IndexArrays& ix, Plan& p) {
+  static_assert(kThreads == 256 || kThreads == 512, "block size");
   const int tid = threadIdx.x;
   const int T = h.T, N = h.N;
   if (tid == 0) {
     static_cast<PlanHead&>(p) = h;
     p.consistent = 1;
   }
-  for (int i = tid; i <= T; i += 256) {
+  for (int i = tid; i <= T; i += kThreads) {
     p.fork_off[i] = ix.fork_off[i];
     p.prefix_table_off[i] = ix.prefix_table_off[i];
     if (i < T) p.prefix_len[i] = ix.prefix_len[i];
   }
-  for (int i = tid; i <= N; i += 256) {
+  for (int i = tid; i <= N; i += kThreads) {
     p.suffix_table_off[i] = ix.suffix_table_off[i];
     if (i < N) p.suffix_len[i] = ix.suffix_len[i];
   }
@@ -169,7 +171,7 @@ __device__ __forceinline__ void plan_build_lds(const PlanHead& h, const IndexArr
   const int excl = base + incl - (c0 + c1);
   if (f0 < N) p.tileS[f0] = excl;
   if (f0 + 1 < N) p.tileS[f0 + 1] = excl + c0;
-  if (tid == 255) {
+  if (tid == kThreads - 1) {
     p.tileS[N] = base + incl;
     if ((int64_t)(base + incl) != ps.tiles - ps.prefix_tiles) p.consistent = 0;
   }

@@ -23,30 +23,25 @@ struct WorkerRange {
   int R;          // tiles in the range
 };
 
-// All threads of the block call this; `items` holds item_cap descriptors and
-// `ids` holds tile_cap * ids_per_tile block ids.
-// If `scales` is not null (E4M3 KV), scales[e] / scales[cap + e] receive the
-// k / v block scale of ids[e], where cap = tile_cap * ids_per_tile.
-template <int kThreads, int kItemCap, int kIdsPerTile, int kTileCap>
-__device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
-                                      int32_t* ids, float* scales = nullptr) {
+// The item walk of a worker's tile range: every thread computes the same
+// WorkerRange; thread 0 writes one descriptor per item into `items` (at most
+// kItemCap; the host sizes workers so the cap holds).  No barrier at the end.
+template <int kItemCap>
+__device__ WorkerRange worker_walk(const Plan& plan, int part, int w, int32_t* items) {
   const PartPlan& pp = plan.part[part];
-  const int tid = threadIdx.x;
   const int64_t x0 = worker_start(pp, w);
   const int64_t x1 = worker_start(pp, w + 1);
   WorkerRange wr;
   wr.nitems = 0;
   wr.first_ord = 0;
   wr.R = 0;
-  if (x1 <= x0) return wr;
-  // 1. walk the range item by item (identical in every thread; `plan` is in LDS)
   int64_t x = x0;
   int rt = 0;
   while (x < x1 && wr.nitems < kItemCap) {
     const ItemRef it = locate(plan, part, x);
     const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
     if (wr.nitems == 0) wr.first_ord = it.ord;
-    if (tid == 0) {
+    if (threadIdx.x == 0) {
       int32_t* d = items + wr.nitems * kItemInts;
       d[IT_KIND] = it.kind;
       d[IT_T] = it.t;
@@ -71,6 +66,29 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
     rt += n;
     ++wr.nitems;
   }
+  wr.R = rt;
+  return wr;
+}
+
+// The walk only, ending with a barrier so `items` is visible to every thread.
+template <int kItemCap>
+__device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* items) {
+  const WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items);
+  __syncthreads();
+  return wr;
+}
+
+// All threads of the block call this; `items` holds item_cap descriptors and
+// `ids` holds tile_cap * ids_per_tile block ids.
+// If `scales` is not null (E4M3 KV), scales[e] / scales[cap + e] receive the
+// k / v block scale of ids[e], where cap = tile_cap * ids_per_tile.
+template <int kThreads, int kItemCap, int kIdsPerTile, int kTileCap>
+__device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
+                                      int32_t* ids, float* scales = nullptr) {
+  const int tid = threadIdx.x;
+  WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items);
+  if (wr.R <= 0) return wr;
+  const int rt = wr.R;
   // the host sizes workers so the caps hold; never index past them
   wr.R = rt < kTileCap ? rt : kTileCap;
   __syncthreads();
