@@ -17,8 +17,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
 SOURCES = ["abi.hip", "attn_mfma.hip", "attn_mfma2.hip", "attn_dot.hip", "merge.hip", "kv_import.hip"]
-# Per-source device flags: the eight-wave kernel keeps MFMA accumulators in VGPRs.
-EXTRA_FLAGS = {"attn_mfma2.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# Per-source device flags: the eight-wave kernel keeps MFMA accumulators in VGPRs and
+# runs without IEEE-mode NaN quieting.
+EXTRA_FLAGS = {"attn_mfma2.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mno-amdgpu-ieee", "-fno-honor-nans"]}
 
 
 def _hipcc() -> str:

@@ -132,11 +132,6 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, i
   a.v_pool = static_cast<const uint8_t*>(b->v_pool);
   a.k_scale = b->k_scale;
   a.v_scale = b->v_scale;
-  a.ix.fork_off = b->fork_off;
-  a.ix.prefix_len = b->prefix_len;
-  a.ix.prefix_table_off = b->prefix_table_off;
-  a.ix.suffix_len = b->suffix_len;
-  a.ix.suffix_table_off = b->suffix_table_off;
   a.prefix_table = b->prefix_table;
   a.suffix_table = b->suffix_table;
   a.ws = static_cast<float*>(workspace);
@@ -148,7 +143,7 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, i
     if (plan.part[kPartMfma].workers > 0) e = launch_attn_mfma_any(a, plan, fp8, stream);
     if (e == hipSuccess && plan.part[kPartDot].workers > 0) e = launch_attn_dot_any(a, plan, fp8, stream);
   }
-  if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ix, a.ws, out, out_lse, stream);
+  if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);
   if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

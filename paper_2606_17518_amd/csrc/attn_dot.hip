@@ -41,7 +41,7 @@ struct TokVec {
 };
 
 template <int D, bool FP8>
-__global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, const PlanHead head) {
+__global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, const Plan plan_arg) {
   using C = DotCfg<D, FP8>;
   constexpr int DPL = C::kDPL;
   constexpr int NP = DPL / 2;     // bf16 pairs per lane
@@ -49,9 +49,8 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
   constexpr int TB = C::kTB;
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
   __shared__ Plan splan;
-  plan_build_lds(head, a.ix, splan);
+  plan_to_lds<256>(plan_arg, splan);
   const Plan& plan = splan;
-  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   int32_t* ids = reinterpret_cast<int32_t*>(lds + C::kOffIds);
   const PartPlan& pp = plan.part[kPartDot];
@@ -309,7 +308,7 @@ template <int D, bool FP8>
 hipError_t launch_attn_dot_t(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
   const int W = plan.part[kPartDot].workers;
   if (W <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_dot_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, static_cast<const PlanHead&>(plan));
+  hipLaunchKernelGGL((attn_dot_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, plan);
   return hipGetLastError();
 }
 

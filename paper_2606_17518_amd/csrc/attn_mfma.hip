@@ -58,16 +58,15 @@ struct MfmaCfg {
 };
 
 template <int D, bool FP8>
-__global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const PlanHead head) {
+__global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, const Plan plan_arg) {
   using C = MfmaCfg<D, FP8>;
   constexpr int TT = C::kTT;
   constexpr int KS = D / 32;   // k-steps of S^T
   constexpr int DT = D / 16;   // d-tiles of O^T
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
   __shared__ Plan splan;
-  plan_build_lds(head, a.ix, splan);
+  plan_to_lds<256>(plan_arg, splan);
   const Plan& plan = splan;
-  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   int32_t* ids = reinterpret_cast<int32_t*>(lds + C::kOffIds);
 
@@ -407,7 +406,7 @@ template <int D, bool FP8>
 hipError_t launch_attn_mfma_t(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_mfma_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, static_cast<const PlanHead&>(plan));
+  hipLaunchKernelGGL((attn_mfma_kernel<D, FP8>), dim3(W), dim3(256), 0, stream, a, plan);
   return hipGetLastError();
 }
 
@@ -416,9 +415,9 @@ int mfma_tile_tokens(int D, bool fp8) {
   return D == 128 ? MfmaCfg<128, false>::kTT : MfmaCfg<64, false>::kTT;
 }
 int mfma_item_cap() { return MfmaCfg<128, false>::kItemCap; }
-// bf16 KV runs on the eight-wave kernel (attn_mfma2.hip), which has no per-worker tile cap.
+// bf16 KV runs on the eight-wave kernel (attn_mfma2.hip).
 int mfma_tile_cap(int D, bool fp8) {
-  if (!fp8) return 1 << 24;
+  if (!fp8) return mfma2_tile_cap(D);
   return D == 128 ? MfmaCfg<128, true>::kTileCap : MfmaCfg<64, true>::kTileCap;
 }
 

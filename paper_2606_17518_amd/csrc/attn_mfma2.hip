@@ -29,7 +29,10 @@
 //
 // The accumulators live in VGPRs: this file is compiled with MFMA operands and
 // results in VGPRs (-amdgpu-mfma-vgpr-form), which leaves the whole 256-register
-// budget of a two-waves-per-SIMD kernel to one register file.
+// budget of a two-waves-per-SIMD kernel to one register file.  It is also
+// compiled without IEEE-mode NaN quieting (-mno-amdgpu-ieee -fno-honor-nans):
+// the row maxima would otherwise cost three instructions per element.  Masked
+// scores are -inf, never NaN, and infinities keep their meaning.
 //
 // Math per 32-token slab and 16-row tile (as in the four-wave kernel):
 // S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with keys taken so that each lane's
@@ -62,7 +65,11 @@ struct Cfg {
   static constexpr int kOffItems = kStages * kStageB;
   static constexpr int kOffML = kOffItems + kItemCap * kItemInts * 4;
   static constexpr int kMLBytes = kWaves * 2 * 64 * 2 * 4;   // [wave][nt][lane] (m, l)
-  static constexpr int kLdsBytes = kOffML + kMLBytes;
+  static constexpr int kOffIds = kOffML + kMLBytes;
+  static constexpr int kIdCap = 2048;                 // block ids of a worker's range
+  static constexpr int kIdsPerTile = kTT / 16;
+  static constexpr int kTileCap = kIdCap / kIdsPerTile;
+  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
   static_assert(kDmaT * 2 == kDmaSlot, "a tile slot is four instructions per wave");
   static_assert(kDmaT * kWaves * 1024 == kTileB, "tile split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
@@ -76,8 +83,27 @@ __device__ __forceinline__ int swz_q(int row) { return D == 128 ? (row & 15) : (
 
 // One wave instruction: 64 lanes x 16 bytes from gbase + voff (per lane) into
 // LDS at lds_addr + 16 * lane.  gbase and lds_addr must be wave-uniform.
+// (The readfirstlanes only restate what holds: the compiler cannot always
+// prove these operands uniform, and an SGPR operand must be.)
 __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gbase), "s"(lds_addr) : "m0");
+  const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+  const uint32_t glo = __builtin_amdgcn_readfirstlane((uint32_t)g);
+  const uint32_t ghi = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+  const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gu), "s"(l) : "m0");
+}
+
+// acc *= alpha in place.  Tying the registers in an asm statement keeps the
+// accumulator in the same VGPRs on both sides of the (rare, wave-uniform)
+// rescale branch; written as plain code, the compiler keeps two copies of all
+// accumulators and moves them on every slab.
+__device__ __forceinline__ void scale_acc_v(f32x4& acc, float alpha) {
+  float x0 = acc[0], x1 = acc[1], x2 = acc[2], x3 = acc[3];
+  asm volatile("v_mul_f32 %0, %0, %4\n\tv_mul_f32 %1, %1, %4\n\tv_mul_f32 %2, %2, %4\n\tv_mul_f32 %3, %3, %4"
+               : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3)
+               : "v"(alpha));
+  acc = f32x4{x0, x1, x2, x3};
 }
 
 template <int N>
@@ -106,7 +132,7 @@ __device__ __forceinline__ void vm_wait_le(int n) {
 }  // namespace mfma2
 
 template <int D>
-__global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, const PlanHead head) {
+__global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, const Plan plan_arg) {
   using namespace mfma2;
   using C = Cfg<D>;
   constexpr int TT = C::kTT;
@@ -115,9 +141,8 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   constexpr int DT = D / 16;   // d-tiles of O^T
   __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLdsBytes];
   __shared__ Plan splan;
-  plan_build_lds<512>(head, a.ix, splan);
+  plan_to_lds<512>(plan_arg, splan);
   const Plan& plan = splan;
-  if (!plan.consistent) return;   // host mirrors disagree with the device arrays
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   float* ml = reinterpret_cast<float*>(lds + C::kOffML);
 
@@ -133,7 +158,33 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   const int S = R + wr.nitems;   // slots: a q slot per item, then its tiles
   const uint32_t lds_base = (uint32_t)(size_t)((SG_LDS uint8_t*)lds);
 
-  auto field = [&](int ii, int f) { return uniform(items[ii * kItemInts + f]); };
+  // Item descriptors are read from LDS once per item and kept in scalar registers.
+  struct Desc {
+    int kind, t, f, j, ord, tile0, ntile, nv, taboff, nrows, row0, lastblk, rtile0;
+  };
+  auto load_desc = [&](int ii) {
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    const SG_LDS i32x4* p = reinterpret_cast<const SG_LDS i32x4*>((SG_LDS uint8_t*)lds + C::kOffItems + ii * kItemInts * 4);
+    const i32x4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
+    static_assert(IT_KIND == 0 && IT_T == 1 && IT_F == 2 && IT_J == 3 && IT_ORD == 5 && IT_TILE0 == 6 &&
+                  IT_NTILE == 7 && IT_NVALID == 8 && IT_TABOFF == 9 && IT_NROWS == 10 && IT_ROW0 == 11 &&
+                  IT_RTILE0 == 12 && IT_LASTBLK == 14, "descriptor layout");
+    Desc d;
+    d.kind = uniform(v0[0]);
+    d.t = uniform(v0[1]);
+    d.f = uniform(v0[2]);
+    d.j = uniform(v0[3]);
+    d.ord = uniform(v1[1]);
+    d.tile0 = uniform(v1[2]);
+    d.ntile = uniform(v1[3]);
+    d.nv = uniform(v2[0]);
+    d.taboff = uniform(v2[1]);
+    d.nrows = uniform(v2[2]);
+    d.row0 = uniform(v2[3]);
+    d.lastblk = uniform(v3[2]);
+    d.rtile0 = uniform(v3[0]);
+    return d;
+  };
 
   // ---- issue side ------------------------------------------------------------
   const int64_t head_stride = (int64_t)D * 2;                  // bytes between kv heads of a token
@@ -151,49 +202,63 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     kch[i] = p ^ swz_k<CPR>(tit[i]);
     vch[i] = p ^ swz_v<CPR>(tit[i]);
   }
-  typedef const __attribute__((address_space(4))) int32_t* cint_ptr;
-  // block index (within the item) and physical id of this wave's block of tile k of item ii
-  auto wave_block = [&](int ii, int k) {
-    const int bi = (field(ii, IT_TILE0) + k) * (TT / 16) + wblk;
-    const int last = field(ii, IT_LASTBLK);
-    return bi < last ? bi : last;
+  // lane offsets within the block for a tile whose tokens are all valid
+  uint32_t kofs[2], vofs[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    kofs[i] = (uint32_t)(tit[i] & 15) * tok_stride + (uint32_t)(kch[i] * 16);
+    vofs[i] = (uint32_t)(tit[i] & 15) * tok_stride + (uint32_t)(vch[i] * 16);
+  }
+  // block index (within the item) of this wave's block of tile k, clamped to the last valid block
+  auto wave_block = [&](const Desc& d, int k) {
+    const int bi = (d.tile0 + k) * (TT / 16) + wblk;
+    return bi < d.lastblk ? bi : d.lastblk;
   };
-  auto block_id = [&](int ii, int k) -> int {
-    const cint_ptr tab = (cint_ptr)(field(ii, IT_KIND) == 0 ? a.prefix_table : a.suffix_table);
-    return tab[field(ii, IT_TABOFF) + wave_block(ii, k)];
-  };
-  auto issue_slot = [&](int ii, int k, int id, int stage) {
+  // physical id of that block, from the ids the worker gathered into LDS
+  const int32_t* ids = reinterpret_cast<const int32_t*>(lds + C::kOffIds);
+  auto block_id = [&](const Desc& d, int k) -> int { return uniform(ids[(d.rtile0 + k) * C::kIdsPerTile + wblk]); };
+  auto issue_slot = [&](const Desc& d, int k, int id, int stage) {
     const uint32_t st = lds_base + (uint32_t)(stage * C::kStageB);
     if (k < 0) {
       // q rows of the item (rows past its end repeat its last row)
-      const int32_t* d = items + ii * kItemInts;
-      const int nrows = field(ii, IT_NROWS);
 #pragma unroll
       for (int i = 0; i < C::kDmaSlot; ++i) {
         const int n = wave * C::kDmaSlot + i;
         const int row = (n * C::kRPI + lane / CPR) & (C::kMaxRows - 1);
-        const int rr = row < nrows ? row : nrows - 1;
+        const int rr = row < d.nrows ? row : d.nrows - 1;
         int fork = 0, hq = 0;
-        item_row(plan, d, rr, &fork, &hq);
+        item_row_fork_head(plan, d.kind, d.t, d.f, d.j, d.row0, rr, &fork, &hq);
         const int chunk = (lane % CPR) ^ swz_q<D>(row);
         const uint32_t voff = (uint32_t)(((int64_t)fork * plan.Hq + hq) * head_stride) + (uint32_t)(chunk * 16);
         dma16(a.q, voff, st + (uint32_t)(n * 1024));
       }
     } else {
-      const int j = field(ii, IT_J);
-      const int nv = field(ii, IT_NVALID);
-      const int tile = field(ii, IT_TILE0) + k;
-      const int bi = wave_block(ii, k);
-      const uint8_t* kb = a.k_pool + (int64_t)id * blk_stride + j * head_stride;
-      const uint8_t* vb = a.v_pool + (int64_t)id * blk_stride + j * head_stride;
+      const int tile = d.tile0 + k;
+      const uint8_t* kb = a.k_pool + (int64_t)id * blk_stride + d.j * head_stride;
+      const uint8_t* vb = a.v_pool + (int64_t)id * blk_stride + d.j * head_stride;
+      uint32_t ko[2], vo[2];
+      if ((tile + 1) * TT <= d.nv) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          ko[i] = kofs[i];
+          vo[i] = vofs[i];
+        }
+      } else {
+        const int bi = wave_block(d, k);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          int tok = tile * TT + tit[i];
+          tok = tok < d.nv ? tok : d.nv - 1;   // tokens past the end re-read the last valid one
+          const uint32_t row_off = (uint32_t)(tok - bi * 16) * tok_stride;
+          ko[i] = row_off + (uint32_t)(kch[i] * 16);
+          vo[i] = row_off + (uint32_t)(vch[i] * 16);
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        int tok = tile * TT + tit[i];
-        tok = tok < nv ? tok : nv - 1;   // tokens past the end re-read the last valid one
-        const uint32_t row_off = (uint32_t)(tok - bi * 16) * tok_stride;
         const int n = wave * 2 + i;
-        dma16(kb, row_off + (uint32_t)(kch[i] * 16), st + (uint32_t)(n * 1024));
-        dma16(vb, row_off + (uint32_t)(vch[i] * 16), st + (uint32_t)(C::kTileB + n * 1024));
+        dma16(kb, ko[i], st + (uint32_t)(n * 1024));
+        dma16(vb, vo[i], st + (uint32_t)(C::kTileB + n * 1024));
       }
     }
   };
@@ -213,8 +278,8 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   int NT = 1, RG = 1, TG = 1, rg = 0, tg = 0;
   bool active = false;
 
-  auto begin_item = [&](int ii, int stage) {
-    const int nrows = field(ii, IT_NROWS);
+  auto begin_item = [&](const Desc& d, int stage) {
+    const int nrows = d.nrows;
     NT = nrows > 64 ? 2 : 1;
     const int RS = 16 * NT;
     RG = (nrows + RS - 1) / RS;
@@ -241,8 +306,9 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   };
 
   // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
-  auto slab = [&](auto nt_c, int stage, int sb, int valid) {
+  auto slab = [&](auto nt_c, auto mask_c, int stage, int sb, int valid) {
     constexpr int NTc = decltype(nt_c)::value;
+    constexpr bool kMask = decltype(mask_c)::value;   // the slab runs past the tile's valid tokens
     const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
     const SG_LDS uint8_t* vb = kb + C::kTileB;
     f32x4 s[2][NTc];
@@ -264,7 +330,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       }
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
-    if (sb + 32 > valid) {
+    if constexpr (kMask) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -288,7 +354,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
         m_run[nt] = m_new;
         l_run[nt] *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
+        for (int dt = 0; dt < DT; ++dt) scale_acc_v(acc[nt][dt], alpha);
       }
       const float mc = m_run[nt] * a.c_log2;
       float p[8];
@@ -321,23 +387,32 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     }
   };
 
-  auto compute_tile = [&](int ii, int k, int stage) {
+  auto compute_tile = [&](const Desc& d, int k, int stage) {
     if (!active) return;
-    const int tile = field(ii, IT_TILE0) + k;
-    const int rem = field(ii, IT_NVALID) - tile * TT;
+    const int tile = d.tile0 + k;
+    const int rem = d.nv - tile * TT;
     const int valid = rem < TT ? rem : TT;
     const int ntok = TT / TG;
     const int tok0 = tg * ntok;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using Full = std::integral_constant<bool, false>;
+    using Part = std::integral_constant<bool, true>;
     for (int sb = tok0; sb < tok0 + ntok && sb < valid; sb += 32) {
-      if (NT == 2) slab(std::integral_constant<int, 2>(), stage, sb, valid);
-      else slab(std::integral_constant<int, 1>(), stage, sb, valid);
+      if (sb + 32 <= valid) {
+        if (NT == 2) slab(I2(), Full(), stage, sb, valid);
+        else slab(I1(), Full(), stage, sb, valid);
+      } else {
+        if (NT == 2) slab(I2(), Part(), stage, sb, valid);
+        else slab(I1(), Part(), stage, sb, valid);
+      }
     }
   };
 
   // Combine the token groups of the item through the stage just consumed and
   // write token group 0's normalised partial.  Every wave calls this (it has
   // barriers); returns the number of vector-memory stores this wave issued.
-  auto finish_item = [&](int ii, int stage) -> int {
+  auto finish_item = [&](const Desc& d, int stage) -> int {
     float lrow[2];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) lrow[nt] = rows4_sum(l_run[nt]);
@@ -391,7 +466,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       }
     }
     if (!(active && tg == 0)) return 0;
-    const int kseg = field(ii, IT_ORD) - first_ord;
+    const int kseg = d.ord - first_ord;
     const int64_t slot = slot_of(pp, w, kseg);
     if (slot < 0) return 0;
     float* o = a.ws + pp.o_base + slot * pp.slot_rows * D;
@@ -415,26 +490,49 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   };
 
   // ---- the slot loop -------------------------------------------------------------
-  auto advance = [&](int& ii, int& k) {
-    if (k + 1 < field(ii, IT_NTILE)) {
+  const int nitems = wr.nitems;
+  auto advance = [&](int& ii, int& k, Desc& d) {
+    if (k + 1 < d.ntile) {
       ++k;
     } else {
       ++ii;
       k = -1;
+      if (ii < nitems) d = load_desc(ii);
     }
   };
   int is_ii = 0, is_k = -1, is_id = 0, issued = 0;   // next slot to issue and its block id
-  for (int p = 0; p < 3; ++p) {
+  Desc is_d = load_desc(0);
+  // slot 0 is the first item's q rows; its load overlaps the gather of every
+  // block id the range reads (clamped to each item's last valid block)
+  issue_slot(is_d, is_k, 0, 0);
+  advance(is_ii, is_k, is_d);
+  ++issued;
+  {
+    int32_t* idw = reinterpret_cast<int32_t*>(lds + C::kOffIds);
+    const int nid = (R < C::kTileCap ? R : C::kTileCap) * C::kIdsPerTile;
+    for (int e = tid; e < nid; e += C::kThreads) {
+      const int r = e / C::kIdsPerTile;
+      int ii = 0;
+      while (ii + 1 < nitems && items[(ii + 1) * kItemInts + IT_RTILE0] <= r) ++ii;
+      const int32_t* dd = items + ii * kItemInts;
+      int bi = (dd[IT_TILE0] + (r - dd[IT_RTILE0])) * C::kIdsPerTile + e % C::kIdsPerTile;
+      if (bi > dd[IT_LASTBLK]) bi = dd[IT_LASTBLK];
+      idw[e] = (dd[IT_KIND] == 0 ? a.prefix_table : a.suffix_table)[dd[IT_TABOFF] + bi];
+    }
+  }
+  __syncthreads();
+  for (int p = 1; p < 3; ++p) {
     if (issued < S) {
-      if (is_k >= 0) is_id = block_id(is_ii, is_k);
-      issue_slot(is_ii, is_k, is_id, issued & 3);
-      advance(is_ii, is_k);
+      if (is_k >= 0) is_id = block_id(is_d, is_k);
+      issue_slot(is_d, is_k, is_id, issued & 3);
+      advance(is_ii, is_k, is_d);
       ++issued;
     }
   }
-  if (issued < S && is_k >= 0) is_id = block_id(is_ii, is_k);
+  if (issued < S && is_k >= 0) is_id = block_id(is_d, is_k);
   int st1 = 0, st2 = 0, st3 = 0;   // stores issued one, two and three iterations ago
   int cp_ii = 0, cp_k = -1;
+  Desc cp_d = load_desc(0);
   for (int s = 0; s < S; ++s) {
     // slot s has landed once at most the operations issued after it are
     // outstanding: the later slots' loads and the stores of the last three
@@ -442,23 +540,23 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     vm_wait_le(C::kDmaSlot * (issued - 1 - s) + st1 + st2 + st3);
     lds_barrier();
     if (issued < S) {
-      issue_slot(is_ii, is_k, is_id, issued & 3);   // into the stage consumed last iteration
-      advance(is_ii, is_k);
+      issue_slot(is_d, is_k, is_id, issued & 3);   // into the stage consumed last iteration
+      advance(is_ii, is_k, is_d);
       ++issued;
-      if (issued < S && is_k >= 0) is_id = block_id(is_ii, is_k);   // used next iteration
+      if (issued < S && is_k >= 0) is_id = block_id(is_d, is_k);   // used next iteration
     }
     const int stage = s & 3;
     int st0 = 0;
     if (cp_k < 0) {
-      begin_item(cp_ii, stage);
+      begin_item(cp_d, stage);
     } else {
-      compute_tile(cp_ii, cp_k, stage);
-      if (cp_k == field(cp_ii, IT_NTILE) - 1) st0 = finish_item(cp_ii, stage);
+      compute_tile(cp_d, cp_k, stage);
+      if (cp_k == cp_d.ntile - 1) st0 = finish_item(cp_d, stage);
     }
     st3 = st2;
     st2 = st1;
     st1 = st0;
-    advance(cp_ii, cp_k);
+    advance(cp_ii, cp_k, cp_d);
   }
 }
 
@@ -466,12 +564,13 @@ hipError_t launch_attn_mfma2(const AttnArgs& a, const Plan& plan, hipStream_t st
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
   if (plan.D == 128)
-    hipLaunchKernelGGL((attn_mfma2_kernel<128>), dim3(W), dim3(512), 0, stream, a, static_cast<const PlanHead&>(plan));
+    hipLaunchKernelGGL((attn_mfma2_kernel<128>), dim3(W), dim3(512), 0, stream, a, plan);
   else
-    hipLaunchKernelGGL((attn_mfma2_kernel<64>), dim3(W), dim3(512), 0, stream, a, static_cast<const PlanHead&>(plan));
+    hipLaunchKernelGGL((attn_mfma2_kernel<64>), dim3(W), dim3(512), 0, stream, a, plan);
   return hipGetLastError();
 }
 
 int mfma2_item_cap() { return mfma2::Cfg<128>::kItemCap; }
+int mfma2_tile_cap(int D) { return D == 128 ? mfma2::Cfg<128>::kTileCap : mfma2::Cfg<64>::kTileCap; }
 
 }  // namespace specgen

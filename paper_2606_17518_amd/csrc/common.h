@@ -100,7 +100,6 @@ struct AttnArgs {
   const uint8_t* __restrict__ v_pool;
   const float* __restrict__ k_scale;       // [blocks] (E4M3 only)
   const float* __restrict__ v_scale;
-  IndexArrays ix;                          // lengths and table offsets (device)
   const int32_t* __restrict__ prefix_table;
   const int32_t* __restrict__ suffix_table;
   float* __restrict__ ws;                  // workspace (partials)

@@ -16,6 +16,7 @@ int mfma_tile_cap(int D, bool fp8);
 // attn_mfma2.hip (bf16 KV)
 hipError_t launch_attn_mfma2(const AttnArgs& a, const Plan& plan, hipStream_t stream);
 int mfma2_item_cap();
+int mfma2_tile_cap(int D);
 // attn_dot.hip
 hipError_t launch_attn_dot_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
 int dot_tile_tokens(int D);
@@ -23,8 +24,7 @@ int dot_rows();
 int dot_item_cap();
 int dot_tile_cap(int D);
 // merge.hip
-hipError_t launch_fork_merge(const Plan& plan, const IndexArrays& ix, const float* ws, void* out, float* out_lse,
-                             hipStream_t stream);
+hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream);
 hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S, int64_t R, int D, void* out,
                             bool out_bf16, float* out_lse, hipStream_t stream);
 // kv_import.hip

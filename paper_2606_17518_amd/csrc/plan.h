@@ -53,19 +53,17 @@ struct PartPlan {
   int32_t trace_begin;    // their positions in Plan::ptrace: [trace_begin, +n_traces)
 };
 
-// The scalar part of the plan, computed on the host and passed as a kernel
-// argument.  Kernel arguments live in memory that is slow for the device to
-// read, so only this small header travels that way; the arrays of Plan are
-// rebuilt by every workgroup in LDS from the batch's device index arrays
-// (plan_build_lds), with the same formulas as the host planner.
+// The scalar part of the plan.
 struct PlanHead {
   int32_t T, N, Hq, Hkv, g, D;
   int32_t policy, pad_;
   PartPlan part[2];
 };
 
-struct Plan : PlanHead {
-  int32_t consistent;               // device build only: arrays agree with the header
+// The whole plan, computed on the host from the length mirrors and passed to
+// every kernel by value (about 7.3 KB of kernel arguments); each workgroup
+// copies it into LDS with one vector load per thread (plan_to_lds).
+struct alignas(16) Plan : PlanHead {
   int32_t fork_off[kMaxTraces + 1];
   int32_t prefix_len[kMaxTraces];
   int32_t trace_part[kMaxTraces];   // partition of trace t's prefix items
@@ -77,16 +75,6 @@ struct Plan : PlanHead {
   int32_t prefix_table_off[kMaxTraces + 1];   // host mirrors of the batch's index arrays
   int32_t suffix_len[kMaxForks];
   int32_t suffix_table_off[kMaxForks + 1];
-  int32_t scan_tmp[16];             // device build scratch
-};
-
-// Device copies of the batch's index arrays the plan is rebuilt from.
-struct IndexArrays {
-  const int32_t* fork_off;          // [T+1]
-  const int32_t* prefix_len;        // [T]
-  const int32_t* prefix_table_off;  // [T+1]
-  const int32_t* suffix_len;        // [N]
-  const int32_t* suffix_table_off;  // [N+1]
 };
 
 SG_HD int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
@@ -106,75 +94,16 @@ SG_HD int part_of_suffix(int policy) { return policy == kPolicyDot ? kPartDot : 
 SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) { return (w * pp.tiles) / pp.workers; }
 
 #ifdef __HIPCC__
-// Rebuild the plan's arrays in LDS (all kThreads threads of the block call
-// this; kThreads is 256 or 512).  Mirrors the host planner: traces are grouped by
-// partition with running tile / item counts, suffix tiles are an exclusive
-// scan over forks.  Sets p.consistent = 0 if the totals disagree with the
-// host header (host mirrors and device arrays differ).  Ends with a barrier.
-template <int kThreads = 256>
-__device__ __forceinline__ void plan_build_lds(const PlanHead& h, const IndexArrays& ix, Plan& p) {
-  static_assert(kThreads == 256 || kThreads == 512, "block size");
-  const int tid = threadIdx.x;
-  const int T = h.T, N = h.N;
-  if (tid == 0) {
-    static_cast<PlanHead&>(p) = h;
-    p.consistent = 1;
-  }
-  for (int i = tid; i <= T; i += kThreads) {
-    p.fork_off[i] = ix.fork_off[i];
-    p.prefix_table_off[i] = ix.prefix_table_off[i];
-    if (i < T) p.prefix_len[i] = ix.prefix_len[i];
-  }
-  for (int i = tid; i <= N; i += kThreads) {
-    p.suffix_table_off[i] = ix.suffix_table_off[i];
-    if (i < N) p.suffix_len[i] = ix.suffix_len[i];
-  }
-  __syncthreads();
-  if (tid == 0) {   // T <= 32: a short serial pass
-    int pos = 0;
-    for (int X = 0; X < 2; ++X) {
-      const PartPlan& pp = h.part[X];
-      int64_t tiles = 0, items = 0;
-      for (int t = 0; t < T; ++t) {
-        const int rows = (p.fork_off[t + 1] - p.fork_off[t]) * h.g;
-        if (part_of_trace(h.policy, rows) != X) continue;
-        p.trace_part[t] = X;
-        p.trace_pos[t] = pos;
-        p.ptrace[pos] = t;
-        p.tileP[pos] = (int32_t)tiles;
-        p.ordP[pos] = (int32_t)items;
-        const int rb = cdiv(rows, pp.rbs);
-        tiles += (int64_t)h.Hkv * rb * cdiv(p.prefix_len[t], pp.tt);
-        items += (int64_t)h.Hkv * rb;
-        ++pos;
-      }
-      if (tiles != pp.prefix_tiles || items != pp.n_prefix_items || pos - pp.trace_begin != pp.n_traces)
-        p.consistent = 0;
-    }
-  }
-  // exclusive scan of suffix tiles over forks: thread i owns forks 2i, 2i+1
-  const PartPlan& ps = h.part[part_of_suffix(h.policy)];
-  const int per = h.Hkv * ps.suffix_rb;
-  const int f0 = 2 * tid;
-  const int c0 = f0 < N ? per * cdiv(p.suffix_len[f0], ps.tt) : 0;
-  const int c1 = f0 + 1 < N ? per * cdiv(p.suffix_len[f0 + 1], ps.tt) : 0;
-  int incl = c0 + c1;
-  const int lane = tid & 63;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
-  }
-  if (lane == 63) p.scan_tmp[tid >> 6] = incl;
-  __syncthreads();
-  int base = 0;
-  for (int wv = 0; wv < (tid >> 6); ++wv) base += p.scan_tmp[wv];
-  const int excl = base + incl - (c0 + c1);
-  if (f0 < N) p.tileS[f0] = excl;
-  if (f0 + 1 < N) p.tileS[f0 + 1] = excl + c0;
-  if (tid == kThreads - 1) {
-    p.tileS[N] = base + incl;
-    if ((int64_t)(base + incl) != ps.tiles - ps.prefix_tiles) p.consistent = 0;
-  }
+// Copy the plan from the kernel arguments into LDS.  All kThreads threads of
+// the block call this; it ends with a barrier.
+template <int kThreads>
+__device__ __forceinline__ void plan_to_lds(const Plan& karg, Plan& p) {
+  static_assert(sizeof(Plan) % 16 == 0, "plan copies in 16-byte pieces");
+  constexpr int kPieces = (int)(sizeof(Plan) / 16);
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  const u32x4_t* src = reinterpret_cast<const u32x4_t*>(&karg);
+  u32x4_t* dst = reinterpret_cast<u32x4_t*>(&p);
+  for (int i = threadIdx.x; i < kPieces; i += kThreads) dst[i] = src[i];
   __syncthreads();
 }
 #endif
@@ -244,6 +173,62 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
   r.first = x - r.tile;
   r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
   return r;
+}
+
+// The item that follows `cur` in partition `part` (cur must not be the last
+// one); equal to locate(p, part, cur.first + cur.tiles).  Steps within a trace
+// or fork in O(1) and falls back to locate() where it would have to skip over
+// forks without suffix tokens or cross into the suffix items.
+SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
+  const PartPlan& pp = p.part[part];
+  const int64_t x = cur.first + cur.tiles;
+  ItemRef r = cur;
+  r.first = x;
+  r.tile = 0;
+  r.ord = cur.ord + 1;
+  if (cur.kind == 0) {
+    const int rb_count = cdiv(trace_rows(p, cur.t), pp.rbs);
+    if (cur.rb + 1 < rb_count) {
+      r.rb = cur.rb + 1;
+      return r;
+    }
+    if (cur.j + 1 < p.Hkv) {
+      r.j = cur.j + 1;
+      r.rb = 0;
+      return r;
+    }
+    const int pos = p.trace_pos[cur.t] + 1;
+    if (pos < pp.trace_begin + pp.n_traces) {
+      r.t = p.ptrace[pos];
+      r.j = 0;
+      r.rb = 0;
+      r.tiles = cdiv(p.prefix_len[r.t], pp.tt);
+      return r;
+    }
+    return locate(p, part, x);
+  }
+  if (cur.rb + 1 < pp.suffix_rb) {
+    r.rb = cur.rb + 1;
+    return r;
+  }
+  if (cur.j + 1 < p.Hkv) {
+    r.j = cur.j + 1;
+    r.rb = 0;
+    return r;
+  }
+  const int f = cur.f + 1;
+  if (f < p.N) {
+    const int per_fork = p.Hkv * pp.suffix_rb;
+    const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
+    if (tiles > 0) {
+      r.f = f;
+      r.j = 0;
+      r.rb = 0;
+      r.tiles = tiles;
+      return r;
+    }
+  }
+  return locate(p, part, x);
 }
 
 // Trace of fork f (fork_off is nondecreasing; empty traces are rejected).

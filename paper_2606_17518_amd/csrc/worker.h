@@ -37,8 +37,10 @@ __device__ WorkerRange worker_walk(const Plan& plan, int part, int w, int32_t* i
   wr.R = 0;
   int64_t x = x0;
   int rt = 0;
+  ItemRef it;
+  it.kind = -1;
   while (x < x1 && wr.nitems < kItemCap) {
-    const ItemRef it = locate(plan, part, x);
+    it = wr.nitems == 0 ? locate(plan, part, x) : next_item(plan, part, it);
     const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
     if (wr.nitems == 0) wr.first_ord = it.ord;
     if (threadIdx.x == 0) {

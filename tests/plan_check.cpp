@@ -8,7 +8,8 @@
 //   - per-worker item count and tile count stay within the kernels' caps;
 //   - each row's merge finds exactly the (worker, segment) pairs that
 //     processed its prefix item and its suffix item, with in-range slots;
-//   - each item row maps back to the (fork, q head) it belongs to.
+//   - each item row maps back to the (fork, q head) it belongs to;
+//   - stepping from an item to the next (next_item) agrees with locate().
 // Built and run by tests/test_plan.py with g++ (no GPU involved).
 #include <cstdio>
 #include <cstdlib>
@@ -114,6 +115,23 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
     }
   }
   for (int X = 0; X < 2; ++X) CHECK(ptile[X] == plan.part[X].tiles, "partition %d tile total", X);
+  // the incremental step between items agrees with locate() at every item boundary
+  for (int X = 0; X < 2; ++X) {
+    const PartPlan& pp = plan.part[X];
+    int64_t x = 0;
+    while (x < pp.tiles) {
+      const ItemRef it = locate(plan, X, x);
+      const int64_t nx = it.first + it.tiles;
+      if (nx < pp.tiles) {
+        const ItemRef a = next_item(plan, X, it);
+        const ItemRef b = locate(plan, X, nx);
+        CHECK(a.kind == b.kind && a.t == b.t && a.f == b.f && a.j == b.j && a.rb == b.rb && a.tiles == b.tiles &&
+                  a.tile == b.tile && a.first == b.first && a.ord == b.ord,
+              "next_item differs from locate at tile %lld of partition %d", (long long)nx, X);
+      }
+      x = nx;
+    }
+  }
   // merge lookups
   auto same = [&](const ItemParts& ip, int ord) -> bool {
     const auto& v = segs.at({ip.part, ord});
