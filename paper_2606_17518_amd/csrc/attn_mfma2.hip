@@ -19,11 +19,12 @@
 // inline asm: the compiler does not see them, so it neither drains them
 // (vmcnt(0)) before LDS reads nor reorders them across the LDS barriers.
 //
-// Rows and tokens.  An item with r rows uses row groups of 16 (r <= 64) or 32
-// (r > 64) rows, RG = ceil(r / rows per group) <= 4 of them, and splits each
-// tile's tokens over TG = min(TT/32, 8/RG) token groups: wave w computes row
-// group w % RG over token group w / RG (two waves per SIMD for the 128-row
-// prefix items, so one wave's softmax overlaps the other's MFMAs).  At the
+// Rows and tokens.  An item with r rows uses RG = ceil(r / 32) <= 4 row groups
+// of 32 rows and splits each tile's tokens over TG = min(TT/32, 8/RG) token
+// groups: wave w computes row group w % RG over token group w / RG (two waves
+// per SIMD for the 128-row prefix items, so one wave's softmax overlaps the
+// other's MFMAs).  Items with fewer rows pad their last row group; they are
+// bound by their K/V bytes, not by the matrix cores.  At the
 // item's end the token groups are combined through the stage that was just
 // consumed, and token group 0 writes the normalised partial (o, lse).
 //
@@ -94,18 +95,6 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gu), "s"(l) : "m0");
 }
 
-// acc *= alpha in place.  Tying the registers in an asm statement keeps the
-// accumulator in the same VGPRs on both sides of the (rare, wave-uniform)
-// rescale branch; written as plain code, the compiler keeps two copies of all
-// accumulators and moves them on every slab.
-__device__ __forceinline__ void scale_acc_v(f32x4& acc, float alpha) {
-  float x0 = acc[0], x1 = acc[1], x2 = acc[2], x3 = acc[3];
-  asm volatile("v_mul_f32 %0, %0, %4\n\tv_mul_f32 %1, %1, %4\n\tv_mul_f32 %2, %2, %4\n\tv_mul_f32 %3, %3, %4"
-               : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3)
-               : "v"(alpha));
-  acc = f32x4{x0, x1, x2, x3};
-}
-
 template <int N>
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
@@ -152,10 +141,14 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   const int wave = uniform(tid >> 6);
   const int w = blockIdx.x;
   const WorkerRange wr = worker_items<C::kItemCap>(plan, kPartMfma, w, items);
-  const int R = wr.R;
-  const int first_ord = wr.first_ord;
+  // The walk reads LDS, so the compiler cannot prove its results uniform;
+  // without these readfirstlanes every loop-carried value of the slot loop
+  // would live in VGPRs under exec masks.
+  const int R = uniform(wr.R);
+  const int first_ord = uniform(wr.first_ord);
+  const int nitems = uniform(wr.nitems);
   if (R <= 0) return;
-  const int S = R + wr.nitems;   // slots: a q slot per item, then its tiles
+  const int S = R + nitems;   // slots: a q slot per item, then its tiles
   const uint32_t lds_base = (uint32_t)(size_t)((SG_LDS uint8_t*)lds);
 
   // Item descriptors are read from LDS once per item and kept in scalar registers.
@@ -275,13 +268,13 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   bf16x8 qop[2][KS];
   f32x4 acc[2][DT];
   float m_run[2], l_run[2];
-  int NT = 1, RG = 1, TG = 1, rg = 0, tg = 0;
+  constexpr int NT = 2;   // 16-row MFMA tiles per row group
+  int RG = 1, TG = 1, rg = 0, tg = 0;
   bool active = false;
 
   auto begin_item = [&](const Desc& d, int stage) {
     const int nrows = d.nrows;
-    NT = nrows > 64 ? 2 : 1;
-    const int RS = 16 * NT;
+    constexpr int RS = 16 * NT;
     RG = (nrows + RS - 1) / RS;
     TG = (TT / 32) < (C::kWaves / RG) ? (TT / 32) : (C::kWaves / RG);
     rg = wave % RG;
@@ -306,8 +299,8 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   };
 
   // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
-  auto slab = [&](auto nt_c, auto mask_c, int stage, int sb, int valid) {
-    constexpr int NTc = decltype(nt_c)::value;
+  auto slab = [&](auto mask_c, int stage, int sb, int valid) {
+    constexpr int NTc = NT;
     constexpr bool kMask = decltype(mask_c)::value;   // the slab runs past the tile's valid tokens
     const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
     const SG_LDS uint8_t* vb = kb + C::kTileB;
@@ -354,7 +347,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
         m_run[nt] = m_new;
         l_run[nt] *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) scale_acc_v(acc[nt][dt], alpha);
+        for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
       }
       const float mc = m_run[nt] * a.c_log2;
       float p[8];
@@ -392,21 +385,11 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     const int tile = d.tile0 + k;
     const int rem = d.nv - tile * TT;
     const int valid = rem < TT ? rem : TT;
-    const int ntok = TT / TG;
-    const int tok0 = tg * ntok;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using Full = std::integral_constant<bool, false>;
-    using Part = std::integral_constant<bool, true>;
-    for (int sb = tok0; sb < tok0 + ntok && sb < valid; sb += 32) {
-      if (sb + 32 <= valid) {
-        if (NT == 2) slab(I2(), Full(), stage, sb, valid);
-        else slab(I1(), Full(), stage, sb, valid);
-      } else {
-        if (NT == 2) slab(I2(), Part(), stage, sb, valid);
-        else slab(I1(), Part(), stage, sb, valid);
-      }
-    }
+    const int tok0 = tg * (TT / TG);
+    const int tok1 = (tok0 + TT / TG) < valid ? (tok0 + TT / TG) : valid;   // this wave's tokens: [tok0, tok1)
+    int sb = tok0;
+    for (; sb + 32 <= tok1; sb += 32) slab(std::integral_constant<bool, false>(), stage, sb, valid);
+    if (sb < tok1) slab(std::integral_constant<bool, true>(), stage, sb, valid);   // partial last slab
   };
 
   // Combine the token groups of the item through the stage just consumed and
@@ -418,7 +401,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     for (int nt = 0; nt < 2; ++nt) lrow[nt] = rows4_sum(l_run[nt]);
     if (TG > 1) {
       float* cb = reinterpret_cast<float*>(lds + stage * C::kStageB);
-      const int wave_bytes = NT * DT * 64 * 16;
+      constexpr int wave_bytes = NT * DT * 64 * 16;
       const int per_round = C::kStageB / wave_bytes;      // writers whose accumulators fit at once
       const int writers = (TG - 1) * RG;
       const int rounds = (writers + per_round - 1) / per_round;
@@ -471,7 +454,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     if (slot < 0) return 0;
     float* o = a.ws + pp.o_base + slot * pp.slot_rows * D;
     float* ls = a.ws + pp.lse_base + slot * pp.slot_rows;
-    const int RS = 16 * NT;
+    constexpr int RS = 16 * NT;
     int stores = 0;
     // every lane stores (rows past the item's end land in unused rows of the
     // slot), so the number of stores is the same on every path
@@ -490,7 +473,6 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   };
 
   // ---- the slot loop -------------------------------------------------------------
-  const int nitems = wr.nitems;
   auto advance = [&](int& ii, int& k, Desc& d) {
     if (k + 1 < d.ntile) {
       ++k;
@@ -537,7 +519,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     // slot s has landed once at most the operations issued after it are
     // outstanding: the later slots' loads and the stores of the last three
     // iterations (slot s was issued three iterations ago)
-    vm_wait_le(C::kDmaSlot * (issued - 1 - s) + st1 + st2 + st3);
+    vm_wait_le(uniform(C::kDmaSlot * (issued - 1 - s) + st1 + st2 + st3));
     lds_barrier();
     if (issued < S) {
       issue_slot(is_d, is_k, is_id, issued & 3);   // into the stage consumed last iteration
@@ -551,7 +533,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       begin_item(cp_d, stage);
     } else {
       compute_tile(cp_d, cp_k, stage);
-      if (cp_k == cp_d.ntile - 1) st0 = finish_item(cp_d, stage);
+      if (cp_k == cp_d.ntile - 1) st0 = uniform(finish_item(cp_d, stage));
     }
     st3 = st2;
     st2 = st1;

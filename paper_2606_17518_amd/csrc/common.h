@@ -42,11 +42,14 @@ __device__ __forceinline__ float wave_max_xor(float v, int mask) {
 // acc *= alpha for an MFMA accumulator that lives in AGPRs: read, scale and
 // write back inside one asm block so the compiler keeps the accumulator in
 // AGPRs instead of shuttling every accumulator through VGPRs around the
-// (rare) rescale branch.
+// (rare) rescale branch.  alpha usually comes straight from v_exp_f32, and a
+// VALU read of a transcendental result needs wait states the compiler cannot
+// insert inside an asm block, hence the leading s_nop.
 __device__ __forceinline__ void scale_acc(f32x4& acc, float alpha) {
   float x0 = acc[0], x1 = acc[1], x2 = acc[2], x3 = acc[3];
   float t;
   asm volatile(
+      "s_nop 4\n\t"
       "v_accvgpr_read_b32 %4, %0\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %0, %4\n\t"
       "v_accvgpr_read_b32 %4, %1\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %1, %4\n\t"
       "v_accvgpr_read_b32 %4, %2\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %2, %4\n\t"
