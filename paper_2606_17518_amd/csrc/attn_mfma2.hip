@@ -140,7 +140,8 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int w = blockIdx.x;
-  const WorkerRange wr = worker_items<C::kItemCap>(plan, kPartMfma, w, items);
+  const WorkerRange wr =
+      worker_items<C::kItemCap>(plan, kPartMfma, w, items, reinterpret_cast<int32_t*>(a.ws + pp.info_base));
   // The walk reads LDS, so the compiler cannot prove its results uniform;
   // without these readfirstlanes every loop-carried value of the slot loop
   // would live in VGPRs under exec masks.

@@ -97,23 +97,33 @@ hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S,
 // covered its prefix item and its suffix item ---------------------------------
 
 // Row merge for D in {64, 128}: lanes read 16 bytes each, so one load
-// instruction covers 64 / (D/4) parts; loads for up to 8 instructions' worth
-// of parts are issued before any is consumed, so a row costs a few memory
-// latencies rather than one per part.
+// instruction covers PPI = 64 / (D/4) parts.  A batch is up to 64 parts: each
+// lane loads one part's lse and the wave issues the o loads of every part of
+// the batch before it waits for any of them, so a row of up to a batch of
+// parts costs one memory round trip.
 template <int D, typename PO, typename PL>
 __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse, uint16_t* out_row,
                                              float* out_lse_p) {
   constexpr int LPP = D / 4;       // lanes per part
   constexpr int PPI = 64 / LPP;    // parts per load instruction
-  constexpr int U = 8;             // load instructions in flight
+  constexpr int U = (D == 128) ? 24 : 16;   // load instructions per batch
+  constexpr int kBatch = PPI * U;  // parts per batch (<= 64: one lse per lane)
+  static_assert(kBatch <= 64, "one lse per lane");
   const int lane = threadIdx.x & 63;
   const int gsl = lane / LPP;      // part slot of this lane within an instruction
   const int c4 = (lane % LPP) * 4; // first of the 4 dims this lane owns
   float M = -INFINITY, z = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int p0 = 0; p0 < nparts; p0 += 64) {
-    const int p = p0 + lane;
-    const float l = p < nparts ? part_lse(p) : -INFINITY;
+  for (int p0 = 0; p0 < nparts; p0 += kBatch) {
+    const int cnt = (nparts - p0) < kBatch ? (nparts - p0) : kBatch;
+    const float l = lane < cnt ? part_lse(p0 + lane) : -INFINITY;
+    f32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int q = u * PPI + gsl;
+      const int qc = q < cnt ? q : cnt - 1;   // slots past the batch re-read its last part
+      v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
+    }
     float cm = l;
     for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
     const float Mn = fmaxf(M, cm);
@@ -126,21 +136,12 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse,
     float zs = wl;
     for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
     z += zs;
-    const int cnt = (nparts - p0) < 64 ? (nparts - p0) : 64;
-    for (int q0 = 0; q0 < cnt; q0 += PPI * U) {
-      f32x4 v[U];
-      float wq[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int q = q0 + u * PPI + gsl;
-        const int qc = q < cnt ? q : cnt - 1;
-        wq[u] = __shfl(wl, qc, 64);
-        if (q >= cnt) wq[u] = 0.f;
-        v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (wq[u] != 0.f) acc += wq[u] * v[u];   // an empty part's o may be garbage
+    for (int u = 0; u < U; ++u) {
+      const int q = u * PPI + gsl;
+      float wq = __shfl(wl, q < 64 ? q : 63, 64);
+      if (q >= cnt) wq = 0.f;
+      if (wq != 0.f) acc += wq * v[u];   // an empty part's o may be garbage
     }
   }
   // sum the PPI lane groups
@@ -172,20 +173,58 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
   if (row >= (int64_t)plan.N * plan.Hq) return;
   const int f = (int)(row / plan.Hq);
   const int h = (int)(row % plan.Hq);
-  const ItemParts P = prefix_parts_of_row(plan, f, h);
-  const int np = P.w_hi - P.w_lo + 1;
-  ItemParts S;
-  const int ns = suffix_parts_of_row(plan, f, h, &S) ? S.w_hi - S.w_lo + 1 : 0;
-  auto slot_ptr = [&](const ItemParts& ip, int i, bool lse) -> int64_t {
-    const PartPlan& q = plan.part[ip.part];
-    const int w = ip.w_lo + i;
-    const int k = (i == 0) ? ip.k_lo : 0;
-    const int64_t slot = (int64_t)w * q.kmax + k;
-    return lse ? q.lse_base + slot * q.slot_rows + ip.row : q.o_base + (slot * q.slot_rows + ip.row) * D;
+  // The item table (written by the partial kernels' walks) gives each item's
+  // first and last worker and its segment index in the first one.  Part i of
+  // an item sits in slot (w_lo + i) * kmax + (i == 0 ? k_lo : 0), so relative
+  // to part 0 it is i * kmax - k_lo slots further (plain scalars: a lane picks
+  // the prefix or the suffix item by its part index).
+  int X = 0, ord = 0, r = 0;
+  int64_t o0[2] = {0, 0}, l0[2] = {0, 0};
+  int kmax[2] = {1, 1}, klo[2] = {0, 0}, n[2] = {0, 0}, srows[2] = {1, 1};
+  bool ok = true;
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const bool has = s2 == 0 ? (prefix_item_of_row(plan, f, h, &X, &ord, &r), true)
+                             : suffix_item_of_row(plan, f, h, &X, &ord, &r);
+    if (!has) continue;
+    const PartPlan& pp = plan.part[X];
+    const int32_t* info = reinterpret_cast<const int32_t*>(ws + pp.info_base) + 3 * (int64_t)ord;
+    const int w_lo = info[0], w_hi = info[1], k_lo = info[2];
+    if (ord < 0 || ord >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 || k_lo >= pp.kmax) {
+      ok = false;
+      continue;
+    }
+    const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
+    o0[s2] = pp.o_base + (slot0 * pp.slot_rows + r) * D;
+    l0[s2] = pp.lse_base + slot0 * pp.slot_rows + r;
+    kmax[s2] = pp.kmax;
+    klo[s2] = k_lo;
+    n[s2] = w_hi - w_lo + 1;
+    srows[s2] = pp.slot_rows;
+  }
+  if (!ok) {   // the item table is inconsistent: fail loudly rather than read out of range
+    const int lane = threadIdx.x & 63;
+    for (int d = lane; d < D; d += 64) out[row * D + d] = 0x7FC0;   // bf16 NaN
+    if (out_lse && lane == 0) out_lse[row] = __builtin_nanf("");
+    return;
+  }
+  const int np = n[0];
+  const int64_t pO0 = o0[0], sO0 = o0[1], pL0 = l0[0], sL0 = l0[1];
+  const int pK = kmax[0], sK = kmax[1], pKlo = klo[0], sKlo = klo[1], pR = srows[0], sR = srows[1];
+  auto rel_slots = [&](int p) -> int64_t {   // slots between part p and its item's part 0
+    const bool pre = p < np;
+    const int i = pre ? p : p - np;
+    return i == 0 ? 0 : (int64_t)i * (pre ? pK : sK) - (pre ? pKlo : sKlo);
   };
-  auto po = [&](int p) { return p < np ? ws + slot_ptr(P, p, false) : ws + slot_ptr(S, p - np, false); };
-  auto pl = [&](int p) { return p < np ? ws[slot_ptr(P, p, true)] : ws[slot_ptr(S, p - np, true)]; };
-  merge_row_v4<D>(np + ns, po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
+  auto po = [&](int p) {
+    const bool pre = p < np;
+    return ws + (pre ? pO0 : sO0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * D;
+  };
+  auto pl = [&](int p) {
+    const bool pre = p < np;
+    return ws[(pre ? pL0 : sL0) + rel_slots(p) * (int64_t)(pre ? pR : sR)];
+  };
+  merge_row_v4<D>(np + n[1], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {

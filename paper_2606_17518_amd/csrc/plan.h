@@ -41,6 +41,10 @@ struct PartPlan {
   int64_t prefix_tiles;   // tiles of its prefix items (they come first)
   int64_t o_base;         // float offset of slot 0's o in the workspace
   int64_t lse_base;       // float offset of slot 0's lse
+  int64_t info_base;      // float offset of the item table: per item ordinal three
+                          // int32 (first worker, last worker, segment index in the first)
+  int32_t n_items;        // items of the partition (prefix, then suffix)
+  int32_t pad_;
   int32_t workers;        // W (0: partition unused)
   int32_t kmax;           // max items touched by one worker
   int32_t tt;             // tokens per tile
@@ -231,6 +235,52 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   return locate(p, part, x);
 }
 
+// The items of worker w's tile range, in order.  For each one calls
+// visit(it, n, rt, i, k): it = the item (it.tile = its first tile in the
+// range), n = its tiles in the range, rt = the range-relative index of its
+// first tile, i = its position in the range, k = it.ord - (ordinal of the
+// range's first item), which is the partial-slot index (w * kmax + k).  At
+// most item_cap items are visited.
+struct WorkerRange {
+  int nitems;     // items touched (non-empty)
+  int first_ord;  // ordinal of the first one
+  int R;          // tiles in the range
+};
+template <typename Visit>
+SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, Visit&& visit) {
+  const PartPlan& pp = p.part[part];
+  const int64_t x0 = worker_start(pp, w);
+  const int64_t x1 = worker_start(pp, w + 1);
+  WorkerRange wr;
+  wr.nitems = 0;
+  wr.first_ord = 0;
+  wr.R = 0;
+  int64_t x = x0;
+  ItemRef it;
+  it.kind = -1;
+  while (x < x1 && wr.nitems < item_cap) {
+    it = wr.nitems == 0 ? locate(p, part, x) : next_item(p, part, it);
+    const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
+    if (wr.nitems == 0) wr.first_ord = it.ord;
+    visit(it, n, wr.R, wr.nitems, it.ord - wr.first_ord);
+    x += n;
+    wr.R += n;
+    ++wr.nitems;
+  }
+  return wr;
+}
+
+// The item-table entry a walk records: the worker holding an item's first
+// tile stores itself and the item's slot index there, the worker holding its
+// last tile stores itself.  info holds three int32 per item ordinal.
+SG_HD void record_item(int32_t* info, const ItemRef& it, int n, int w, int k) {
+  if (it.tile == 0) {
+    info[3 * it.ord + 0] = w;
+    info[3 * it.ord + 2] = k;
+  }
+  if (it.tile + n == it.tiles) info[3 * it.ord + 1] = w;
+}
+
 // Trace of fork f (fork_off is nondecreasing; empty traces are rejected).
 SG_HD int trace_of_fork(const Plan& p, int f) {
   int lo = 0, hi = p.T - 1;
@@ -302,6 +352,33 @@ SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
   const int item = j * pp.suffix_rb + rb;
   *out = item_parts(p, X, pp.prefix_tiles + p.tileS[f] + (int64_t)item * tiles, tiles,
                     pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
+  return true;
+}
+
+// The prefix item of row (f, h): its partition, ordinal and the row inside it.
+SG_HD void prefix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, int* row) {
+  const int g = p.g, j = h / g, hh = h - j * g;
+  const int t = trace_of_fork(p, f);
+  const int ri = (f - p.fork_off[t]) * g + hh;
+  const int X = p.trace_part[t];
+  const PartPlan& pp = p.part[X];
+  const int rbc = cdiv(trace_rows(p, t), pp.rbs);
+  const int rb = ri / pp.rbs;
+  *part = X;
+  *ord = p.ordP[p.trace_pos[t]] + j * rbc + rb;
+  *row = ri - rb * pp.rbs;
+}
+
+// The suffix item of row (f, h); false if the fork has no suffix tokens.
+SG_HD bool suffix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, int* row) {
+  const int g = p.g, j = h / g, hh = h - j * g;
+  const int X = part_of_suffix(p.policy);
+  const PartPlan& pp = p.part[X];
+  if (p.tileS[f + 1] == p.tileS[f]) return false;
+  const int rb = hh / pp.rbs;
+  *part = X;
+  *ord = pp.n_prefix_items + (f * p.Hkv + j) * pp.suffix_rb + rb;
+  *row = hh - rb * pp.rbs;
   return true;
 }
 

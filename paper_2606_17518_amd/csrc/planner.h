@@ -149,6 +149,9 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     off = align_up(off + slots * pp.slot_rows * D, kAlignFloats);
     pp.lse_base = off;
     off = align_up(off + slots * pp.slot_rows, kAlignFloats);
+    pp.n_items = pp.n_prefix_items + (pp.has_suffix ? N * Hkv * pp.suffix_rb : 0);
+    pp.info_base = off;
+    off = align_up(off + 3 * (int64_t)pp.n_items, kAlignFloats);
   }
   *ws_floats = off;
   return kPlanOk;

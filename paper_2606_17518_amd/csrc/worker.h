@@ -17,65 +17,45 @@ enum {
 constexpr int kItemInts = 16;
 static_assert(IT_COUNT <= kItemInts, "item descriptor size");
 
-struct WorkerRange {
-  int nitems;     // items touched (non-empty)
-  int first_ord;  // ordinal of the first one
-  int R;          // tiles in the range
-};
-
 // The item walk of a worker's tile range: every thread computes the same
 // WorkerRange; thread 0 writes one descriptor per item into `items` (at most
-// kItemCap; the host sizes workers so the cap holds).  No barrier at the end.
+// kItemCap; the host sizes workers so the cap holds).  It also records, in
+// the partition's item table `info` (three int32 per item ordinal), which
+// worker starts the item and its segment index there, and which worker ends
+// it, so the merge finds an item's partials with one load.  No barrier at the
+// end.
 template <int kItemCap>
-__device__ WorkerRange worker_walk(const Plan& plan, int part, int w, int32_t* items) {
+__device__ WorkerRange worker_walk(const Plan& plan, int part, int w, int32_t* items, int32_t* info) {
   const PartPlan& pp = plan.part[part];
-  const int64_t x0 = worker_start(pp, w);
-  const int64_t x1 = worker_start(pp, w + 1);
-  WorkerRange wr;
-  wr.nitems = 0;
-  wr.first_ord = 0;
-  wr.R = 0;
-  int64_t x = x0;
-  int rt = 0;
-  ItemRef it;
-  it.kind = -1;
-  while (x < x1 && wr.nitems < kItemCap) {
-    it = wr.nitems == 0 ? locate(plan, part, x) : next_item(plan, part, it);
-    const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
-    if (wr.nitems == 0) wr.first_ord = it.ord;
-    if (threadIdx.x == 0) {
-      int32_t* d = items + wr.nitems * kItemInts;
-      d[IT_KIND] = it.kind;
-      d[IT_T] = it.t;
-      d[IT_F] = it.f;
-      d[IT_J] = it.j;
-      d[IT_RB] = it.rb;
-      d[IT_ORD] = it.ord;
-      d[IT_TILE0] = it.tile;
-      d[IT_NTILE] = n;
-      d[IT_RTILE0] = rt;
-      d[IT_TILES] = it.tiles;
-      const int r0 = it.rb * pp.rbs;
-      const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
-      d[IT_NROWS] = (rows - r0) < pp.rbs ? (rows - r0) : pp.rbs;
-      d[IT_ROW0] = r0;
-      const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
-      d[IT_NVALID] = nv;
-      d[IT_TABOFF] = it.kind == 0 ? plan.prefix_table_off[it.t] : plan.suffix_table_off[it.f];
-      d[IT_LASTBLK] = (nv - 1) / 16;
-    }
-    x += n;
-    rt += n;
-    ++wr.nitems;
-  }
-  wr.R = rt;
-  return wr;
+  return walk_range(plan, part, w, kItemCap, [&](const ItemRef& it, int n, int rt, int i, int k) {
+    if (threadIdx.x != 0) return;
+    int32_t* d = items + i * kItemInts;
+    d[IT_KIND] = it.kind;
+    d[IT_T] = it.t;
+    d[IT_F] = it.f;
+    d[IT_J] = it.j;
+    d[IT_RB] = it.rb;
+    d[IT_ORD] = it.ord;
+    d[IT_TILE0] = it.tile;
+    d[IT_NTILE] = n;
+    d[IT_RTILE0] = rt;
+    d[IT_TILES] = it.tiles;
+    const int r0 = it.rb * pp.rbs;
+    const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
+    d[IT_NROWS] = (rows - r0) < pp.rbs ? (rows - r0) : pp.rbs;
+    d[IT_ROW0] = r0;
+    const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+    d[IT_NVALID] = nv;
+    d[IT_TABOFF] = it.kind == 0 ? plan.prefix_table_off[it.t] : plan.suffix_table_off[it.f];
+    d[IT_LASTBLK] = (nv - 1) / 16;
+    record_item(info, it, n, w, k);
+  });
 }
 
 // The walk only, ending with a barrier so `items` is visible to every thread.
 template <int kItemCap>
-__device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* items) {
-  const WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items);
+__device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* items, int32_t* info) {
+  const WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items, info);
   __syncthreads();
   return wr;
 }
@@ -88,7 +68,8 @@ template <int kThreads, int kItemCap, int kIdsPerTile, int kTileCap>
 __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
                                       int32_t* ids, float* scales = nullptr) {
   const int tid = threadIdx.x;
-  WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items);
+  WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items,
+                                         reinterpret_cast<int32_t*>(a.ws + plan.part[part].info_base));
   if (wr.R <= 0) return wr;
   const int rt = wr.R;
   // the host sizes workers so the caps hold; never index past them

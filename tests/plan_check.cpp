@@ -9,7 +9,9 @@
 //   - each row's merge finds exactly the (worker, segment) pairs that
 //     processed its prefix item and its suffix item, with in-range slots;
 //   - each item row maps back to the (fork, q head) it belongs to;
-//   - stepping from an item to the next (next_item) agrees with locate().
+//   - stepping from an item to the next (next_item) agrees with locate();
+//   - the item table the walks record gives the merge the same workers and
+//     slot index as the plan's own lookup.
 // Built and run by tests/test_plan.py with g++ (no GPU involved).
 #include <cstdio>
 #include <cstdlib>
@@ -45,32 +47,34 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
   char err[256];
   const int rc = plan_build(in, [&] { return cus; }, &plan, &wsf, err, sizeof err);
   CHECK(rc == kPlanOk, "case %llu: plan_build failed: %s", (unsigned long long)case_id, err);
-  // segments per (partition, item ordinal)
+  // segments per (partition, item ordinal), from the walk the kernels run;
+  // the walk also fills the item table the merge reads
   std::map<std::pair<int, int>, std::vector<Seg>> segs;
+  std::vector<int32_t> tables[2];   // the item table of each partition (three int32 per item)
   for (int X = 0; X < 2; ++X) {
     const PartPlan& pp = plan.part[X];
     if (pp.workers == 0) {
       CHECK(pp.tiles == 0, "partition %d has tiles but no workers", X);
       continue;
     }
+    CHECK(pp.info_base + 3 * (int64_t)pp.n_items <= wsf, "item table past the workspace");
+    tables[X].assign(3 * (size_t)pp.n_items, -7);
     for (int w = 0; w < pp.workers; ++w) {
       const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
       CHECK(x1 - x0 <= in.tile_cap[X], "worker %d has %lld tiles > cap", w, (long long)(x1 - x0));
       int64_t x = x0;
-      int nitems = 0, first_ord = -1;
-      while (x < x1) {
-        const ItemRef it = locate(plan, X, x);
-        CHECK(it.kind >= 0, "tile %lld not located", (long long)x);
-        CHECK(it.tile >= 0 && it.tile < it.tiles, "tile index");
-        const int n = (int)std::min<int64_t>(it.tiles - it.tile, x1 - x);
-        if (first_ord < 0) first_ord = it.ord;
-        const int k = it.ord - first_ord;
-        CHECK(k >= 0 && k < pp.kmax, "k %d kmax %d", k, pp.kmax);
+      bool fine = true;
+      const WorkerRange wr = walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
+        if (it.kind < 0 || it.first + it.tile != x || rt != x - x0 || k < 0 || k >= pp.kmax || it.ord >= pp.n_items)
+          fine = false;
         segs[{X, it.ord}].push_back(Seg{w, k, x, n});
+        if (it.ord >= 0 && it.ord < pp.n_items) record_item(tables[X].data(), it, n, w, k);
         x += n;
-        ++nitems;
-      }
-      CHECK(nitems <= in.item_cap[X], "worker %d touches %d items > cap", w, nitems);
+        (void)i;
+      });
+      CHECK(fine, "worker %d of partition %d: walk out of order or slot index out of range", w, X);
+      CHECK(wr.R == x1 - x0, "worker %d walked %d of %lld tiles (item cap %d)", w, wr.R, (long long)(x1 - x0),
+            in.item_cap[X]);
     }
   }
   // enumerate items independently of locate() and check coverage
@@ -135,6 +139,9 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
   // merge lookups
   auto same = [&](const ItemParts& ip, int ord) -> bool {
     const auto& v = segs.at({ip.part, ord});
+    const int32_t* e = tables[ip.part].data() + 3 * (int64_t)ord;
+    CHECK(e[0] == ip.w_lo && e[1] == ip.w_hi && e[2] == ip.k_lo, "item table (%d,%d,%d) vs parts (%d,%d,%d) at ord %d",
+          e[0], e[1], e[2], ip.w_lo, ip.w_hi, ip.k_lo, ord);
     CHECK((int)v.size() == ip.w_hi - ip.w_lo + 1, "merge finds %d parts, %zu processed",
           ip.w_hi - ip.w_lo + 1, v.size());
     for (size_t i = 0; i < v.size(); ++i) {
@@ -169,6 +176,13 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       ord += j * rbc + ri / rbs;
       const ItemParts P = prefix_parts_of_row(plan, f, h);
       CHECK(P.part == X, "prefix partition");
+      {
+        int xp = -1, op = -1, rp = -1;
+        prefix_item_of_row(plan, f, h, &xp, &op, &rp);
+        CHECK(xp == X && op == ord && rp == P.row, "prefix_item_of_row (%d,%d,%d) vs (%d,%d,%d)", xp, op, rp, X, ord,
+              P.row);
+        CHECK(op < plan.part[X].n_items, "prefix ordinal past the item table");
+      }
       if (!same(P, ord)) return false;
       int ff, hh2;
       item_row_fork_head(plan, 0, t, -1, j, (ri / rbs) * rbs, P.row, &ff, &hh2);
@@ -176,12 +190,22 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       ItemParts S;
       const bool has = suffix_parts_of_row(plan, f, h, &S);
       CHECK(has == (in.suffix_len[f] > 0), "suffix presence");
+      if (!has) {
+        int xs, os, rs;
+        CHECK(!suffix_item_of_row(plan, f, h, &xs, &os, &rs), "suffix_item_of_row without suffix tokens");
+      }
       if (has) {
         const int Xs = part_of_suffix(in.policy);
         const int rbss = in.rbs[Xs];
         const int srb = (g + rbss - 1) / rbss;
         const int sord = plan.part[Xs].n_prefix_items + (f * in.Hkv + j) * srb + hh / rbss;
         if (!same(S, sord)) return false;
+        int xs = -1, os = -1, rs = -1;
+        CHECK(suffix_item_of_row(plan, f, h, &xs, &os, &rs), "suffix_item_of_row presence");
+        CHECK(xs == Xs && os == sord && rs == S.row, "suffix_item_of_row (%d,%d,%d) vs (%d,%d,%d)", xs, os, rs, Xs,
+              sord, S.row);
+        CHECK(os < plan.part[Xs].n_items, "suffix ordinal past the item table");
+        CHECK(plan.part[Xs].info_base + 3 * (int64_t)plan.part[Xs].n_items <= wsf, "item table past workspace");
         item_row_fork_head(plan, 1, t, f, j, (hh / rbss) * rbss, S.row, &ff, &hh2);
         CHECK(ff == f && hh2 == h, "suffix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
       }
