@@ -120,9 +120,12 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse,
     f32x4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int q = u * PPI + gsl;
-      const int qc = q < cnt ? q : cnt - 1;   // slots past the batch re-read its last part
-      v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
+      v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (u * PPI < cnt) {   // wave-uniform: only instructions that hold a part
+        const int q = u * PPI + gsl;
+        const int qc = q < cnt ? q : cnt - 1;   // the last instruction's spare slots re-read its last part
+        v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
+      }
     }
     float cm = l;
     for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
@@ -178,18 +181,28 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
   // an item sits in slot (w_lo + i) * kmax + (i == 0 ? k_lo : 0), so relative
   // to part 0 it is i * kmax - k_lo slots further (plain scalars: a lane picks
   // the prefix or the suffix item by its part index).
-  int X = 0, ord = 0, r = 0;
+  int Xs[2] = {0, 0}, ords[2] = {0, 0}, rs[2] = {0, 0};
+  bool has[2];
+  prefix_item_of_row(plan, f, h, &Xs[0], &ords[0], &rs[0]);
+  has[0] = true;
+  has[1] = suffix_item_of_row(plan, f, h, &Xs[1], &ords[1], &rs[1]);
+  // both table entries are loaded before either is used
+  int32_t e[2][3];
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const int32_t* info = reinterpret_cast<const int32_t*>(ws + plan.part[Xs[s2]].info_base) + 3 * (int64_t)ords[s2];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) e[s2][c] = has[s2] ? info[c] : 0;
+  }
   int64_t o0[2] = {0, 0}, l0[2] = {0, 0};
   int kmax[2] = {1, 1}, klo[2] = {0, 0}, n[2] = {0, 0}, srows[2] = {1, 1};
   bool ok = true;
 #pragma unroll
   for (int s2 = 0; s2 < 2; ++s2) {
-    const bool has = s2 == 0 ? (prefix_item_of_row(plan, f, h, &X, &ord, &r), true)
-                             : suffix_item_of_row(plan, f, h, &X, &ord, &r);
-    if (!has) continue;
+    if (!has[s2]) continue;
+    const int X = Xs[s2], ord = ords[s2], r = rs[s2];
     const PartPlan& pp = plan.part[X];
-    const int32_t* info = reinterpret_cast<const int32_t*>(ws + pp.info_base) + 3 * (int64_t)ord;
-    const int w_lo = info[0], w_hi = info[1], k_lo = info[2];
+    const int w_lo = e[s2][0], w_hi = e[s2][1], k_lo = e[s2][2];
     if (ord < 0 || ord >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 || k_lo >= pp.kmax) {
       ok = false;
       continue;
