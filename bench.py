@@ -35,9 +35,14 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+# the kernel that serves bf16 KV on the MFMA path, and the sources it includes
+PARTIAL_KERNEL = "attn_bf16_kernel<128>"
+PARTIAL_SOURCES = ("attn_bf16.hip", "worker.h", "common.h", "plan.h")
+
+
 def source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("attn_mfma.hip", "worker.h", "common.h", "plan.h"):
+    for f in PARTIAL_SOURCES:
         with open(os.path.join(ROOT, "paper_2606_17518_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -190,7 +195,7 @@ def main():
                     "p50": round(float(np.median(attn_ms)) * 1e3, 2), "p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
                     "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2)},
         "attn_algorithmic_bytes": int(attn_bytes),
-        "roofline": {"kernel": "attn_mfma_kernel (partials phase)", "bound": "hbm", "achieved": round(achieved, 2),
+        "roofline": {"kernel": PARTIAL_KERNEL + " (partials phase)", "bound": "hbm", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic_from_profile(args.workload), "algorithmic_bytes_per_launch": int(kern_bytes)},
     }

@@ -20,10 +20,16 @@
  *    the P_t prefix tokens of t followed by the S_f suffix tokens of f; the
  *    current decode token's own K/V is expected to be in the suffix already.
  *  - Grouped-query heads: q head h reads kv head h / (Hq / Hkv).
- *  - KV pools are paged: [num_blocks][block_size=16][Hkv][D], row-major.  A
- *    block table lists physical block ids in logical order; the last block of
- *    a prefix or suffix may be partly filled, and its unused slots are never
- *    read.  A fork's suffix starts at slot 0 of its own first block.
+ *  - KV pools are paged in blocks of 16 tokens.  One block of one tensor is
+ *    contiguous and holds Hkv head slices of 16*D elements each:
+ *      K pool [num_blocks][Hkv][16][D]  (16 token rows of D values),
+ *      V pool [num_blocks][Hkv][D][16]  (transposed: D rows of 16 tokens),
+ *    i.e. K element (block b, kv head j, slot t, dim d) sits at
+ *    ((b*Hkv + j)*16 + t)*D + d and the V element at ((b*Hkv + j)*D + d)*16 + t.
+ *    A block table lists physical block ids in logical order; the last block
+ *    of a prefix or suffix may be partly filled, and the values in its unused
+ *    slots do not matter (they may be any bits, NaN included).  A fork's
+ *    suffix starts at slot 0 of its own first block.
  *  - out is bf16 (round to nearest even from fp32); out_lse is the natural-log
  *    log-sum-exp of the scaled scores, fp32.
  *  - E4M3 KV is the OCP 8-bit "E4M3FN" format (bias 7, max 448, no inf,
@@ -83,8 +89,8 @@ typedef struct {
   int32_t reserved;          /* must be 0                                        */
   /* device memory, caller-owned */
   const void *q;             /* [N][Hq][D] bf16                                  */
-  const void *k_pool;        /* [num_blocks][16][Hkv][D] kv_dtype                */
-  const void *v_pool;        /* same layout as k_pool                           */
+  const void *k_pool;        /* [num_blocks][Hkv][16][D] kv_dtype                */
+  const void *v_pool;        /* [num_blocks][Hkv][D][16] kv_dtype (transposed)   */
   const float *k_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
   const float *v_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
   const int32_t *fork_off;   /* [T+1], fork_off[0] = 0, nondecreasing, [T] = N;

@@ -110,7 +110,8 @@ typedef struct {
   int32_t kv_dtype;                  /* 0 = bf16, 1 = OCP E4M3 + block scale  */
   int32_t pad_;
   const uint16_t *q;                 /* [N][Hq][D] bf16 bits                  */
-  const void *k_pool, *v_pool;       /* [num_blocks][bs][Hkv][D]              */
+  const void *k_pool;                /* [num_blocks][Hkv][bs][D]              */
+  const void *v_pool;                /* [num_blocks][Hkv][D][bs]              */
   const float *k_scale, *v_scale;    /* [num_blocks] (E4M3 only)              */
   const int32_t *fork_off;           /* [T+1]                                 */
   const int32_t *prefix_len;         /* [T]                                   */
@@ -123,7 +124,8 @@ typedef struct {
 
 /* Element d of kv head j of logical token i of fork f (trace t): tokens
  * 0..P_t-1 come from the trace's prefix blocks, tokens P_t.. from the fork's
- * own suffix blocks; each block holds bs consecutive tokens. */
+ * own suffix blocks; each block holds bs consecutive tokens.  Inside a block,
+ * head j's K is bs rows of D elements and its V is D rows of bs elements. */
 static double kv_elem(const specgen_ref_batch_t *b, int is_v, int32_t t,
                       int32_t f, int64_t i, int32_t j, int32_t d) {
   const int32_t bs = b->block_size;
@@ -137,8 +139,9 @@ static double kv_elem(const specgen_ref_batch_t *b, int is_v, int32_t t,
     blk = b->suffix_table[b->suffix_table_off[f] + s / bs];
     slot = s % bs;
   }
-  const int64_t idx =
-      ((blk * bs + slot) * b->num_kv_heads + j) * (int64_t)b->head_dim + d;
+  const int64_t D = b->head_dim;
+  const int64_t head = blk * b->num_kv_heads + j;
+  const int64_t idx = is_v ? (head * D + d) * bs + slot : (head * bs + slot) * D + d;
   const void *pool = is_v ? b->v_pool : b->k_pool;
   if (b->kv_dtype == 0) return specgen_ref_bf16_to_f64(((const uint16_t *)pool)[idx]);
   const float *scale = is_v ? b->v_scale : b->k_scale;

@@ -1,4 +1,4 @@
-// attn_mfma2.hip -- the bf16 shared-prefix (and suffix) partial-attention
+// attn_bf16.hip -- the bf16 shared-prefix (and suffix) partial-attention
 // kernel on gfx950 matrix cores: eight waves per workgroup, tiles streamed
 // from HBM straight into LDS.
 //
@@ -8,25 +8,38 @@
 // once for all its forks, Sec. 4.2 / Sec. 8.7) or the g heads of one fork
 // (suffix item).
 //
+// KV layout.  Inside a pool block, kv head j's K is 16 token rows of D values
+// and its V is D rows of 16 token values (V transposed), each 16*D*2 bytes.
+// A tile of TT tokens is TT/16 such block slices per tensor.
+//
 // Slots.  The worker's range is a sequence of 32 KiB slots: for each item one
-// "q slot" (the item's query rows, up to 128 x D bf16) followed by its tiles
-// (TT tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
+// "q slot" (its query rows, up to 128 x D bf16) followed by its tiles (TT
+// tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
 // stages with three slots in flight.  Every wave moves exactly four 1 KiB
 // pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no VGPR
-// staging), so the number of vector-memory operations a wave has in flight
-// is known exactly and the wait for slot s is "vmcnt <= 4 x (slots issued
-// after s) + partial stores issued since".  These loads are issued from
-// inline asm: the compiler does not see them, so it neither drains them
-// (vmcnt(0)) before LDS reads nor reorders them across the LDS barriers.
+// staging; nontemporal, the KV is read once): waves 0-3 the K block slices of
+// a tile, waves 4-7 its V slices.  So the number of vector-memory operations
+// a wave has in flight is known exactly and the wait for slot s is
+// "vmcnt <= 4 x (slots issued after s) + partial stores issued since".  These
+// loads are issued from inline asm: the compiler does not see them, so it
+// neither drains them (vmcnt(0)) before LDS reads nor reorders them across
+// the LDS barriers.
 //
 // Rows and tokens.  An item with r rows uses RG = ceil(r / 32) <= 4 row groups
 // of 32 rows and splits each tile's tokens over TG = min(TT/32, 8/RG) token
 // groups: wave w computes row group w % RG over token group w / RG (two waves
 // per SIMD for the 128-row prefix items, so one wave's softmax overlaps the
 // other's MFMAs).  Items with fewer rows pad their last row group; they are
-// bound by their K/V bytes, not by the matrix cores.  At the
-// item's end the token groups are combined through the stage that was just
-// consumed, and token group 0 writes the normalised partial (o, lse).
+// bound by their K/V bytes, not by the matrix cores.  At the item's end the
+// token groups are combined through the stage that was just consumed, and
+// token group 0 writes the normalised partial (o, lse).
+//
+// Math per 32-token slab and 16-row N-tile: S^T = K Q^T on
+// v_mfma_f32_16x16x32_bf16 (A = 16 keys x 32 dims from LDS, B = Q^T in
+// VGPRs) with the keys of the two S^T tiles taken so that each lane's 8 scores
+// are the 8 consecutive tokens the PV operand needs; online softmax in base 2
+// with lazy rescaling; O^T += V^T P^T, where the A operand (16 dims x 32
+// tokens) is one 16-byte LDS read per lane because V is stored transposed.
 //
 // The accumulators live in VGPRs: this file is compiled with MFMA operands and
 // results in VGPRs (-amdgpu-mfma-vgpr-form), which leaves the whole 256-register
@@ -34,15 +47,10 @@
 // compiled without IEEE-mode NaN quieting (-mno-amdgpu-ieee -fno-honor-nans):
 // the row maxima would otherwise cost three instructions per element.  Masked
 // scores are -inf, never NaN, and infinities keep their meaning.
-//
-// Math per 32-token slab and 16-row tile (as in the four-wave kernel):
-// S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with keys taken so that each lane's
-// scores are the 8 consecutive tokens the PV operand needs, online softmax in
-// base 2 with lazy rescaling, O^T += V^T P^T with V^T from ds_read_b64_tr_b16.
 #include "worker.h"
 
 namespace specgen {
-namespace mfma2 {
+namespace bf16k {
 
 // The running max moves only when a new score would give a probability above
 // 2^kRescaleLog2 relative to it.
@@ -53,14 +61,16 @@ struct Cfg {
   static constexpr int kThreads = 512;
   static constexpr int kWaves = 8;
   static constexpr int kTT = (D == 128) ? 64 : 128;   // tokens per tile
-  static constexpr int kRowB = D * 2;                 // bytes per token (or q) row
+  static constexpr int kRowB = D * 2;                 // bytes per K (or q) row
   static constexpr int kCPR = kRowB / 16;             // 16-byte chunks per row
-  static constexpr int kTileB = kTT * kRowB;          // K (or V) bytes of a tile
+  static constexpr int kTileB = kTT * kRowB;          // K (or V) bytes of a tile: 16 KiB
+  static constexpr int kSliceB = 16 * kRowB;          // one block's slice of one kv head and tensor
   static constexpr int kStageB = 2 * kTileB;          // one slot
   static constexpr int kStages = 4;
-  static constexpr int kRPI = 1024 / kRowB;           // rows moved by one wave instruction
-  static constexpr int kDmaT = kTileB / 1024 / kWaves;  // instructions per wave per tensor
+  static constexpr int kRPI = 1024 / kRowB;           // K rows moved by one wave instruction
   static constexpr int kDmaSlot = 4;                  // instructions per wave per slot
+  static constexpr int kSlicesPerWave = kTT / 16 / 4; // block slices of a tile per wave (4 waves per tensor)
+  static constexpr int kPiecesPerSlice = kSliceB / 1024;
   static constexpr int kItemCap = 64;
   static constexpr int kMaxRows = 128;                // rows per item (row block)
   static constexpr int kOffItems = kStages * kStageB;
@@ -71,10 +81,10 @@ struct Cfg {
   static constexpr int kIdsPerTile = kTT / 16;
   static constexpr int kTileCap = kIdCap / kIdsPerTile;
   static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
-  static_assert(kDmaT * 2 == kDmaSlot, "a tile slot is four instructions per wave");
-  static_assert(kDmaT * kWaves * 1024 == kTileB, "tile split over the waves");
+  static_assert(kSlicesPerWave * kPiecesPerSlice == kDmaSlot, "a tile slot is four instructions per wave");
+  static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
-  static_assert(kMaxRows / kRPI <= kDmaSlot * kWaves, "q slot split over the waves");
+  static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
 };
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
@@ -83,16 +93,16 @@ template <int D>
 __device__ __forceinline__ int swz_q(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
 
 // One wave instruction: 64 lanes x 16 bytes from gbase + voff (per lane) into
-// LDS at lds_addr + 16 * lane.  gbase and lds_addr must be wave-uniform.
-// (The readfirstlanes only restate what holds: the compiler cannot always
-// prove these operands uniform, and an SGPR operand must be.)
+// LDS at lds_addr + 16 * lane, nontemporal.  gbase and lds_addr must be
+// wave-uniform.  (The readfirstlanes only restate what holds: the compiler
+// cannot always prove these operands uniform, and an SGPR operand must be.)
 __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t lds_addr) {
   const uint64_t g = reinterpret_cast<uint64_t>(gbase);
   const uint32_t glo = __builtin_amdgcn_readfirstlane((uint32_t)g);
   const uint32_t ghi = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
   const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
   const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gu), "s"(l) : "m0");
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
 }
 
 template <int N>
@@ -118,11 +128,11 @@ __device__ __forceinline__ void vm_wait_le(int n) {
   else vm_wait<0>();
 }
 
-}  // namespace mfma2
+}  // namespace bf16k
 
 template <int D>
-__global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, const Plan plan_arg) {
-  using namespace mfma2;
+__global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, const Plan plan_arg) {
+  using namespace bf16k;
   using C = Cfg<D>;
   constexpr int TT = C::kTT;
   constexpr int CPR = C::kCPR;
@@ -154,15 +164,15 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
 
   // Item descriptors are read from LDS once per item and kept in scalar registers.
   struct Desc {
-    int kind, t, f, j, ord, tile0, ntile, nv, taboff, nrows, row0, lastblk, rtile0;
+    int kind, t, f, j, ord, tile0, ntile, nv, nrows, row0, lastblk, rtile0;
   };
   auto load_desc = [&](int ii) {
     typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
     const SG_LDS i32x4* p = reinterpret_cast<const SG_LDS i32x4*>((SG_LDS uint8_t*)lds + C::kOffItems + ii * kItemInts * 4);
     const i32x4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
     static_assert(IT_KIND == 0 && IT_T == 1 && IT_F == 2 && IT_J == 3 && IT_ORD == 5 && IT_TILE0 == 6 &&
-                  IT_NTILE == 7 && IT_NVALID == 8 && IT_TABOFF == 9 && IT_NROWS == 10 && IT_ROW0 == 11 &&
-                  IT_RTILE0 == 12 && IT_LASTBLK == 14, "descriptor layout");
+                  IT_NTILE == 7 && IT_NVALID == 8 && IT_NROWS == 10 && IT_ROW0 == 11 && IT_RTILE0 == 12 &&
+                  IT_LASTBLK == 14, "descriptor layout");
     Desc d;
     d.kind = uniform(v0[0]);
     d.t = uniform(v0[1]);
@@ -172,7 +182,6 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     d.tile0 = uniform(v1[2]);
     d.ntile = uniform(v1[3]);
     d.nv = uniform(v2[0]);
-    d.taboff = uniform(v2[1]);
     d.nrows = uniform(v2[2]);
     d.row0 = uniform(v2[3]);
     d.lastblk = uniform(v3[2]);
@@ -181,37 +190,39 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   };
 
   // ---- issue side ------------------------------------------------------------
-  const int64_t head_stride = (int64_t)D * 2;                  // bytes between kv heads of a token
-  const uint32_t tok_stride = (uint32_t)(plan.Hkv * head_stride);  // bytes between tokens of a block
-  const int64_t blk_stride = 16 * (int64_t)tok_stride;
-  // this wave's blocks within a tile: tokens [16 * wblk, +16) of the tile hold
-  // both of its K (and V) instructions
-  const int wblk = (D == 128) ? (wave >> 1) : wave;
-  int tit[2], kch[2], vch[2];   // lane constants: token within the tile, swizzled source chunk
+  const int64_t head_stride = (int64_t)D * 2;   // bytes between q heads of a fork
+  const int64_t slice_stride = C::kSliceB;      // bytes between kv heads of a block
+  const int64_t blk_stride = (int64_t)plan.Hkv * slice_stride;
+  const bool is_v = wave >= 4;                  // waves 0-3 move K, waves 4-7 move V
+  const int wq = wave & 3;
+  // Lane constants for piece i of slice b of this wave (tile block
+  // kb = wq * kSlicesPerWave + b).  K: LDS chunk p of tile token row tt holds
+  // source chunk p ^ swz_k(tt).  V: the slice is D rows of 32 bytes (16 tokens);
+  // LDS position 2d + (h ^ bit 3 of d) holds the 16-byte half h of row d, so a
+  // 16-lane read of 16 consecutive rows hits distinct banks.  One instruction
+  // moves 1 KiB of the slice; for V, lanes with bit 4 set swap their halves.
+  constexpr int NB = C::kSlicesPerWave, NI = C::kPiecesPerSlice;
+  uint32_t src_off[NB][NI];   // byte offset in the block slice, full tile
+  int ptok[NI];               // K: token row of the slice this lane moves
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int n = wave * 2 + i;
-    tit[i] = n * C::kRPI + lane / CPR;
-    const int p = lane % CPR;
-    kch[i] = p ^ swz_k<CPR>(tit[i]);
-    vch[i] = p ^ swz_v<CPR>(tit[i]);
-  }
-  // lane offsets within the block for a tile whose tokens are all valid
-  uint32_t kofs[2], vofs[2];
+  for (int i = 0; i < NI; ++i) ptok[i] = i * C::kRPI + lane / CPR;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    kofs[i] = (uint32_t)(tit[i] & 15) * tok_stride + (uint32_t)(kch[i] * 16);
-    vofs[i] = (uint32_t)(tit[i] & 15) * tok_stride + (uint32_t)(vch[i] * 16);
-  }
-  // block index (within the item) of this wave's block of tile k, clamped to the last valid block
-  auto wave_block = [&](const Desc& d, int k) {
-    const int bi = (d.tile0 + k) * (TT / 16) + wblk;
-    return bi < d.lastblk ? bi : d.lastblk;
-  };
-  // physical id of that block, from the ids the worker gathered into LDS
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      if (is_v) {
+        src_off[b][i] = (uint32_t)(1024 * i + 16 * (lane ^ ((lane >> 4) & 1)));
+      } else {
+        const int tt = (wq * NB + b) * 16 + ptok[i];
+        src_off[b][i] = (uint32_t)(ptok[i] * C::kRowB + (((lane % CPR) ^ swz_k<CPR>(tt)) << 4));
+      }
+    }
+  // physical id of slice b of this wave in tile k of item d, from the ids the worker gathered into LDS
   const int32_t* ids = reinterpret_cast<const int32_t*>(lds + C::kOffIds);
-  auto block_id = [&](const Desc& d, int k) -> int { return uniform(ids[(d.rtile0 + k) * C::kIdsPerTile + wblk]); };
-  auto issue_slot = [&](const Desc& d, int k, int id, int stage) {
+  auto block_id = [&](const Desc& d, int k, int b) -> int {
+    return uniform(ids[(d.rtile0 + k) * C::kIdsPerTile + wq * NB + b]);
+  };
+  auto issue_slot = [&](const Desc& d, int k, const int (&id)[NB], int stage) {
     const uint32_t st = lds_base + (uint32_t)(stage * C::kStageB);
     if (k < 0) {
       // q rows of the item (rows past its end repeat its last row)
@@ -228,31 +239,27 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       }
     } else {
       const int tile = d.tile0 + k;
-      const uint8_t* kb = a.k_pool + (int64_t)id * blk_stride + d.j * head_stride;
-      const uint8_t* vb = a.v_pool + (int64_t)id * blk_stride + d.j * head_stride;
-      uint32_t ko[2], vo[2];
-      if ((tile + 1) * TT <= d.nv) {
+      const uint8_t* pool = is_v ? a.v_pool : a.k_pool;
+      const uint32_t tens = is_v ? (uint32_t)C::kTileB : 0u;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          ko[i] = kofs[i];
-          vo[i] = vofs[i];
+      for (int b = 0; b < NB; ++b) {
+        const int kb = wq * NB + b;   // block within the tile
+        const uint8_t* sb = pool + (int64_t)id[b] * blk_stride + d.j * slice_stride;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          uint32_t off = src_off[b][i];
+          if (!is_v && (tile + 1) * TT > d.nv) {
+            // K rows of tokens past the item's end re-read its last valid token
+            // (finite; their scores are masked).  V slices are moved whole: the
+            // math zeroes the values of tokens past the end.
+            int bi = tile * C::kIdsPerTile + kb;
+            bi = bi < d.lastblk ? bi : d.lastblk;
+            int tok = tile * TT + kb * 16 + ptok[i];
+            tok = tok < d.nv ? tok : d.nv - 1;
+            off = (uint32_t)((tok - bi * 16) * C::kRowB) + (off & (uint32_t)(C::kRowB - 1));
+          }
+          dma16(sb, off, st + tens + (uint32_t)(kb * C::kSliceB + i * 1024));
         }
-      } else {
-        const int bi = wave_block(d, k);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          int tok = tile * TT + tit[i];
-          tok = tok < d.nv ? tok : d.nv - 1;   // tokens past the end re-read the last valid one
-          const uint32_t row_off = (uint32_t)(tok - bi * 16) * tok_stride;
-          ko[i] = row_off + (uint32_t)(kch[i] * 16);
-          vo[i] = row_off + (uint32_t)(vch[i] * 16);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int n = wave * 2 + i;
-        dma16(kb, ko[i], st + (uint32_t)(n * 1024));
-        dma16(vb, vo[i], st + (uint32_t)(C::kTileB + n * 1024));
       }
     }
   };
@@ -262,10 +269,9 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   const int ln = lane & 15;    // row within an N-tile / key within an S^T tile
   const int k_lane_tok = 8 * (ln >> 2) + (ln & 3);
   const int k_lane_swz = swz_k<CPR>(k_lane_tok);
-  const int v_lane_tok = 8 * G + (ln >> 2);
-  const int v_lane_swz0 = swz_v<CPR>(v_lane_tok);
-  const int v_lane_swz1 = swz_v<CPR>(v_lane_tok + 4);
-  const int vsub = ln & 3;
+  // V^T operand of d-tile dt for a slab at token sb: block sb/16 + G/2 of the
+  // tile, row d = 16 dt + ln, half G & 1 -> LDS position 2d + (half ^ bit 3 of d)
+  const int v_lane_off = (G >> 1) * C::kSliceB + 32 * ln + 16 * ((G & 1) ^ ((ln >> 3) & 1));
   bf16x8 qop[2][KS];
   f32x4 acc[2][DT];
   float m_run[2], l_run[2];
@@ -283,14 +289,12 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     active = wave < RG * TG;
     const SG_LDS uint8_t* qb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      if (nt < NT) {
-        const int row = rg * RS + nt * 16 + ln;
+    for (int nt = 0; nt < NT; ++nt) {
+      const int row = rg * RS + nt * 16 + ln;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const int slot = (ks * 4 + G) ^ swz_q<D>(row);
-          qop[nt][ks] = *reinterpret_cast<const SG_LDS bf16x8*>(qb + row * C::kRowB + slot * 16);
-        }
+      for (int ks = 0; ks < KS; ++ks) {
+        const int slot = (ks * 4 + G) ^ swz_q<D>(row);
+        qop[nt][ks] = *reinterpret_cast<const SG_LDS bf16x8*>(qb + row * C::kRowB + slot * 16);
       }
       m_run[nt] = -INFINITY;
       l_run[nt] = 0.f;
@@ -301,15 +305,14 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
 
   // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
   auto slab = [&](auto mask_c, int stage, int sb, int valid) {
-    constexpr int NTc = NT;
     constexpr bool kMask = decltype(mask_c)::value;   // the slab runs past the tile's valid tokens
     const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
     const SG_LDS uint8_t* vb = kb + C::kTileB;
-    f32x4 s[2][NTc];
+    f32x4 s[2][NT];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int nt = 0; nt < NTc; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < NT; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
     const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
 #pragma unroll
@@ -318,7 +321,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       const bf16x8 A0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
       const bf16x8 A1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
 #pragma unroll
-      for (int nt = 0; nt < NTc; ++nt) {
+      for (int nt = 0; nt < NT; ++nt) {
         s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, qop[nt][ks], s[0][nt], 0, 0, 0);
         s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, qop[nt][ks], s[1][nt], 0, 0, 0);
       }
@@ -331,12 +334,12 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
         for (int e = 0; e < 4; ++e)
           if (sb + 8 * G + 4 * u + e >= valid) {
 #pragma unroll
-            for (int nt = 0; nt < NTc; ++nt) s[u][nt][e] = -INFINITY;
+            for (int nt = 0; nt < NT; ++nt) s[u][nt][e] = -INFINITY;
           }
     }
-    bf16x8 pop[NTc];
+    bf16x8 pop[NT];
 #pragma unroll
-    for (int nt = 0; nt < NTc; ++nt) {
+    for (int nt = 0; nt < NT; ++nt) {
       float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
                        fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
       mx = rows4_max(mx);
@@ -365,19 +368,23 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       pk[3] = pack_bf16x2(p[6], p[7]);
       pop[nt] = __builtin_bit_cast(bf16x8, pk);
     }
-    // O^T += V^T P^T ; the transposing read gives lane (G, ln) V[sb+8G+4h+e][16dt+ln]
-    const SG_LDS uint8_t* v_row0 = vb + (sb + v_lane_tok) * C::kRowB;
-    const SG_LDS uint8_t* v_row1 = v_row0 + 4 * C::kRowB;
+    // O^T += V^T P^T: lane (G, ln) reads V[sb+8G+0..7][16dt+ln] in one 16-byte load
+    u32x4 vkeep = {~0u, ~0u, ~0u, ~0u};   // masked slab: keep only the values of valid tokens
+    if constexpr (kMask) {
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int t0 = sb + 8 * G + 2 * e2;
+        vkeep[e2] = (t0 < valid ? 0x0000FFFFu : 0u) | (t0 + 1 < valid ? 0xFFFF0000u : 0u);
+      }
+    }
+    const SG_LDS uint8_t* vrow = vb + (sb >> 4) * C::kSliceB + v_lane_off;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const int ch = 2 * dt + (vsub >> 1);
-      const int off0 = ((ch ^ v_lane_swz0) << 4) + ((vsub & 1) << 3);
-      const int off1 = ((ch ^ v_lane_swz1) << 4) + ((vsub & 1) << 3);
-      const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row0 + off0));
-      const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row1 + off1));
-      const bf16x8 A = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+      u32x4 vv = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
+      if constexpr (kMask) vv &= vkeep;   // values past the end may be any bits, NaN included
+      const bf16x8 A = __builtin_bit_cast(bf16x8, vv);
 #pragma unroll
-      for (int nt = 0; nt < NTc; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
+      for (int nt = 0; nt < NT; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
     }
   };
 
@@ -412,14 +419,13 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
         if (active && tg >= 1 && windex / per_round == r) {
           float* dst = cb + (windex % per_round) * (wave_bytes / 4);
 #pragma unroll
-          for (int nt = 0; nt < 2; ++nt)
-            if (nt < NT) {
+          for (int nt = 0; nt < NT; ++nt) {
 #pragma unroll
-              for (int dt = 0; dt < DT; ++dt)
-                *reinterpret_cast<f32x4*>(dst + ((nt * DT + dt) * 64 + lane) * 4) = acc[nt][dt];
-              ml[((wave * 2 + nt) * 64 + lane) * 2 + 0] = m_run[nt];
-              ml[((wave * 2 + nt) * 64 + lane) * 2 + 1] = lrow[nt];
-            }
+            for (int dt = 0; dt < DT; ++dt)
+              *reinterpret_cast<f32x4*>(dst + ((nt * DT + dt) * 64 + lane) * 4) = acc[nt][dt];
+            ml[((wave * 2 + nt) * 64 + lane) * 2 + 0] = m_run[nt];
+            ml[((wave * 2 + nt) * 64 + lane) * 2 + 1] = lrow[nt];
+          }
         }
         lds_barrier();
         if (active && tg == 0) {
@@ -429,22 +435,22 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
             const int pw = t2 * RG + rg;   // the partner wave
             const float* src = cb + (wi % per_round) * (wave_bytes / 4);
 #pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-              if (nt < NT) {
-                const float m1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 0];
-                const float l1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 1];
-                const float m = fmaxf(m_run[nt], m1);
-                const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
-                const float a0 = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
-                const float a1 = __builtin_amdgcn_exp2f(m1 * a.c_log2 - mc);
+            for (int nt = 0; nt < NT; ++nt) {
+              // a token group that saw no token of the item has m = -inf, l = 0, acc = 0
+              const float m1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 0];
+              const float l1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 1];
+              const float m = fmaxf(m_run[nt], m1);
+              const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
+              const float a0 = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
+              const float a1 = __builtin_amdgcn_exp2f(m1 * a.c_log2 - mc);
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                  const f32x4 o1 = *reinterpret_cast<const f32x4*>(src + ((nt * DT + dt) * 64 + lane) * 4);
-                  acc[nt][dt] = acc[nt][dt] * a0 + o1 * a1;
-                }
-                lrow[nt] = lrow[nt] * a0 + l1 * a1;
-                m_run[nt] = m;
+              for (int dt = 0; dt < DT; ++dt) {
+                const f32x4 o1 = *reinterpret_cast<const f32x4*>(src + ((nt * DT + dt) * 64 + lane) * 4);
+                acc[nt][dt] = acc[nt][dt] * a0 + o1 * a1;
               }
+              lrow[nt] = lrow[nt] * a0 + l1 * a1;
+              m_run[nt] = m;
+            }
           }
         }
       }
@@ -460,16 +466,15 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     // every lane stores (rows past the item's end land in unused rows of the
     // slot), so the number of stores is the same on every path
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-      if (nt < NT) {
-        const int row = rg * RS + nt * 16 + ln;
-        const float inv = 1.f / lrow[nt];
+    for (int nt = 0; nt < NT; ++nt) {
+      const int row = rg * RS + nt * 16 + ln;
+      const float inv = 1.f / lrow[nt];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G) = acc[nt][dt] * inv;
-        ls[row] = m_run[nt] * a.sm_scale + __logf(lrow[nt]);
-        stores += DT + 1;
-      }
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G) = acc[nt][dt] * inv;
+      ls[row] = m_run[nt] * a.sm_scale + __logf(lrow[nt]);
+      stores += DT + 1;
+    }
     return stores;
   };
 
@@ -483,11 +488,14 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       if (ii < nitems) d = load_desc(ii);
     }
   };
-  int is_ii = 0, is_k = -1, is_id = 0, issued = 0;   // next slot to issue and its block id
+  int is_ii = 0, is_k = -1, issued = 0;   // next slot to issue
+  int is_id[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) is_id[b] = 0;
   Desc is_d = load_desc(0);
   // slot 0 is the first item's q rows; its load overlaps the gather of every
   // block id the range reads (clamped to each item's last valid block)
-  issue_slot(is_d, is_k, 0, 0);
+  issue_slot(is_d, is_k, is_id, 0);
   advance(is_ii, is_k, is_d);
   ++issued;
   {
@@ -504,15 +512,21 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
     }
   }
   __syncthreads();
-  for (int p = 1; p < 3; ++p) {
+  auto load_ids = [&]() {   // block ids of the next slot to issue, if it is a tile
+    if (issued < S && is_k >= 0) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) is_id[b] = block_id(is_d, is_k, b);
+    }
+  };
+  for (int p = 1; p < C::kStages - 1; ++p) {
     if (issued < S) {
-      if (is_k >= 0) is_id = block_id(is_d, is_k);
+      load_ids();
       issue_slot(is_d, is_k, is_id, issued & 3);
       advance(is_ii, is_k, is_d);
       ++issued;
     }
   }
-  if (issued < S && is_k >= 0) is_id = block_id(is_d, is_k);
+  load_ids();
   int st1 = 0, st2 = 0, st3 = 0;   // stores issued one, two and three iterations ago
   int cp_ii = 0, cp_k = -1;
   Desc cp_d = load_desc(0);
@@ -526,7 +540,7 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
       issue_slot(is_d, is_k, is_id, issued & 3);   // into the stage consumed last iteration
       advance(is_ii, is_k, is_d);
       ++issued;
-      if (issued < S && is_k >= 0) is_id = block_id(is_d, is_k);   // used next iteration
+      load_ids();   // used next iteration
     }
     const int stage = s & 3;
     int st0 = 0;
@@ -543,17 +557,17 @@ __global__ void __launch_bounds__(512, 1) attn_mfma2_kernel(const AttnArgs a, co
   }
 }
 
-hipError_t launch_attn_mfma2(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
+hipError_t launch_attn_bf16(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
   if (plan.D == 128)
-    hipLaunchKernelGGL((attn_mfma2_kernel<128>), dim3(W), dim3(512), 0, stream, a, plan);
+    hipLaunchKernelGGL((attn_bf16_kernel<128>), dim3(W), dim3(512), 0, stream, a, plan);
   else
-    hipLaunchKernelGGL((attn_mfma2_kernel<64>), dim3(W), dim3(512), 0, stream, a, plan);
+    hipLaunchKernelGGL((attn_bf16_kernel<64>), dim3(W), dim3(512), 0, stream, a, plan);
   return hipGetLastError();
 }
 
-int mfma2_item_cap() { return mfma2::Cfg<128>::kItemCap; }
-int mfma2_tile_cap(int D) { return D == 128 ? mfma2::Cfg<128>::kTileCap : mfma2::Cfg<64>::kTileCap; }
+int bf16_item_cap() { return bf16k::Cfg<128>::kItemCap; }
+int bf16_tile_cap(int D) { return D == 128 ? bf16k::Cfg<128>::kTileCap : bf16k::Cfg<64>::kTileCap; }
 
 }  // namespace specgen

@@ -9,7 +9,8 @@
 // online-softmax state (m, l, o) per row.  Streams are combined with
 // cross-lane shuffles, waves through LDS, and one normalised partial (o, lse)
 // per item is written for the log-sum-exp merge.  K/V come straight from HBM
-// into registers, one tile ahead of the math.
+// into registers, one tile ahead of the math (V, stored transposed, as the
+// stream's 4 consecutive tokens of each of the lane's dims).
 #include "worker.h"
 
 namespace specgen {
@@ -67,11 +68,16 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
   if (R <= 0) return;
   const int nitems = wr.nitems;
 
-  const int64_t head_stride = (int64_t)D * C::kGElem;
-  const int64_t tok_stride = (int64_t)plan.Hkv * head_stride;
+  // Inside a pool block, kv head j's K is 16 token rows of D values and its V
+  // is D rows of 16 token values (V transposed).  A lane loads, for each of
+  // its stream's TB tokens, its DPL dims of K, and for each of its DPL dims the
+  // stream's TB consecutive tokens of V.
+  const int64_t slice_b = (int64_t)16 * D * C::kGElem;
+  constexpr int VW = TB * C::kGElem / 4;   // 32-bit words of TB tokens of one V dim
   typedef typename std::conditional<FP8, uint32_t[DPL / 4], uint32_t[DPL / 2]>::type raw_t;
   struct Raw {
-    raw_t k[TB], v[TB];
+    raw_t k[TB];
+    uint32_t v[DPL][VW];
   };
   // this lane's tokens of tile r: wave*16 + grp*4 + i (one 16-token block per wave)
   auto load_tile = [&](Raw& raw, int r) {
@@ -81,35 +87,41 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
     const int j = uniform(d[IT_J]);
     const int nv = uniform(d[IT_NVALID]);
     const int tbase = (uniform(d[IT_TILE0]) + (r - uniform(d[IT_RTILE0]))) * C::kTT;
+    // clamped tokens sit in the item's last block, which ids[] already holds
     const int blk = ids[r * C::kIdsPerTile + wave];
+    const uint8_t* kslice = a.k_pool + ((int64_t)blk * plan.Hkv + j) * slice_b;
+    const uint8_t* vslice = a.v_pool + ((int64_t)blk * plan.Hkv + j) * slice_b;
 #pragma unroll
     for (int i = 0; i < TB; ++i) {
       int ti = tbase + wave * 16 + grp * TB + i;
       if (ti >= nv) ti = nv - 1;
-      // clamped tokens sit in the item's last block, which ids[] already holds
-      const int64_t off = ((int64_t)blk * 16 + (ti & 15)) * tok_stride + j * head_stride + sub * DPL * C::kGElem;
+      const int64_t off = (int64_t)(ti & 15) * D * C::kGElem + sub * DPL * C::kGElem;
       if constexpr (FP8) {
         if constexpr (DPL == 8) {
-          const u32x2 kk = *reinterpret_cast<const u32x2*>(a.k_pool + off);
-          const u32x2 vv = *reinterpret_cast<const u32x2*>(a.v_pool + off);
+          const u32x2 kk = *reinterpret_cast<const u32x2*>(kslice + off);
           raw.k[i][0] = kk[0]; raw.k[i][1] = kk[1];
-          raw.v[i][0] = vv[0]; raw.v[i][1] = vv[1];
         } else {
-          raw.k[i][0] = *reinterpret_cast<const uint32_t*>(a.k_pool + off);
-          raw.v[i][0] = *reinterpret_cast<const uint32_t*>(a.v_pool + off);
+          raw.k[i][0] = *reinterpret_cast<const uint32_t*>(kslice + off);
         }
       } else {
         if constexpr (DPL == 8) {
-          const u32x4 kk = *reinterpret_cast<const u32x4*>(a.k_pool + off);
-          const u32x4 vv = *reinterpret_cast<const u32x4*>(a.v_pool + off);
+          const u32x4 kk = *reinterpret_cast<const u32x4*>(kslice + off);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) { raw.k[i][e] = kk[e]; raw.v[i][e] = vv[e]; }
+          for (int e = 0; e < 4; ++e) raw.k[i][e] = kk[e];
         } else {
-          const u32x2 kk = *reinterpret_cast<const u32x2*>(a.k_pool + off);
-          const u32x2 vv = *reinterpret_cast<const u32x2*>(a.v_pool + off);
+          const u32x2 kk = *reinterpret_cast<const u32x2*>(kslice + off);
           raw.k[i][0] = kk[0]; raw.k[i][1] = kk[1];
-          raw.v[i][0] = vv[0]; raw.v[i][1] = vv[1];
         }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) {
+      const int64_t off = (int64_t)((sub * DPL + e) * 16 + grp * TB) * C::kGElem;
+      if constexpr (VW == 2) {
+        const u32x2 vv = *reinterpret_cast<const u32x2*>(vslice + off);
+        raw.v[e][0] = vv[0]; raw.v[e][1] = vv[1];
+      } else {
+        raw.v[e][0] = *reinterpret_cast<const uint32_t*>(vslice + off);
       }
     }
   };
@@ -163,16 +175,25 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
     uint32_t kp[TB][NP];
     float vf[TB][DPL];
 #pragma unroll
-    for (int i = 0; i < TB; ++i) {
-      pairs(raw.k[i], kp[i]);
-      uint32_t vp[NP];
-      pairs(raw.v[i], vp);
+    for (int i = 0; i < TB; ++i) pairs(raw.k[i], kp[i]);
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        vf[i][2 * q] = __uint_as_float(vp[q] << 16);
-        vf[i][2 * q + 1] = __uint_as_float(vp[q] & 0xFFFF0000u);
+    for (int e = 0; e < DPL; ++e) {
+      if constexpr (FP8) {   // exact E4M3 decode of the TB tokens of dim e
+        const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(raw.v[e][0], false);
+        const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(raw.v[e][0], true);
+        vf[0][e] = lo[0]; vf[1][e] = lo[1]; vf[2][e] = hi[0]; vf[3][e] = hi[1];
+      } else {
+#pragma unroll
+        for (int i = 0; i < TB; ++i) vf[i][e] = __uint_as_float((raw.v[e][i >> 1] >> (16 * (i & 1))) << 16);
       }
     }
+    // values of tokens past the item's end may be any bits, NaN included
+#pragma unroll
+    for (int i = 0; i < TB; ++i)
+      if (tok0 + i >= nv) {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) vf[i][e] = 0.f;
+      }
     float ksc = 1.f, vsc = 1.f;
     if constexpr (FP8) {
       ksc = scales[r * C::kIdsPerTile + wave];

@@ -9,14 +9,16 @@
 // per fork (forks reuse the prefix cache, Sec. 4.2 / Sec. 8.7).  For a suffix
 // item the rows are one fork's g query heads (padded to 32 rows per wave).
 //
-// Data path per tile (D=128 bf16: 64 tokens, 16 KiB of K + 16 KiB of V):
-//   HBM --global_load_dwordx4--> VGPRs (two tiles in flight) --ds_write_b128-->
-//   XOR-swizzled LDS --ds_read_b128 (K) / ds_read_b64_tr_b16 (V)--> MFMA.
+// This kernel serves E4M3 KV (bf16 KV has its own kernel, attn_bf16.hip).
+// Data path per tile (D=128: 64 tokens, 8 KiB of K codes + 8 KiB of V codes):
+//   HBM --global_load_dwordx2--> VGPRs (three tiles in flight) --exact E4M3 to
+//   bf16, ds_write_b128--> swizzled LDS --ds_read_b128 (K rows; V^T rows, as V
+//   is stored transposed)--> MFMA.
 // Per 32-token slab and 16-row N-tile, S^T = K Q^T on v_mfma_f32_16x16x32_bf16
 // (A = 16 keys x 32 dims, B = Q^T 32 dims x 16 rows); the keys of the two S^T
 // tiles are taken in the order that makes each lane's scores the 8
 // consecutive tokens PV consumes, so the scores feed O^T = V^T P^T (A = V^T 16
-// dims x 32 tokens from the transposing LDS read, B = P^T) without a shuffle.
+// dims x 32 tokens, one 16-byte LDS read per lane, B = P^T) without a shuffle.
 // Online softmax in fp32 per row; each worker writes one normalised partial
 // (o, lse) per item it touched, merged later by the log-sum-exp rule.
 #include "kernels.h"
@@ -36,6 +38,7 @@ struct MfmaCfg {
   static constexpr int kRowB = D * 2;                 // LDS bytes per token row (bf16)
   static constexpr int kCPR = kRowB / 16;             // 16-byte chunks per LDS row
   static constexpr int kTileB = kTT * kRowB;          // LDS bytes of one K or V tile
+  static constexpr int kSliceB = 16 * kRowB;          // LDS bytes of one block's V^T slice
   static constexpr int kLoads = kTileB / 16 / kThreads;  // chunks per thread per tensor
   static constexpr int kGElem = FP8 ? 1 : 2;          // pool bytes per element
   static constexpr int kGChunk = 8 * kGElem;          // pool bytes per LDS chunk
@@ -84,9 +87,11 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   if (R <= 0) return;
 
   // ---- loads: tile r of the range into registers ------------------------------
+  // Inside a pool block, kv head j's K is 16 token rows of D values and its V
+  // is D rows of 16 token values (V transposed).  A K chunk is 8 values of one
+  // token; a V chunk is 8 tokens of one dim (half h of row d of a block slice).
   typedef typename std::conditional<FP8, u32x2, u32x4>::type chunk_t;
-  const int64_t head_stride = (int64_t)D * C::kGElem;               // bytes between kv heads
-  const int64_t tok_stride = (int64_t)plan.Hkv * head_stride;       // bytes between tokens
+  const int64_t slice_b = (int64_t)16 * D * C::kGElem;   // one block's slice of one kv head
   auto tile_item = [&](int r) { return item_of_tile(items, nitems, r); };
   // Loads are issued unconditionally so the compiler can count outstanding
   // vector loads exactly across the pipeline; past the range end every lane
@@ -104,15 +109,23 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
 #pragma unroll
     for (int it = 0; it < C::kLoads; ++it) {
       const int c = it * C::kThreads + tid;
+      // K: token row tok, chunk part
       const int tok = c / C::kCPR;
       const int part = c % C::kCPR;
       int ti = tbase + tok;
-      if (ti >= nv) ti = nv - 1;
-      const int blk = ids[rr * C::kIdsPerTile + tok / 16];
-      int64_t off = ((int64_t)blk * 16 + (ti & 15)) * tok_stride + j * head_stride + part * C::kGChunk;
-      off = real ? off : 0;
-      rk[it] = *reinterpret_cast<const chunk_t*>(kp + off);
-      rv[it] = *reinterpret_cast<const chunk_t*>(vp + off);
+      if (ti >= nv) ti = nv - 1;   // rows past the item's end re-read its last valid token
+      const int kblk = ids[rr * C::kIdsPerTile + tok / 16];
+      int64_t koff = ((int64_t)kblk * plan.Hkv + j) * slice_b + (int64_t)(ti & 15) * D * C::kGElem + part * C::kGChunk;
+      // V: block kb of the tile, row d, half h
+      const int kb = c / (2 * D);
+      const int dd = (c % (2 * D)) >> 1;
+      const int h = c & 1;
+      const int vblk = ids[rr * C::kIdsPerTile + kb];
+      int64_t voff = ((int64_t)vblk * plan.Hkv + j) * slice_b + (int64_t)(dd * 16 + 8 * h) * C::kGElem;
+      koff = real ? koff : 0;
+      voff = real ? voff : 0;
+      rk[it] = *reinterpret_cast<const chunk_t*>(kp + koff);
+      rv[it] = *reinterpret_cast<const chunk_t*>(vp + voff);
     }
   };
   auto to_lds_chunk = [&](const chunk_t& v) -> u32x4 {
@@ -132,16 +145,31 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
       return v;
     }
   };
-  auto store = [&](const chunk_t (&rk)[C::kLoads], const chunk_t (&rv)[C::kLoads], int stage_off) {
+  // V chunk c of tile r lands at LDS position 2d + (h ^ bit 3 of d) of its block
+  // slice (a 16-lane read of 16 consecutive dims hits distinct banks); values of
+  // tokens past the item's end may be any bits and are zeroed here.
+  auto store = [&](const chunk_t (&rk)[C::kLoads], const chunk_t (&rv)[C::kLoads], int stage_off, int r) {
+    const int rr = r < R ? r : R - 1;
+    const int32_t* d = items + uniform(tile_item(rr)) * kItemInts;
+    const int nv = uniform(d[IT_NVALID]);
+    const int tbase = (uniform(d[IT_TILE0]) + (rr - uniform(d[IT_RTILE0]))) * TT;
 #pragma unroll
     for (int it = 0; it < C::kLoads; ++it) {
       const int c = it * C::kThreads + tid;
       const int tok = c / C::kCPR;
       const int part = c % C::kCPR;
       const int kpos = tok * C::kRowB + ((part ^ swz_k<C::kCPR>(tok)) << 4);
-      const int vpos = tok * C::kRowB + ((part ^ swz_v<C::kCPR>(tok)) << 4);
+      const int kb = c / (2 * D);
+      const int dd = (c % (2 * D)) >> 1;
+      const int h = c & 1;
+      const int vpos = kb * C::kSliceB + 16 * (2 * dd + (h ^ ((dd >> 3) & 1)));
+      u32x4 vv = to_lds_chunk(rv[it]);
+      const int t0 = tbase + kb * 16 + 8 * h;   // first token of the chunk
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2)
+        vv[e2] &= (t0 + 2 * e2 < nv ? 0x0000FFFFu : 0u) | (t0 + 2 * e2 + 1 < nv ? 0xFFFF0000u : 0u);
       *reinterpret_cast<SG_LDS u32x4*>((SG_LDS uint8_t*)lds + stage_off + kpos) = to_lds_chunk(rk[it]);
-      *reinterpret_cast<SG_LDS u32x4*>((SG_LDS uint8_t*)lds + stage_off + C::kTileB + vpos) = to_lds_chunk(rv[it]);
+      *reinterpret_cast<SG_LDS u32x4*>((SG_LDS uint8_t*)lds + stage_off + C::kTileB + vpos) = vv;
     }
   };
 
@@ -150,13 +178,11 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   const int ln = lane & 15;    // row within an N-tile / key within an S^T tile
   // Lane-constant parts of the LDS addresses (slab bases are multiples of 32):
   // the key this lane feeds to S^T tile a (tile b is 4 keys later) and its
-  // swizzle, and the keys / swizzles of this lane's two transposing V reads.
+  // swizzle, and this lane's V^T operand position: block sb/16 + G/2 of the
+  // tile, row d = 16 dt + ln, half G & 1.
   const int k_lane_tok = 8 * (ln >> 2) + (ln & 3);
   const int k_lane_swz = swz_k<C::kCPR>(k_lane_tok);
-  const int v_lane_tok = 8 * G + (ln >> 2);
-  const int v_lane_swz0 = swz_v<C::kCPR>(v_lane_tok);
-  const int v_lane_swz1 = swz_v<C::kCPR>(v_lane_tok + 4);
-  const int vsub = ln & 3;
+  const int v_lane_off = (G >> 1) * C::kSliceB + 32 * ln + 16 * ((G & 1) ^ ((ln >> 3) & 1));
   bf16x8 qop[2][KS];
   f32x4 acc[2][DT];
   float m_run[2], l_run[2];
@@ -279,17 +305,11 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
         pk[3] = pack_bf16x2(p[6], p[7]);
         pop[nt] = __builtin_bit_cast(bf16x8, pk);
       }
-      // O^T += V^T P^T ; the transposing read gives lane (G, ln) V[sb+8G+4h+e][16dt+ln]
-      const SG_LDS uint8_t* v_row0 = vb + (sb + v_lane_tok) * C::kRowB;
-      const SG_LDS uint8_t* v_row1 = v_row0 + 4 * C::kRowB;
+      // O^T += V^T P^T: lane (G, ln) reads V[sb+8G+0..7][16dt+ln] in one 16-byte load
+      const SG_LDS uint8_t* vrow = vb + (sb >> 4) * C::kSliceB + v_lane_off;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int ch = 2 * dt + (vsub >> 1);
-        const int off0 = ((ch ^ v_lane_swz0) << 4) + ((vsub & 1) << 3);
-        const int off1 = ((ch ^ v_lane_swz1) << 4) + ((vsub & 1) << 3);
-        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row0 + off0));
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((SG_LDS bf16x4*)(v_row1 + off1));
-        const bf16x8 A = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8 A = *reinterpret_cast<const SG_LDS bf16x8*>(vrow + dt * 512);
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
       }
@@ -367,7 +387,7 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   issue(kA, vA, 0);
   issue(kB, vB, 1);
   issue(kC, vC, 2);
-  store(kA, vA, stage_of(0));
+  store(kA, vA, stage_of(0), 0);
   issue(kA, vA, 3);
   lds_barrier();
 
@@ -388,15 +408,15 @@ __global__ void __launch_bounds__(256, 1) attn_mfma_kernel(const AttnArgs a, con
   // the loads behind them are harmless re-reads of q.
   for (int r = 0; r < R; r += 3) {
     step(r, stage_of(r));
-    store(kB, vB, stage_of(r + 1));
+    store(kB, vB, stage_of(r + 1), r + 1);
     issue(kB, vB, r + 4);
     lds_barrier();
     step(r + 1, stage_of(r + 1));
-    store(kC, vC, stage_of(r + 2));
+    store(kC, vC, stage_of(r + 2), r + 2);
     issue(kC, vC, r + 5);
     lds_barrier();
     step(r + 2, stage_of(r + 2));
-    store(kA, vA, stage_of(r + 3));
+    store(kA, vA, stage_of(r + 3), r + 3);
     issue(kA, vA, r + 6);
     lds_barrier();
   }
@@ -415,14 +435,14 @@ int mfma_tile_tokens(int D, bool fp8) {
   return D == 128 ? MfmaCfg<128, false>::kTT : MfmaCfg<64, false>::kTT;
 }
 int mfma_item_cap() { return MfmaCfg<128, false>::kItemCap; }
-// bf16 KV runs on the eight-wave kernel (attn_mfma2.hip).
+// bf16 KV runs on the four-wave 64-rows-per-wave kernel (attn_bf16.hip).
 int mfma_tile_cap(int D, bool fp8) {
-  if (!fp8) return mfma2_tile_cap(D);
+  if (!fp8) return bf16_tile_cap(D);
   return D == 128 ? MfmaCfg<128, true>::kTileCap : MfmaCfg<64, true>::kTileCap;
 }
 
 hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream) {
-  if (!fp8) return launch_attn_mfma2(a, plan, stream);
+  if (!fp8) return launch_attn_bf16(a, plan, stream);
   return plan.D == 128 ? launch_attn_mfma_t<128, true>(a, plan, stream) : launch_attn_mfma_t<64, true>(a, plan, stream);
 }
 

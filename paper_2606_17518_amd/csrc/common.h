@@ -99,7 +99,8 @@ __device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >
 // Partial-result and plan arguments shared by the attention kernels.
 struct AttnArgs {
   const uint16_t* __restrict__ q;          // [N][Hq][D] bf16 bits
-  const uint8_t* __restrict__ k_pool;      // [blocks][16][Hkv][D] kv elements
+  const uint8_t* __restrict__ k_pool;      // [blocks][Hkv][16][D] kv elements
+  // v_pool: [blocks][Hkv][D][16] (transposed)
   const uint8_t* __restrict__ v_pool;
   const float* __restrict__ k_scale;       // [blocks] (E4M3 only)
   const float* __restrict__ v_scale;

@@ -4,7 +4,7 @@
 // restores it into the serving cache instead of recomputing the prefix
 // (Sec. 6.2.3).  Here the restored copy sits in a contiguous staging buffer
 // and every staging block i is scattered to pool block dst[i].  A block is
-// contiguous in both places ([16][Hkv][D] of one tensor), so the copy is a
+// contiguous in both places (16 tokens x Hkv x D of one tensor), so the copy is a
 // stream of coalesced 16-byte loads and stores: one workgroup per (tensor,
 // staging block), each thread moving 16-byte vectors, loads batched ahead of
 // stores so several are in flight per thread.  Ids outside the pool are

@@ -16,6 +16,11 @@ Draw order (numpy PCG64, one generator per batch):
      E4M3 with one fp32 scale per physical block = amax / 448 (1 if amax = 0);
   5. every pool slot that holds no valid token is set to NaN (bf16 0x7FC0,
      E4M3 0x7F), as is the scale of every unused block.
+
+Pool layout (one block of 16 tokens is contiguous, each kv head's slice of a
+block is contiguous inside it):
+  K pool [num_blocks][Hkv][16][D]  -- token rows of D elements;
+  V pool [num_blocks][Hkv][D][16]  -- transposed: rows of 16 tokens per dim.
 """
 from __future__ import annotations
 
@@ -44,8 +49,8 @@ class ForkBatch:
     sm_scale: float
     kv_dtype: str                       # "bf16" | "fp8_e4m3"
     q: np.ndarray                       # [N][Hq][D] uint16 (bf16 bits)
-    k_pool: np.ndarray                  # [NB][bs][Hkv][D] uint16 bits or uint8 codes
-    v_pool: np.ndarray
+    k_pool: np.ndarray                  # [NB][Hkv][bs][D] uint16 bits or uint8 codes
+    v_pool: np.ndarray                  # [NB][Hkv][D][bs]
     k_scale: Optional[np.ndarray]       # [NB] float32 (E4M3 only)
     v_scale: Optional[np.ndarray]
     fork_off: np.ndarray                # [T+1] int32
@@ -184,6 +189,7 @@ def make_fork_batch(*, prefix_lens: Sequence[int] | None = None,
     nan = E4M3_NAN if fp8 else BF16_NAN
     pools, scales, logical, logical_sc = [], [], [], []
     for which in ("k", "v"):
+        # pools are built token-major ([NB][bs][Hkv][D]) and laid out at the end
         pool = np.full((num_blocks, bs, Hkv, D), nan, dtype=el_dt)
         scale = np.full(num_blocks, np.nan, dtype=np.float32) if fp8 else None
         seg_logical = [] if keep_logical else None
@@ -219,7 +225,9 @@ def make_fork_batch(*, prefix_lens: Sequence[int] | None = None,
             if keep_logical:
                 seg_logical.append(flat[:n].copy())
                 seg_sc.append(np.repeat(scale[blocks], bs)[:n].copy() if fp8 else np.ones(n, np.float32))
-        pools.append(pool)
+        # K: [NB][Hkv][bs][D]; V: [NB][Hkv][D][bs]
+        axes = (0, 2, 1, 3) if which == "k" else (0, 2, 3, 1)
+        pools.append(np.ascontiguousarray(pool.transpose(axes)))
         scales.append(scale)
         logical.append(seg_logical)
         logical_sc.append(seg_sc)

@@ -276,7 +276,7 @@ def test_fork_independence():
     # perturb fork 2's suffix values (its own blocks only)
     ids = b.suffix_table[b.suffix_table_off[2]:b.suffix_table_off[3]]
     rng = np.random.default_rng(99)
-    b.v_pool[ids, :16] = synth.fork_batch._to_bf16_bits(rng.standard_normal(b.v_pool[ids, :16].shape).astype(np.float32))
+    b.v_pool[ids] = synth.fork_batch._to_bf16_bits(rng.standard_normal(b.v_pool[ids].shape).astype(np.float32))
     o2, l2 = oracle.fork_decode_attn(b)
     for f in range(4):
         if f == 2:

@@ -29,15 +29,16 @@ def test_unused_slots_are_nan_and_used_slots_finite():
     b = synth.make_fork_batch(prefix_lens=[21], forks_per_trace=2, suffix_lens=[0, 5], num_q_heads=2,
                               num_kv_heads=1, head_dim=8, seed=8)
     as_f32 = (b.k_pool.astype(np.uint32) << 16).view(np.float32)
-    kf = np.isnan(as_f32)
-    used = np.zeros(b.k_pool.shape[:2], bool)
+    kf = np.isnan(as_f32).transpose(0, 2, 1, 3)            # K [NB][Hkv][16][D] -> [NB][16][Hkv][D]
+    vf = np.isnan((b.v_pool.astype(np.uint32) << 16).view(np.float32)).transpose(0, 3, 1, 2)  # V [NB][Hkv][D][16]
+    used = np.zeros((b.num_blocks, 16), bool)
     pt = b.prefix_table
     used[pt[0], :16] = True
     used[pt[1], :5] = True
     st = b.suffix_table
     used[st[0], :5] = True
-    assert np.all(~kf[used])
-    assert np.all(kf[~used])
+    assert np.all(~kf[used]) and np.all(~vf[used])
+    assert np.all(kf[~used]) and np.all(vf[~used])
 
 
 def test_fp8_scales_positive_on_used_blocks():
