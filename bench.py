@@ -144,36 +144,47 @@ def main():
             "prefix restore mismatch"
         import_bytes = (len(imp[0]) and sum(2 * t[2] for t in imp[0])) * len(ids) + 4 * len(ids)
 
-    def step(k, evs):
+    def step(k, evs, split):
+        """One step: restore replica k % R's prefix, then attend over replica
+        (k+1) % R.  split=False times the whole attention call with one event
+        pair; split=True records an event between its two kernels as well."""
         r_imp, r_att = k % R, (k + 1) % R
         evs[0].record(stream)
         if imp is not None:
             sg.specgen_kv_import(imp[r_imp], ids_d, b.num_blocks, stream=stream)
         evs[1].record(stream)
-        sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_PARTIALS, None, None, ws, stream=stream)
-        evs[2].record(stream)
-        sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_MERGE, out, lse, ws, stream=stream)
+        if split:
+            sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_PARTIALS, None, None, ws, stream=stream)
+            evs[2].record(stream)
+            sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_MERGE, out, lse, ws, stream=stream)
+        else:
+            sg.specgen_fork_decode_attn(reps[r_att], out, lse, ws, stream=stream)
         evs[3].record(stream)
 
     total = args.warmup + args.steps
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
     log(f"warmup {args.warmup}")
     for k in range(args.warmup):
-        step(k, events[k])
+        step(k, events[k], False)
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
     t0 = time.perf_counter()
     for k in range(args.warmup, total):
-        step(k, events[k])
+        step(k, events[k], False)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     timed = events[args.warmup:]
     imp_ms = np.array([e[0].elapsed_time(e[1]) for e in timed])
-    part_ms = np.array([e[1].elapsed_time(e[2]) for e in timed])
-    merge_ms = np.array([e[2].elapsed_time(e[3]) for e in timed])
-    attn_ms = part_ms + merge_ms
-    assert torch.isfinite(out.float()).all(), "non-finite attention output"
-
+    attn_ms = np.array([e[1].elapsed_time(e[3]) for e in timed])
+    # the same steps again with an event between the two kernels: the partial
+    # kernel's own duration (the roofline figure) and the merge's
+    log(f"timing {args.steps} steps with the phases split")
+    sevents = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        step(total + k, sevents[k], True)
+    torch.cuda.synchronize()
+    part_ms = np.array([e[1].elapsed_time(e[2]) for e in sevents])
+    merge_ms = np.array([e[2].elapsed_time(e[3]) for e in sevents])
     attn_bytes = b.algorithmic_bytes()
     out_bytes = N * Hq * (D * 2 + 4)
     kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
@@ -193,7 +204,9 @@ def main():
         "fork_tokens_per_s": round(N / attn_s, 1),
         "attn_us": {"mean": round(float(attn_ms.mean()) * 1e3, 2), "p10": round(float(np.percentile(attn_ms, 10)) * 1e3, 2),
                     "p50": round(float(np.median(attn_ms)) * 1e3, 2), "p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
-                    "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2)},
+                    "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2),
+                    "note": "mean/p10/p50/p90: whole call between two events; partials/merge: the kernels "
+                            "timed separately in a second run of the same steps"},
         "attn_algorithmic_bytes": int(attn_bytes),
         "roofline": {"kernel": PARTIAL_KERNEL + " (partials phase)", "bound": "hbm", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),

@@ -30,9 +30,11 @@
 // groups: wave w computes row group w % RG over token group w / RG (two waves
 // per SIMD for the 128-row prefix items, so one wave's softmax overlaps the
 // other's MFMAs).  Items with fewer rows pad their last row group; they are
-// bound by their K/V bytes, not by the matrix cores.  At the item's end the
-// token groups are combined through the stage that was just consumed, and
-// token group 0 writes the normalised partial (o, lse).
+// bound by their K/V bytes, not by the matrix cores (one wave's dependent
+// chain through a 32-token slab takes about 0.9 us, so a tile is always split
+// over two waves).  At the item's end the token groups are combined through the
+// stage that was just consumed, and token group 0 writes the normalised
+// partial (o, lse).
 //
 // Math per 32-token slab and 16-row N-tile: S^T = K Q^T on
 // v_mfma_f32_16x16x32_bf16 (A = 16 keys x 32 dims from LDS, B = Q^T in
@@ -85,6 +87,8 @@ struct Cfg {
   static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
+  static_assert(kTileCap <= kThreads, "the walk takes one tile of the range per thread");
+  static_assert(kMLBytes >= (kWaves + 1) * 4, "the walk's scratch fits the ML area");
 };
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
@@ -150,8 +154,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int w = blockIdx.x;
-  const WorkerRange wr =
-      worker_items<C::kItemCap>(plan, kPartMfma, w, items, reinterpret_cast<int32_t*>(a.ws + pp.info_base));
+  // the walk of the worker's range and the gather of every block id it reads
+  // (the ML area is free until the first item ends)
+  const WorkerRange wr = worker_walk_tiles<C::kThreads, C::kItemCap, C::kIdsPerTile>(
+      a, plan, kPartMfma, w, items, reinterpret_cast<int32_t*>(lds + C::kOffIds), reinterpret_cast<int32_t*>(ml));
   // The walk reads LDS, so the compiler cannot prove its results uniform;
   // without these readfirstlanes every loop-carried value of the slot loop
   // would live in VGPRs under exec masks.
@@ -463,10 +469,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     float* ls = a.ws + pp.lse_base + slot * pp.slot_rows;
     constexpr int RS = 16 * NT;
     int stores = 0;
-    // every lane stores (rows past the item's end land in unused rows of the
-    // slot), so the number of stores is the same on every path
+    // every lane of an N-tile that holds rows of the item stores (rows past the
+    // item's end land in unused rows of the slot), so the count is wave-uniform
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      if (rg * RS + nt * 16 >= d.nrows) break;
       const int row = rg * RS + nt * 16 + ln;
       const float inv = 1.f / lrow[nt];
 #pragma unroll
@@ -493,25 +500,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
   for (int b = 0; b < NB; ++b) is_id[b] = 0;
   Desc is_d = load_desc(0);
-  // slot 0 is the first item's q rows; its load overlaps the gather of every
-  // block id the range reads (clamped to each item's last valid block)
+  // slot 0 is the first item's q rows
   issue_slot(is_d, is_k, is_id, 0);
   advance(is_ii, is_k, is_d);
   ++issued;
-  {
-    int32_t* idw = reinterpret_cast<int32_t*>(lds + C::kOffIds);
-    const int nid = (R < C::kTileCap ? R : C::kTileCap) * C::kIdsPerTile;
-    for (int e = tid; e < nid; e += C::kThreads) {
-      const int r = e / C::kIdsPerTile;
-      int ii = 0;
-      while (ii + 1 < nitems && items[(ii + 1) * kItemInts + IT_RTILE0] <= r) ++ii;
-      const int32_t* dd = items + ii * kItemInts;
-      int bi = (dd[IT_TILE0] + (r - dd[IT_RTILE0])) * C::kIdsPerTile + e % C::kIdsPerTile;
-      if (bi > dd[IT_LASTBLK]) bi = dd[IT_LASTBLK];
-      idw[e] = (dd[IT_KIND] == 0 ? a.prefix_table : a.suffix_table)[dd[IT_TABOFF] + bi];
-    }
-  }
-  __syncthreads();
   auto load_ids = [&]() {   // block ids of the next slot to issue, if it is a tile
     if (issued < S && is_k >= 0) {
 #pragma unroll

@@ -44,7 +44,8 @@ struct PartPlan {
   int64_t info_base;      // float offset of the item table: per item ordinal three
                           // int32 (first worker, last worker, segment index in the first)
   int32_t n_items;        // items of the partition (prefix, then suffix)
-  int32_t pad_;
+  int32_t per_lo;         // tiles / W: every worker gets per_lo tiles, the first
+  int32_t n_hi;           // tiles % W workers one more
   int32_t workers;        // W (0: partition unused)
   int32_t kmax;           // max items touched by one worker
   int32_t tt;             // tokens per tile
@@ -82,6 +83,7 @@ struct alignas(16) Plan : PlanHead {
 };
 
 SG_HD int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+SG_HD int32_t cdiv32(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
 
 
@@ -95,7 +97,11 @@ SG_HD int part_of_trace(int policy, int rows) {
 
 SG_HD int part_of_suffix(int policy) { return policy == kPolicyDot ? kPartDot : kPartMfma; }
 
-SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) { return (w * pp.tiles) / pp.workers; }
+// First tile of worker w: workers [0, n_hi) take per_lo + 1 tiles, the rest
+// per_lo (no division, so the kernels evaluate it cheaply).
+SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) {
+  return w * pp.per_lo + (w < pp.n_hi ? w : (int64_t)pp.n_hi);
+}
 
 #ifdef __HIPCC__
 // Copy the plan from the kernel arguments into LDS.  All kThreads threads of
@@ -114,7 +120,9 @@ __device__ __forceinline__ void plan_to_lds(const Plan& karg, Plan& p) {
 
 // Worker owning tile x: the largest w with worker_start(w) <= x.
 SG_HD int32_t worker_of_tile(const PartPlan& pp, int64_t x) {
-  return (int32_t)(((x + 1) * (int64_t)pp.workers - 1) / pp.tiles);
+  const int64_t big = (int64_t)pp.n_hi * (pp.per_lo + 1);   // tiles of the larger ranges
+  if (x < big) return (int32_t)(x / (pp.per_lo + 1));
+  return (int32_t)(pp.n_hi + (x - big) / pp.per_lo);
 }
 
 struct ItemRef {
@@ -143,21 +151,21 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
       if (p.tileP[mid] <= x) lo = mid; else hi = mid - 1;
     }
     const int t = p.ptrace[lo];
-    const int rb_count = cdiv(trace_rows(p, t), pp.rbs);
-    const int tiles = cdiv(p.prefix_len[t], pp.tt);
-    const int64_t local = x - p.tileP[lo];
-    const int item = (int)(local / tiles);
+    const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
+    const int tiles = cdiv32(p.prefix_len[t], pp.tt);
+    const int local = (int)(x - p.tileP[lo]);   // tile counts fit in int32 (the planner checks)
+    const int item = local / tiles;
     r.kind = 0;
     r.t = t;
     r.j = item / rb_count;
     r.rb = item % rb_count;
     r.tiles = tiles;
-    r.tile = (int)(local % tiles);
+    r.tile = local - item * tiles;
     r.first = x - r.tile;
     r.ord = p.ordP[lo] + item;
     return r;
   }
-  const int64_t xs = x - pp.prefix_tiles;
+  const int xs = (int)(x - pp.prefix_tiles);
   int lo = 0, hi = p.N - 1;   // largest f with tileS[f] <= xs
   while (lo < hi) {
     int mid = (lo + hi + 1) >> 1;
@@ -166,14 +174,14 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
   const int f = lo;
   const int per_fork = p.Hkv * pp.suffix_rb;
   const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
-  const int64_t local = xs - p.tileS[f];
-  const int item = (int)(local / tiles);
+  const int local = xs - p.tileS[f];
+  const int item = local / tiles;
   r.kind = 1;
   r.f = f;
   r.j = item / pp.suffix_rb;
   r.rb = item % pp.suffix_rb;
   r.tiles = tiles;
-  r.tile = (int)(local % tiles);
+  r.tile = local - item * tiles;
   r.first = x - r.tile;
   r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
   return r;
@@ -191,7 +199,7 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   r.tile = 0;
   r.ord = cur.ord + 1;
   if (cur.kind == 0) {
-    const int rb_count = cdiv(trace_rows(p, cur.t), pp.rbs);
+    const int rb_count = cdiv32(trace_rows(p, cur.t), pp.rbs);
     if (cur.rb + 1 < rb_count) {
       r.rb = cur.rb + 1;
       return r;
@@ -206,7 +214,7 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
       r.t = p.ptrace[pos];
       r.j = 0;
       r.rb = 0;
-      r.tiles = cdiv(p.prefix_len[r.t], pp.tt);
+      r.tiles = cdiv32(p.prefix_len[r.t], pp.tt);
       return r;
     }
     return locate(p, part, x);
@@ -268,6 +276,27 @@ SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, V
     ++wr.nitems;
   }
   return wr;
+}
+
+// The parallel form of walk_range: what tile x of worker w's range [x0, x1)
+// contributes.  `starts` marks the first tile of an item's segment in the
+// range (x == x0 or the item's own first tile); there, n is the segment's
+// length.  The segments in order of x are exactly walk_range's visits; the
+// visit index of a segment is the number of starting tiles before it, and its
+// slot index is it.ord minus the ordinal of tile x0's item.
+struct TileInRange {
+  ItemRef it;
+  bool starts;
+  int n;
+};
+SG_HD TileInRange tile_in_range(const Plan& p, int part, int64_t x0, int64_t x1, int64_t x) {
+  TileInRange r;
+  r.it = locate(p, part, x);
+  r.starts = (x == x0) || r.it.tile == 0;
+  const int64_t left = x1 - x;
+  const int rest = r.it.tiles - r.it.tile;
+  r.n = rest < left ? rest : (int)left;
+  return r;
 }
 
 // The item-table entry a walk records: the worker holding an item's first

@@ -130,6 +130,8 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     int64_t W = std::min<int64_t>(pp.tiles, (int64_t)cus_fn());
     for (;;) {
       pp.workers = (int32_t)W;
+      pp.per_lo = (int32_t)(pp.tiles / W);
+      pp.n_hi = (int32_t)(pp.tiles % W);
       const int64_t per = (pp.tiles + W - 1) / W;
       int kmax = 0;
       for (int64_t w = 0; w < W; ++w) {

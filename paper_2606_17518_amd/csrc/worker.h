@@ -60,6 +60,90 @@ __device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* 
   return wr;
 }
 
+// The walk and the block-id gather in one pass, for kernels whose ranges hold
+// at most one tile per thread (R <= kThreads): thread i locates tile x0 + i
+// (tile_in_range), loads the kIdsPerTile block ids of that tile (clamped to
+// its item's last valid block) into ids[i * kIdsPerTile ..], and the thread at
+// the first tile of each item's segment writes the item's descriptor and its
+// item-table entries.  Items are numbered by counting starting tiles with wave
+// ballots, so nothing runs serially and the only memory round trip is the id
+// loads.  `scratch` is kThreads / 64 + 1 ints of LDS.  Ends with a barrier.
+template <int kThreads, int kItemCap, int kIdsPerTile>
+__device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
+                                         int32_t* ids, int32_t* scratch) {
+  constexpr int kW = kThreads / 64;
+  const PartPlan& pp = plan.part[part];
+  int32_t* info = reinterpret_cast<int32_t*>(a.ws + pp.info_base);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
+  const int R = (int)(x1 - x0);
+  const bool mine = tid < R;
+  TileInRange tr;
+  tr.starts = false;
+  tr.n = 0;
+  int32_t id[kIdsPerTile];
+  if (mine) {
+    tr = tile_in_range(plan, part, x0, x1, x0 + tid);
+    const ItemRef& it = tr.it;
+    const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+    const int lastblk = (nv - 1) / 16;
+    const int32_t* tab = it.kind == 0 ? a.prefix_table + plan.prefix_table_off[it.t]
+                                      : a.suffix_table + plan.suffix_table_off[it.f];
+#pragma unroll
+    for (int b = 0; b < kIdsPerTile; ++b) {
+      const int bi = it.tile * kIdsPerTile + b;
+      id[b] = tab[bi < lastblk ? bi : lastblk];
+    }
+  }
+  const uint64_t starts = __ballot(tr.starts);
+  if (lane == 0) scratch[wave] = __popcll(starts);
+  if (tid == 0) scratch[kW] = mine ? tr.it.ord : 0;
+  __syncthreads();
+  int base = 0, total = 0;
+#pragma unroll
+  for (int v = 0; v < kW; ++v) {
+    base += v < wave ? scratch[v] : 0;
+    total += scratch[v];
+  }
+  const int first_ord = scratch[kW];
+  if (tr.starts) {
+    const int i = base + __popcll(starts & ((1ull << lane) - 1));
+    if (i < kItemCap) {
+      const ItemRef& it = tr.it;
+      int32_t* d = items + i * kItemInts;
+      d[IT_KIND] = it.kind;
+      d[IT_T] = it.t;
+      d[IT_F] = it.f;
+      d[IT_J] = it.j;
+      d[IT_RB] = it.rb;
+      d[IT_ORD] = it.ord;
+      d[IT_TILE0] = it.tile;
+      d[IT_NTILE] = tr.n;
+      d[IT_RTILE0] = tid;
+      d[IT_TILES] = it.tiles;
+      const int r0 = it.rb * pp.rbs;
+      const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
+      d[IT_NROWS] = (rows - r0) < pp.rbs ? (rows - r0) : pp.rbs;
+      d[IT_ROW0] = r0;
+      const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+      d[IT_NVALID] = nv;
+      d[IT_TABOFF] = it.kind == 0 ? plan.prefix_table_off[it.t] : plan.suffix_table_off[it.f];
+      d[IT_LASTBLK] = (nv - 1) / 16;
+      record_item(info, it, tr.n, w, it.ord - first_ord);
+    }
+  }
+  if (mine) {
+#pragma unroll
+    for (int b = 0; b < kIdsPerTile; ++b) ids[tid * kIdsPerTile + b] = id[b];
+  }
+  __syncthreads();
+  WorkerRange wr;
+  wr.nitems = total < kItemCap ? total : kItemCap;
+  wr.first_ord = first_ord;
+  wr.R = R;
+  return wr;
+}
+
 // All threads of the block call this; `items` holds item_cap descriptors and
 // `ids` holds tile_cap * ids_per_tile block ids.
 // If `scales` is not null (E4M3 KV), scales[e] / scales[cap + e] receive the

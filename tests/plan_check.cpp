@@ -73,6 +73,26 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
         (void)i;
       });
       CHECK(fine, "worker %d of partition %d: walk out of order or slot index out of range", w, X);
+      // the parallel form (one tile per thread) must give the same segments
+      {
+        struct V { int ord, tile, n, rt, i, k; };
+        std::vector<V> serial;
+        walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
+          serial.push_back(V{it.ord, it.tile, n, rt, i, k});
+        });
+        std::vector<V> par;
+        int first_ord = 0;
+        for (int64_t xx = x0; xx < x1; ++xx) {
+          const TileInRange t = tile_in_range(plan, X, x0, x1, xx);
+          if (xx == x0) first_ord = t.it.ord;
+          if (t.starts) par.push_back(V{t.it.ord, t.it.tile, t.n, (int)(xx - x0), (int)par.size(), t.it.ord - first_ord});
+        }
+        bool same = serial.size() == par.size();
+        for (size_t q = 0; same && q < par.size(); ++q)
+          same = serial[q].ord == par[q].ord && serial[q].tile == par[q].tile && serial[q].n == par[q].n &&
+                 serial[q].rt == par[q].rt && serial[q].i == par[q].i && serial[q].k == par[q].k;
+        CHECK(same, "worker %d of partition %d: per-tile walk differs from the serial walk", w, X);
+      }
       CHECK(wr.R == x1 - x0, "worker %d walked %d of %lld tiles (item cap %d)", w, wr.R, (long long)(x1 - x0),
             in.item_cap[X]);
     }
