@@ -90,6 +90,10 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.item_cap[1] = dot_item_cap();
   in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128, fp8);
   in.tile_cap[1] = dot_tile_cap(in.D);
+  // An item costs a worker about two tiles' time on the MFMA path (its q slot
+  // and the token-group combine at its end) and about one on the dot path.
+  in.charge[0] = 2;
+  in.charge[1] = 1;
   char err[256];
   const int rc = plan_build(in, [] { return device_cus(); }, plan, ws_floats, err, sizeof err);
   if (rc == kPlanInvalid) return fail(SPECGEN_ERR_INVALID_ARG, "%s", err);

@@ -88,7 +88,7 @@ struct Cfg {
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
   static_assert(kTileCap <= kThreads, "the walk takes one tile of the range per thread");
-  static_assert(kMLBytes >= (kWaves + 1) * 4, "the walk's scratch fits the ML area");
+  static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
 };
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
@@ -476,10 +476,12 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       if (rg * RS + nt * 16 >= d.nrows) break;
       const int row = rg * RS + nt * 16 + ln;
       const float inv = 1.f / lrow[nt];
+      // partials are read once, by the merge: nontemporal stores keep them out
+      // of the caches' retention
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G) = acc[nt][dt] * inv;
-      ls[row] = m_run[nt] * a.sm_scale + __logf(lrow[nt]);
+        __builtin_nontemporal_store(acc[nt][dt] * inv, reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G));
+      __builtin_nontemporal_store(m_run[nt] * a.sm_scale + __logf(lrow[nt]), ls + row);
       stores += DT + 1;
     }
     return stores;

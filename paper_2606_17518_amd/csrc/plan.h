@@ -13,8 +13,12 @@
 // chosen by the path policy.  Within a partition the items are laid out in a
 // fixed order -- prefix items (trace-major, then j, then rb), then suffix
 // items (fork-major, then j, then rb) -- and each item is cut into tiles of
-// `tt` tokens.  The partition's tile sequence is split evenly over W workers
-// (workgroups): worker w takes tiles [start(w), start(w+1)).  A worker emits
+// `tt` tokens.  In the partition's tile sequence every item is preceded by
+// `charge` empty tiles: they stand for the item's fixed cost in a worker (its
+// query rows and its end), so workers whose ranges hold many short items get
+// fewer tiles of data.  The sequence is split evenly over W workers
+// (workgroups): worker w takes positions [start(w), start(w+1)) and processes
+// the real tiles among them.  A worker emits
 // one partial (o, lse) per item it touches, into slot w * kmax + k where k is
 // the item's ordinal minus the ordinal of the worker's first item.  The merge
 // finds the workers covering an item from its tile range alone.
@@ -56,6 +60,7 @@ struct PartPlan {
   int32_t suffix_rb;      // row blocks per suffix (fork, head): ceil(g / rbs)
   int32_t n_traces;       // traces whose prefix items are in the partition
   int32_t trace_begin;    // their positions in Plan::ptrace: [trace_begin, +n_traces)
+  int32_t charge;         // empty tiles in front of every item
 };
 
 // The scalar part of the plan.
@@ -128,14 +133,19 @@ SG_HD int32_t worker_of_tile(const PartPlan& pp, int64_t x) {
 struct ItemRef {
   int32_t kind;      // 0 prefix, 1 suffix, -1 past the end
   int32_t t, f, j, rb;
-  int32_t tiles;     // tiles of the item
-  int32_t tile;      // tile of x within the item
-  int64_t first;     // partition tile index of the item's first tile
+  int32_t tiles;     // tiles of the item (its data)
+  int32_t tile;      // tile of x within the item; -charge..-1 for its empty tiles
+  int64_t first;     // sequence position of the item's first tile of data
   int32_t ord;       // ordinal of the item in the partition
 };
 
-// The item containing partition tile x.  Suffix items need ceil(S_f/tt),
-// which equals (tileS[f+1]-tileS[f]) / (Hkv * suffix_rb).
+// Sequence positions taken by one suffix item of fork f (0 if S_f = 0): its
+// charge plus ceil(S_f / tt); tileS holds their per-fork prefix sums.
+SG_HD int32_t suffix_span(const Plan& p, const PartPlan& pp, int f) {
+  return (p.tileS[f + 1] - p.tileS[f]) / (p.Hkv * pp.suffix_rb);
+}
+
+// The item at partition sequence position x.
 SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
   const PartPlan& pp = p.part[part];
   ItemRef r;
@@ -153,14 +163,15 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
     const int t = p.ptrace[lo];
     const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
     const int tiles = cdiv32(p.prefix_len[t], pp.tt);
+    const int span = tiles + pp.charge;
     const int local = (int)(x - p.tileP[lo]);   // tile counts fit in int32 (the planner checks)
-    const int item = local / tiles;
+    const int item = local / span;
     r.kind = 0;
     r.t = t;
     r.j = item / rb_count;
     r.rb = item % rb_count;
     r.tiles = tiles;
-    r.tile = local - item * tiles;
+    r.tile = local - item * span - pp.charge;
     r.first = x - r.tile;
     r.ord = p.ordP[lo] + item;
     return r;
@@ -172,28 +183,28 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
     if (p.tileS[mid] <= xs) lo = mid; else hi = mid - 1;
   }
   const int f = lo;
-  const int per_fork = p.Hkv * pp.suffix_rb;
-  const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
+  const int span = suffix_span(p, pp, f);
   const int local = xs - p.tileS[f];
-  const int item = local / tiles;
+  const int item = local / span;
   r.kind = 1;
   r.f = f;
   r.j = item / pp.suffix_rb;
   r.rb = item % pp.suffix_rb;
-  r.tiles = tiles;
-  r.tile = local - item * tiles;
+  r.tiles = span - pp.charge;
+  r.tile = local - item * span - pp.charge;
   r.first = x - r.tile;
   r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
   return r;
 }
 
 // The item that follows `cur` in partition `part` (cur must not be the last
-// one); equal to locate(p, part, cur.first + cur.tiles).  Steps within a trace
-// or fork in O(1) and falls back to locate() where it would have to skip over
+// one), at its first tile of data: equal to
+// locate(p, part, cur.first + cur.tiles + charge).  Steps within a trace or
+// fork in O(1) and falls back to locate() where it would have to skip over
 // forks without suffix tokens or cross into the suffix items.
 SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   const PartPlan& pp = p.part[part];
-  const int64_t x = cur.first + cur.tiles;
+  const int64_t x = cur.first + cur.tiles + pp.charge;
   ItemRef r = cur;
   r.first = x;
   r.tile = 0;
@@ -230,8 +241,7 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   }
   const int f = cur.f + 1;
   if (f < p.N) {
-    const int per_fork = p.Hkv * pp.suffix_rb;
-    const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
+    const int tiles = suffix_span(p, pp, f) - pp.charge;
     if (tiles > 0) {
       r.f = f;
       r.j = 0;
@@ -243,16 +253,17 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   return locate(p, part, x);
 }
 
-// The items of worker w's tile range, in order.  For each one calls
-// visit(it, n, rt, i, k): it = the item (it.tile = its first tile in the
-// range), n = its tiles in the range, rt = the range-relative index of its
-// first tile, i = its position in the range, k = it.ord - (ordinal of the
-// range's first item), which is the partial-slot index (w * kmax + k).  At
-// most item_cap items are visited.
+// The items of worker w's range, in order.  For each one with tiles of data
+// in the range calls visit(it, n, rt, i, k): it = the item (it.tile = its
+// first tile in the range), n = its tiles in the range, rt = the number of
+// data tiles of the range before them (empty tiles do not count), i = its
+// position among the visited items, k = it.ord - (ordinal of the item at the
+// range's first position), which is the partial-slot index (w * kmax + k).
+// At most item_cap items are visited.
 struct WorkerRange {
-  int nitems;     // items touched (non-empty)
-  int first_ord;  // ordinal of the first one
-  int R;          // tiles in the range
+  int nitems;     // items visited
+  int first_ord;  // ordinal of the item at the range's first position
+  int R;          // data tiles in the range
 };
 template <typename Visit>
 SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, Visit&& visit) {
@@ -263,36 +274,46 @@ SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, V
   wr.nitems = 0;
   wr.first_ord = 0;
   wr.R = 0;
+  if (x0 >= x1) return wr;
+  ItemRef it = locate(p, part, x0);
+  wr.first_ord = it.ord;
   int64_t x = x0;
-  ItemRef it;
-  it.kind = -1;
+  if (it.tile < 0) {   // the range starts on the item's empty tiles
+    x = it.first;
+    it.tile = 0;
+  }
   while (x < x1 && wr.nitems < item_cap) {
-    it = wr.nitems == 0 ? locate(p, part, x) : next_item(p, part, it);
     const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
-    if (wr.nitems == 0) wr.first_ord = it.ord;
     visit(it, n, wr.R, wr.nitems, it.ord - wr.first_ord);
-    x += n;
     wr.R += n;
     ++wr.nitems;
+    x += n;
+    if (x >= x1) break;
+    it = next_item(p, part, it);
+    x = it.first;   // past the next item's empty tiles
   }
   return wr;
 }
 
-// The parallel form of walk_range: what tile x of worker w's range [x0, x1)
-// contributes.  `starts` marks the first tile of an item's segment in the
-// range (x == x0 or the item's own first tile); there, n is the segment's
-// length.  The segments in order of x are exactly walk_range's visits; the
-// visit index of a segment is the number of starting tiles before it, and its
-// slot index is it.ord minus the ordinal of tile x0's item.
+// The parallel form of walk_range: what position x of worker w's range
+// [x0, x1) contributes.  `data` marks a tile of data (not an item's empty
+// tile); `starts` marks the first data tile of an item's segment in the range
+// (x == x0 or the item's own first data tile); there, n is the segment's
+// length.  The segments in order of x are exactly walk_range's visits: the
+// visit index of a segment is the number of starting positions before it, its
+// rt the number of data positions before it, and its slot index it.ord minus
+// the ordinal of the item at x0.
 struct TileInRange {
   ItemRef it;
+  bool data;
   bool starts;
   int n;
 };
 SG_HD TileInRange tile_in_range(const Plan& p, int part, int64_t x0, int64_t x1, int64_t x) {
   TileInRange r;
   r.it = locate(p, part, x);
-  r.starts = (x == x0) || r.it.tile == 0;
+  r.data = r.it.tile >= 0;
+  r.starts = r.data && (x == x0 || r.it.tile == 0);
   const int64_t left = x1 - x;
   const int rest = r.it.tiles - r.it.tile;
   r.n = rest < left ? rest : (int)left;
@@ -366,7 +387,8 @@ SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h) {
   const int tiles = cdiv(p.prefix_len[t], pp.tt);
   const int pos = p.trace_pos[t];
   const int item = j * rbc + rb;
-  return item_parts(p, X, (int64_t)p.tileP[pos] + (int64_t)item * tiles, tiles, p.ordP[pos] + item, ri - rb * pp.rbs);
+  return item_parts(p, X, (int64_t)p.tileP[pos] + (int64_t)item * (tiles + pp.charge) + pp.charge, tiles,
+                    p.ordP[pos] + item, ri - rb * pp.rbs);
 }
 
 // The suffix item of row (f, h); returns false if the fork has no suffix tokens.
@@ -375,11 +397,11 @@ SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
   const int X = part_of_suffix(p.policy);
   const PartPlan& pp = p.part[X];
   const int per_fork = p.Hkv * pp.suffix_rb;
-  const int tiles = (p.tileS[f + 1] - p.tileS[f]) / per_fork;
-  if (tiles <= 0) return false;
+  const int span = suffix_span(p, pp, f);
+  if (span <= 0) return false;
   const int rb = hh / pp.rbs;
   const int item = j * pp.suffix_rb + rb;
-  *out = item_parts(p, X, pp.prefix_tiles + p.tileS[f] + (int64_t)item * tiles, tiles,
+  *out = item_parts(p, X, pp.prefix_tiles + p.tileS[f] + (int64_t)item * span + pp.charge, span - pp.charge,
                     pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
   return true;
 }

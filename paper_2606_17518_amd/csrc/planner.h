@@ -26,6 +26,7 @@ struct PlanInputs {
   int rbs[2];                 // rows per row block
   int item_cap[2];            // max items per worker
   int tile_cap[2];            // max tiles per worker
+  int charge[2];              // empty sequence positions in front of every item
 };
 
 constexpr int64_t kAlignFloats = 64;   // 256-byte alignment of workspace regions
@@ -83,6 +84,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     pp.rbs = in.rbs[X];
     pp.slot_rows = in.rbs[X];
     pp.trace_begin = pos;
+    pp.charge = in.charge[X];
     int64_t tiles = 0, items = 0;
     for (int t = 0; t < T; ++t) {
       const int rows = (fo[t + 1] - fo[t]) * g;
@@ -93,7 +95,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
       plan->tileP[pos] = (int32_t)tiles;
       plan->ordP[pos] = (int32_t)items;
       const int rb = cdiv(rows, pp.rbs);
-      tiles += (int64_t)Hkv * rb * cdiv(in.prefix_len[t], pp.tt);
+      tiles += (int64_t)Hkv * rb * (cdiv(in.prefix_len[t], pp.tt) + pp.charge);
       items += (int64_t)Hkv * rb;
       if (tiles > INT32_MAX || items > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
       ++pos;
@@ -111,7 +113,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     int64_t acc = 0;
     for (int f = 0; f < N; ++f) {
       plan->tileS[f] = (int32_t)acc;
-      acc += (int64_t)Hkv * pp.suffix_rb * cdiv(in.suffix_len[f], pp.tt);
+      if (in.suffix_len[f] > 0) acc += (int64_t)Hkv * pp.suffix_rb * (cdiv(in.suffix_len[f], pp.tt) + pp.charge);
       if (acc > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
     }
     plan->tileS[N] = (int32_t)acc;

@@ -61,13 +61,14 @@ __device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* 
 }
 
 // The walk and the block-id gather in one pass, for kernels whose ranges hold
-// at most one tile per thread (R <= kThreads): thread i locates tile x0 + i
-// (tile_in_range), loads the kIdsPerTile block ids of that tile (clamped to
-// its item's last valid block) into ids[i * kIdsPerTile ..], and the thread at
-// the first tile of each item's segment writes the item's descriptor and its
-// item-table entries.  Items are numbered by counting starting tiles with wave
-// ballots, so nothing runs serially and the only memory round trip is the id
-// loads.  `scratch` is kThreads / 64 + 1 ints of LDS.  Ends with a barrier.
+// at most one sequence position per thread: thread i locates position x0 + i
+// (tile_in_range); a data tile loads its kIdsPerTile block ids (clamped to its
+// item's last valid block) into ids[c * kIdsPerTile ..], where c counts the
+// data tiles before it, and the thread at the first data tile of each item's
+// segment writes the item's descriptor and its item-table entries.  Items and
+// data tiles are numbered with wave ballots, so nothing runs serially and the
+// only memory round trip is the id loads.  `scratch` is 2 * kThreads / 64 + 1
+// ints of LDS.  Ends with a barrier.
 template <int kThreads, int kItemCap, int kIdsPerTile>
 __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
                                          int32_t* ids, int32_t* scratch) {
@@ -76,38 +77,47 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
   int32_t* info = reinterpret_cast<int32_t*>(a.ws + pp.info_base);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
-  const int R = (int)(x1 - x0);
-  const bool mine = tid < R;
+  const bool mine = tid < (int)(x1 - x0);
   TileInRange tr;
-  tr.starts = false;
+  tr.data = tr.starts = false;
   tr.n = 0;
   int32_t id[kIdsPerTile];
   if (mine) {
     tr = tile_in_range(plan, part, x0, x1, x0 + tid);
-    const ItemRef& it = tr.it;
-    const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
-    const int lastblk = (nv - 1) / 16;
-    const int32_t* tab = it.kind == 0 ? a.prefix_table + plan.prefix_table_off[it.t]
-                                      : a.suffix_table + plan.suffix_table_off[it.f];
+    if (tr.data) {
+      const ItemRef& it = tr.it;
+      const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+      const int lastblk = (nv - 1) / 16;
+      const int32_t* tab = it.kind == 0 ? a.prefix_table + plan.prefix_table_off[it.t]
+                                        : a.suffix_table + plan.suffix_table_off[it.f];
 #pragma unroll
-    for (int b = 0; b < kIdsPerTile; ++b) {
-      const int bi = it.tile * kIdsPerTile + b;
-      id[b] = tab[bi < lastblk ? bi : lastblk];
+      for (int b = 0; b < kIdsPerTile; ++b) {
+        const int bi = it.tile * kIdsPerTile + b;
+        id[b] = tab[bi < lastblk ? bi : lastblk];
+      }
     }
   }
   const uint64_t starts = __ballot(tr.starts);
-  if (lane == 0) scratch[wave] = __popcll(starts);
-  if (tid == 0) scratch[kW] = mine ? tr.it.ord : 0;
+  const uint64_t data = __ballot(tr.data);
+  if (lane == 0) {
+    scratch[wave] = __popcll(starts);
+    scratch[kW + wave] = __popcll(data);
+  }
+  if (tid == 0) scratch[2 * kW] = mine ? tr.it.ord : 0;
   __syncthreads();
-  int base = 0, total = 0;
+  int ibase = 0, items_total = 0, dbase = 0, data_total = 0;
 #pragma unroll
   for (int v = 0; v < kW; ++v) {
-    base += v < wave ? scratch[v] : 0;
-    total += scratch[v];
+    ibase += v < wave ? scratch[v] : 0;
+    items_total += scratch[v];
+    dbase += v < wave ? scratch[kW + v] : 0;
+    data_total += scratch[kW + v];
   }
-  const int first_ord = scratch[kW];
+  const int first_ord = scratch[2 * kW];
+  const uint64_t below = (1ull << lane) - 1;
+  const int c = dbase + __popcll(data & below);   // data tiles before this one
   if (tr.starts) {
-    const int i = base + __popcll(starts & ((1ull << lane) - 1));
+    const int i = ibase + __popcll(starts & below);
     if (i < kItemCap) {
       const ItemRef& it = tr.it;
       int32_t* d = items + i * kItemInts;
@@ -119,7 +129,7 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
       d[IT_ORD] = it.ord;
       d[IT_TILE0] = it.tile;
       d[IT_NTILE] = tr.n;
-      d[IT_RTILE0] = tid;
+      d[IT_RTILE0] = c;
       d[IT_TILES] = it.tiles;
       const int r0 = it.rb * pp.rbs;
       const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
@@ -132,15 +142,15 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
       record_item(info, it, tr.n, w, it.ord - first_ord);
     }
   }
-  if (mine) {
+  if (tr.data) {
 #pragma unroll
-    for (int b = 0; b < kIdsPerTile; ++b) ids[tid * kIdsPerTile + b] = id[b];
+    for (int b = 0; b < kIdsPerTile; ++b) ids[c * kIdsPerTile + b] = id[b];
   }
   __syncthreads();
   WorkerRange wr;
-  wr.nitems = total < kItemCap ? total : kItemCap;
+  wr.nitems = items_total < kItemCap ? items_total : kItemCap;
   wr.first_ord = first_ord;
-  wr.R = R;
+  wr.R = data_total;
   return wr;
 }
 

@@ -62,14 +62,19 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
     for (int w = 0; w < pp.workers; ++w) {
       const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
       CHECK(x1 - x0 <= in.tile_cap[X], "worker %d has %lld tiles > cap", w, (long long)(x1 - x0));
-      int64_t x = x0;
+      int64_t x = x0;      // position after the previous segment
+      int64_t data = 0;    // data tiles visited so far
       bool fine = true;
       const WorkerRange wr = walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
-        if (it.kind < 0 || it.first + it.tile != x || rt != x - x0 || k < 0 || k >= pp.kmax || it.ord >= pp.n_items)
+        const int64_t at = it.first + it.tile;
+        // only an item's empty positions may lie between two segments
+        if (it.kind < 0 || it.tile < 0 || at < x || at > x + pp.charge || at + n > x1 || rt != data || k < 0 ||
+            k >= pp.kmax || it.ord >= pp.n_items)
           fine = false;
-        segs[{X, it.ord}].push_back(Seg{w, k, x, n});
+        segs[{X, it.ord}].push_back(Seg{w, k, at, n});
         if (it.ord >= 0 && it.ord < pp.n_items) record_item(tables[X].data(), it, n, w, k);
-        x += n;
+        x = at + n;
+        data += n;
         (void)i;
       });
       CHECK(fine, "worker %d of partition %d: walk out of order or slot index out of range", w, X);
@@ -81,11 +86,12 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
           serial.push_back(V{it.ord, it.tile, n, rt, i, k});
         });
         std::vector<V> par;
-        int first_ord = 0;
+        int first_ord = 0, ndata = 0;
         for (int64_t xx = x0; xx < x1; ++xx) {
           const TileInRange t = tile_in_range(plan, X, x0, x1, xx);
           if (xx == x0) first_ord = t.it.ord;
-          if (t.starts) par.push_back(V{t.it.ord, t.it.tile, t.n, (int)(xx - x0), (int)par.size(), t.it.ord - first_ord});
+          if (t.starts) par.push_back(V{t.it.ord, t.it.tile, t.n, ndata, (int)par.size(), t.it.ord - first_ord});
+          ndata += t.data ? 1 : 0;
         }
         bool same = serial.size() == par.size();
         for (size_t q = 0; same && q < par.size(); ++q)
@@ -93,7 +99,9 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
                  serial[q].rt == par[q].rt && serial[q].i == par[q].i && serial[q].k == par[q].k;
         CHECK(same, "worker %d of partition %d: per-tile walk differs from the serial walk", w, X);
       }
-      CHECK(wr.R == x1 - x0, "worker %d walked %d of %lld tiles (item cap %d)", w, wr.R, (long long)(x1 - x0),
+      int64_t ndata = 0;
+      for (int64_t xx = x0; xx < x1; ++xx) ndata += locate(plan, X, xx).tile >= 0 ? 1 : 0;
+      CHECK(wr.R == ndata, "worker %d walked %d of %lld data tiles (item cap %d)", w, wr.R, (long long)ndata,
             in.item_cap[X]);
     }
   }
@@ -108,7 +116,8 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       return true;
     }
     CHECK(itv != segs.end(), "item (%d, %d) never processed", X, ord);
-    int64_t expect = ptile[X];
+    // an item takes `charge` empty positions, then its data tiles
+    int64_t expect = ptile[X] + in.charge[X];
     int total = 0;
     for (const Seg& s : itv->second) {
       CHECK(s.first == expect, "item tiles not contiguous");
@@ -116,7 +125,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       total += s.n;
     }
     CHECK(total == tiles, "item covered %d of %d tiles", total, tiles);
-    ptile[X] += tiles;
+    ptile[X] += in.charge[X] + tiles;
     return true;
   };
   for (int X = 0; X < 2; ++X) {
@@ -145,10 +154,11 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
     int64_t x = 0;
     while (x < pp.tiles) {
       const ItemRef it = locate(plan, X, x);
+      CHECK(it.tile == -pp.charge, "an item starts with its empty positions");
       const int64_t nx = it.first + it.tiles;
       if (nx < pp.tiles) {
         const ItemRef a = next_item(plan, X, it);
-        const ItemRef b = locate(plan, X, nx);
+        const ItemRef b = locate(plan, X, nx + pp.charge);
         CHECK(a.kind == b.kind && a.t == b.t && a.f == b.f && a.j == b.j && a.rb == b.rb && a.tiles == b.tiles &&
                   a.tile == b.tile && a.first == b.first && a.ord == b.ord,
               "next_item differs from locate at tile %lld of partition %d", (long long)nx, X);
@@ -271,6 +281,8 @@ int main(int argc, char** argv) {
     in.rbs[0] = 128;
     in.rbs[1] = 16;
     in.item_cap[0] = in.item_cap[1] = 64;
+    in.charge[0] = U(0, 3);   // the library uses 2 and 1; any value must give a valid split
+    in.charge[1] = U(0, 2);
     in.tile_cap[0] = 2048 / (in.tt[0] / 16);
     in.tile_cap[1] = 2048 / 4;
     const int cus = U(0, 2) == 0 ? U(1, 16) : 256;
