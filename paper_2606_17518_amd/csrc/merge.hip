@@ -6,8 +6,7 @@
 // One wavefront merges one output row: lane p first takes part p's lse to
 // find the running max and weights (chunks of 64 parts, rescaled between
 // chunks), then all lanes sweep the parts over the head dimension.
-#include "common.h"
-#include "plan.h"
+#include "merge.h"
 
 namespace specgen {
 
@@ -96,148 +95,14 @@ hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S,
 // ---- fork merge: the parts of row (f, h) are the partials of the workers that
 // covered its prefix item and its suffix item ---------------------------------
 
-// Row merge for D in {64, 128}: lanes read 16 bytes each, so one load
-// instruction covers PPI = 64 / (D/4) parts.  A batch is up to 64 parts: each
-// lane loads one part's lse and the wave issues the o loads of every part of
-// the batch before it waits for any of them, so a row of up to a batch of
-// parts costs one memory round trip.
-template <int D, typename PO, typename PL>
-__device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse, uint16_t* out_row,
-                                             float* out_lse_p) {
-  constexpr int LPP = D / 4;       // lanes per part
-  constexpr int PPI = 64 / LPP;    // parts per load instruction
-  constexpr int U = (D == 128) ? 24 : 16;   // load instructions per batch
-  constexpr int kBatch = PPI * U;  // parts per batch (<= 64: one lse per lane)
-  static_assert(kBatch <= 64, "one lse per lane");
-  const int lane = threadIdx.x & 63;
-  const int gsl = lane / LPP;      // part slot of this lane within an instruction
-  const int c4 = (lane % LPP) * 4; // first of the 4 dims this lane owns
-  float M = -INFINITY, z = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int p0 = 0; p0 < nparts; p0 += kBatch) {
-    const int cnt = (nparts - p0) < kBatch ? (nparts - p0) : kBatch;
-    const float l = lane < cnt ? part_lse(p0 + lane) : -INFINITY;
-    f32x4 v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (u * PPI < cnt) {   // wave-uniform: only instructions that hold a part
-        const int q = u * PPI + gsl;
-        const int qc = q < cnt ? q : cnt - 1;   // the last instruction's spare slots re-read its last part
-        v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
-      }
-    }
-    float cm = l;
-    for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
-    const float Mn = fmaxf(M, cm);
-    if (Mn == -INFINITY) continue;          // every part so far empty (wave-uniform)
-    const float rescale = __expf(M - Mn);   // M = -inf -> 0
-    z *= rescale;
-    acc *= rescale;
-    M = Mn;
-    const float wl = (l == -INFINITY) ? 0.f : __expf(l - M);
-    float zs = wl;
-    for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
-    z += zs;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int q = u * PPI + gsl;
-      float wq = __shfl(wl, q < 64 ? q : 63, 64);
-      if (q >= cnt) wq = 0.f;
-      if (wq != 0.f) acc += wq * v[u];   // an empty part's o may be garbage
-    }
-  }
-  // sum the PPI lane groups
-#pragma unroll
-  for (int o = LPP; o < 64; o <<= 1) {
-    acc[0] += __shfl_xor(acc[0], o, 64);
-    acc[1] += __shfl_xor(acc[1], o, 64);
-    acc[2] += __shfl_xor(acc[2], o, 64);
-    acc[3] += __shfl_xor(acc[3], o, 64);
-  }
-  const bool empty = (M == -INFINITY);
-  if (gsl == 0) {
-    const float inv = empty ? 0.f : 1.f / z;
-    u32x2 pk;
-    pk[0] = pack_bf16x2(empty ? 0.f : acc[0] * inv, empty ? 0.f : acc[1] * inv);
-    pk[1] = pack_bf16x2(empty ? 0.f : acc[2] * inv, empty ? 0.f : acc[3] * inv);
-    *reinterpret_cast<u32x2*>(out_row + c4) = pk;
-  }
-  if (out_lse_p && lane == 0) *out_lse_p = empty ? -INFINITY : M + __logf(z);
-}
-
 template <int D>
 __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, const float* __restrict__ ws, uint16_t* __restrict__ out,
                                                          float* __restrict__ out_lse) {
   __shared__ Plan splan;
   plan_to_lds<256>(plan_arg, splan);
-  const Plan& plan = splan;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= (int64_t)plan.N * plan.Hq) return;
-  const int f = (int)(row / plan.Hq);
-  const int h = (int)(row % plan.Hq);
-  // The item table (written by the partial kernels' walks) gives each item's
-  // first and last worker and its segment index in the first one.  Part i of
-  // an item sits in slot (w_lo + i) * kmax + (i == 0 ? k_lo : 0), so relative
-  // to part 0 it is i * kmax - k_lo slots further (plain scalars: a lane picks
-  // the prefix or the suffix item by its part index).
-  int Xs[2] = {0, 0}, ords[2] = {0, 0}, rs[2] = {0, 0};
-  bool has[2];
-  prefix_item_of_row(plan, f, h, &Xs[0], &ords[0], &rs[0]);
-  has[0] = true;
-  has[1] = suffix_item_of_row(plan, f, h, &Xs[1], &ords[1], &rs[1]);
-  // both table entries are loaded before either is used
-  int32_t e[2][3];
-#pragma unroll
-  for (int s2 = 0; s2 < 2; ++s2) {
-    const int32_t* info = reinterpret_cast<const int32_t*>(ws + plan.part[Xs[s2]].info_base) + 3 * (int64_t)ords[s2];
-#pragma unroll
-    for (int c = 0; c < 3; ++c) e[s2][c] = has[s2] ? info[c] : 0;
-  }
-  int64_t o0[2] = {0, 0}, l0[2] = {0, 0};
-  int kmax[2] = {1, 1}, klo[2] = {0, 0}, n[2] = {0, 0}, srows[2] = {1, 1};
-  bool ok = true;
-#pragma unroll
-  for (int s2 = 0; s2 < 2; ++s2) {
-    if (!has[s2]) continue;
-    const int X = Xs[s2], ord = ords[s2], r = rs[s2];
-    const PartPlan& pp = plan.part[X];
-    const int w_lo = e[s2][0], w_hi = e[s2][1], k_lo = e[s2][2];
-    if (ord < 0 || ord >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 || k_lo >= pp.kmax) {
-      ok = false;
-      continue;
-    }
-    const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
-    o0[s2] = pp.o_base + (slot0 * pp.slot_rows + r) * D;
-    l0[s2] = pp.lse_base + slot0 * pp.slot_rows + r;
-    kmax[s2] = pp.kmax;
-    klo[s2] = k_lo;
-    n[s2] = w_hi - w_lo + 1;
-    srows[s2] = pp.slot_rows;
-  }
-  if (!ok) {   // the item table is inconsistent: fail loudly rather than read out of range
-    const int lane = threadIdx.x & 63;
-    for (int d = lane; d < D; d += 64) out[row * D + d] = 0x7FC0;   // bf16 NaN
-    if (out_lse && lane == 0) out_lse[row] = __builtin_nanf("");
-    return;
-  }
-  const int np = n[0];
-  const int64_t pO0 = o0[0], sO0 = o0[1], pL0 = l0[0], sL0 = l0[1];
-  const int pK = kmax[0], sK = kmax[1], pKlo = klo[0], sKlo = klo[1], pR = srows[0], sR = srows[1];
-  auto rel_slots = [&](int p) -> int64_t {   // slots between part p and its item's part 0
-    const bool pre = p < np;
-    const int i = pre ? p : p - np;
-    return i == 0 ? 0 : (int64_t)i * (pre ? pK : sK) - (pre ? pKlo : sKlo);
-  };
-  auto po = [&](int p) {
-    const bool pre = p < np;
-    return ws + (pre ? pO0 : sO0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * D;
-  };
-  auto pl = [&](int p) {
-    const bool pre = p < np;
-    return ws[(pre ? pL0 : sL0) + rel_slots(p) * (int64_t)(pre ? pR : sR)];
-  };
-  merge_row_v4<D>(np + n[1], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
+  if (row >= (int64_t)splan.N * splan.Hq) return;
+  fork_merge_row<D>(splan, ws, row, out, out_lse);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
