@@ -52,7 +52,7 @@ def source_hash() -> str:
 def traffic_from_profile(workload: str):
     """HBM traffic of the partial kernel from committed rocprofv3 counter runs,
     only if they were taken on the current kernel source."""
-    p = os.path.join(ROOT, "profiles", f"traffic_attn_mfma_{workload}.json")
+    p = os.path.join(ROOT, "profiles", f"traffic_partials_{workload}.json")
     if not os.path.exists(p):
         return None
     with open(p) as fh:
