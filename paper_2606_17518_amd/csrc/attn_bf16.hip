@@ -54,6 +54,20 @@
 namespace specgen {
 namespace bf16k {
 
+// l + the sum of the 8 bf16 probabilities packed in pk: the denominator adds
+// exactly the weights the PV product uses (one dot2 with (1, 1) per pair).
+// The elements are copied to scalars first: __builtin_bit_cast applied to an
+// element of an ext_vector_type value reads element 0 whatever the index.
+__device__ __forceinline__ float row_sum_bf16(const u32x4 pk, float l) {
+  const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  const uint32_t w0 = pk.x, w1 = pk.y, w2 = pk.z, w3 = pk.w;
+  float a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), one, 0.f, false);
+  float a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), one, l, false);
+  a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), one, a0, false);
+  a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), one, a1, false);
+  return a0 + a1;
+}
+
 // The running max moves only when a new score would give a probability above
 // 2^kRescaleLog2 relative to it.
 constexpr float kRescaleLog2 = 8.f;
@@ -282,7 +296,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   f32x4 acc[2][DT];
   float m_run[2], l_run[2];
   constexpr int NT = 2;   // 16-row MFMA tiles per row group
-  int RG = 1, TG = 1, rg = 0, tg = 0;
+  int RG = 1, TG = 1, rg = 0, tg = 0, tpg = TT;   // tpg: tokens of a tile per token group
   bool active = false;
 
   auto begin_item = [&](const Desc& d, int stage) {
@@ -292,6 +306,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     TG = (TT / 32) < (C::kWaves / RG) ? (TT / 32) : (C::kWaves / RG);
     rg = wave % RG;
     tg = wave / RG;
+    tpg = TT / TG;
     active = wave < RG * TG;
     const SG_LDS uint8_t* qb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
 #pragma unroll
@@ -314,6 +329,17 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     constexpr bool kMask = decltype(mask_c)::value;   // the slab runs past the tile's valid tokens
     const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
     const SG_LDS uint8_t* vb = kb + C::kTileB;
+    // V^T operands: lane (G, ln) reads V[sb+8G+0..7][16dt+ln] in one 16-byte
+    // load.  They are read with the keys, so the reads overlap the score MFMAs
+    // and the softmax rather than waiting in front of the PV product.
+    u32x4 vkeep = {~0u, ~0u, ~0u, ~0u};   // masked slab: keep only the values of valid tokens
+    if constexpr (kMask) {
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int t0 = sb + 8 * G + 2 * e2;
+        vkeep[e2] = (t0 < valid ? 0x0000FFFFu : 0u) | (t0 + 1 < valid ? 0xFFFF0000u : 0u);
+      }
+    }
     f32x4 s[2][NT];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -321,15 +347,23 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       for (int nt = 0; nt < NT; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
     const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
+    bf16x8 ka[KS], kbo[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cho = (((4 * ks + G) ^ k_lane_swz) << 4);
-      const bf16x8 A0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
-      const bf16x8 A1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
+      ka[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
+      kbo[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
+    }
+    const SG_LDS uint8_t* vrow = vb + (sb >> 4) * C::kSliceB + v_lane_off;
+    u32x4 vraw[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vraw[dt] = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, qop[nt][ks], s[0][nt], 0, 0, 0);
-        s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, qop[nt][ks], s[1][nt], 0, 0, 0);
+        s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qop[nt][ks], s[0][nt], 0, 0, 0);
+        s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kbo[ks], qop[nt][ks], s[1][nt], 0, 0, 0);
       }
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
@@ -343,54 +377,74 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
             for (int nt = 0; nt < NT; ++nt) s[u][nt][e] = -INFINITY;
           }
     }
-    bf16x8 pop[NT];
+    // this lane's max over its 8 scores of each row; the row max (over the 4
+    // lanes of a row) is only needed when the reference max moves
+    float mx[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      float mx = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
-                       fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
-      mx = rows4_max(mx);
-      // lazy rescaling: the reference max only moves when a score exceeds it
-      // by more than 2^kRescaleLog2 in probability (wave-uniform decision)
-      if (__builtin_amdgcn_ballot_w64(mx * a.c_log2 > m_run[nt] * a.c_log2 + kRescaleLog2)) {
-        const float m_new = fmaxf(m_run[nt], mx);
+    for (int nt = 0; nt < NT; ++nt)
+      mx[nt] = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                     fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+    // Lazy rescaling: the reference max only moves when a score exceeds it by
+    // more than 2^kRescaleLog2 in probability (one wave-uniform decision for
+    // both N-tiles; m_run is the same on the 4 lanes of a row).
+    if (__builtin_amdgcn_ballot_w64(mx[0] * a.c_log2 > m_run[0] * a.c_log2 + kRescaleLog2 ||
+                                   mx[1] * a.c_log2 > m_run[1] * a.c_log2 + kRescaleLog2)) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const float m_new = fmaxf(m_run[nt], rows4_max(mx[nt]));
         const float alpha = __builtin_amdgcn_exp2f((m_run[nt] - m_new) * a.c_log2);
         m_run[nt] = m_new;
         l_run[nt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
       }
-      const float mc = m_run[nt] * a.c_log2;
-      float p[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(fmaf(s[0][nt][e], a.c_log2, -mc));
-        p[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][nt][e], a.c_log2, -mc));
-      }
-      l_run[nt] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-      u32x4 pk;
-      pk[0] = pack_bf16x2(p[0], p[1]);
-      pk[1] = pack_bf16x2(p[2], p[3]);
-      pk[2] = pack_bf16x2(p[4], p[5]);
-      pk[3] = pack_bf16x2(p[6], p[7]);
-      pop[nt] = __builtin_bit_cast(bf16x8, pk);
     }
-    // O^T += V^T P^T: lane (G, ln) reads V[sb+8G+0..7][16dt+ln] in one 16-byte load
-    u32x4 vkeep = {~0u, ~0u, ~0u, ~0u};   // masked slab: keep only the values of valid tokens
-    if constexpr (kMask) {
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        const int t0 = sb + 8 * G + 2 * e2;
-        vkeep[e2] = (t0 < valid ? 0x0000FFFFu : 0u) | (t0 + 1 < valid ? 0xFFFF0000u : 0u);
-      }
-    }
-    const SG_LDS uint8_t* vrow = vb + (sb >> 4) * C::kSliceB + v_lane_off;
+    bf16x8 vop[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      u32x4 vv = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
+      u32x4 vv = vraw[dt];
       if constexpr (kMask) vv &= vkeep;   // values past the end may be any bits, NaN included
-      const bf16x8 A = __builtin_bit_cast(bf16x8, vv);
+      vop[dt] = __builtin_bit_cast(bf16x8, vv);
+    }
+    // P = exp2(S - m) in bf16, then O^T += V^T P^T; the exponentials of N-tile 1
+    // are interleaved with the PV MFMAs of N-tile 0
+    const float mc0 = m_run[0] * a.c_log2, mc1 = m_run[1] * a.c_log2;
+    float p0[8], p1[8];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, pop[nt], acc[nt][dt], 0, 0, 0);
+    for (int e = 0; e < 4; ++e) {
+      p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], a.c_log2, -mc0));
+      p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], a.c_log2, -mc0));
+    }
+    u32x4 pk0;
+    pk0[0] = pack_bf16x2(p0[0], p0[1]);
+    pk0[1] = pack_bf16x2(p0[2], p0[3]);
+    pk0[2] = pack_bf16x2(p0[4], p0[5]);
+    pk0[3] = pack_bf16x2(p0[6], p0[7]);
+    l_run[0] = row_sum_bf16(pk0, l_run[0]);
+    const bf16x8 pop0 = __builtin_bit_cast(bf16x8, pk0);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop0, acc[0][dt], 0, 0, 0);
+      if (dt < 8) p1[dt] = __builtin_amdgcn_exp2f(fmaf(s[dt >> 2][1][dt & 3], a.c_log2, -mc1));
+    }
+#pragma unroll
+    for (int e = DT; e < 8; ++e)   // D = 64: fewer PV MFMAs than exponentials
+      p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], a.c_log2, -mc1));
+    u32x4 pk1;
+    pk1[0] = pack_bf16x2(p1[0], p1[1]);
+    pk1[1] = pack_bf16x2(p1[2], p1[3]);
+    pk1[2] = pack_bf16x2(p1[4], p1[5]);
+    pk1[3] = pack_bf16x2(p1[6], p1[7]);
+    l_run[1] = row_sum_bf16(pk1, l_run[1]);
+    const bf16x8 pop1 = __builtin_bit_cast(bf16x8, pk1);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop1, acc[1][dt], 0, 0, 0);
+    // pin the interleave: (MFMA, TRANS, VALU) x 8 after N-tile 0's softmax
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
     }
   };
 
@@ -399,8 +453,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     const int tile = d.tile0 + k;
     const int rem = d.nv - tile * TT;
     const int valid = rem < TT ? rem : TT;
-    const int tok0 = tg * (TT / TG);
-    const int tok1 = (tok0 + TT / TG) < valid ? (tok0 + TT / TG) : valid;   // this wave's tokens: [tok0, tok1)
+    const int tok0 = tg * tpg;
+    const int tok1 = (tok0 + tpg) < valid ? (tok0 + tpg) : valid;   // this wave's tokens: [tok0, tok1)
     int sb = tok0;
     for (; sb + 32 <= tok1; sb += 32) slab(std::integral_constant<bool, false>(), stage, sb, valid);
     if (sb < tok1) slab(std::integral_constant<bool, true>(), stage, sb, valid);   // partial last slab
