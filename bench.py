@@ -36,8 +36,14 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-# the kernel that serves bf16 KV on the MFMA path, and the sources it includes
-PARTIAL_KERNEL = "attn_bf16_kernel<128>"
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of the MI355X
+
+
+# the partial kernel of the MFMA path (bf16 or E4M3 KV), and the sources it includes
+def partial_kernel(D: int, fp8: bool) -> str:
+    return f"attn_bf16_kernel<{D}, {'true' if fp8 else 'false'}>"
+
+
 PARTIAL_SOURCES = ("attn_bf16.hip", "worker.h", "common.h", "plan.h")
 
 
@@ -200,6 +206,23 @@ def main():
     part_s = float(part_ms.mean()) / 1e3
     value = attn_bytes / attn_s / 1e9
     achieved = kern_bytes / part_s / 1e9
+    # matrix work of the partial kernel: S = q K^T and P V over every key of
+    # every (fork, q head) row, 2 flops per multiply-add each
+    keys = sum(int(b.prefix_len[t]) * int(b.fork_off[t + 1] - b.fork_off[t]) for t in range(b.num_traces)) \
+        + int(b.suffix_len.sum())
+    kern_flops = 4.0 * D * Hq * keys
+    fp8 = b.kv_dtype != "bf16"
+    if fp8:   # E4M3 KV: 2r/e flop per byte puts the MFMA path above the ridge
+        tflops = kern_flops / part_s / 1e12
+        roofline = {"kernel": partial_kernel(D, True) + " (partials phase)", "bound": "mfma",
+                    "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload),
+                    "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2)}
+    else:
+        roofline = {"kernel": partial_kernel(D, False) + " (partials phase)", "bound": "hbm",
+                    "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profile(args.workload),
+                    "algorithmic_bytes_per_launch": int(kern_bytes)}
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True,
@@ -216,9 +239,7 @@ def main():
                     "note": "mean/p10/p50/p90: whole call between two events; partials/merge: the kernels "
                             "timed separately in a second run of the same steps"},
         "attn_algorithmic_bytes": int(attn_bytes),
-        "roofline": {"kernel": PARTIAL_KERNEL + " (partials phase)", "bound": "hbm", "achieved": round(achieved, 2),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic_from_profile(args.workload), "algorithmic_bytes_per_launch": int(kern_bytes)},
+        "roofline": roofline,
     }
     if imp is not None:
         res["import"] = {"blocks": int(len(ids)), "bytes": int(import_bytes), "us": round(float(imp_ms.mean()) * 1e3, 2),

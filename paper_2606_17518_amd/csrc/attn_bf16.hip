@@ -72,7 +72,7 @@ __device__ __forceinline__ float row_sum_bf16(const u32x4 pk, float l) {
 // 2^kRescaleLog2 relative to it.
 constexpr float kRescaleLog2 = 8.f;
 
-template <int D>
+template <int D, bool FP8>
 struct Cfg {
   static constexpr int kThreads = 512;
   static constexpr int kWaves = 8;
@@ -96,13 +96,23 @@ struct Cfg {
   static constexpr int kIdCap = 2048;                 // block ids of a worker's range
   static constexpr int kIdsPerTile = kTT / 16;
   static constexpr int kTileCap = kIdCap / kIdsPerTile;
-  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
+  // E4M3 KV: a tile slot lands its K and V codes in the stage's upper half
+  // (converted to the bf16 layout in place once it has landed), and its
+  // blocks' k / v scales in a per-stage area: per wave 32 bytes of each.
+  static constexpr int kF8Slice = 16 * D;             // code bytes of one block slice
+  static constexpr int kF8K = kTileB;                 // stage offset of the K codes
+  static constexpr int kF8V = kTileB + kTileB / 2;    // and of the V codes
+  static constexpr int kSclStage = kWaves * 64;
+  static constexpr int kOffScl = kOffIds + kIdCap * 4;
+  static constexpr int kLdsBytes = kOffScl + (FP8 ? kStages * kSclStage : 0);
   static_assert(kSlicesPerWave * kPiecesPerSlice == kDmaSlot, "a tile slot is four instructions per wave");
   static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
   static_assert(kTileCap <= kThreads, "the walk takes one tile of the range per thread");
   static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
+  static_assert(!FP8 || (kSlicesPerWave * (kF8Slice / 1024) == 2 && kTT / 16 <= 8),
+                "an E4M3 tile slot is two code instructions and two scale instructions per wave");
 };
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
@@ -121,6 +131,28 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
   const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
   const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
+}
+
+// One wave instruction moving 4 bytes per active lane from gbase + voff into
+// LDS at lds_addr + 4 * lane (same uniformity rules as dma16).
+__device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, uint32_t lds_addr) {
+  const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+  const uint32_t glo = __builtin_amdgcn_readfirstlane((uint32_t)g);
+  const uint32_t ghi = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+  const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
+}
+
+// Four E4M3 codes -> four bf16 (exact: every E4M3 value, NaN included, has a
+// bf16 encoding; the hardware converts to fp32 and the upper halves are kept).
+__device__ __forceinline__ u32x2 e4m3x4_to_bf16x4(uint32_t w) {
+  const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+  const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(w, true);
+  u32x2 r;
+  r[0] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
+  r[1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+  return r;
 }
 
 template <int N>
@@ -148,10 +180,10 @@ __device__ __forceinline__ void vm_wait_le(int n) {
 
 }  // namespace bf16k
 
-template <int D>
+template <int D, bool FP8>
 __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, const Plan plan_arg) {
   using namespace bf16k;
-  using C = Cfg<D>;
+  using C = Cfg<D, FP8>;
   constexpr int TT = C::kTT;
   constexpr int CPR = C::kCPR;
   constexpr int KS = D / 32;   // k-steps of S^T
@@ -257,6 +289,29 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         const uint32_t voff = (uint32_t)(((int64_t)fork * plan.Hq + hq) * head_stride) + (uint32_t)(chunk * 16);
         dma16(a.q, voff, st + (uint32_t)(n * 1024));
       }
+    } else if constexpr (FP8) {
+      // this wave's block slices of the tile's K (waves 0-3) or V (waves 4-7)
+      // codes, as they are; then the k and v scales of the tile's blocks
+      // (lanes < TT / 16), one copy per wave
+      constexpr int NI8 = C::kF8Slice / 1024;
+      const uint8_t* pool = is_v ? a.v_pool : a.k_pool;
+      const int64_t blk8 = (int64_t)plan.Hkv * C::kF8Slice;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int kb = wq * NB + b;
+        const uint8_t* sb = pool + (int64_t)id[b] * blk8 + (int64_t)d.j * C::kF8Slice;
+#pragma unroll
+        for (int i = 0; i < NI8; ++i)
+          dma16(sb, (uint32_t)(1024 * i + 16 * lane),
+                st + (uint32_t)((is_v ? C::kF8V : C::kF8K) + kb * C::kF8Slice + i * 1024));
+      }
+      constexpr int nblk = TT / 16;
+      const int sid = ids[(d.rtile0 + k) * C::kIdsPerTile + (lane & (nblk - 1))];
+      const uint32_t sl = lds_base + (uint32_t)(C::kOffScl + stage * C::kSclStage + wave * 64);
+      if (lane < nblk) {
+        dma4(a.k_scale, (uint32_t)sid * 4u, sl);
+        dma4(a.v_scale, (uint32_t)sid * 4u, sl + 32u);
+      }
     } else {
       const int tile = d.tile0 + k;
       const uint8_t* pool = is_v ? a.v_pool : a.k_pool;
@@ -283,6 +338,46 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       }
     }
   };
+
+  // E4M3: once a tile slot has landed, every thread turns one 16-byte chunk of
+  // K codes and one of V codes into the bf16 layout the MFMA path reads (K
+  // rows swizzled, V^T slices with halves swapped on bit 3 of the row), in
+  // place: all codes are read before the barrier, written after it.  Codes of
+  // tokens past an item's end are converted too; scores and values of those
+  // tokens are masked later, as for bf16.
+  auto convert_tile = [&](int stage) {
+    uint8_t* st8 = lds + stage * C::kStageB;
+    const u32x4 ck = *reinterpret_cast<const u32x4*>(st8 + C::kF8K + tid * 16);
+    const u32x4 cv = *reinterpret_cast<const u32x4*>(st8 + C::kF8V + tid * 16);
+    lds_barrier();
+    // K chunk: 16 dims of one token row of block slice kb
+    {
+      const int o = tid * 16;
+      const int kb = o / C::kF8Slice;
+      const int tok = (o % C::kF8Slice) / D;
+      const int c8 = (o % D) / 8;                  // first bf16 chunk of the 16 dims
+      const int tt = kb * 16 + tok;
+      const u32x2 b0 = e4m3x4_to_bf16x4(ck[0]), b1 = e4m3x4_to_bf16x4(ck[1]);
+      const u32x2 b2 = e4m3x4_to_bf16x4(ck[2]), b3 = e4m3x4_to_bf16x4(ck[3]);
+      const int sw = swz_k<CPR>(tt);
+      *reinterpret_cast<u32x4*>(st8 + tt * C::kRowB + ((c8 ^ sw) << 4)) = u32x4{b0[0], b0[1], b1[0], b1[1]};
+      *reinterpret_cast<u32x4*>(st8 + tt * C::kRowB + (((c8 + 1) ^ sw) << 4)) = u32x4{b2[0], b2[1], b3[0], b3[1]};
+    }
+    // V chunk: the 16 tokens of row d of block slice kb
+    {
+      const int o = tid * 16;
+      const int kb = o / C::kF8Slice;
+      const int dd = (o % C::kF8Slice) / 16;
+      const int sw = (dd >> 3) & 1;
+      uint8_t* vs = st8 + C::kTileB + kb * C::kSliceB;
+      const u32x2 b0 = e4m3x4_to_bf16x4(cv[0]), b1 = e4m3x4_to_bf16x4(cv[1]);
+      const u32x2 b2 = e4m3x4_to_bf16x4(cv[2]), b3 = e4m3x4_to_bf16x4(cv[3]);
+      *reinterpret_cast<u32x4*>(vs + (2 * dd + sw) * 16) = u32x4{b0[0], b0[1], b1[0], b1[1]};
+      *reinterpret_cast<u32x4*>(vs + (2 * dd + (1 ^ sw)) * 16) = u32x4{b2[0], b2[1], b3[0], b3[1]};
+    }
+    lds_barrier();
+  };
+  static_assert(!FP8 || C::kTT * D == 16 * C::kThreads, "one K and one V code chunk per thread");
 
   // ---- compute side ------------------------------------------------------------
   const int G = lane >> 4;     // 16-lane group
@@ -367,6 +462,18 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       }
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
+    // (all in block (sb + 8G) / 16 of the tile)
+    float vsc = 1.f;
+    if constexpr (FP8) {
+      const float* scl = reinterpret_cast<const float*>(lds + C::kOffScl + stage * C::kSclStage + wave * 64);
+      const int blk = (sb + 8 * G) >> 4;
+      const float ksc = scl[blk];
+      vsc = scl[8 + blk];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) s[u][nt] *= ksc;
+    }
     if constexpr (kMask) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -415,12 +522,17 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], a.c_log2, -mc0));
       p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], a.c_log2, -mc0));
     }
+    if constexpr (FP8) {   // the row sum excludes the value scale, which P carries into PV
+      l_run[0] += ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p0[e] *= vsc;
+    }
     u32x4 pk0;
     pk0[0] = pack_bf16x2(p0[0], p0[1]);
     pk0[1] = pack_bf16x2(p0[2], p0[3]);
     pk0[2] = pack_bf16x2(p0[4], p0[5]);
     pk0[3] = pack_bf16x2(p0[6], p0[7]);
-    l_run[0] = row_sum_bf16(pk0, l_run[0]);
+    if constexpr (!FP8) l_run[0] = row_sum_bf16(pk0, l_run[0]);
     const bf16x8 pop0 = __builtin_bit_cast(bf16x8, pk0);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -430,12 +542,17 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int e = DT; e < 8; ++e)   // D = 64: fewer PV MFMAs than exponentials
       p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], a.c_log2, -mc1));
+    if constexpr (FP8) {
+      l_run[1] += ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p1[e] *= vsc;
+    }
     u32x4 pk1;
     pk1[0] = pack_bf16x2(p1[0], p1[1]);
     pk1[1] = pack_bf16x2(p1[2], p1[3]);
     pk1[2] = pack_bf16x2(p1[4], p1[5]);
     pk1[3] = pack_bf16x2(p1[6], p1[7]);
-    l_run[1] = row_sum_bf16(pk1, l_run[1]);
+    if constexpr (!FP8) l_run[1] = row_sum_bf16(pk1, l_run[1]);
     const bf16x8 pop1 = __builtin_bit_cast(bf16x8, pk1);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop1, acc[1][dt], 0, 0, 0);
@@ -595,6 +712,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     if (cp_k < 0) {
       begin_item(cp_d, stage);
     } else {
+      if constexpr (FP8) convert_tile(stage);
       compute_tile(cp_d, cp_k, stage);
       if (cp_k == cp_d.ntile - 1) st0 = uniform(finish_item(cp_d, stage));
     }
@@ -605,17 +723,29 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   }
 }
 
-hipError_t launch_attn_bf16(const AttnArgs& a, const Plan& plan, hipStream_t stream) {
+// Partial kernel of the MFMA partition: bf16 KV, or E4M3 KV decoded exactly to
+// bf16 in LDS.
+hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream) {
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
-  if (plan.D == 128)
-    hipLaunchKernelGGL((attn_bf16_kernel<128>), dim3(W), dim3(512), 0, stream, a, plan);
-  else
-    hipLaunchKernelGGL((attn_bf16_kernel<64>), dim3(W), dim3(512), 0, stream, a, plan);
+  if (plan.D == 128) {
+    if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(W), dim3(512), 0, stream, a, plan);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(W), dim3(512), 0, stream, a, plan);
+  } else {
+    if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(W), dim3(512), 0, stream, a, plan);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(W), dim3(512), 0, stream, a, plan);
+  }
   return hipGetLastError();
 }
 
-int bf16_item_cap() { return bf16k::Cfg<128>::kItemCap; }
-int bf16_tile_cap(int D) { return D == 128 ? bf16k::Cfg<128>::kTileCap : bf16k::Cfg<64>::kTileCap; }
+int mfma_tile_tokens(int D, bool fp8) {
+  (void)fp8;
+  return D == 128 ? bf16k::Cfg<128, false>::kTT : bf16k::Cfg<64, false>::kTT;
+}
+int mfma_tile_cap(int D, bool fp8) {
+  (void)fp8;
+  return D == 128 ? bf16k::Cfg<128, false>::kTileCap : bf16k::Cfg<64, false>::kTileCap;
+}
+int mfma_item_cap() { return bf16k::Cfg<128, false>::kItemCap; }
 
 }  // namespace specgen

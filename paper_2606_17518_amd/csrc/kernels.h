@@ -8,15 +8,11 @@
 
 namespace specgen {
 
-// attn_mfma.hip
+// attn_bf16.hip (MFMA partition: bf16 or E4M3 KV)
 hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
 int mfma_tile_tokens(int D, bool fp8);
 int mfma_item_cap();
 int mfma_tile_cap(int D, bool fp8);
-// attn_bf16.hip (bf16 KV)
-hipError_t launch_attn_bf16(const AttnArgs& a, const Plan& plan, hipStream_t stream);
-int bf16_item_cap();
-int bf16_tile_cap(int D);
 // attn_dot.hip
 hipError_t launch_attn_dot_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
 int dot_tile_tokens(int D);

@@ -1,7 +1,6 @@
 // merge.h -- the log-sum-exp merge of one output row of fork-decode attention
-// from the partial results the split attention kernels left in the workspace.
-// Used by the merge kernel (merge.hip) and by the bf16 attention kernel when
-// it runs the merge itself after a grid-wide barrier.
+// from the partial results the split attention kernels left in the workspace
+// (used by the merge kernel, merge.hip).
 //
 // Partials over disjoint key sets combine exactly: with M = max_s lse_s and
 // w_s = exp(lse_s - M), out = sum_s w_s o_s / sum_s w_s and
