@@ -96,23 +96,22 @@ struct Cfg {
   static constexpr int kIdCap = 2048;                 // block ids of a worker's range
   static constexpr int kIdsPerTile = kTT / 16;
   static constexpr int kTileCap = kIdCap / kIdsPerTile;
-  // E4M3 KV: a tile slot lands its K and V codes in the stage's upper half
-  // (converted to the bf16 layout in place once it has landed), and its
-  // blocks' k / v scales in a per-stage area: per wave 32 bytes of each.
+  // E4M3 KV: a tile slot lands 1 KiB pieces of K and V codes (two
+  // instructions per wave instead of four), each at the start of the 2 KiB run
+  // of the bf16 tile that its converting wave writes: K code piece n (64
+  // chunks of 16 bytes: 8 token rows for D = 128, 16 for D = 64) fills bf16
+  // K rows at 2 KiB * n, V code piece n the V^T rows at kTileB + 2 KiB * n.
+  // Each wave then converts its own pieces in place, with no barrier.
   static constexpr int kF8Slice = 16 * D;             // code bytes of one block slice
-  static constexpr int kF8K = kTileB;                 // stage offset of the K codes
-  static constexpr int kF8V = kTileB + kTileB / 2;    // and of the V codes
-  static constexpr int kSclStage = kWaves * 64;
-  static constexpr int kOffScl = kOffIds + kIdCap * 4;
-  static constexpr int kLdsBytes = kOffScl + (FP8 ? kStages * kSclStage : 0);
+  static constexpr int kTileDma = FP8 ? 2 : kDmaSlot; // instructions per wave of a tile slot
+  static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
   static_assert(kSlicesPerWave * kPiecesPerSlice == kDmaSlot, "a tile slot is four instructions per wave");
   static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
   static_assert(kTileCap <= kThreads, "the walk takes one tile of the range per thread");
   static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
-  static_assert(!FP8 || (kSlicesPerWave * (kF8Slice / 1024) == 2 && kTT / 16 <= 8),
-                "an E4M3 tile slot is two code instructions and two scale instructions per wave");
+  static_assert(!FP8 || kSlicesPerWave * (kF8Slice / 1024) == kTileDma, "E4M3 code instructions per wave");
 };
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
@@ -131,17 +130,6 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
   const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
   const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
-}
-
-// One wave instruction moving 4 bytes per active lane from gbase + voff into
-// LDS at lds_addr + 4 * lane (same uniformity rules as dma16).
-__device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, uint32_t lds_addr) {
-  const uint64_t g = reinterpret_cast<uint64_t>(gbase);
-  const uint32_t glo = __builtin_amdgcn_readfirstlane((uint32_t)g);
-  const uint32_t ghi = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
-  const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
-  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
 }
 
 // Four E4M3 codes -> four bf16 (exact: every E4M3 value, NaN included, has a
@@ -291,8 +279,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       }
     } else if constexpr (FP8) {
       // this wave's block slices of the tile's K (waves 0-3) or V (waves 4-7)
-      // codes, as they are; then the k and v scales of the tile's blocks
-      // (lanes < TT / 16), one copy per wave
+      // codes, as they are
       constexpr int NI8 = C::kF8Slice / 1024;
       const uint8_t* pool = is_v ? a.v_pool : a.k_pool;
       const int64_t blk8 = (int64_t)plan.Hkv * C::kF8Slice;
@@ -303,14 +290,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
         for (int i = 0; i < NI8; ++i)
           dma16(sb, (uint32_t)(1024 * i + 16 * lane),
-                st + (uint32_t)((is_v ? C::kF8V : C::kF8K) + kb * C::kF8Slice + i * 1024));
-      }
-      constexpr int nblk = TT / 16;
-      const int sid = ids[(d.rtile0 + k) * C::kIdsPerTile + (lane & (nblk - 1))];
-      const uint32_t sl = lds_base + (uint32_t)(C::kOffScl + stage * C::kSclStage + wave * 64);
-      if (lane < nblk) {
-        dma4(a.k_scale, (uint32_t)sid * 4u, sl);
-        dma4(a.v_scale, (uint32_t)sid * 4u, sl + 32u);
+                st + (uint32_t)((is_v ? C::kTileB : 0) + 2048 * (kb * NI8 + i)));
       }
     } else {
       const int tile = d.tile0 + k;
@@ -339,20 +319,22 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     }
   };
 
-  // E4M3: once a tile slot has landed, every thread turns one 16-byte chunk of
-  // K codes and one of V codes into the bf16 layout the MFMA path reads (K
-  // rows swizzled, V^T slices with halves swapped on bit 3 of the row), in
-  // place: all codes are read before the barrier, written after it.  Codes of
-  // tokens past an item's end are converted too; scores and values of those
-  // tokens are masked later, as for bf16.
+  // E4M3: once a tile slot has landed (one iteration before it is computed),
+  // every wave turns its K code piece and V code piece (lane: one 16-byte chunk
+  // of each) into the bf16 layout the MFMA path reads -- K rows swizzled, V^T
+  // slices with halves swapped on bit 3 of the row -- inside the 2 KiB runs
+  // that hold them: it reads its codes before it writes (one wave's LDS
+  // operations run in order), and no other wave touches those runs, so no
+  // barrier; the next iteration's barrier publishes the tile.  Codes of tokens
+  // past an item's end are converted too; their scores and values are masked
+  // later, as for bf16.
   auto convert_tile = [&](int stage) {
     uint8_t* st8 = lds + stage * C::kStageB;
-    const u32x4 ck = *reinterpret_cast<const u32x4*>(st8 + C::kF8K + tid * 16);
-    const u32x4 cv = *reinterpret_cast<const u32x4*>(st8 + C::kF8V + tid * 16);
-    lds_barrier();
+    const u32x4 ck = *reinterpret_cast<const u32x4*>(st8 + 2048 * wave + 16 * lane);
+    const u32x4 cv = *reinterpret_cast<const u32x4*>(st8 + C::kTileB + 2048 * wave + 16 * lane);
+    const int o = tid * 16;   // byte of the chunk within the tile's codes of one tensor
     // K chunk: 16 dims of one token row of block slice kb
     {
-      const int o = tid * 16;
       const int kb = o / C::kF8Slice;
       const int tok = (o % C::kF8Slice) / D;
       const int c8 = (o % D) / 8;                  // first bf16 chunk of the 16 dims
@@ -365,7 +347,6 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     }
     // V chunk: the 16 tokens of row d of block slice kb
     {
-      const int o = tid * 16;
       const int kb = o / C::kF8Slice;
       const int dd = (o % C::kF8Slice) / 16;
       const int sw = (dd >> 3) & 1;
@@ -375,9 +356,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       *reinterpret_cast<u32x4*>(vs + (2 * dd + sw) * 16) = u32x4{b0[0], b0[1], b1[0], b1[1]};
       *reinterpret_cast<u32x4*>(vs + (2 * dd + (1 ^ sw)) * 16) = u32x4{b2[0], b2[1], b3[0], b3[1]};
     }
-    lds_barrier();
   };
   static_assert(!FP8 || C::kTT * D == 16 * C::kThreads, "one K and one V code chunk per thread");
+  static_assert(!FP8 || 2 * C::kTileB == 2048 * 2 * C::kWaves, "a 2 KiB run of each tensor per wave");
 
   // ---- compute side ------------------------------------------------------------
   const int G = lane >> 4;     // 16-lane group
@@ -420,7 +401,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   };
 
   // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
-  auto slab = [&](auto mask_c, int stage, int sb, int valid) {
+  auto slab = [&](auto mask_c, int stage, int sb, int valid, int idb) {
     constexpr bool kMask = decltype(mask_c)::value;   // the slab runs past the tile's valid tokens
     const SG_LDS uint8_t* kb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
     const SG_LDS uint8_t* vb = kb + C::kTileB;
@@ -465,10 +446,21 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     // (all in block (sb + 8G) / 16 of the tile)
     float vsc = 1.f;
     if constexpr (FP8) {
-      const float* scl = reinterpret_cast<const float*>(lds + C::kOffScl + stage * C::kSclStage + wave * 64);
-      const int blk = (sb + 8 * G) >> 4;
-      const float ksc = scl[blk];
-      vsc = scl[8 + blk];
+      // the slab's two blocks (ids[idb + sb/16] and the next): lanes G < 2 hold
+      // keys of the first
+      // of the first.  Scalar loads (the constant address space): a vector load
+      // would sit in the vmcnt queue behind the slots in flight.
+      typedef const __attribute__((address_space(4))) float* cfp;
+      const int id0 = uniform(ids[idb + (sb >> 4)]);
+      const int id1 = uniform(ids[idb + (sb >> 4) + 1]);
+      const cfp ks = (cfp)a.k_scale;
+      const cfp vs = (cfp)a.v_scale;
+      // (each value is pinned wave-uniform, so the two loads are not merged
+      // into one per-lane load of a selected address)
+      auto sload = [](cfp p, int i) { return __int_as_float(uniform(__float_as_int(p[i]))); };
+      const float k0 = sload(ks, id0), k1 = sload(ks, id1), v0 = sload(vs, id0), v1 = sload(vs, id1);
+      const float ksc = G < 2 ? k0 : k1;
+      vsc = G < 2 ? v0 : v1;
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -572,9 +564,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     const int valid = rem < TT ? rem : TT;
     const int tok0 = tg * tpg;
     const int tok1 = (tok0 + tpg) < valid ? (tok0 + tpg) : valid;   // this wave's tokens: [tok0, tok1)
+    const int idb = (d.rtile0 + k) * C::kIdsPerTile;   // the tile's block ids in LDS
     int sb = tok0;
-    for (; sb + 32 <= tok1; sb += 32) slab(std::integral_constant<bool, false>(), stage, sb, valid);
-    if (sb < tok1) slab(std::integral_constant<bool, true>(), stage, sb, valid);   // partial last slab
+    for (; sb + 32 <= tok1; sb += 32) slab(std::integral_constant<bool, false>(), stage, sb, valid, idb);
+    if (sb < tok1) slab(std::integral_constant<bool, true>(), stage, sb, valid, idb);   // partial last slab
   };
 
   // Combine the token groups of the item through the stage just consumed and
@@ -673,52 +666,55 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
   for (int b = 0; b < NB; ++b) is_id[b] = 0;
   Desc is_d = load_desc(0);
-  // slot 0 is the first item's q rows
-  issue_slot(is_d, is_k, is_id, 0);
-  advance(is_ii, is_k, is_d);
-  ++issued;
+  // Vector-memory operations this wave has issued (DMA instructions and
+  // partial stores), and the count right after the DMAs of slots s .. s + 3 of
+  // iteration s (the slot issued during iteration s is s + 3): vmcnt retires
+  // in order, so slot t has landed once at most ops - mark(t) operations are
+  // outstanding.  Fixed roles shifted once per iteration, never an indexed
+  // array (which the compiler would place in scratch memory).
+  int ops = 0;
+  int mk0 = 0, mk1 = 0, mk2 = 0, mk3 = 0;
   auto load_ids = [&]() {   // block ids of the next slot to issue, if it is a tile
     if (issued < S && is_k >= 0) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) is_id[b] = block_id(is_d, is_k, b);
     }
   };
-  for (int p = 1; p < C::kStages - 1; ++p) {
-    if (issued < S) {
-      load_ids();
-      issue_slot(is_d, is_k, is_id, issued & 3);
-      advance(is_ii, is_k, is_d);
-      ++issued;
-    }
-  }
-  load_ids();
-  int st1 = 0, st2 = 0, st3 = 0;   // stores issued one, two and three iterations ago
+  auto issue_next = [&]() {   // slot `issued` into its stage (the one consumed last iteration)
+    issue_slot(is_d, is_k, is_id, issued & 3);
+    ops += is_k < 0 ? C::kDmaSlot : C::kTileDma;
+    advance(is_ii, is_k, is_d);
+    ++issued;
+    load_ids();   // for the next issue
+    return ops;
+  };
+  // slots 0 .. 2 (slot 0 is the first item's q rows)
+  static_assert(C::kStages == 4, "three slots ahead");
+  if (issued < S) mk0 = issue_next();
+  if (issued < S) mk1 = issue_next();
+  if (issued < S) mk2 = issue_next();
   int cp_ii = 0, cp_k = -1;
   Desc cp_d = load_desc(0);
   for (int s = 0; s < S; ++s) {
-    // slot s has landed once at most the operations issued after it are
-    // outstanding: the later slots' loads and the stores of the last three
-    // iterations (slot s was issued three iterations ago)
-    vm_wait_le(uniform(C::kDmaSlot * (issued - 1 - s) + st1 + st2 + st3));
+    // E4M3 converts the next tile during this iteration, so it waits for that slot
+    vm_wait_le(uniform(ops - ((FP8 && s + 1 < S) ? mk1 : mk0)));
     lds_barrier();
-    if (issued < S) {
-      issue_slot(is_d, is_k, is_id, issued & 3);   // into the stage consumed last iteration
-      advance(is_ii, is_k, is_d);
-      ++issued;
-      load_ids();   // used next iteration
-    }
+    if (issued < S) mk3 = issue_next();
     const int stage = s & 3;
+    if constexpr (FP8) {
+      if (s + 1 < S && cp_k + 1 < cp_d.ntile) convert_tile((s + 1) & 3);   // slot s + 1 is a tile
+    }
     int st0 = 0;
     if (cp_k < 0) {
       begin_item(cp_d, stage);
     } else {
-      if constexpr (FP8) convert_tile(stage);
       compute_tile(cp_d, cp_k, stage);
       if (cp_k == cp_d.ntile - 1) st0 = uniform(finish_item(cp_d, stage));
     }
-    st3 = st2;
-    st2 = st1;
-    st1 = st0;
+    ops += st0;
+    mk0 = mk1;
+    mk1 = mk2;
+    mk2 = mk3;
     advance(cp_ii, cp_k, cp_d);
   }
 }
