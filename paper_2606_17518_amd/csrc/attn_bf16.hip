@@ -629,8 +629,6 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     const int kseg = d.ord - first_ord;
     const int64_t slot = slot_of(pp, w, kseg);
     if (slot < 0) return 0;
-    float* o = a.ws + pp.o_base + slot * pp.slot_rows * D;
-    float* ls = a.ws + pp.lse_base + slot * pp.slot_rows;
     constexpr int RS = 16 * NT;
     int stores = 0;
     // every lane of an N-tile that holds rows of the item stores (rows past the
@@ -639,14 +637,36 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     for (int nt = 0; nt < NT; ++nt) {
       if (rg * RS + nt * 16 >= d.nrows) break;
       const int row = rg * RS + nt * 16 + ln;
-      const float inv = 1.f / lrow[nt];
-      // partials are read once, by the merge: nontemporal stores keep them out
-      // of the caches' retention
+      // the row's largest |o| (its 4 lanes hold 32 dims each) sets its fp16 scale
+      float amax = 0.f;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        __builtin_nontemporal_store(acc[nt][dt] * inv, reinterpret_cast<f32x4*>(o + row * D + dt * 16 + 4 * G));
-      __builtin_nontemporal_store(m_run[nt] * a.sm_scale + __logf(lrow[nt]), ls + row);
-      stores += DT + 1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) amax = fmaxf(amax, fabsf(acc[nt][dt][e]));
+      amax = rows4_max(amax);
+      const float inv_l = 1.f / lrow[nt];
+      const uint32_t kexp = (uint32_t)part_row_k(__float_as_uint(amax * inv_l));
+      const float mul = inv_l * __uint_as_float((254u - kexp) << 23);
+      const float dec = __uint_as_float(kexp << 23);
+      uint32_t* orow = reinterpret_cast<uint32_t*>(a.ws + part_o_off(pp, slot, row, D));
+      // d-tiles 2p and 2p+1: lane (G, ln) holds dims 16*dt + 4G .. +3 of each;
+      // one row swap between lane groups G and G^1 leaves every lane 8
+      // consecutive dims, 16*(2p + (G&1)) + 8*(G>>1) .. +7, stored as 16 bytes
+      // (the four lanes of a row write 64 contiguous bytes per instruction)
+#pragma unroll
+      for (int p2 = 0; p2 < DT / 2; ++p2) {
+        const f32x4 x = acc[nt][2 * p2] * mul, y = acc[nt][2 * p2 + 1] * mul;
+        const auto r0 = __builtin_amdgcn_permlane16_swap(pack_f16x2(x[0], x[1]), pack_f16x2(y[0], y[1]), false, false);
+        const auto r1 = __builtin_amdgcn_permlane16_swap(pack_f16x2(x[2], x[3]), pack_f16x2(y[2], y[3]), false, false);
+        const u32x4 chunk = {r0[0], r1[0], r0[1], r1[1]};
+        const int dim0 = (2 * p2 + (G & 1)) * 16 + 8 * (G >> 1);
+        // partials are read once, by the merge: nontemporal stores keep them out
+        // of the caches' retention
+        __builtin_nontemporal_store(chunk, reinterpret_cast<u32x4*>(orow + dim0 / 2));
+      }
+      const f32x2 ld = {m_run[nt] * a.sm_scale + __logf(lrow[nt]), dec};
+      __builtin_nontemporal_store(ld, reinterpret_cast<f32x2*>(a.ws + part_l_off(pp, slot, row)));
+      stores += DT / 2 + 1;
     }
     return stores;
   };

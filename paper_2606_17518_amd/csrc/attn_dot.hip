@@ -279,14 +279,14 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
       constexpr int PER = RWS * D / C::kThreads;   // 8 (D=128) or 4 (D=64)
       const int row = tid / (D / PER);
       const int d0 = (tid % (D / PER)) * PER;
-      if (row < nrows) {
-        float m = -INFINITY;
+      const bool live = row < nrows;
+      float m = -INFINITY, l = 0.f, acc[PER];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+      if (live) {
 #pragma unroll
         for (int wv = 0; wv < 4; ++wv) m = fmaxf(m, comb_m[wv * RWS + row]);
         const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
-        float l = 0.f, acc[PER];
-#pragma unroll
-        for (int e = 0; e < PER; ++e) acc[e] = 0.f;
 #pragma unroll
         for (int wv = 0; wv < 4; ++wv) {
           const float sc = __builtin_amdgcn_exp2f(comb_m[wv * RWS + row] * a.c_log2 - mc);
@@ -294,14 +294,32 @@ __global__ void __launch_bounds__(256, 1) attn_dot_kernel(const AttnArgs a, cons
 #pragma unroll
           for (int e = 0; e < PER; ++e) acc[e] += comb[(wv * RWS + row) * D + d0 + e] * sc;
         }
+      }
+      // the row's largest |o| sets its fp16 scale (its D / PER threads are
+      // consecutive lanes)
+      float amax = 0.f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) amax = fmaxf(amax, fabsf(acc[e]));
+#pragma unroll
+      for (int o = 1; o < D / PER; o <<= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+      if (live) {
         const int k = uniform(d[IT_ORD]) - wr.first_ord;
         const int64_t slot = slot_of(pp, w, k);
         if (slot >= 0) {
-          float* op = a.ws + pp.o_base + (slot * pp.slot_rows + row) * D + d0;
-          const float inv = 1.f / l;
-#pragma unroll
-          for (int e = 0; e < PER; ++e) op[e] = acc[e] * inv;
-          if (d0 == 0) a.ws[pp.lse_base + slot * pp.slot_rows + row] = m * a.sm_scale + __logf(l);
+          const float inv_l = 1.f / l;
+          const uint32_t kexp = (uint32_t)part_row_k(__float_as_uint(amax * inv_l));
+          const float mul = inv_l * __uint_as_float((254u - kexp) << 23);
+          uint32_t* op = reinterpret_cast<uint32_t*>(a.ws + part_o_off(pp, slot, row, D)) + d0 / 2;
+          if constexpr (PER == 8) {
+            *reinterpret_cast<u32x4*>(op) = u32x4{pack_f16x2(acc[0] * mul, acc[1] * mul), pack_f16x2(acc[2] * mul, acc[3] * mul),
+                                                  pack_f16x2(acc[4] * mul, acc[5] * mul), pack_f16x2(acc[6] * mul, acc[7] * mul)};
+          } else {
+            static_assert(PER == 4, "4 or 8 dims per thread");
+            *reinterpret_cast<u32x2*>(op) = u32x2{pack_f16x2(acc[0] * mul, acc[1] * mul), pack_f16x2(acc[2] * mul, acc[3] * mul)};
+          }
+          if (d0 == 0)
+            *reinterpret_cast<f32x2*>(a.ws + part_l_off(pp, slot, row)) =
+                f32x2{m * a.sm_scale + __logf(l), __uint_as_float(kexp << 23)};
         }
       }
     }

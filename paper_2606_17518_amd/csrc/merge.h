@@ -11,35 +11,39 @@
 
 namespace specgen {
 
-// Row merge for D in {64, 128}: lanes read 16 bytes each, so one load
-// instruction covers PPI = 64 / (D/4) parts.  A batch is up to 64 parts: each
-// lane loads one part's lse and the wave issues the o loads of every part of
-// the batch before it waits for any of them, so a row of up to a batch of
-// parts costs one memory round trip.
+// Row merge for D in {64, 128} over partial rows stored as fp16 with a
+// per-row power-of-two scale (plan.h, part_row_k): lanes read 16 bytes (8
+// dims) each, so one load instruction covers PPI = 64 / (D/8) parts.  A batch
+// is up to 64 parts: each lane loads one part's (lse, dec) pair and the wave
+// issues the o loads of every part of the batch before it waits for any of
+// them, so a row of up to 64 parts costs one memory round trip.
 template <int D, typename PO, typename PL>
-__device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse, uint16_t* out_row,
+__device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, uint16_t* out_row,
                                              float* out_lse_p) {
-  constexpr int LPP = D / 4;       // lanes per part
+  constexpr int LPP = D / 8;       // lanes per part
   constexpr int PPI = 64 / LPP;    // parts per load instruction
-  constexpr int U = (D == 128) ? 24 : 16;   // load instructions per batch
-  constexpr int kBatch = PPI * U;  // parts per batch (<= 64: one lse per lane)
-  static_assert(kBatch <= 64, "one lse per lane");
+  constexpr int U = 64 / PPI;      // load instructions per batch
+  constexpr int kBatch = PPI * U;  // parts per batch: one (lse, dec) per lane
+  static_assert(kBatch == 64, "one part per lane");
   const int lane = threadIdx.x & 63;
   const int gsl = lane / LPP;      // part slot of this lane within an instruction
-  const int c4 = (lane % LPP) * 4; // first of the 4 dims this lane owns
+  const int c8 = (lane % LPP) * 8; // first of the 8 dims this lane owns
   float M = -INFINITY, z = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
   for (int p0 = 0; p0 < nparts; p0 += kBatch) {
     const int cnt = (nparts - p0) < kBatch ? (nparts - p0) : kBatch;
-    const float l = lane < cnt ? part_lse(p0 + lane) : -INFINITY;
-    f32x4 v[U];
+    const f32x2 ld = lane < cnt ? part_ld(p0 + lane) : f32x2{-INFINITY, 0.f};
+    const float l = ld[0];
+    u32x4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      v[u] = u32x4{0u, 0u, 0u, 0u};
       if (u * PPI < cnt) {   // wave-uniform: only instructions that hold a part
         const int q = u * PPI + gsl;
         const int qc = q < cnt ? q : cnt - 1;   // the last instruction's spare slots re-read its last part
-        v[u] = *reinterpret_cast<const f32x4*>(part_o(p0 + qc) + c4);
+        v[u] = *reinterpret_cast<const u32x4*>(part_o(p0 + qc) + c8 / 2);
       }
     }
     float cm = l;
@@ -48,35 +52,41 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_lse,
     if (Mn == -INFINITY) continue;          // every part so far empty (wave-uniform)
     const float rescale = __expf(M - Mn);   // M = -inf -> 0
     z *= rescale;
-    acc *= rescale;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= rescale;
     M = Mn;
     const float wl = (l == -INFINITY) ? 0.f : __expf(l - M);
     float zs = wl;
     for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
     z += zs;
+    const float wo = wl * ld[1];            // the weight of the stored (scaled) values
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int q = u * PPI + gsl;
-      float wq = __shfl(wl, q < 64 ? q : 63, 64);
+      float wq = __shfl(wo, q < 64 ? q : 63, 64);
       if (q >= cnt) wq = 0.f;
-      if (wq != 0.f) acc += wq * v[u];   // an empty part's o may be garbage
+      if (wq != 0.f) {   // an empty part's o may be garbage
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const f32x2 x = unpack_f16x2(v[u][h]);
+          acc[2 * h] = fmaf(wq, x[0], acc[2 * h]);
+          acc[2 * h + 1] = fmaf(wq, x[1], acc[2 * h + 1]);
+        }
+      }
     }
   }
   // sum the PPI lane groups
 #pragma unroll
-  for (int o = LPP; o < 64; o <<= 1) {
-    acc[0] += __shfl_xor(acc[0], o, 64);
-    acc[1] += __shfl_xor(acc[1], o, 64);
-    acc[2] += __shfl_xor(acc[2], o, 64);
-    acc[3] += __shfl_xor(acc[3], o, 64);
-  }
+  for (int o = LPP; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, 64);
   const bool empty = (M == -INFINITY);
   if (gsl == 0) {
     const float inv = empty ? 0.f : 1.f / z;
-    u32x2 pk;
-    pk[0] = pack_bf16x2(empty ? 0.f : acc[0] * inv, empty ? 0.f : acc[1] * inv);
-    pk[1] = pack_bf16x2(empty ? 0.f : acc[2] * inv, empty ? 0.f : acc[3] * inv);
-    *reinterpret_cast<u32x2*>(out_row + c4) = pk;
+    u32x4 pk;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) pk[h] = pack_bf16x2(empty ? 0.f : acc[2 * h] * inv, empty ? 0.f : acc[2 * h + 1] * inv);
+    *reinterpret_cast<u32x4*>(out_row + c8) = pk;
   }
   if (out_lse_p && lane == 0) *out_lse_p = empty ? -INFINITY : M + __logf(z);
 }
@@ -121,8 +131,8 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
       continue;
     }
     const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
-    o0[s2] = pp.o_base + (slot0 * pp.slot_rows + r) * D;
-    l0[s2] = pp.lse_base + slot0 * pp.slot_rows + r;
+    o0[s2] = part_o_off(pp, slot0, r, D);
+    l0[s2] = part_l_off(pp, slot0, r);
     kmax[s2] = pp.kmax;
     klo[s2] = k_lo;
     n[s2] = w_hi - w_lo + 1;
@@ -142,13 +152,13 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
     const int i = pre ? p : p - np;
     return i == 0 ? 0 : (int64_t)i * (pre ? pK : sK) - (pre ? pKlo : sKlo);
   };
-  auto po = [&](int p) {
+  auto po = [&](int p) {   // the part's o row: D fp16 values, two per uint32
     const bool pre = p < np;
-    return ws + (pre ? pO0 : sO0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * D;
+    return reinterpret_cast<const uint32_t*>(ws + (pre ? pO0 : sO0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * (D / 2));
   };
-  auto pl = [&](int p) {
+  auto pl = [&](int p) {   // its (lse, dec) pair
     const bool pre = p < np;
-    return ws[(pre ? pL0 : sL0) + rel_slots(p) * (int64_t)(pre ? pR : sR)];
+    return *reinterpret_cast<const f32x2*>(ws + (pre ? pL0 : sL0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * 2);
   };
   merge_row_v4<D>(np + n[1], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }

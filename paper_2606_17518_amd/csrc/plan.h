@@ -43,8 +43,8 @@ enum { kPolicyAuto = 0, kPolicyDot = 1, kPolicyMfma = 2 };
 struct PartPlan {
   int64_t tiles;          // total tiles of the partition
   int64_t prefix_tiles;   // tiles of its prefix items (they come first)
-  int64_t o_base;         // float offset of slot 0's o in the workspace
-  int64_t lse_base;       // float offset of slot 0's lse
+  int64_t o_base;         // float offset of slot 0's o (fp16 rows, see part_row_k) in the workspace
+  int64_t lse_base;       // float offset of slot 0's (lse, dec) pairs
   int64_t info_base;      // float offset of the item table: per item ordinal three
                           // int32 (first worker, last worker, segment index in the first)
   int32_t n_items;        // items of the partition (prefix, then suffix)
@@ -431,6 +431,27 @@ SG_HD bool suffix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, 
   *ord = pp.n_prefix_items + (f * p.Hkv + j) * pp.suffix_rb + rb;
   *row = hh - rb * pp.rbs;
   return true;
+}
+
+// Storage of one partial row.  The normalised partial output o (a convex
+// combination of value rows) is kept as fp16 times a power of two chosen per
+// row: with mx = max_d |o_d| and e its biased fp32 exponent, k = clamp(e - 14,
+// 1, 240), the row stores fp16(o_d * 2^(127-k)) (so its largest element lies
+// in [2^14, 2^15)) and, beside its lse, dec = 2^(k-127), so o_d = stored_d *
+// dec.  Any finite o fits, and each element keeps fp16's 11-bit significand
+// relative to the row's largest: the rounding is 2^-12 of mx at most, 8x
+// below the bf16 rounding of the final output.
+SG_HD int32_t part_row_k(uint32_t mx_bits) {
+  const int32_t e = (int32_t)((mx_bits >> 23) & 0xFF);
+  const int32_t k = e - 14;
+  return k < 1 ? 1 : (k > 240 ? 240 : k);
+}
+// float offsets of the o row (fp16: 2 per float) and of the (lse, dec) pair
+SG_HD int64_t part_o_off(const PartPlan& pp, int64_t slot, int row, int D) {
+  return pp.o_base + (slot * pp.slot_rows + row) * (int64_t)(D / 2);
+}
+SG_HD int64_t part_l_off(const PartPlan& pp, int64_t slot, int row) {
+  return pp.lse_base + 2 * (slot * pp.slot_rows + row);
 }
 
 // Partial-slot index of (worker w, item of ordinal ord), or -1 if out of range.

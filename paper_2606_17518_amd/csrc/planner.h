@@ -149,10 +149,11 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     if (pp.kmax > in.item_cap[X] || (pp.tiles + pp.workers - 1) / pp.workers > in.tile_cap[X])
       SG_FAIL(kPlanUnsupported, "work split exceeds the kernel's per-worker capacity");
     const int64_t slots = (int64_t)pp.workers * pp.kmax;
+    // o: fp16 [slots][slot_rows][D] (D is even); lse: (lse, dec) float pairs
     pp.o_base = off;
-    off = align_up(off + slots * pp.slot_rows * D, kAlignFloats);
+    off = align_up(off + slots * pp.slot_rows * D / 2, kAlignFloats);
     pp.lse_base = off;
-    off = align_up(off + slots * pp.slot_rows, kAlignFloats);
+    off = align_up(off + 2 * slots * pp.slot_rows, kAlignFloats);
     pp.n_items = pp.n_prefix_items + (pp.has_suffix ? N * Hkv * pp.suffix_rb : 0);
     pp.info_base = off;
     off = align_up(off + 3 * (int64_t)pp.n_items, kAlignFloats);

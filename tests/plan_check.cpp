@@ -180,8 +180,9 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       const PartPlan& pp = plan.part[ip.part];
       const int64_t slot = slot_of(pp, v[i].w, v[i].k);
       CHECK(slot >= 0, "slot out of range");
-      CHECK(pp.o_base + (slot * pp.slot_rows + ip.row + 1) * in.D <= wsf, "o slot past workspace");
-      CHECK(pp.lse_base + slot * pp.slot_rows + ip.row < wsf, "lse slot past workspace");
+      CHECK(part_o_off(pp, slot, ip.row + 1, in.D) <= pp.lse_base, "o slot past its region");
+      CHECK(part_l_off(pp, slot, ip.row) + 2 <= pp.info_base, "lse slot past its region");
+      CHECK(pp.info_base <= wsf, "regions past workspace");
       CHECK(ip.row >= 0 && ip.row < pp.slot_rows, "row in item");
     }
     return true;
