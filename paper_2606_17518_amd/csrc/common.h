@@ -87,6 +87,24 @@ __device__ __forceinline__ float rows4_sum(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Max / sum over the 16 lanes of each row with DPP moves (quad swaps, then
+// the half-row and row mirrors): VALU work, no LDS round trip.
+#define SG_DPP(v, ctrl) __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), (ctrl), 0xF, 0xF, false))
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, SG_DPP(v, 0xB1));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, SG_DPP(v, 0x4E));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, SG_DPP(v, 0x141));   // row_half_mirror
+  return fmaxf(v, SG_DPP(v, 0x140));   // row_mirror
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += SG_DPP(v, 0xB1);
+  v += SG_DPP(v, 0x4E);
+  v += SG_DPP(v, 0x141);
+  return v + SG_DPP(v, 0x140);
+}
+// v + the value of lane l ^ 8 (rotation by 8 within the 16-lane row)
+__device__ __forceinline__ float xor8_sum(float v) { return v + SG_DPP(v, 0x128); }
+
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Workgroup barrier for LDS hand-offs only: waits for this wave's LDS

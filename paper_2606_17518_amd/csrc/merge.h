@@ -24,7 +24,7 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
   constexpr int PPI = 64 / LPP;    // parts per load instruction
   constexpr int U = 64 / PPI;      // load instructions per batch
   constexpr int kBatch = PPI * U;  // parts per batch: one (lse, dec) per lane
-  static_assert(kBatch == 64, "one part per lane");
+  static_assert(kBatch == 64 && (LPP == 16 || LPP == 8), "one part per lane; lane groups of 16 or 8");
   const int lane = threadIdx.x & 63;
   const int gsl = lane / LPP;      // part slot of this lane within an instruction
   const int c8 = (lane % LPP) * 8; // first of the 8 dims this lane owns
@@ -46,9 +46,7 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
         v[u] = *reinterpret_cast<const u32x4*>(part_o(p0 + qc) + c8 / 2);
       }
     }
-    float cm = l;
-    for (int o = 32; o >= 1; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o, 64));
-    const float Mn = fmaxf(M, cm);
+    const float Mn = fmaxf(M, rows4_max(row16_max(l)));
     if (Mn == -INFINITY) continue;          // every part so far empty (wave-uniform)
     const float rescale = __expf(M - Mn);   // M = -inf -> 0
     z *= rescale;
@@ -56,9 +54,7 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
     for (int e = 0; e < 8; ++e) acc[e] *= rescale;
     M = Mn;
     const float wl = (l == -INFINITY) ? 0.f : __expf(l - M);
-    float zs = wl;
-    for (int o = 32; o >= 1; o >>= 1) zs += __shfl_xor(zs, o, 64);
-    z += zs;
+    z += rows4_sum(row16_sum(wl));
     const float wo = wl * ld[1];            // the weight of the stored (scaled) values
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -75,11 +71,13 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
       }
     }
   }
-  // sum the PPI lane groups
+  // sum the PPI lane groups: the four 16-lane rows (D = 128), or the eight
+  // 8-lane halves of rows (D = 64)
 #pragma unroll
-  for (int o = LPP; o < 64; o <<= 1)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, 64);
+  for (int e = 0; e < 8; ++e) {
+    if constexpr (LPP == 8) acc[e] = xor8_sum(acc[e]);
+    acc[e] = rows4_sum(acc[e]);
+  }
   const bool empty = (M == -INFINITY);
   if (gsl == 0) {
     const float inv = empty ? 0.f : 1.f / z;

@@ -124,10 +124,13 @@ __device__ __forceinline__ void plan_to_lds(const Plan& karg, Plan& p) {
 #endif
 
 // Worker owning tile x: the largest w with worker_start(w) <= x.
+// Tile positions fit in 32 bits (the planner rejects larger partitions), so
+// the divisions are 32-bit.
 SG_HD int32_t worker_of_tile(const PartPlan& pp, int64_t x) {
-  const int64_t big = (int64_t)pp.n_hi * (pp.per_lo + 1);   // tiles of the larger ranges
-  if (x < big) return (int32_t)(x / (pp.per_lo + 1));
-  return (int32_t)(pp.n_hi + (x - big) / pp.per_lo);
+  const uint32_t big = (uint32_t)pp.n_hi * (uint32_t)(pp.per_lo + 1);   // tiles of the larger ranges
+  const uint32_t xx = (uint32_t)x;
+  if (xx < big) return (int32_t)(xx / (uint32_t)(pp.per_lo + 1));
+  return (int32_t)((uint32_t)pp.n_hi + (xx - big) / (uint32_t)pp.per_lo);
 }
 
 struct ItemRef {
@@ -382,9 +385,9 @@ SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h) {
   const int ri = (f - p.fork_off[t]) * g + hh;
   const int X = p.trace_part[t];
   const PartPlan& pp = p.part[X];
-  const int rbc = cdiv(trace_rows(p, t), pp.rbs);
+  const int rbc = cdiv32(trace_rows(p, t), pp.rbs);
   const int rb = ri / pp.rbs;
-  const int tiles = cdiv(p.prefix_len[t], pp.tt);
+  const int tiles = cdiv32(p.prefix_len[t], pp.tt);
   const int pos = p.trace_pos[t];
   const int item = j * rbc + rb;
   return item_parts(p, X, (int64_t)p.tileP[pos] + (int64_t)item * (tiles + pp.charge) + pp.charge, tiles,
@@ -413,7 +416,7 @@ SG_HD void prefix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, 
   const int ri = (f - p.fork_off[t]) * g + hh;
   const int X = p.trace_part[t];
   const PartPlan& pp = p.part[X];
-  const int rbc = cdiv(trace_rows(p, t), pp.rbs);
+  const int rbc = cdiv32(trace_rows(p, t), pp.rbs);
   const int rb = ri / pp.rbs;
   *part = X;
   *ord = p.ordP[p.trace_pos[t]] + j * rbc + rb;
