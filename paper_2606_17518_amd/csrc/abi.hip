@@ -90,10 +90,21 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.item_cap[1] = dot_item_cap();
   in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128, fp8);
   in.tile_cap[1] = dot_tile_cap(in.D);
-  // An item costs a worker about two tiles' time on the MFMA path (its q slot
-  // and the token-group combine at its end) and about one on the dot path.
-  in.charge[0] = 2;
+  // Unit prices of the split, from per-worker timelines of the MFMA kernel on
+  // MI355X: a tile of an item of 1, 2 or 4 groups of 32 rows took 1.16-1.20,
+  // 1.20 and 1.48 us with bf16 KV (1.56 and 1.96 us for 1 and 4 groups with
+  // E4M3), and an item's fixed cost (q slot, token-group combine, partial
+  // stores) about two tiles of 4 groups.  In eighths of that tile: 6, 6, 7, 8
+  // and 16.  The dot path prices every tile alike and an item at one tile.
+  const int mfma_rg[5] = {0, 6, 6, 7, 8};
+  for (int r = 0; r < 5; ++r) {
+    in.wt_rg[0][r] = mfma_rg[r];
+    in.wt_rg[1][r] = 1;
+  }
+  in.charge[0] = 16;
   in.charge[1] = 1;
+  in.unit_cap[0] = INT32_MAX;   // the MFMA walk takes one lane per item: any number of units
+  in.unit_cap[1] = in.tile_cap[1];
   char err[256];
   const int rc = plan_build(in, [] { return device_cus(); }, plan, ws_floats, err, sizeof err);
   if (rc == kPlanInvalid) return fail(SPECGEN_ERR_INVALID_ARG, "%s", err);

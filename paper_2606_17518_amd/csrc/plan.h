@@ -13,15 +13,18 @@
 // chosen by the path policy.  Within a partition the items are laid out in a
 // fixed order -- prefix items (trace-major, then j, then rb), then suffix
 // items (fork-major, then j, then rb) -- and each item is cut into tiles of
-// `tt` tokens.  In the partition's tile sequence every item is preceded by
-// `charge` empty tiles: they stand for the item's fixed cost in a worker (its
-// query rows and its end), so workers whose ranges hold many short items get
-// fewer tiles of data.  The sequence is split evenly over W workers
-// (workgroups): worker w takes positions [start(w), start(w+1)) and processes
-// the real tiles among them.  A worker emits
-// one partial (o, lse) per item it touches, into slot w * kmax + k where k is
-// the item's ordinal minus the ordinal of the worker's first item.  The merge
-// finds the workers covering an item from its tile range alone.
+// `tt` tokens.
+//
+// Units.  The split is made over a sequence of units that prices the work:
+// every item takes `charge` units for its fixed cost in a worker (its query
+// rows and its end), then a price per tile that grows with the rows the item
+// computes: wtP[] for the prefix items of each trace, wt_suf for suffix items
+// (g rows of one fork).  The sequence is split evenly over W
+// workers (workgroups): worker w takes units [start(w), start(w+1)) and
+// processes the tiles whose first unit lies there.  A worker emits one partial
+// (o, lse) per item it touches, into slot w * kmax + k where k is the item's
+// ordinal minus the ordinal of the item at the worker's first unit.  The merge
+// finds the workers covering an item from its units alone.
 #pragma once
 #include <stdint.h>
 
@@ -41,15 +44,15 @@ enum { kPartMfma = 0, kPartDot = 1 };
 enum { kPolicyAuto = 0, kPolicyDot = 1, kPolicyMfma = 2 };
 
 struct PartPlan {
-  int64_t tiles;          // total tiles of the partition
-  int64_t prefix_tiles;   // tiles of its prefix items (they come first)
+  int64_t units;          // total units of the partition
+  int64_t prefix_units;   // units of its prefix items (they come first)
   int64_t o_base;         // float offset of slot 0's o (fp16 rows, see part_row_k) in the workspace
   int64_t lse_base;       // float offset of slot 0's (lse, dec) pairs
   int64_t info_base;      // float offset of the item table: per item ordinal three
                           // int32 (first worker, last worker, segment index in the first)
   int32_t n_items;        // items of the partition (prefix, then suffix)
-  int32_t per_lo;         // tiles / W: every worker gets per_lo tiles, the first
-  int32_t n_hi;           // tiles % W workers one more
+  int32_t per_lo;         // units / W: every worker gets per_lo units, the first
+  int32_t n_hi;           // units % W workers one more
   int32_t workers;        // W (0: partition unused)
   int32_t kmax;           // max items touched by one worker
   int32_t tt;             // tokens per tile
@@ -60,7 +63,9 @@ struct PartPlan {
   int32_t suffix_rb;      // row blocks per suffix (fork, head): ceil(g / rbs)
   int32_t n_traces;       // traces whose prefix items are in the partition
   int32_t trace_begin;    // their positions in Plan::ptrace: [trace_begin, +n_traces)
-  int32_t charge;         // empty tiles in front of every item
+  int32_t charge;         // units in front of every item (its fixed cost)
+  int32_t wt_suf;         // units per tile of a suffix item
+  int32_t wt_max;         // the largest tile price of the partition
 };
 
 // The scalar part of the plan.
@@ -79,9 +84,10 @@ struct alignas(16) Plan : PlanHead {
   int32_t trace_part[kMaxTraces];   // partition of trace t's prefix items
   int32_t trace_pos[kMaxTraces];    // index of t in ptrace
   int32_t ptrace[kMaxTraces];       // traces grouped by partition, ascending within each
-  int32_t tileP[kMaxTraces];        // (by ptrace position) first tile of the trace's prefix items
+  int32_t unitP[kMaxTraces];        // (by ptrace position) first unit of the trace's prefix items
   int32_t ordP[kMaxTraces];         // (by ptrace position) ordinal of its first prefix item
-  int32_t tileS[kMaxForks + 1];     // first tile of fork f's suffix items, relative to prefix_tiles
+  int32_t wtP[kMaxTraces];          // (by ptrace position) units per tile of its prefix items
+  int32_t unitS[kMaxForks + 1];     // first unit of fork f's suffix items, relative to prefix_units
   int32_t prefix_table_off[kMaxTraces + 1];   // host mirrors of the batch's index arrays
   int32_t suffix_len[kMaxForks];
   int32_t suffix_table_off[kMaxForks + 1];
@@ -102,7 +108,7 @@ SG_HD int part_of_trace(int policy, int rows) {
 
 SG_HD int part_of_suffix(int policy) { return policy == kPolicyDot ? kPartDot : kPartMfma; }
 
-// First tile of worker w: workers [0, n_hi) take per_lo + 1 tiles, the rest
+// First unit of worker w: workers [0, n_hi) take per_lo + 1 units, the rest
 // per_lo (no division, so the kernels evaluate it cheaply).
 SG_HD int64_t worker_start(const PartPlan& pp, int64_t w) {
   return w * pp.per_lo + (w < pp.n_hi ? w : (int64_t)pp.n_hi);
@@ -123,11 +129,11 @@ __device__ __forceinline__ void plan_to_lds(const Plan& karg, Plan& p) {
 }
 #endif
 
-// Worker owning tile x: the largest w with worker_start(w) <= x.
-// Tile positions fit in 32 bits (the planner rejects larger partitions), so
-// the divisions are 32-bit.
-SG_HD int32_t worker_of_tile(const PartPlan& pp, int64_t x) {
-  const uint32_t big = (uint32_t)pp.n_hi * (uint32_t)(pp.per_lo + 1);   // tiles of the larger ranges
+// Worker owning unit x: the largest w with worker_start(w) <= x.  Units fit
+// in 32 bits (the planner rejects larger partitions), so the divisions are
+// 32-bit.
+SG_HD int32_t worker_of_unit(const PartPlan& pp, int64_t x) {
+  const uint32_t big = (uint32_t)pp.n_hi * (uint32_t)(pp.per_lo + 1);   // units of the larger ranges
   const uint32_t xx = (uint32_t)x;
   if (xx < big) return (int32_t)(xx / (uint32_t)(pp.per_lo + 1));
   return (int32_t)((uint32_t)pp.n_hi + (xx - big) / (uint32_t)pp.per_lo);
@@ -137,80 +143,85 @@ struct ItemRef {
   int32_t kind;      // 0 prefix, 1 suffix, -1 past the end
   int32_t t, f, j, rb;
   int32_t tiles;     // tiles of the item (its data)
-  int32_t tile;      // tile of x within the item; -charge..-1 for its empty tiles
-  int64_t first;     // sequence position of the item's first tile of data
+  int32_t w;         // units per tile of the item
+  int32_t off;       // units from the start of the item's tile 0 to x (< 0 in its charge)
+  int32_t tile;      // tile holding x (off / w), -1 in the charge
+  int64_t first;     // sequence unit where the item's tile 0 starts
   int32_t ord;       // ordinal of the item in the partition
 };
 
-// Sequence positions taken by one suffix item of fork f (0 if S_f = 0): its
-// charge plus ceil(S_f / tt); tileS holds their per-fork prefix sums.
+// Units taken by one suffix item of fork f (0 if S_f = 0): its charge plus
+// ceil(S_f / tt) tiles of wt_suf units; unitS holds their per-fork prefix sums.
 SG_HD int32_t suffix_span(const Plan& p, const PartPlan& pp, int f) {
-  return (p.tileS[f + 1] - p.tileS[f]) / (p.Hkv * pp.suffix_rb);
+  return (p.unitS[f + 1] - p.unitS[f]) / (p.Hkv * pp.suffix_rb);
 }
 
-// The item at partition sequence position x.
+// The item at partition sequence unit x.
 SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
   const PartPlan& pp = p.part[part];
   ItemRef r;
   r.kind = -1;
-  r.t = r.f = r.j = r.rb = r.tiles = r.tile = r.ord = 0;
+  r.t = r.f = r.j = r.rb = r.tiles = r.tile = r.off = r.ord = 0;
+  r.w = 1;
   r.first = 0;
-  if (x < 0 || x >= pp.tiles) return r;
-  if (x < pp.prefix_tiles) {
-    // largest position i in the partition's trace list with tileP[i] <= x
+  if (x < 0 || x >= pp.units) return r;
+  int local, span, item;
+  if (x < pp.prefix_units) {
+    // largest position i in the partition's trace list with unitP[i] <= x
     int lo = pp.trace_begin, hi = pp.trace_begin + pp.n_traces - 1;
     while (lo < hi) {
       int mid = (lo + hi + 1) >> 1;
-      if (p.tileP[mid] <= x) lo = mid; else hi = mid - 1;
+      if (p.unitP[mid] <= x) lo = mid; else hi = mid - 1;
     }
     const int t = p.ptrace[lo];
     const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
-    const int tiles = cdiv32(p.prefix_len[t], pp.tt);
-    const int span = tiles + pp.charge;
-    const int local = (int)(x - p.tileP[lo]);   // tile counts fit in int32 (the planner checks)
-    const int item = local / span;
+    r.tiles = cdiv32(p.prefix_len[t], pp.tt);
+    r.w = p.wtP[lo];
+    span = r.tiles * r.w + pp.charge;
+    local = (int)(x - p.unitP[lo]);   // unit counts fit in int32 (the planner checks)
+    item = local / span;
     r.kind = 0;
     r.t = t;
     r.j = item / rb_count;
     r.rb = item % rb_count;
-    r.tiles = tiles;
-    r.tile = local - item * span - pp.charge;
-    r.first = x - r.tile;
     r.ord = p.ordP[lo] + item;
-    return r;
+  } else {
+    const int xs = (int)(x - pp.prefix_units);
+    int lo = 0, hi = p.N - 1;   // largest f with unitS[f] <= xs
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (p.unitS[mid] <= xs) lo = mid; else hi = mid - 1;
+    }
+    const int f = lo;
+    span = suffix_span(p, pp, f);
+    r.w = pp.wt_suf;
+    r.tiles = (span - pp.charge) / r.w;
+    local = xs - p.unitS[f];
+    item = local / span;
+    r.kind = 1;
+    r.f = f;
+    r.j = item / pp.suffix_rb;
+    r.rb = item % pp.suffix_rb;
+    r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
   }
-  const int xs = (int)(x - pp.prefix_tiles);
-  int lo = 0, hi = p.N - 1;   // largest f with tileS[f] <= xs
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (p.tileS[mid] <= xs) lo = mid; else hi = mid - 1;
-  }
-  const int f = lo;
-  const int span = suffix_span(p, pp, f);
-  const int local = xs - p.tileS[f];
-  const int item = local / span;
-  r.kind = 1;
-  r.f = f;
-  r.j = item / pp.suffix_rb;
-  r.rb = item % pp.suffix_rb;
-  r.tiles = span - pp.charge;
-  r.tile = local - item * span - pp.charge;
-  r.first = x - r.tile;
-  r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
+  r.off = local - item * span - pp.charge;
+  r.tile = r.off >= 0 ? r.off / r.w : -1;
+  r.first = x - r.off;
   return r;
 }
 
 // The item that follows `cur` in partition `part` (cur must not be the last
-// one), at its first tile of data: equal to
-// locate(p, part, cur.first + cur.tiles + charge).  Steps within a trace or
-// fork in O(1) and falls back to locate() where it would have to skip over
-// forks without suffix tokens or cross into the suffix items.
+// one), with x at its tile 0: equal to locate(p, part, cur.first +
+// cur.tiles * cur.w + charge).  Steps within a trace or fork in O(1) and falls
+// back to locate() where it would have to skip over forks without suffix
+// tokens or cross into the suffix items.
 SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   const PartPlan& pp = p.part[part];
-  const int64_t x = cur.first + cur.tiles + pp.charge;
+  const int64_t x = cur.first + (int64_t)cur.tiles * cur.w + pp.charge;
   ItemRef r = cur;
   r.first = x;
   r.tile = 0;
+  r.off = 0;
   r.ord = cur.ord + 1;
   if (cur.kind == 0) {
     const int rb_count = cdiv32(trace_rows(p, cur.t), pp.rbs);
@@ -229,6 +240,7 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
       r.j = 0;
       r.rb = 0;
       r.tiles = cdiv32(p.prefix_len[r.t], pp.tt);
+      r.w = p.wtP[pos];
       return r;
     }
     return locate(p, part, x);
@@ -244,29 +256,29 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   }
   const int f = cur.f + 1;
   if (f < p.N) {
-    const int tiles = suffix_span(p, pp, f) - pp.charge;
-    if (tiles > 0) {
+    const int span = suffix_span(p, pp, f);
+    if (span > 0) {
       r.f = f;
       r.j = 0;
       r.rb = 0;
-      r.tiles = tiles;
+      r.tiles = (span - pp.charge) / pp.wt_suf;
       return r;
     }
   }
   return locate(p, part, x);
 }
 
-// The items of worker w's range, in order.  For each one with tiles of data
-// in the range calls visit(it, n, rt, i, k): it = the item (it.tile = its
-// first tile in the range), n = its tiles in the range, rt = the number of
-// data tiles of the range before them (empty tiles do not count), i = its
-// position among the visited items, k = it.ord - (ordinal of the item at the
-// range's first position), which is the partial-slot index (w * kmax + k).
-// At most item_cap items are visited.
+// The items of worker w's range, in order.  For each one with tiles in the
+// range (tiles whose first unit lies in it) calls visit(it, n, rt, i, k): it =
+// the item (it.tile = its first tile in the range), n = its tiles in the
+// range, rt = the number of tiles of the range before them, i = its position
+// among the visited items, k = it.ord - (ordinal of the item at the range's
+// first unit), which is the partial-slot index (w * kmax + k).  At most
+// item_cap items are visited.
 struct WorkerRange {
   int nitems;     // items visited
-  int first_ord;  // ordinal of the item at the range's first position
-  int R;          // data tiles in the range
+  int first_ord;  // ordinal of the item at the range's first unit
+  int R;          // tiles in the range
 };
 template <typename Visit>
 SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, Visit&& visit) {
@@ -280,46 +292,100 @@ SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, V
   if (x0 >= x1) return wr;
   ItemRef it = locate(p, part, x0);
   wr.first_ord = it.ord;
-  int64_t x = x0;
-  if (it.tile < 0) {   // the range starts on the item's empty tiles
-    x = it.first;
-    it.tile = 0;
-  }
-  while (x < x1 && wr.nitems < item_cap) {
-    const int n = (int)((it.tiles - it.tile) < (x1 - x) ? (it.tiles - it.tile) : (x1 - x));
-    visit(it, n, wr.R, wr.nitems, it.ord - wr.first_ord);
-    wr.R += n;
-    ++wr.nitems;
-    x += n;
-    if (x >= x1) break;
+  int t = it.off <= 0 ? 0 : cdiv32(it.off, it.w);   // first tile starting at or after x0
+  for (;;) {
+    const int64_t u = it.first + (int64_t)t * it.w;   // where tile t starts
+    if (u >= x1) break;
+    if (t < it.tiles) {
+      if (wr.nitems >= item_cap) break;
+      const int left = cdiv(x1 - u, it.w);            // tile starts left in the range
+      const int n = (it.tiles - t) < left ? (it.tiles - t) : left;
+      ItemRef v = it;
+      v.tile = t;
+      v.off = t * it.w;
+      visit(v, n, wr.R, wr.nitems, it.ord - wr.first_ord);
+      wr.R += n;
+      ++wr.nitems;
+      if (t + n < it.tiles) break;   // the range ends inside this item
+    }
+    const int64_t end = it.first + (int64_t)it.tiles * it.w;   // where the next item's charge starts
+    if (end >= pp.units || end + pp.charge >= x1) break;
     it = next_item(p, part, it);
-    x = it.first;   // past the next item's empty tiles
+    t = 0;
   }
   return wr;
 }
 
-// The parallel form of walk_range: what position x of worker w's range
-// [x0, x1) contributes.  `data` marks a tile of data (not an item's empty
-// tile); `starts` marks the first data tile of an item's segment in the range
-// (x == x0 or the item's own first data tile); there, n is the segment's
-// length.  The segments in order of x are exactly walk_range's visits: the
-// visit index of a segment is the number of starting positions before it, its
-// rt the number of data positions before it, and its slot index it.ord minus
-// the ordinal of the item at x0.
-struct TileInRange {
-  ItemRef it;
-  bool data;
-  bool starts;
+// The item of ordinal ord of partition `part`, at its tile 0 (kind -1 past
+// the last item).  A suffix item of a fork without suffix tokens has no tiles.
+SG_HD ItemRef item_at_ord(const Plan& p, int part, int ord) {
+  const PartPlan& pp = p.part[part];
+  ItemRef r;
+  r.kind = -1;
+  r.t = r.f = r.j = r.rb = r.tiles = r.tile = r.off = 0;
+  r.w = 1;
+  r.first = 0;
+  r.ord = ord;
+  if (ord < 0 || ord >= pp.n_items) return r;
+  if (ord < pp.n_prefix_items) {
+    int lo = pp.trace_begin, hi = pp.trace_begin + pp.n_traces - 1;   // largest i with ordP[i] <= ord
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (p.ordP[mid] <= ord) lo = mid; else hi = mid - 1;
+    }
+    const int t = p.ptrace[lo];
+    const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
+    const int item = ord - p.ordP[lo];
+    r.kind = 0;
+    r.t = t;
+    r.j = item / rb_count;
+    r.rb = item - r.j * rb_count;
+    r.tiles = cdiv32(p.prefix_len[t], pp.tt);
+    r.w = p.wtP[lo];
+    r.first = (int64_t)p.unitP[lo] + (int64_t)item * (r.tiles * r.w + pp.charge) + pp.charge;
+    return r;
+  }
+  const int per_fork = p.Hkv * pp.suffix_rb;
+  const int idx = ord - pp.n_prefix_items;
+  const int f = idx / per_fork, rem = idx - f * per_fork;
+  const int span = suffix_span(p, pp, f);
+  r.kind = 1;
+  r.f = f;
+  r.j = rem / pp.suffix_rb;
+  r.rb = rem - r.j * pp.suffix_rb;
+  r.w = pp.wt_suf;
+  r.tiles = span > 0 ? (span - pp.charge) / r.w : 0;
+  r.first = pp.prefix_units + p.unitS[f] + (int64_t)rem * span + pp.charge;
+  return r;
+}
+
+// The parallel form of walk_range, one lane per item: lane k of a wave takes
+// the item of ordinal ord0 + k, where ord0 is the ordinal of the item at the
+// range's first unit x0 (the planner bounds k by kmax <= 64 for every item a
+// range touches).  `n` is the number of its tiles whose first unit lies in
+// [x0, x1) (0: not visited), from tile `t`.  The visited lanes in order are
+// exactly walk_range's visits: a visit's index is the number of visited lanes
+// before it, its rt the sum of their n, and its slot index k.
+struct LaneItem {
+  ItemRef it;   // it.tile = t
   int n;
 };
-SG_HD TileInRange tile_in_range(const Plan& p, int part, int64_t x0, int64_t x1, int64_t x) {
-  TileInRange r;
-  r.it = locate(p, part, x);
-  r.data = r.it.tile >= 0;
-  r.starts = r.data && (x == x0 || r.it.tile == 0);
-  const int64_t left = x1 - x;
-  const int rest = r.it.tiles - r.it.tile;
-  r.n = rest < left ? rest : (int)left;
+SG_HD LaneItem lane_item(const Plan& p, int part, int64_t x0, int64_t x1, int ord0, int k) {
+  LaneItem r;
+  r.it = item_at_ord(p, part, ord0 + k);
+  r.n = 0;
+  if (r.it.kind < 0 || r.it.tiles == 0) return r;
+  const int64_t d0 = x0 - r.it.first, d1 = x1 - r.it.first;   // range relative to the item's tile 0
+  if (d1 <= 0) return r;
+  const int w = r.it.w;
+  const int t0 = d0 <= 0 ? 0 : (int)((d0 + w - 1) / w);        // first tile starting at or after x0
+  const int t1e = (int)((d1 + w - 1) / w);                     // tiles starting before x1
+  const int t1 = t1e < r.it.tiles ? t1e : r.it.tiles;
+  if (t1 > t0) {
+    r.it.tile = t0;
+    r.it.off = t0 * w;
+    r.n = t1 - t0;
+  }
   return r;
 }
 
@@ -366,13 +432,13 @@ struct ItemParts {
   int row;         // row inside the item
 };
 
-SG_HD ItemParts item_parts(const Plan& p, int part, int64_t first_tile, int tiles, int ord, int row) {
+SG_HD ItemParts item_parts(const Plan& p, int part, int64_t first_unit, int tiles, int w, int ord, int row) {
   const PartPlan& pp = p.part[part];
   ItemParts ip;
   ip.part = part;
   ip.row = row;
-  ip.w_lo = worker_of_tile(pp, first_tile);
-  ip.w_hi = worker_of_tile(pp, first_tile + tiles - 1);
+  ip.w_lo = worker_of_unit(pp, first_unit);
+  ip.w_hi = worker_of_unit(pp, first_unit + (int64_t)(tiles - 1) * w);
   const ItemRef f0 = locate(p, part, worker_start(pp, ip.w_lo));
   ip.k_lo = ord - f0.ord;
   return ip;
@@ -390,8 +456,8 @@ SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h) {
   const int tiles = cdiv32(p.prefix_len[t], pp.tt);
   const int pos = p.trace_pos[t];
   const int item = j * rbc + rb;
-  return item_parts(p, X, (int64_t)p.tileP[pos] + (int64_t)item * (tiles + pp.charge) + pp.charge, tiles,
-                    p.ordP[pos] + item, ri - rb * pp.rbs);
+  return item_parts(p, X, (int64_t)p.unitP[pos] + (int64_t)item * (tiles * p.wtP[pos] + pp.charge) + pp.charge, tiles,
+                    p.wtP[pos], p.ordP[pos] + item, ri - rb * pp.rbs);
 }
 
 // The suffix item of row (f, h); returns false if the fork has no suffix tokens.
@@ -404,8 +470,8 @@ SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
   if (span <= 0) return false;
   const int rb = hh / pp.rbs;
   const int item = j * pp.suffix_rb + rb;
-  *out = item_parts(p, X, pp.prefix_tiles + p.tileS[f] + (int64_t)item * span + pp.charge, span - pp.charge,
-                    pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
+  *out = item_parts(p, X, pp.prefix_units + p.unitS[f] + (int64_t)item * span + pp.charge,
+                    (span - pp.charge) / pp.wt_suf, pp.wt_suf, pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
   return true;
 }
 
@@ -428,7 +494,7 @@ SG_HD bool suffix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, 
   const int g = p.g, j = h / g, hh = h - j * g;
   const int X = part_of_suffix(p.policy);
   const PartPlan& pp = p.part[X];
-  if (p.tileS[f + 1] == p.tileS[f]) return false;
+  if (p.unitS[f + 1] == p.unitS[f]) return false;
   const int rb = hh / pp.rbs;
   *part = X;
   *ord = pp.n_prefix_items + (f * p.Hkv + j) * pp.suffix_rb + rb;

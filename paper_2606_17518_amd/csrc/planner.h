@@ -26,8 +26,14 @@ struct PlanInputs {
   int rbs[2];                 // rows per row block
   int item_cap[2];            // max items per worker
   int tile_cap[2];            // max tiles per worker
-  int charge[2];              // empty sequence positions in front of every item
+  int unit_cap[2];            // max units per worker
+  int charge[2];              // units in front of every item
+  int wt_rg[2][5];            // units per tile of an item of 1..4 row groups of 32 rows ([0] unused)
 };
+
+// Row groups of 32 rows of an item of `rows` rows (at most 4: row blocks hold
+// at most 128 rows).
+inline int row_groups(int rows) { return rows <= 32 ? 1 : rows <= 64 ? 2 : rows <= 96 ? 3 : 4; }
 
 constexpr int64_t kAlignFloats = 64;   // 256-byte alignment of workspace regions
 
@@ -85,25 +91,33 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     pp.slot_rows = in.rbs[X];
     pp.trace_begin = pos;
     pp.charge = in.charge[X];
-    int64_t tiles = 0, items = 0;
+    for (int r = 1; r <= 4; ++r)
+      if (in.wt_rg[X][r] < 1) SG_FAIL(kPlanInvalid, "unit prices must be positive");
+    if (pp.charge < 0) SG_FAIL(kPlanInvalid, "unit prices must be positive");
+    pp.wt_suf = in.wt_rg[X][row_groups(std::min(g, pp.rbs))];
+    pp.wt_max = pp.wt_suf;
+    int64_t units = 0, items = 0;
     for (int t = 0; t < T; ++t) {
       const int rows = (fo[t + 1] - fo[t]) * g;
       if (part_of_trace(in.policy, rows) != X) continue;
       plan->trace_part[t] = X;
       plan->trace_pos[t] = pos;
       plan->ptrace[pos] = t;
-      plan->tileP[pos] = (int32_t)tiles;
+      plan->unitP[pos] = (int32_t)units;
       plan->ordP[pos] = (int32_t)items;
+      // one price for all the trace's prefix items: that of its first (fullest) row block
+      plan->wtP[pos] = in.wt_rg[X][row_groups(std::min(rows, pp.rbs))];
+      pp.wt_max = std::max(pp.wt_max, plan->wtP[pos]);
       const int rb = cdiv(rows, pp.rbs);
-      tiles += (int64_t)Hkv * rb * (cdiv(in.prefix_len[t], pp.tt) + pp.charge);
+      units += (int64_t)Hkv * rb * ((int64_t)cdiv(in.prefix_len[t], pp.tt) * plan->wtP[pos] + pp.charge);
       items += (int64_t)Hkv * rb;
-      if (tiles > INT32_MAX || items > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
+      if (units > INT32_MAX || items > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
       ++pos;
     }
     pp.n_traces = pos - pp.trace_begin;
-    pp.prefix_tiles = tiles;
+    pp.prefix_units = units;
     pp.n_prefix_items = (int32_t)items;
-    pp.tiles = tiles;
+    pp.units = units;
     pp.has_suffix = (X == xs);
     pp.suffix_rb = cdiv(g, pp.rbs);
   }
@@ -112,41 +126,52 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     PartPlan& pp = plan->part[xs];
     int64_t acc = 0;
     for (int f = 0; f < N; ++f) {
-      plan->tileS[f] = (int32_t)acc;
-      if (in.suffix_len[f] > 0) acc += (int64_t)Hkv * pp.suffix_rb * (cdiv(in.suffix_len[f], pp.tt) + pp.charge);
+      plan->unitS[f] = (int32_t)acc;
+      if (in.suffix_len[f] > 0)
+        acc += (int64_t)Hkv * pp.suffix_rb * ((int64_t)cdiv(in.suffix_len[f], pp.tt) * pp.wt_suf + pp.charge);
       if (acc > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
     }
-    plan->tileS[N] = (int32_t)acc;
-    pp.tiles += acc;
+    plan->unitS[N] = (int32_t)acc;
+    pp.units += acc;
+    if (pp.units > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
     if ((int64_t)pp.n_prefix_items + (int64_t)N * Hkv * pp.suffix_rb > INT32_MAX)
       SG_FAIL(kPlanUnsupported, "batch too large");
   }
   // workers: one per compute unit, more while a worker's range would exceed
-  // the kernel's per-worker capacity (items it can describe, tiles it can hold)
+  // the kernel's per-worker capacity (items it can describe, units it walks,
+  // tiles it can hold)
   int64_t off = 0;
   for (int X = 0; X < 2; ++X) {
     PartPlan& pp = plan->part[X];
     pp.workers = 0;
     pp.kmax = 0;
-    if (pp.tiles == 0) continue;
-    int64_t W = std::min<int64_t>(pp.tiles, (int64_t)cus_fn());
+    if (pp.units == 0) continue;
+    // Every worker's range spans at least the largest tile price, so each
+    // worker between the first and the last of an item's workers holds a tile
+    // of it (the merge takes one part from each of them).
+    const int64_t wcap = std::max<int64_t>(1, pp.units / pp.wt_max);
+    int64_t W = std::min<int64_t>(wcap, (int64_t)cus_fn());
+    int tmax = 0;   // most tiles any worker holds
     for (;;) {
       pp.workers = (int32_t)W;
-      pp.per_lo = (int32_t)(pp.tiles / W);
-      pp.n_hi = (int32_t)(pp.tiles % W);
-      const int64_t per = (pp.tiles + W - 1) / W;
+      pp.per_lo = (int32_t)(pp.units / W);
+      pp.n_hi = (int32_t)(pp.units % W);
+      const int64_t per = (pp.units + W - 1) / W;
       int kmax = 0;
+      tmax = 0;
       for (int64_t w = 0; w < W; ++w) {
         const int64_t a = worker_start(pp, w), e = worker_start(pp, w + 1);
         if (e <= a) continue;
         const int k = locate(*plan, X, e - 1).ord - locate(*plan, X, a).ord + 1;
         if (k > kmax) kmax = k;
+        const int tiles = walk_range(*plan, X, w, INT32_MAX, [](const ItemRef&, int, int, int, int) {}).R;
+        if (tiles > tmax) tmax = tiles;
       }
       pp.kmax = kmax;
-      if ((per <= in.tile_cap[X] && kmax <= in.item_cap[X]) || W == pp.tiles) break;
-      W = std::min<int64_t>(pp.tiles, W * 2);
+      if ((per <= in.unit_cap[X] && tmax <= in.tile_cap[X] && kmax <= in.item_cap[X]) || W == wcap) break;
+      W = std::min<int64_t>(wcap, W * 2);
     }
-    if (pp.kmax > in.item_cap[X] || (pp.tiles + pp.workers - 1) / pp.workers > in.tile_cap[X])
+    if (pp.kmax > in.item_cap[X] || tmax > in.tile_cap[X] || (pp.units + pp.workers - 1) / pp.workers > in.unit_cap[X])
       SG_FAIL(kPlanUnsupported, "work split exceeds the kernel's per-worker capacity");
     const int64_t slots = (int64_t)pp.workers * pp.kmax;
     // o: fp16 [slots][slot_rows][D] (D is even); lse: (lse, dec) float pairs

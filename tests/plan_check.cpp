@@ -1,8 +1,8 @@
 // plan_check.cpp -- CPU replay of the fork-decode work split.
 //
-// Builds plans for random batch shapes with the host planner, then replays
-// every worker's walk the way the attention kernels do (locate, segment
-// lengths, segment index k) and every output row's merge lookup the way the
+// Builds plans for random batch shapes and unit prices with the host planner,
+// then replays every worker's walk the way the attention kernels do (locate,
+// segment lengths, segment index k) and every output row's merge lookup the way the
 // merge kernel does, and checks:
 //   - every tile of every work item is processed exactly once;
 //   - per-worker item count and tile count stay within the kernels' caps;
@@ -10,6 +10,7 @@
 //     processed its prefix item and its suffix item, with in-range slots;
 //   - each item row maps back to the (fork, q head) it belongs to;
 //   - stepping from an item to the next (next_item) agrees with locate();
+//   - per-worker units and tiles stay within the kernels' caps;
 //   - the item table the walks record gives the merge the same workers and
 //     slot index as the plan's own lookup.
 // Built and run by tests/test_plan.py with g++ (no GPU involved).
@@ -41,11 +42,20 @@ struct Seg {
   int n;          // tiles
 };
 
-static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
+static int g_unsupported = 0;
+
+// lib_prices: the library's unit prices, with which every generated shape
+// must plan; with random prices the planner may answer "unsupported" (a
+// range would touch more items than a kernel can describe), never wrongly.
+static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib_prices) {
   Plan plan;
   int64_t wsf = 0;
   char err[256];
   const int rc = plan_build(in, [&] { return cus; }, &plan, &wsf, err, sizeof err);
+  if (rc == kPlanUnsupported && !lib_prices) {
+    ++g_unsupported;
+    return true;
+  }
   CHECK(rc == kPlanOk, "case %llu: plan_build failed: %s", (unsigned long long)case_id, err);
   // segments per (partition, item ordinal), from the walk the kernels run;
   // the walk also fills the item table the merge reads
@@ -54,29 +64,32 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
   for (int X = 0; X < 2; ++X) {
     const PartPlan& pp = plan.part[X];
     if (pp.workers == 0) {
-      CHECK(pp.tiles == 0, "partition %d has tiles but no workers", X);
+      CHECK(pp.units == 0, "partition %d has units but no workers", X);
       continue;
     }
     CHECK(pp.info_base + 3 * (int64_t)pp.n_items <= wsf, "item table past the workspace");
     tables[X].assign(3 * (size_t)pp.n_items, -7);
     for (int w = 0; w < pp.workers; ++w) {
       const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
-      CHECK(x1 - x0 <= in.tile_cap[X], "worker %d has %lld tiles > cap", w, (long long)(x1 - x0));
-      int64_t x = x0;      // position after the previous segment
-      int64_t data = 0;    // data tiles visited so far
+      CHECK(x1 - x0 <= in.unit_cap[X], "worker %d has %lld units > cap", w, (long long)(x1 - x0));
+      int64_t x = x0;      // unit after the previous segment's last tile start
+      int64_t data = 0;    // tiles visited so far
       bool fine = true;
       const WorkerRange wr = walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
-        const int64_t at = it.first + it.tile;
-        // only an item's empty positions may lie between two segments
-        if (it.kind < 0 || it.tile < 0 || at < x || at > x + pp.charge || at + n > x1 || rt != data || k < 0 ||
+        const int64_t at = it.first + (int64_t)it.tile * it.w;   // unit where the segment's first tile starts
+        // segments in order, inside the range (every tile start of a segment in
+        // [x0, x1)), none before x0 missed
+        if (it.kind < 0 || it.tile < 0 || n < 1 || it.tile + n > it.tiles || at < x || at < x0 ||
+            at + (int64_t)(n - 1) * it.w >= x1 || (it.tile > 0 && at - it.w >= x0) || rt != data || k < 0 ||
             k >= pp.kmax || it.ord >= pp.n_items)
           fine = false;
         segs[{X, it.ord}].push_back(Seg{w, k, at, n});
         if (it.ord >= 0 && it.ord < pp.n_items) record_item(tables[X].data(), it, n, w, k);
-        x = at + n;
+        x = at + (int64_t)(n - 1) * it.w + 1;
         data += n;
         (void)i;
       });
+      CHECK(wr.R <= in.tile_cap[X], "worker %d holds %d tiles > cap", w, wr.R);
       CHECK(fine, "worker %d of partition %d: walk out of order or slot index out of range", w, X);
       // the parallel form (one tile per thread) must give the same segments
       {
@@ -85,22 +98,27 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
         walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
           serial.push_back(V{it.ord, it.tile, n, rt, i, k});
         });
-        std::vector<V> par;
-        int first_ord = 0, ndata = 0;
-        for (int64_t xx = x0; xx < x1; ++xx) {
-          const TileInRange t = tile_in_range(plan, X, x0, x1, xx);
-          if (xx == x0) first_ord = t.it.ord;
-          if (t.starts) par.push_back(V{t.it.ord, t.it.tile, t.n, ndata, (int)par.size(), t.it.ord - first_ord});
-          ndata += t.data ? 1 : 0;
+        std::vector<V> par;   // one lane per item ordinal, as the MFMA kernel's walk
+        const int ord0 = locate(plan, X, x0).ord;
+        int rt = 0;
+        for (int k = 0; k < 64; ++k) {
+          const LaneItem li = lane_item(plan, X, x0, x1, ord0, k);
+          if (li.n > 0) {
+            par.push_back(V{li.it.ord, li.it.tile, li.n, rt, (int)par.size(), k});
+            rt += li.n;
+          }
         }
         bool same = serial.size() == par.size();
         for (size_t q = 0; same && q < par.size(); ++q)
           same = serial[q].ord == par[q].ord && serial[q].tile == par[q].tile && serial[q].n == par[q].n &&
                  serial[q].rt == par[q].rt && serial[q].i == par[q].i && serial[q].k == par[q].k;
-        CHECK(same, "worker %d of partition %d: per-tile walk differs from the serial walk", w, X);
+        CHECK(same, "worker %d of partition %d: per-lane walk differs from the serial walk", w, X);
       }
-      int64_t ndata = 0;
-      for (int64_t xx = x0; xx < x1; ++xx) ndata += locate(plan, X, xx).tile >= 0 ? 1 : 0;
+      int64_t ndata = 0;   // tile starts in the range
+      for (int64_t xx = x0; xx < x1; ++xx) {
+        const ItemRef r = locate(plan, X, xx);
+        ndata += (r.off >= 0 && r.off % r.w == 0) ? 1 : 0;
+      }
       CHECK(wr.R == ndata, "worker %d walked %d of %lld data tiles (item cap %d)", w, wr.R, (long long)ndata,
             in.item_cap[X]);
     }
@@ -109,23 +127,23 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
   const int g = in.Hq / in.Hkv;
   int64_t ptile[2] = {0, 0};
   int pord[2] = {0, 0};
-  auto cover = [&](int X, int ord, int tiles) -> bool {
+  auto cover = [&](int X, int ord, int tiles, int wt) -> bool {
     auto itv = segs.find({X, ord});
     if (tiles == 0) {
       CHECK(itv == segs.end(), "empty item has segments");
       return true;
     }
     CHECK(itv != segs.end(), "item (%d, %d) never processed", X, ord);
-    // an item takes `charge` empty positions, then its data tiles
+    // an item takes `charge` units, then its tiles of wt units each
     int64_t expect = ptile[X] + in.charge[X];
     int total = 0;
     for (const Seg& s : itv->second) {
       CHECK(s.first == expect, "item tiles not contiguous");
-      expect += s.n;
+      expect += (int64_t)s.n * wt;
       total += s.n;
     }
     CHECK(total == tiles, "item covered %d of %d tiles", total, tiles);
-    ptile[X] += in.charge[X] + tiles;
+    ptile[X] += in.charge[X] + (int64_t)tiles * wt;
     return true;
   };
   for (int X = 0; X < 2; ++X) {
@@ -135,7 +153,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
       const int rb = (rows + in.rbs[X] - 1) / in.rbs[X];
       const int tiles = (in.prefix_len[t] + in.tt[X] - 1) / in.tt[X];
       for (int i = 0; i < in.Hkv * rb; ++i)
-        if (!cover(X, pord[X]++, tiles)) return false;
+        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(rows, in.rbs[X]))])) return false;
     }
   }
   {
@@ -144,24 +162,24 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id) {
     for (int f = 0; f < in.N; ++f) {
       const int tiles = (in.suffix_len[f] + in.tt[X] - 1) / in.tt[X];
       for (int i = 0; i < in.Hkv * rb; ++i)
-        if (!cover(X, pord[X]++, tiles)) return false;
+        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(g, in.rbs[X]))])) return false;
     }
   }
-  for (int X = 0; X < 2; ++X) CHECK(ptile[X] == plan.part[X].tiles, "partition %d tile total", X);
+  for (int X = 0; X < 2; ++X) CHECK(ptile[X] == plan.part[X].units, "partition %d unit total", X);
   // the incremental step between items agrees with locate() at every item boundary
   for (int X = 0; X < 2; ++X) {
     const PartPlan& pp = plan.part[X];
     int64_t x = 0;
-    while (x < pp.tiles) {
+    while (x < pp.units) {
       const ItemRef it = locate(plan, X, x);
-      CHECK(it.tile == -pp.charge, "an item starts with its empty positions");
-      const int64_t nx = it.first + it.tiles;
-      if (nx < pp.tiles) {
+      CHECK(it.off == -pp.charge, "an item starts with its charge");
+      const int64_t nx = it.first + (int64_t)it.tiles * it.w;
+      if (nx < pp.units) {
         const ItemRef a = next_item(plan, X, it);
         const ItemRef b = locate(plan, X, nx + pp.charge);
         CHECK(a.kind == b.kind && a.t == b.t && a.f == b.f && a.j == b.j && a.rb == b.rb && a.tiles == b.tiles &&
-                  a.tile == b.tile && a.first == b.first && a.ord == b.ord,
-              "next_item differs from locate at tile %lld of partition %d", (long long)nx, X);
+                  a.tile == b.tile && a.off == b.off && a.w == b.w && a.first == b.first && a.ord == b.ord,
+              "next_item differs from locate at unit %lld of partition %d", (long long)nx, X);
       }
       x = nx;
     }
@@ -282,18 +300,32 @@ int main(int argc, char** argv) {
     in.rbs[0] = 128;
     in.rbs[1] = 16;
     in.item_cap[0] = in.item_cap[1] = 64;
-    in.charge[0] = U(0, 3);   // the library uses 2 and 1; any value must give a valid split
-    in.charge[1] = U(0, 2);
-    in.tile_cap[0] = 2048 / (in.tt[0] / 16);
+    // unit prices: the library's (MFMA 8 / 6 / 16, dot 1 / 1 / 1) or random;
+    // any positive prices must give a valid split
+    const bool lib_prices = U(0, 1) != 0;
+    if (lib_prices) {
+      const int mfma_rg[5] = {0, 6, 6, 7, 8};
+      for (int r = 0; r < 5; ++r) { in.wt_rg[0][r] = mfma_rg[r]; in.wt_rg[1][r] = 1; }
+      in.charge[0] = 16;
+      in.charge[1] = 1;
+    } else {
+      for (int X = 0; X < 2; ++X) {
+        for (int r = 0; r < 5; ++r) in.wt_rg[X][r] = U(1, 8);
+        in.charge[X] = U(0, 20);
+      }
+    }
+    in.tile_cap[0] = 2560 / (in.tt[0] / 16);
     in.tile_cap[1] = 2048 / 4;
+    in.unit_cap[0] = 1 << 30;   // the MFMA walk has no unit limit
+    in.unit_cap[1] = in.tile_cap[1];
     const int cus = U(0, 2) == 0 ? U(1, 16) : 256;
-    if (!check_plan(in, cus, (uint64_t)c)) {
+    if (!check_plan(in, cus, (uint64_t)c, lib_prices)) {
       fprintf(stderr, "case %d: D=%d policy=%d g=%d Hkv=%d T=%d N=%d cus=%d\n", c, in.D, in.policy, g, in.Hkv,
               in.T, in.N, cus);
       return 1;
     }
     ++done;
   }
-  printf("OK %d plans\n", done);
+  printf("OK %d plans (%d with random prices unsupported)\n", done, g_unsupported);
   return 0;
 }
