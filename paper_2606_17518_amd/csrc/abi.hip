@@ -103,8 +103,8 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   }
   in.charge[0] = 16;
   in.charge[1] = 1;
-  in.unit_cap[0] = INT32_MAX;   // the MFMA walk takes one lane per item: any number of units
-  in.unit_cap[1] = in.tile_cap[1];
+  in.walk_threads[0] = mfma_walk_threads();
+  in.walk_threads[1] = 0;   // the dot kernel walks serially
   char err[256];
   const int rc = plan_build(in, [] { return device_cus(); }, plan, ws_floats, err, sizeof err);
   if (rc == kPlanInvalid) return fail(SPECGEN_ERR_INVALID_ARG, "%s", err);

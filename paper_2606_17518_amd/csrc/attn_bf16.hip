@@ -762,5 +762,6 @@ int mfma_tile_cap(int D, bool fp8) {
   return D == 128 ? bf16k::Cfg<128, false>::kTileCap : bf16k::Cfg<64, false>::kTileCap;
 }
 int mfma_item_cap() { return bf16k::Cfg<128, false>::kItemCap; }
+int mfma_walk_threads() { return bf16k::Cfg<128, false>::kThreads; }
 
 }  // namespace specgen

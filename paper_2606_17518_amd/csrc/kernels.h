@@ -13,6 +13,7 @@ hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, h
 int mfma_tile_tokens(int D, bool fp8);
 int mfma_item_cap();
 int mfma_tile_cap(int D, bool fp8);
+int mfma_walk_threads();
 // attn_dot.hip
 hipError_t launch_attn_dot_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
 int dot_tile_tokens(int D);

@@ -316,76 +316,39 @@ SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, V
   return wr;
 }
 
-// The item of ordinal ord of partition `part`, at its tile 0 (kind -1 past
-// the last item).  A suffix item of a fork without suffix tokens has no tiles.
-SG_HD ItemRef item_at_ord(const Plan& p, int part, int ord) {
-  const PartPlan& pp = p.part[part];
-  ItemRef r;
-  r.kind = -1;
-  r.t = r.f = r.j = r.rb = r.tiles = r.tile = r.off = 0;
-  r.w = 1;
-  r.first = 0;
-  r.ord = ord;
-  if (ord < 0 || ord >= pp.n_items) return r;
-  if (ord < pp.n_prefix_items) {
-    int lo = pp.trace_begin, hi = pp.trace_begin + pp.n_traces - 1;   // largest i with ordP[i] <= ord
-    while (lo < hi) {
-      int mid = (lo + hi + 1) >> 1;
-      if (p.ordP[mid] <= ord) lo = mid; else hi = mid - 1;
-    }
-    const int t = p.ptrace[lo];
-    const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
-    const int item = ord - p.ordP[lo];
-    r.kind = 0;
-    r.t = t;
-    r.j = item / rb_count;
-    r.rb = item - r.j * rb_count;
-    r.tiles = cdiv32(p.prefix_len[t], pp.tt);
-    r.w = p.wtP[lo];
-    r.first = (int64_t)p.unitP[lo] + (int64_t)item * (r.tiles * r.w + pp.charge) + pp.charge;
-    return r;
-  }
-  const int per_fork = p.Hkv * pp.suffix_rb;
-  const int idx = ord - pp.n_prefix_items;
-  const int f = idx / per_fork, rem = idx - f * per_fork;
-  const int span = suffix_span(p, pp, f);
-  r.kind = 1;
-  r.f = f;
-  r.j = rem / pp.suffix_rb;
-  r.rb = rem - r.j * pp.suffix_rb;
-  r.w = pp.wt_suf;
-  r.tiles = span > 0 ? (span - pp.charge) / r.w : 0;
-  r.first = pp.prefix_units + p.unitS[f] + (int64_t)rem * span + pp.charge;
-  return r;
-}
-
-// The parallel form of walk_range, one lane per item: lane k of a wave takes
-// the item of ordinal ord0 + k, where ord0 is the ordinal of the item at the
-// range's first unit x0 (the planner bounds k by kmax <= 64 for every item a
-// range touches).  `n` is the number of its tiles whose first unit lies in
-// [x0, x1) (0: not visited), from tile `t`.  The visited lanes in order are
-// exactly walk_range's visits: a visit's index is the number of visited lanes
-// before it, its rt the sum of their n, and its slot index k.
-struct LaneItem {
-  ItemRef it;   // it.tile = t
+// The parallel form of walk_range: what the chunk [u0, u0 + c) of worker w's
+// range [x0, x1) contributes, for chunks no longer than any tile price or the
+// charge (so a chunk holds at most one tile start, and the next item's tile 0
+// never shares a chunk with the tile start it follows).  `data` marks a tile
+// starting in the chunk (it.tile = that tile); `starts` marks the first tile
+// of an item's segment in the range (the item's tile 0, or its first tile at
+// or after x0); there, n is the segment's length in tiles.  The segments in
+// order of u0 are exactly walk_range's visits: the visit index of a segment is
+// the number of starting chunks before it, its rt the number of data chunks
+// before it, and its slot index it.ord minus the ordinal of the item at x0.
+struct TileInRange {
+  ItemRef it;
+  bool data;
+  bool starts;
   int n;
 };
-SG_HD LaneItem lane_item(const Plan& p, int part, int64_t x0, int64_t x1, int ord0, int k) {
-  LaneItem r;
-  r.it = item_at_ord(p, part, ord0 + k);
+SG_HD TileInRange tile_in_chunk(const Plan& p, int part, int64_t x0, int64_t x1, int64_t u0, int c) {
+  TileInRange r;
+  r.it = locate(p, part, u0);
+  r.data = r.starts = false;
   r.n = 0;
-  if (r.it.kind < 0 || r.it.tiles == 0) return r;
-  const int64_t d0 = x0 - r.it.first, d1 = x1 - r.it.first;   // range relative to the item's tile 0
-  if (d1 <= 0) return r;
+  if (r.it.kind < 0) return r;
   const int w = r.it.w;
-  const int t0 = d0 <= 0 ? 0 : (int)((d0 + w - 1) / w);        // first tile starting at or after x0
-  const int t1e = (int)((d1 + w - 1) / w);                     // tiles starting before x1
-  const int t1 = t1e < r.it.tiles ? t1e : r.it.tiles;
-  if (t1 > t0) {
-    r.it.tile = t0;
-    r.it.off = t0 * w;
-    r.n = t1 - t0;
-  }
+  const int t = r.it.off <= 0 ? 0 : cdiv32(r.it.off, w);   // first tile starting at or after u0
+  if (t >= r.it.tiles) return r;
+  const int64_t s = r.it.first + (int64_t)t * w;
+  if (s >= u0 + c || s >= x1) return r;
+  r.it.tile = t;
+  r.it.off = t * w;
+  r.data = true;
+  r.starts = t == 0 || s - w < x0;
+  const int left = cdiv(x1 - s, w);
+  r.n = (r.it.tiles - t) < left ? (r.it.tiles - t) : left;
   return r;
 }
 

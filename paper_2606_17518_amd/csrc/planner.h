@@ -26,7 +26,7 @@ struct PlanInputs {
   int rbs[2];                 // rows per row block
   int item_cap[2];            // max items per worker
   int tile_cap[2];            // max tiles per worker
-  int unit_cap[2];            // max units per worker
+  int walk_threads[2];        // threads of a parallel walk (0: serial walk, no unit limit)
   int charge[2];              // units in front of every item
   int wt_rg[2][5];            // units per tile of an item of 1..4 row groups of 32 rows ([0] unused)
 };
@@ -81,6 +81,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   for (int f = 0; f < N; ++f) plan->suffix_len[f] = in.suffix_len[f];
   for (int f = 0; f <= N; ++f) plan->suffix_table_off[f] = in.suffix_table_off[f];
   const int xs = part_of_suffix(in.policy);
+  int64_t unit_cap[2];   // units per worker a kernel's walk can take
 
   // prefix items, traces grouped by partition
   int pos = 0;
@@ -96,6 +97,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     if (pp.charge < 0) SG_FAIL(kPlanInvalid, "unit prices must be positive");
     pp.wt_suf = in.wt_rg[X][row_groups(std::min(g, pp.rbs))];
     pp.wt_max = pp.wt_suf;
+    int wt_min = pp.wt_suf;
     int64_t units = 0, items = 0;
     for (int t = 0; t < T; ++t) {
       const int rows = (fo[t + 1] - fo[t]) * g;
@@ -108,6 +110,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
       // one price for all the trace's prefix items: that of its first (fullest) row block
       plan->wtP[pos] = in.wt_rg[X][row_groups(std::min(rows, pp.rbs))];
       pp.wt_max = std::max(pp.wt_max, plan->wtP[pos]);
+      wt_min = std::min(wt_min, plan->wtP[pos]);
       const int rb = cdiv(rows, pp.rbs);
       units += (int64_t)Hkv * rb * ((int64_t)cdiv(in.prefix_len[t], pp.tt) * plan->wtP[pos] + pp.charge);
       items += (int64_t)Hkv * rb;
@@ -115,6 +118,10 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
       ++pos;
     }
     pp.n_traces = pos - pp.trace_begin;
+    // a parallel walk examines chunks of at most min(price, charge) units per
+    // thread, so that a chunk holds at most one tile start
+    unit_cap[X] = in.walk_threads[X] > 0 ? (int64_t)in.walk_threads[X] * std::max(1, std::min(wt_min, pp.charge))
+                                         : INT64_MAX;
     pp.prefix_units = units;
     pp.n_prefix_items = (int32_t)items;
     pp.units = units;
@@ -168,10 +175,10 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
         if (tiles > tmax) tmax = tiles;
       }
       pp.kmax = kmax;
-      if ((per <= in.unit_cap[X] && tmax <= in.tile_cap[X] && kmax <= in.item_cap[X]) || W == wcap) break;
+      if ((per <= unit_cap[X] && tmax <= in.tile_cap[X] && kmax <= in.item_cap[X]) || W == wcap) break;
       W = std::min<int64_t>(wcap, W * 2);
     }
-    if (pp.kmax > in.item_cap[X] || tmax > in.tile_cap[X] || (pp.units + pp.workers - 1) / pp.workers > in.unit_cap[X])
+    if (pp.kmax > in.item_cap[X] || tmax > in.tile_cap[X] || (pp.units + pp.workers - 1) / pp.workers > unit_cap[X])
       SG_FAIL(kPlanUnsupported, "work split exceeds the kernel's per-worker capacity");
     const int64_t slots = (int64_t)pp.workers * pp.kmax;
     // o: fp16 [slots][slot_rows][D] (D is even); lse: (lse, dec) float pairs

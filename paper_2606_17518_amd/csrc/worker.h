@@ -60,42 +60,69 @@ __device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* 
   return wr;
 }
 
-// The walk and the block-id gather, in two parallel steps.  1: lane k of wave
-// 0 takes the item of ordinal ord0 + k (lane_item) and, if the range holds
-// tiles of it, writes its descriptor -- its index among the visited items and
-// the position of its first tile in the range come from wave prefix sums --
-// and its item-table entries.  2: for each tile i < R of the range, thread
-// i mod kThreads finds the descriptor holding it and loads that tile's
-// kIdsPerTile block ids (clamped to the item's last valid block) into
-// ids[i * kIdsPerTile ..].  The walk reads
-// only the plan in LDS, so the id loads are its one memory round trip.
-// `scratch` holds 3 ints of LDS.  Ends with a barrier.
+// The walk and the block-id gather in one pass: thread i examines the chunk
+// of c = ceil((x1 - x0) / kThreads) units at x0 + i * c (tile_in_chunk; the
+// planner keeps c within every tile price and the charge); a chunk where a
+// tile starts loads the tile's kIdsPerTile block ids (clamped to its item's
+// last valid block) into ids[n * kIdsPerTile ..], where n counts the tiles
+// before it, and the thread at the first tile of each item's segment writes
+// the item's descriptor and its item-table entries.  Items and tiles are
+// numbered with wave ballots, so nothing runs serially and the only memory
+// round trip is the id loads.  `scratch` is 2 * kThreads / 64 + 1 ints of
+// LDS.  Ends with a barrier.
 template <int kThreads, int kItemCap, int kIdsPerTile>
 __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, int part, int w, int32_t* items,
                                          int32_t* ids, int32_t* scratch) {
-  static_assert(kItemCap <= 64, "one lane per item");
+  constexpr int kW = kThreads / 64;
   const PartPlan& pp = plan.part[part];
   int32_t* info = reinterpret_cast<int32_t*>(a.ws + pp.info_base);
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
-  if (tid < 64) {
-    int ord0 = 0;
-    LaneItem li;
-    li.n = 0;
-    if (x0 < x1) {
-      ord0 = locate(plan, part, x0).ord;
-      li = lane_item(plan, part, x0, x1, ord0, lane);
-    }
-    int incl = li.n;   // inclusive prefix sum of tiles over the lanes
+  const int cu = (int)((x1 - x0 + kThreads - 1) / kThreads);   // units per chunk
+  const int64_t u0 = x0 + (int64_t)tid * cu;
+  const bool mine = u0 < x1;
+  TileInRange tr;
+  tr.data = tr.starts = false;
+  tr.n = 0;
+  int32_t id[kIdsPerTile];
+  if (mine) {
+    tr = tile_in_chunk(plan, part, x0, x1, u0, cu);
+    if (tr.data) {
+      const ItemRef& it = tr.it;
+      const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+      const int lastblk = (nv - 1) / 16;
+      const int32_t* tab = it.kind == 0 ? a.prefix_table + plan.prefix_table_off[it.t]
+                                        : a.suffix_table + plan.suffix_table_off[it.f];
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += v;
+      for (int b = 0; b < kIdsPerTile; ++b) {
+        const int bi = it.tile * kIdsPerTile + b;
+        id[b] = tab[bi < lastblk ? bi : lastblk];
+      }
     }
-    const uint64_t vmask = __ballot(li.n > 0);
-    const int i = __popcll(vmask & ((1ull << lane) - 1));
-    if (li.n > 0 && i < kItemCap) {
-      const ItemRef& it = li.it;
+  }
+  const uint64_t starts = __ballot(tr.starts);
+  const uint64_t data = __ballot(tr.data);
+  if (lane == 0) {
+    scratch[wave] = __popcll(starts);
+    scratch[kW + wave] = __popcll(data);
+  }
+  if (tid == 0) scratch[2 * kW] = mine ? tr.it.ord : 0;
+  __syncthreads();
+  int ibase = 0, items_total = 0, dbase = 0, data_total = 0;
+#pragma unroll
+  for (int v = 0; v < kW; ++v) {
+    ibase += v < wave ? scratch[v] : 0;
+    items_total += scratch[v];
+    dbase += v < wave ? scratch[kW + v] : 0;
+    data_total += scratch[kW + v];
+  }
+  const int first_ord = scratch[2 * kW];
+  const uint64_t below = (1ull << lane) - 1;
+  const int c = dbase + __popcll(data & below);   // data tiles before this one
+  if (tr.starts) {
+    const int i = ibase + __popcll(starts & below);
+    if (i < kItemCap) {
+      const ItemRef& it = tr.it;
       int32_t* d = items + i * kItemInts;
       d[IT_KIND] = it.kind;
       d[IT_T] = it.t;
@@ -104,8 +131,8 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
       d[IT_RB] = it.rb;
       d[IT_ORD] = it.ord;
       d[IT_TILE0] = it.tile;
-      d[IT_NTILE] = li.n;
-      d[IT_RTILE0] = incl - li.n;
+      d[IT_NTILE] = tr.n;
+      d[IT_RTILE0] = c;
       d[IT_TILES] = it.tiles;
       const int r0 = it.rb * pp.rbs;
       const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
@@ -115,36 +142,18 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
       d[IT_NVALID] = nv;
       d[IT_TABOFF] = it.kind == 0 ? plan.prefix_table_off[it.t] : plan.suffix_table_off[it.f];
       d[IT_LASTBLK] = (nv - 1) / 16;
-      record_item(info, it, li.n, w, lane);
+      record_item(info, it, tr.n, w, it.ord - first_ord);
     }
-    if (lane == 63) {
-      scratch[0] = incl;
-      scratch[1] = __popcll(vmask);
-    }
-    if (lane == 0) scratch[2] = ord0;
+  }
+  if (tr.data) {
+#pragma unroll
+    for (int b = 0; b < kIdsPerTile; ++b) ids[c * kIdsPerTile + b] = id[b];
   }
   __syncthreads();
   WorkerRange wr;
-  wr.R = scratch[0];
-  wr.nitems = scratch[1] < kItemCap ? scratch[1] : kItemCap;
-  wr.first_ord = scratch[2];
-  for (int r = tid; r < wr.R; r += kThreads) {   // the planner keeps R within the tile capacity
-    int lo = 0, hi = wr.nitems - 1;   // the last descriptor whose first tile in the range is <= r
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (items[mid * kItemInts + IT_RTILE0] <= r) lo = mid; else hi = mid - 1;
-    }
-    const int32_t* d = items + lo * kItemInts;
-    const int tile = d[IT_TILE0] + (r - d[IT_RTILE0]);
-    const int lastblk = d[IT_LASTBLK];
-    const int32_t* tab = (d[IT_KIND] == 0 ? a.prefix_table : a.suffix_table) + d[IT_TABOFF];
-#pragma unroll
-    for (int b = 0; b < kIdsPerTile; ++b) {
-      const int bi = tile * kIdsPerTile + b;
-      ids[r * kIdsPerTile + b] = tab[bi < lastblk ? bi : lastblk];
-    }
-  }
-  __syncthreads();
+  wr.nitems = items_total < kItemCap ? items_total : kItemCap;
+  wr.first_ord = first_ord;
+  wr.R = data_total;
   return wr;
 }
 

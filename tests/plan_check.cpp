@@ -71,7 +71,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     tables[X].assign(3 * (size_t)pp.n_items, -7);
     for (int w = 0; w < pp.workers; ++w) {
       const int64_t x0 = worker_start(pp, w), x1 = worker_start(pp, w + 1);
-      CHECK(x1 - x0 <= in.unit_cap[X], "worker %d has %lld units > cap", w, (long long)(x1 - x0));
+
       int64_t x = x0;      // unit after the previous segment's last tile start
       int64_t data = 0;    // tiles visited so far
       bool fine = true;
@@ -91,28 +91,30 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
       });
       CHECK(wr.R <= in.tile_cap[X], "worker %d holds %d tiles > cap", w, wr.R);
       CHECK(fine, "worker %d of partition %d: walk out of order or slot index out of range", w, X);
-      // the parallel form (one tile per thread) must give the same segments
-      {
+      // the chunked parallel walk of a partition that uses one must give the same segments
+      if (in.walk_threads[X] > 0) {
         struct V { int ord, tile, n, rt, i, k; };
         std::vector<V> serial;
         walk_range(plan, X, w, in.item_cap[X], [&](const ItemRef& it, int n, int rt, int i, int k) {
           serial.push_back(V{it.ord, it.tile, n, rt, i, k});
         });
-        std::vector<V> par;   // one lane per item ordinal, as the MFMA kernel's walk
-        const int ord0 = locate(plan, X, x0).ord;
-        int rt = 0;
-        for (int k = 0; k < 64; ++k) {
-          const LaneItem li = lane_item(plan, X, x0, x1, ord0, k);
-          if (li.n > 0) {
-            par.push_back(V{li.it.ord, li.it.tile, li.n, rt, (int)par.size(), k});
-            rt += li.n;
-          }
+        std::vector<V> par;   // the parallel walk: one chunk of cu units per thread
+        const int threads = in.walk_threads[X];
+        const int cu = (int)((x1 - x0 + threads - 1) / threads);
+        int first_ord = 0, ndata = 0;
+        for (int tt = 0; tt < threads; ++tt) {
+          const int64_t u0 = x0 + (int64_t)tt * cu;
+          if (u0 >= x1) break;
+          const TileInRange t = tile_in_chunk(plan, X, x0, x1, u0, cu);
+          if (tt == 0) first_ord = t.it.ord;
+          if (t.starts) par.push_back(V{t.it.ord, t.it.tile, t.n, ndata, (int)par.size(), t.it.ord - first_ord});
+          ndata += t.data ? 1 : 0;
         }
         bool same = serial.size() == par.size();
         for (size_t q = 0; same && q < par.size(); ++q)
           same = serial[q].ord == par[q].ord && serial[q].tile == par[q].tile && serial[q].n == par[q].n &&
                  serial[q].rt == par[q].rt && serial[q].i == par[q].i && serial[q].k == par[q].k;
-        CHECK(same, "worker %d of partition %d: per-lane walk differs from the serial walk", w, X);
+        CHECK(same, "worker %d of partition %d: chunked walk differs from the serial walk", w, X);
       }
       int64_t ndata = 0;   // tile starts in the range
       for (int64_t xx = x0; xx < x1; ++xx) {
@@ -316,8 +318,8 @@ int main(int argc, char** argv) {
     }
     in.tile_cap[0] = 2560 / (in.tt[0] / 16);
     in.tile_cap[1] = 2048 / 4;
-    in.unit_cap[0] = 1 << 30;   // the MFMA walk has no unit limit
-    in.unit_cap[1] = in.tile_cap[1];
+    in.walk_threads[0] = 512;   // the MFMA kernel's chunked walk
+    in.walk_threads[1] = 0;     // the dot kernel's serial walk
     const int cus = U(0, 2) == 0 ? U(1, 16) : 256;
     if (!check_plan(in, cus, (uint64_t)c, lib_prices)) {
       fprintf(stderr, "case %d: D=%d policy=%d g=%d Hkv=%d T=%d N=%d cus=%d\n", c, in.D, in.policy, g, in.Hkv,
