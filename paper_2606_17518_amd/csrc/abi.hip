@@ -84,7 +84,7 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.suffix_table_off = b->suffix_table_off_h;
   in.tt[0] = mfma_tile_tokens(in.D == 64 ? 64 : 128, fp8);
   in.tt[1] = dot_tile_tokens(in.D);
-  in.rbs[0] = 128;
+  in.rbs[0] = mfma_rows();
   in.rbs[1] = dot_rows();
   in.item_cap[0] = mfma_item_cap();
   in.item_cap[1] = dot_item_cap();
@@ -95,9 +95,11 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   // 1.20 and 1.48 us with bf16 KV (1.56 and 1.96 us for 1 and 4 groups with
   // E4M3), and an item's fixed cost (q slot, token-group combine, partial
   // stores) about two tiles of 4 groups.  In eighths of that tile: 6, 6, 7, 8
-  // and 16.  The dot path prices every tile alike and an item at one tile.
-  const int mfma_rg[5] = {0, 6, 6, 7, 8};
-  for (int r = 0; r < 5; ++r) {
+  // and 16.  Items of 5-8 groups run one token group per wave (each wave
+  // takes both 32-token slabs of a tile).  The dot path prices every tile
+  // alike and an item at one tile.
+  const int mfma_rg[9] = {0, 6, 6, 7, 8, 11, 12, 12, 13};
+  for (int r = 0; r < 9; ++r) {
     in.wt_rg[0][r] = mfma_rg[r];
     in.wt_rg[1][r] = 1;
   }

@@ -88,7 +88,8 @@ struct Cfg {
   static constexpr int kSlicesPerWave = kTT / 16 / 4; // block slices of a tile per wave (4 waves per tensor)
   static constexpr int kPiecesPerSlice = kSliceB / 1024;
   static constexpr int kItemCap = 64;
-  static constexpr int kMaxRows = 128;                // rows per item (row block)
+  static constexpr int kMaxRows = 256;                // rows per item (row block)
+  static constexpr int kQRows = 128;                  // q rows per slot: an item takes 1 or 2 q slots
   static constexpr int kOffItems = kStages * kStageB;
   static constexpr int kOffML = kOffItems + kItemCap * kItemInts * 4;
   static constexpr int kMLBytes = kWaves * 2 * 64 * 2 * 4;   // [wave][nt][lane] (m, l)
@@ -107,11 +108,14 @@ struct Cfg {
   static constexpr int kLdsBytes = kOffIds + kIdCap * 4;
   static_assert(kSlicesPerWave * kPiecesPerSlice == kDmaSlot, "a tile slot is four instructions per wave");
   static_assert(kDmaSlot * kWaves * 1024 == kStageB, "slot split over the waves");
-  static_assert(kMaxRows * kRowB <= kStageB, "q rows of an item fit one slot");
+  static_assert(kQRows * kRowB <= kStageB && 2 * kQRows >= kMaxRows, "q rows of an item fit two slots");
   static_assert(kLdsBytes + (int)sizeof(Plan) <= 163840, "LDS budget");
   static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
   static_assert(!FP8 || kSlicesPerWave * (kF8Slice / 1024) == kTileDma, "E4M3 code instructions per wave");
 };
+
+// q slots of an item of `nrows` rows (128 rows per slot)
+__device__ __forceinline__ int q_slots(int nrows) { return nrows > 128 ? 2 : 1; }
 
 // Chunk swizzle of the q rows in a slot: the 16 rows an MFMA operand read
 // touches land in distinct banks.
@@ -198,7 +202,6 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   const int first_ord = uniform(wr.first_ord);
   const int nitems = uniform(wr.nitems);
   if (R <= 0) return;
-  const int S = R + nitems;   // slots: a q slot per item, then its tiles
   const uint32_t lds_base = (uint32_t)(size_t)((SG_LDS uint8_t*)lds);
 
   // Item descriptors are read from LDS once per item and kept in scalar registers.
@@ -268,8 +271,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
       for (int i = 0; i < C::kDmaSlot; ++i) {
         const int n = wave * C::kDmaSlot + i;
-        const int row = (n * C::kRPI + lane / CPR) & (C::kMaxRows - 1);
-        const int rr = row < d.nrows ? row : d.nrows - 1;
+        const int row = (n * C::kRPI + lane / CPR) & (C::kQRows - 1);   // row within the slot
+        const int rq = row + (q_slots(d.nrows) + k) * C::kQRows;        // row within the item
+        const int rr = rq < d.nrows ? rq : d.nrows - 1;
         int fork = 0, hq = 0;
         item_row_fork_head(plan, d.kind, d.t, d.f, d.j, d.row0, rr, &fork, &hq);
         const int chunk = (lane % CPR) ^ swz_q<D>(row);
@@ -374,7 +378,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   int RG = 1, TG = 1, rg = 0, tg = 0, tpg = TT;   // tpg: tokens of a tile per token group
   bool active = false;
 
-  auto begin_item = [&](const Desc& d, int stage) {
+  // q slot qi (of 1 or 2) of an item: sets up the item's wave layout and
+  // clears the accumulators (again at the second q slot, where no tile of the
+  // item has run yet), and the waves whose 32 rows are in this slot read their
+  // Q^T operands from it.
+  auto begin_item = [&](const Desc& d, int stage, int qi) {
     const int nrows = d.nrows;
     constexpr int RS = 16 * NT;
     RG = (nrows + RS - 1) / RS;
@@ -384,13 +392,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     tpg = TT / TG;
     active = wave < RG * TG;
     const SG_LDS uint8_t* qb = (const SG_LDS uint8_t*)lds + stage * C::kStageB;
+    const bool mine = (rg * RS) / C::kQRows == qi;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int row = rg * RS + nt * 16 + ln;
+      const int row = rg * RS + nt * 16 + ln - qi * C::kQRows;   // row within the slot
+      if (mine) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int slot = (ks * 4 + G) ^ swz_q<D>(row);
-        qop[nt][ks] = *reinterpret_cast<const SG_LDS bf16x8*>(qb + row * C::kRowB + slot * 16);
+        for (int ks = 0; ks < KS; ++ks) {
+          const int slot = (ks * 4 + G) ^ swz_q<D>(row);
+          qop[nt][ks] = *reinterpret_cast<const SG_LDS bf16x8*>(qb + row * C::kRowB + slot * 16);
+        }
       }
       m_run[nt] = -INFINITY;
       l_run[nt] = 0.f;
@@ -398,6 +409,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       for (int dt = 0; dt < DT; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
+
 
   // one 32-token slab starting at token sb of the tile in `stage`; `valid` tokens of the tile are real
   auto slab = [&](auto mask_c, int stage, int sb, int valid, int idb) {
@@ -671,20 +683,26 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   };
 
   // ---- the slot loop -------------------------------------------------------------
+  // Slot k of an item: k < 0 its q slots (-q_slots .. -1), then its tiles.
   auto advance = [&](int& ii, int& k, Desc& d) {
     if (k + 1 < d.ntile) {
       ++k;
     } else {
       ++ii;
-      k = -1;
-      if (ii < nitems) d = load_desc(ii);
+      if (ii < nitems) {
+        d = load_desc(ii);
+        k = -q_slots(d.nrows);
+      }
     }
   };
-  int is_ii = 0, is_k = -1, issued = 0;   // next slot to issue
+  Desc is_d = load_desc(0);
+  int S = R;   // slots: each item's q slots, then its tiles
+  for (int ii = 0; ii < nitems; ++ii) S += q_slots(uniform(items[ii * kItemInts + IT_NROWS]));
+  S = uniform(S);
+  int is_ii = 0, is_k = -q_slots(is_d.nrows), issued = 0;   // next slot to issue
   int is_id[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) is_id[b] = 0;
-  Desc is_d = load_desc(0);
   // Vector-memory operations this wave has issued (DMA instructions and
   // partial stores), and the count right after the DMAs of slots s .. s + 3 of
   // iteration s (the slot issued during iteration s is s + 3): vmcnt retires
@@ -712,8 +730,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   if (issued < S) mk0 = issue_next();
   if (issued < S) mk1 = issue_next();
   if (issued < S) mk2 = issue_next();
-  int cp_ii = 0, cp_k = -1;
   Desc cp_d = load_desc(0);
+  int cp_ii = 0, cp_k = -q_slots(cp_d.nrows);
   for (int s = 0; s < S; ++s) {
     // E4M3 converts the next tile during this iteration, so it waits for that slot
     vm_wait_le(uniform(ops - ((FP8 && s + 1 < S) ? mk1 : mk0)));
@@ -721,11 +739,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     if (issued < S) mk3 = issue_next();
     const int stage = s & 3;
     if constexpr (FP8) {
-      if (s + 1 < S && cp_k + 1 < cp_d.ntile) convert_tile((s + 1) & 3);   // slot s + 1 is a tile
+      if (s + 1 < S && cp_k + 1 >= 0 && cp_k + 1 < cp_d.ntile) convert_tile((s + 1) & 3);   // slot s + 1 is a tile
     }
     int st0 = 0;
     if (cp_k < 0) {
-      begin_item(cp_d, stage);
+      begin_item(cp_d, stage, q_slots(cp_d.nrows) + cp_k);
     } else {
       compute_tile(cp_d, cp_k, stage);
       if (cp_k == cp_d.ntile - 1) st0 = uniform(finish_item(cp_d, stage));
@@ -763,5 +781,6 @@ int mfma_tile_cap(int D, bool fp8) {
 }
 int mfma_item_cap() { return bf16k::Cfg<128, false>::kItemCap; }
 int mfma_walk_threads() { return bf16k::Cfg<128, false>::kThreads; }
+int mfma_rows() { return bf16k::Cfg<128, false>::kMaxRows; }
 
 }  // namespace specgen

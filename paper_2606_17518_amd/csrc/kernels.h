@@ -14,6 +14,7 @@ int mfma_tile_tokens(int D, bool fp8);
 int mfma_item_cap();
 int mfma_tile_cap(int D, bool fp8);
 int mfma_walk_threads();
+int mfma_rows();
 // attn_dot.hip
 hipError_t launch_attn_dot_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
 int dot_tile_tokens(int D);

@@ -28,12 +28,12 @@ struct PlanInputs {
   int tile_cap[2];            // max tiles per worker
   int walk_threads[2];        // threads of a parallel walk (0: serial walk, no unit limit)
   int charge[2];              // units in front of every item
-  int wt_rg[2][5];            // units per tile of an item of 1..4 row groups of 32 rows ([0] unused)
+  int wt_rg[2][9];            // units per tile of an item of 1..8 row groups of 32 rows ([0] unused)
 };
 
-// Row groups of 32 rows of an item of `rows` rows (at most 4: row blocks hold
-// at most 128 rows).
-inline int row_groups(int rows) { return rows <= 32 ? 1 : rows <= 64 ? 2 : rows <= 96 ? 3 : 4; }
+// Row groups of 32 rows of an item of `rows` rows (at most 8: row blocks hold
+// at most 256 rows).
+inline int row_groups(int rows) { return rows <= 32 ? 1 : rows >= 225 ? 8 : (rows + 31) / 32; }
 
 constexpr int64_t kAlignFloats = 64;   // 256-byte alignment of workspace regions
 
@@ -92,7 +92,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     pp.slot_rows = in.rbs[X];
     pp.trace_begin = pos;
     pp.charge = in.charge[X];
-    for (int r = 1; r <= 4; ++r)
+    for (int r = 1; r <= 8; ++r)
       if (in.wt_rg[X][r] < 1) SG_FAIL(kPlanInvalid, "unit prices must be positive");
     if (pp.charge < 0) SG_FAIL(kPlanInvalid, "unit prices must be positive");
     pp.wt_suf = in.wt_rg[X][row_groups(std::min(g, pp.rbs))];

@@ -299,20 +299,20 @@ int main(int argc, char** argv) {
     in.suffix_table_off = sto.data();
     in.tt[0] = in.D == 128 ? 64 : 128;
     in.tt[1] = 64;
-    in.rbs[0] = 128;
+    in.rbs[0] = 256;
     in.rbs[1] = 16;
     in.item_cap[0] = in.item_cap[1] = 64;
     // unit prices: the library's (MFMA 8 / 6 / 16, dot 1 / 1 / 1) or random;
     // any positive prices must give a valid split
     const bool lib_prices = U(0, 1) != 0;
     if (lib_prices) {
-      const int mfma_rg[5] = {0, 6, 6, 7, 8};
-      for (int r = 0; r < 5; ++r) { in.wt_rg[0][r] = mfma_rg[r]; in.wt_rg[1][r] = 1; }
+      const int mfma_rg[9] = {0, 6, 6, 7, 8, 11, 12, 12, 13};
+      for (int r = 0; r < 9; ++r) { in.wt_rg[0][r] = mfma_rg[r]; in.wt_rg[1][r] = 1; }
       in.charge[0] = 16;
       in.charge[1] = 1;
     } else {
       for (int X = 0; X < 2; ++X) {
-        for (int r = 0; r < 5; ++r) in.wt_rg[X][r] = U(1, 8);
+        for (int r = 0; r < 9; ++r) in.wt_rg[X][r] = U(1, 16);
         in.charge[X] = U(0, 20);
       }
     }
