@@ -13,7 +13,7 @@
 // A tile of TT tokens is TT/16 such block slices per tensor.
 //
 // Slots.  The worker's range is a sequence of 32 KiB slots: for each item one
-// "q slot" (its query rows, up to 128 x D bf16) followed by its tiles (TT
+// "q slot" per 128 query rows (128 x D bf16 each) followed by its tiles (TT
 // tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
 // stages with three slots in flight.  Every wave moves exactly four 1 KiB
 // pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no VGPR
@@ -25,16 +25,18 @@
 // neither drains them (vmcnt(0)) before LDS reads nor reorders them across
 // the LDS barriers.
 //
-// Rows and tokens.  An item with r rows uses RG = ceil(r / 32) <= 4 row groups
-// of 32 rows and splits each tile's tokens over TG = min(TT/32, 8/RG) token
-// groups: wave w computes row group w % RG over token group w / RG (two waves
-// per SIMD for the 128-row prefix items, so one wave's softmax overlaps the
-// other's MFMAs).  Items with fewer rows pad their last row group; they are
-// bound by their K/V bytes, not by the matrix cores (one wave's dependent
-// chain through a 32-token slab takes about 0.9 us, so a tile is always split
-// over two waves).  At the item's end the token groups are combined through the
-// stage that was just consumed, and token group 0 writes the normalised
-// partial (o, lse).
+// Rows and tokens.  An item with r <= 256 rows uses RG = ceil(r / 32) row
+// groups of 32 rows and splits each tile's tokens over TG = min(TT/32, 8/RG)
+// token groups: wave w computes row group w % RG over token group w / RG (two
+// waves per SIMD for the 128-row prefix items, so one wave's softmax overlaps
+// the other's MFMAs; one token group for 5-8 row groups, where each wave runs
+// both slabs of a tile).  An item of more than 128 rows has two q slots, and a
+// wave reads its Q^T from the one holding its rows.  Items with fewer rows pad
+// their last row group; they are bound by their K/V bytes, not by the matrix
+// cores (one wave's dependent chain through a 32-token slab takes about 0.9
+// us, so their tiles are split over two waves).  At the item's end the token
+// groups are combined through the stage that was just consumed, and token
+// group 0 writes the normalised partial (o, lse).
 //
 // Math per 32-token slab and 16-row N-tile: S^T = K Q^T on
 // v_mfma_f32_16x16x32_bf16 (A = 16 keys x 32 dims from LDS, B = Q^T in

@@ -76,7 +76,7 @@ struct PlanHead {
 };
 
 // The whole plan, computed on the host from the length mirrors and passed to
-// every kernel by value (about 7.3 KB of kernel arguments); each workgroup
+// every kernel by value (about 7.4 KB of kernel arguments); each workgroup
 // copies it into LDS with one vector load per thread (plan_to_lds).
 struct alignas(16) Plan : PlanHead {
   int32_t fork_off[kMaxTraces + 1];
