@@ -28,6 +28,11 @@ SMALL = [
     ([3, 70, 16], [1, 3, 2], [2, 0, 40, 17, 1, 16], 8, 2, 64, "bf16"),  # three traces
     ([300], 4, [0, 3, 33, 70], 16, 2, 128, "fp8_e4m3"),
     ([65, 190], [2, 3], [1, 0, 16, 17, 80], 32, 8, 64, "fp8_e4m3"),
+    # items of more than 128 rows: two q slots, one token group per wave
+    ([300], 16, list(range(0, 320, 20)), 256, 16, 128, "bf16"),      # r = 256: 8 row groups
+    ([200], 12, [3, 64, 65, 0, 7, 128, 1, 33, 90, 2, 15, 16], 240, 16, 64, "bf16"),  # r = 180, D = 64
+    ([500], 16, list(range(5, 165, 10)), 256, 16, 128, "fp8_e4m3"),  # r = 256 with E4M3
+    ([130], 20, [1] * 20, 160, 8, 64, "fp8_e4m3"),                   # r = 400: row blocks of 256 and 144
 ]
 
 
