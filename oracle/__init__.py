@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for SpecGen's fork-decode attention, LSE merge and KV import.
+"""fp64 CPU oracle for SpecGen's fork-decode attention, LSE merge, KV import/export and append.
 
 TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
 benchmark's ``cpu_baseline`` leg are the only users.  The product library
@@ -68,6 +68,11 @@ def _load():
             lib.specgen_ref_lse_merge.restype = None
             lib.specgen_ref_kv_import.argtypes = [P, P, C.c_int64, P, C.c_int64, C.c_int64]
             lib.specgen_ref_kv_import.restype = C.c_int64
+            lib.specgen_ref_kv_export.argtypes = [P, P, C.c_int64, P, C.c_int64, C.c_int64]
+            lib.specgen_ref_kv_export.restype = C.c_int64
+            lib.specgen_ref_kv_append.argtypes = [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                                  P, P, P, C.c_int64]
+            lib.specgen_ref_kv_append.restype = C.c_int64
             lib.specgen_ref_decode_bf16.argtypes = [P, C.c_int64, P]
             lib.specgen_ref_decode_e4m3.argtypes = [P, C.c_int64, P]
             lib.specgen_ref_max_threads.restype = C.c_int32
@@ -193,3 +198,36 @@ def kv_import(dst_pool: np.ndarray, src: np.ndarray, block_bytes: int, dst_ids, 
     ids = _c(dst_ids, np.int32)
     return int(_load().specgen_ref_kv_import(_ptr(dst_pool), _ptr(s), int(block_bytes), _ptr(ids),
                                              ids.size, int(num_dst_blocks)))
+
+
+def kv_export(staging: np.ndarray, pool: np.ndarray, block_bytes: int, src_ids, num_src_blocks: int) -> int:
+    """Naive block gather, in place on ``staging`` (uint8, contiguous): staging
+    block i receives pool block src_ids[i].  Returns the number of skipped ids."""
+    assert staging.dtype == np.uint8 and staging.flags.c_contiguous
+    p = _c(pool, np.uint8)
+    ids = _c(src_ids, np.int32)
+    return int(_load().specgen_ref_kv_export(_ptr(staging), _ptr(p), int(block_bytes), _ptr(ids),
+                                             ids.size, int(num_src_blocks)))
+
+
+def kv_append(k_pool: np.ndarray, v_pool: np.ndarray, k_new, v_new, pos, suffix_table_off, suffix_table,
+              num_kv_heads: int, head_dim: int) -> int:
+    """Write each fork's new token into its suffix blocks, in place on the pools.
+
+    Pools are contiguous arrays of 1- or 2-byte elements (uint8 codes or uint16
+    bf16 bits) holding num_blocks * Hkv * 16 * D elements; k_new / v_new are
+    [N][Hkv][D] of the same element type.  Returns the number of skipped forks."""
+    assert k_pool.dtype == v_pool.dtype and k_pool.flags.c_contiguous and v_pool.flags.c_contiguous
+    es = k_pool.dtype.itemsize
+    assert es in (1, 2)
+    kn = _c(k_new, k_pool.dtype)
+    vn = _c(v_new, k_pool.dtype)
+    pos = _c(pos, np.int32)
+    off = _c(suffix_table_off, np.int32)
+    tab = _c(suffix_table if suffix_table is not None and np.size(suffix_table) else np.zeros(1, np.int32), np.int32)
+    n = pos.size
+    assert kn.size == vn.size == n * num_kv_heads * head_dim and off.size == n + 1
+    nblocks = k_pool.size // (num_kv_heads * 16 * head_dim)
+    return int(_load().specgen_ref_kv_append(_ptr(k_pool), _ptr(v_pool), _ptr(kn), _ptr(vn), es, n,
+                                             int(num_kv_heads), int(head_dim), _ptr(pos), _ptr(off), _ptr(tab),
+                                             nblocks))

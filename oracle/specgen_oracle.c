@@ -1,6 +1,7 @@
 /*
  * specgen_oracle.c -- plain fp64 CPU oracle for fork-decode attention, the
- * log-sum-exp merge and the KV-block import of SpecGen (arXiv 2606.17518).
+ * log-sum-exp merge, the KV-block import and export and the per-step append
+ * of SpecGen (arXiv 2606.17518).
  *
  * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
  * benchmark's CPU-baseline leg may load this library.  The HIP library never
@@ -17,7 +18,9 @@
  * The paper states no attention formula, no KV layout and no numeric format.
  * This oracle therefore takes the plain definition of single-query softmax
  * attention over the logically ordered keys (prefix tokens, then the fork's
- * own suffix tokens), evaluated in fp64, and a byte-for-byte block copy.
+ * own suffix tokens), evaluated in fp64, byte-for-byte block copies in both
+ * directions, and an element copy of each fork's new token into the paged
+ * layout.
  * The conventions it fixes where the paper is silent (GQA grouping, natural
  * log LSE, paged layout [block][slot][kv_head][dim], OCP E4M3 decode, a
  * block-wide fp32 dequantisation scale) are listed with the header that
@@ -266,6 +269,71 @@ int64_t specgen_ref_kv_import(uint8_t *dst_pool, const uint8_t *src, int64_t blo
       continue;
     }
     memcpy(dst_pool + id * block_bytes, src + i * block_bytes, (size_t)block_bytes);
+  }
+  return bad;
+}
+
+/* ---- KV-block export (migration to the remote cache) --------------------- */
+
+/* The direction opposite to the import: suspending a prefix moves its KV
+ * state out of the serving cache into spare memory (Sec. 6.2.3).  Pool block
+ * src_ids[i] is copied to staging block i; ids outside [0, num_src_blocks)
+ * are skipped and leave staging block i as it was.  Returns the number of
+ * skipped ids. */
+int64_t specgen_ref_kv_export(uint8_t *staging, const uint8_t *pool, int64_t block_bytes,
+                              const int32_t *src_ids, int64_t n, int64_t num_src_blocks) {
+  int64_t bad = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t id = src_ids[i];
+    if (id < 0 || id >= num_src_blocks) {
+      ++bad;
+      continue;
+    }
+    memcpy(staging + i * block_bytes, pool + id * block_bytes, (size_t)block_bytes);
+  }
+  return bad;
+}
+
+/* ---- Per-step append of each fork's new token ----------------------------- */
+
+/* Every decode step of a fork adds one token to its private continuation,
+ * whose KV is kept after the shared reasoning prefix (Sec. 4.2; Sec. 8.7,
+ * prefix caching paragraph).  Fork f's new token takes logical suffix
+ * position pos[f]: block suffix_table[suffix_table_off[f] + pos[f] / 16],
+ * slot pos[f] % 16 (a position that is a multiple of 16 opens the next block
+ * of the fork's table).  For kv head j and dim d, with element size es bytes:
+ *   K pool byte offset ((b*Hkv + j)*16 + slot)*D + d   (times es)
+ *   V pool byte offset ((b*Hkv + j)*D + d)*16 + slot   (times es)
+ * receive k_new[f][j][d] and v_new[f][j][d].  A fork whose position has no
+ * table entry, or whose block id lies outside [0, num_blocks), is skipped.
+ * Returns the number of skipped forks. */
+int64_t specgen_ref_kv_append(uint8_t *k_pool, uint8_t *v_pool, const uint8_t *k_new,
+                              const uint8_t *v_new, int32_t es, int32_t N, int32_t Hkv, int32_t D,
+                              const int32_t *pos, const int32_t *suffix_table_off,
+                              const int32_t *suffix_table, int64_t num_blocks) {
+  int64_t bad = 0;
+  for (int32_t f = 0; f < N; ++f) {
+    const int32_t p = pos[f];
+    const int32_t nb = suffix_table_off[f + 1] - suffix_table_off[f];
+    if (p < 0 || p / 16 >= nb) {
+      ++bad;
+      continue;
+    }
+    const int64_t b = suffix_table[suffix_table_off[f] + p / 16];
+    if (b < 0 || b >= num_blocks) {
+      ++bad;
+      continue;
+    }
+    const int64_t slot = p % 16;
+    for (int32_t j = 0; j < Hkv; ++j) {
+      for (int32_t d = 0; d < D; ++d) {
+        const int64_t src = ((int64_t)f * Hkv + j) * D + d;
+        const int64_t ko = ((b * Hkv + j) * 16 + slot) * D + d;
+        const int64_t vo = ((b * Hkv + j) * D + d) * 16 + slot;
+        memcpy(k_pool + ko * es, k_new + src * es, (size_t)es);
+        memcpy(v_pool + vo * es, v_new + src * es, (size_t)es);
+      }
+    }
   }
   return bad;
 }

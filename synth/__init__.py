@@ -6,8 +6,8 @@ Table "tab:token_overhead" implies roughly 24k tokens per iteration).  The
 paper's own workloads (LLM reasoning traces over KernelBench tasks) are not
 reproduced; these synthetic tensors have the shapes of such caches.
 """
-from .fork_batch import (BLOCK, ForkBatch, ImportCase, make_fork_batch, make_import_case,
-                         prefix_import_from_batch, SENTINEL)
+from .fork_batch import (BLOCK, AppendCase, ForkBatch, ImportCase, make_append_case, make_fork_batch,
+                         make_import_case, prefix_import_from_batch, SENTINEL)
 
 # name -> (fork-batch keyword arguments, import description or None)
 WORKLOADS = {

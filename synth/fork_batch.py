@@ -296,3 +296,69 @@ def prefix_import_from_batch(batch: ForkBatch, trace: int = 0):
         kss = np.ascontiguousarray(batch.k_scale[ids])
         vss = np.ascontiguousarray(batch.v_scale[ids])
     return ks, vs, ids.astype(np.int32), kss, vss
+
+
+# ---- per-step append workloads -------------------------------------------------
+
+@dataclasses.dataclass
+class AppendCase:
+    num_kv_heads: int
+    head_dim: int
+    elem_dtype: type            # np.uint16 (bf16 bits) or np.uint8 (E4M3 codes)
+    k_new: np.ndarray           # [N][Hkv][D]
+    v_new: np.ndarray
+    pos: np.ndarray             # int32 [N], the suffix slot each new token takes
+    suffix_table_off: np.ndarray  # int32 [N+1]
+    suffix_table: np.ndarray      # int32
+
+    @property
+    def num_forks(self) -> int:
+        return int(self.pos.size)
+
+    def algorithmic_bytes(self) -> int:
+        """New K and V read once and written once, positions, offsets and one
+        table entry per fork."""
+        e = np.dtype(self.elem_dtype).itemsize
+        return 2 * 2 * self.k_new.size * e + 4 * (2 * self.num_forks + 1) + 4 * self.num_forks
+
+
+def make_append_case(batch: ForkBatch, seed: int = 0, bad_forks: Sequence[int] = ()) -> AppendCase:
+    """The next decode token of every fork of ``batch``: random K/V elements,
+    position = the current suffix length, and the batch's suffix tables with a
+    fresh block (a pool block no table uses) appended for every fork whose
+    suffix length is a multiple of 16.  ``bad_forks`` get a position past
+    their table (alternately) or a table entry outside the pool."""
+    rng = np.random.default_rng(seed)
+    N, Hkv, D = batch.num_forks, batch.num_kv_heads, batch.head_dim
+    fp8 = batch.kv_dtype != "bf16"
+    el = np.uint8 if fp8 else np.uint16
+    if fp8:
+        k_new = _to_e4m3_codes(rng.uniform(-448, 448, size=(N, Hkv, D)).astype(np.float32))
+        v_new = _to_e4m3_codes(rng.uniform(-448, 448, size=(N, Hkv, D)).astype(np.float32))
+    else:
+        k_new = _to_bf16_bits(rng.standard_normal((N, Hkv, D), dtype=np.float32))
+        v_new = _to_bf16_bits(rng.standard_normal((N, Hkv, D), dtype=np.float32))
+    used = np.zeros(batch.num_blocks, bool)
+    used[batch.prefix_table] = True
+    used[batch.suffix_table] = True
+    free = rng.permutation(np.flatnonzero(~used))
+    pos = batch.suffix_len.astype(np.int64).copy()
+    off = np.zeros(N + 1, np.int64)
+    table = []
+    nfree = 0
+    for f in range(N):
+        ids = list(batch.suffix_table[batch.suffix_table_off[f]:batch.suffix_table_off[f + 1]])
+        if pos[f] % BLOCK == 0:
+            assert nfree < free.size, "pool has no free block for a fresh suffix block"
+            ids.append(int(free[nfree]))
+            nfree += 1
+        table += ids
+        off[f + 1] = off[f] + len(ids)
+    table = np.asarray(table, np.int64)
+    for k, f in enumerate(bad_forks):
+        if k % 2 == 0:
+            pos[f] = (off[f + 1] - off[f]) * BLOCK        # no table entry for this position
+        else:
+            table[off[f] + pos[f] // BLOCK] = batch.num_blocks + f
+    i32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+    return AppendCase(Hkv, D, el, k_new, v_new, i32(pos), i32(off), i32(table))

@@ -322,3 +322,137 @@ def test_import_is_blockwise_memcpy_with_bad_ids_skipped():
         assert np.array_equal(pool, ref.reshape(-1))
         untouched = np.setdiff1d(np.arange(case.num_dst_blocks), case.dst_ids[ok])
         assert np.all(pool.reshape(case.num_dst_blocks, -1)[untouched] == synth.SENTINEL)
+
+
+# ---- KV-block export -------------------------------------------------------------
+
+def test_export_is_blockwise_gather_with_bad_ids_skipped():
+    case = synth.make_import_case(n=12, num_dst_blocks=40, block_bytes=96, num_tensors=1, seed=6, bad_ids=[0, 11])
+    pool = np.random.default_rng(1).integers(0, 256, size=40 * 96, dtype=np.uint8)
+    staging = np.full(12 * 96, synth.SENTINEL, np.uint8)
+    assert oracle.kv_export(staging, pool, 96, case.dst_ids, 40) == 2
+    st = staging.reshape(12, 96)
+    pb = pool.reshape(40, 96)
+    for i, bid in enumerate(case.dst_ids):
+        if 0 <= bid < 40:
+            assert np.array_equal(st[i], pb[bid])
+        else:
+            assert np.all(st[i] == synth.SENTINEL)
+
+
+def test_export_then_import_restores_the_blocks():
+    """A suspended prefix moved out and restored into other pool blocks holds
+    the same bytes: import(export(pool, ids), new_ids) moves block ids[i] to
+    new_ids[i]."""
+    rng = np.random.default_rng(9)
+    nb, bb, n = 64, 512, 20
+    pool = rng.integers(0, 256, size=nb * bb, dtype=np.uint8)
+    ids = rng.permutation(nb)[:n].astype(np.int32)
+    new_ids = rng.permutation(nb)[:n].astype(np.int32)
+    staging = np.zeros(n * bb, np.uint8)
+    assert oracle.kv_export(staging, pool, bb, ids, nb) == 0
+    dst = np.zeros(nb * bb, np.uint8)
+    assert oracle.kv_import(dst, staging, bb, new_ids, nb) == 0
+    for a, b in zip(ids, new_ids):
+        assert np.array_equal(dst[b * bb:(b + 1) * bb], pool[a * bb:(a + 1) * bb])
+
+
+# ---- per-step append -------------------------------------------------------------
+
+def _replay_suffixes(b):
+    """Rebuild every fork's suffix in a NaN-filled copy of the pools by
+    appending its logical tokens one decode step at a time (positions 0..S-1,
+    all forks in one call per step)."""
+    el = b.k_pool.dtype
+    k = np.full_like(b.k_pool, 0xFF if el == np.uint8 else 0x7FC0)
+    v = np.full_like(b.v_pool, 0xFF if el == np.uint8 else 0x7FC0)
+    # the prefixes are not under test: copy them over
+    for t in range(b.num_traces):
+        ids = b.prefix_table[b.prefix_table_off[t]:b.prefix_table_off[t + 1]]
+        k[ids] = b.k_pool[ids]
+        v[ids] = b.v_pool[ids]
+    N, Hkv, D = b.num_forks, b.num_kv_heads, b.head_dim
+    for step in range(int(b.suffix_len.max())):
+        live = [f for f in range(N) if step < b.suffix_len[f]]
+        kn = np.stack([b.k_logical[b.num_traces + f][step] for f in live])
+        vn = np.stack([b.v_logical[b.num_traces + f][step] for f in live])
+        off = np.zeros(len(live) + 1, np.int32)
+        tab = []
+        for i, f in enumerate(live):
+            ids = b.suffix_table[b.suffix_table_off[f]:b.suffix_table_off[f + 1]]
+            tab += list(ids)
+            off[i + 1] = off[i] + len(ids)
+        assert oracle.kv_append(k, v, kn, vn, np.full(len(live), step, np.int32), off, np.asarray(tab, np.int32),
+                                Hkv, D) == 0
+    return k, v
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_append_rebuilds_the_paged_suffixes(kv):
+    """Appending a fork's logical tokens one step at a time reproduces the
+    paged layout that the workload generator writes directly (token-major
+    draw, then transposed into [block][Hkv][16][D] and [block][Hkv][D][16]),
+    at every valid suffix slot, and crosses 16-token block boundaries."""
+    b = synth.make_fork_batch(prefix_lens=[40], forks_per_trace=3, suffix_lens=[1, 16, 37], num_q_heads=4,
+                              num_kv_heads=2, head_dim=16, kv_dtype=kv, seed=21, keep_logical=True)
+    k, v = _replay_suffixes(b)
+    for f in range(b.num_forks):
+        ids = b.suffix_table[b.suffix_table_off[f]:b.suffix_table_off[f + 1]]
+        S = int(b.suffix_len[f])
+        for i, bid in enumerate(ids):
+            n = min(16, S - 16 * i)
+            assert np.array_equal(k[bid][:, :n, :], b.k_pool[bid][:, :n, :])
+            assert np.array_equal(v[bid][:, :, :n], b.v_pool[bid][:, :, :n])
+
+
+def test_append_then_attend_matches_dense_attention():
+    """After the suffixes are rebuilt by appends, fork attention over the pool
+    equals dense attention over the logical prefix + suffix sequence."""
+    b = synth.make_fork_batch(prefix_lens=[50], forks_per_trace=3, suffix_lens=[5, 16, 33], num_q_heads=4,
+                              num_kv_heads=2, head_dim=16, seed=22, keep_logical=True)
+    k, v = _replay_suffixes(b)
+    import copy
+    b2 = copy.copy(b)
+    b2.k_pool, b2.v_pool = k, v
+    o, lse = oracle.fork_decode_attn(b2)
+    G = b.group
+    for f in range(b.num_forks):
+        Kf = oracle.bf16_to_f64(np.concatenate([b.k_logical[0], b.k_logical[1 + f]]))
+        Vf = oracle.bf16_to_f64(np.concatenate([b.v_logical[0], b.v_logical[1 + f]]))
+        for h in range(b.num_q_heads):
+            qd = oracle.bf16_to_f64(b.q[f, h])
+            s = (Kf[:, h // G, :] @ qd) * b.sm_scale
+            m = s.max()
+            w = np.exp(s - m)
+            ref = (w[:, None] * Vf[:, h // G, :]).sum(0) / w.sum()
+            np.testing.assert_allclose(o[f, h], ref, rtol=0, atol=1e-12)
+            assert abs(lse[f, h] - (m + math.log(w.sum()))) < 1e-12
+
+
+def test_append_fresh_block_and_bad_forks():
+    """A fork at a 16-token boundary writes slot 0 of the fresh block listed
+    after its table; forks without a table entry for their position or with an
+    id outside the pool are skipped, counted, and leave the pools unchanged."""
+    b = synth.make_fork_batch(prefix_lens=[20], forks_per_trace=5, suffix_lens=[0, 16, 5, 32, 9], num_q_heads=4,
+                              num_kv_heads=2, head_dim=16, seed=23)
+    case = synth.make_append_case(b, seed=2, bad_forks=[2, 4])
+    k, v = b.k_pool.copy(), b.v_pool.copy()
+    bad = oracle.kv_append(k, v, case.k_new, case.v_new, case.pos, case.suffix_table_off, case.suffix_table,
+                           b.num_kv_heads, b.head_dim)
+    assert bad == 2
+    changed = set()
+    for f in range(b.num_forks):
+        p = int(case.pos[f])
+        if f in (2, 4):
+            continue
+        bid = int(case.suffix_table[case.suffix_table_off[f] + p // 16])
+        if p % 16 == 0:  # the fresh block was appended by the case generator
+            assert case.suffix_table_off[f + 1] - case.suffix_table_off[f] == p // 16 + 1
+        assert np.array_equal(k[bid][:, p % 16, :], case.k_new[f])
+        assert np.array_equal(v[bid][:, :, p % 16], case.v_new[f])
+        changed.add(bid)
+    mask = np.ones(b.num_blocks, bool)
+    mask[list(changed)] = False
+    assert np.array_equal(k[mask], b.k_pool[mask]) and np.array_equal(v[mask], b.v_pool[mask])
+    for bid in changed:
+        assert (k[bid] != b.k_pool[bid]).sum() <= b.num_kv_heads * b.head_dim
