@@ -13,7 +13,10 @@ was restored R-1 steps earlier.
 Prints one JSON line.  `value` is the attention call's achieved HBM rate in
 GB/s: algorithmic bytes (each valid prefix token's K/V once per kv head, each
 suffix token's K/V once, q in, out/lse out, index arrays) over the average
-attention time measured with HIP events on the launch stream.
+attention time measured with HIP events on the launch stream.  The export of
+the same prefix blocks (specgen_kv_export) and the per-step append of every
+fork's next token (specgen_kv_append) are timed on their own and reported
+beside the import; they are not part of `value`.
 """
 from __future__ import annotations
 
@@ -199,6 +202,52 @@ def main():
     torch.cuda.synchronize()
     part_ms = np.array([e[1].elapsed_time(e[2]) for e in sevents])
     merge_ms = np.array([e[2].elapsed_time(e[3]) for e in sevents])
+    # the steps on either side of the restore, each timed on its own: export
+    # (the prefix blocks migrate out to staging, the reverse of the import)
+    # and append (every fork's next token written into its suffix blocks at
+    # slot S_f, a fresh block where S_f is a multiple of 16; the suffix
+    # lengths the attention reads are unchanged, so its inputs stay valid)
+    moves = {}
+    if imp is not None:
+        log(f"timing {args.steps} exports")
+        exp = [[(st, pl, bb_) for (pl, st, bb_) in tensors] for tensors in imp]
+        xevents = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        torch.cuda._sleep(SPIN_CYCLES)
+        for k in range(args.steps):
+            xevents[k][0].record(stream)
+            sg.specgen_kv_export(exp[k % R], ids_d, b.num_blocks, stream=stream)
+            xevents[k][1].record(stream)
+        torch.cuda.synchronize()
+        assert torch.equal(imp[0][0][1], torch.from_numpy(ks.reshape(-1).view(np.uint8)).to(dev)), "export mismatch"
+        exp_ms = np.array([e[0].elapsed_time(e[1]) for e in xevents])
+        moves["export"] = {"blocks": int(len(ids)), "bytes": int(import_bytes),
+                           "us": round(float(exp_ms.mean()) * 1e3, 2),
+                           "gbps": round(import_bytes / (float(exp_ms.mean()) / 1e3) / 1e9, 2)}
+    try:
+        app = synth.make_append_case(b, seed=1)
+    except AssertionError:      # the pool has no free block for a fork at a block boundary
+        app = None
+    if app is not None:
+        log(f"timing {args.steps} appends")
+        el = torch.uint8 if b.kv_dtype != "bf16" else torch.int16
+        kvdt = sg.SPECGEN_FP8_E4M3 if b.kv_dtype != "bf16" else sg.SPECGEN_BF16
+        a_dev = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in
+                 (app.k_new, app.v_new, app.pos, app.suffix_table_off, app.suffix_table)]
+        a_dev[0], a_dev[1] = a_dev[0].view(el), a_dev[1].view(el)
+        aevents = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        torch.cuda._sleep(SPIN_CYCLES)
+        for k in range(args.steps):
+            fb = reps[k % R]
+            aevents[k][0].record(stream)
+            sg.specgen_kv_append(fb.k_pool, fb.v_pool, *a_dev, b.num_kv_heads, D, kv_dtype=kvdt,
+                                 num_blocks=b.num_blocks, stream=stream)
+            aevents[k][1].record(stream)
+        torch.cuda.synchronize()
+        app_ms = np.array([e[0].elapsed_time(e[1]) for e in aevents])
+        app_bytes = app.algorithmic_bytes()
+        moves["append"] = {"forks": N, "fresh_blocks": int(app.fresh_blocks.size), "bytes": int(app_bytes),
+                           "us": round(float(app_ms.mean()) * 1e3, 2),
+                           "gbps": round(app_bytes / (float(app_ms.mean()) / 1e3) / 1e9, 2)}
     attn_bytes = b.algorithmic_bytes()
     out_bytes = N * Hq * (D * 2 + 4)
     kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
@@ -244,6 +293,7 @@ def main():
     if imp is not None:
         res["import"] = {"blocks": int(len(ids)), "bytes": int(import_bytes), "us": round(float(imp_ms.mean()) * 1e3, 2),
                          "gbps": round(import_bytes / (float(imp_ms.mean()) / 1e3) / 1e9, 2)}
+    res.update(moves)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)

@@ -1,6 +1,6 @@
 /*
- * specgen.h -- C ABI of the MI355X (gfx950) fork-decode attention and
- * KV-block import library behind SpecGen's speculative generation
+ * specgen.h -- C ABI of the MI355X (gfx950) fork-decode attention, KV-block
+ * import/export and per-step append library behind SpecGen's speculative generation
  * (arXiv 2606.17518).
  *
  * The paper forks non-reasoning generations off a long reasoning trace; every
@@ -172,6 +172,67 @@ specgen_status_t specgen_kv_import(const specgen_kv_tensor_t *tensors, int32_t n
                                    const int32_t *dst_block_ids, int64_t n,
                                    int64_t num_dst_blocks, int32_t *bad_id_count,
                                    hipStream_t stream);
+
+/* One tensor of a KV-block export: src_pool is [num_src_blocks][block_bytes],
+ * dst_staging is [n][block_bytes] contiguous (the copy a remote cache keeps). */
+typedef struct {
+  void *dst_staging;
+  const void *src_pool;
+  int64_t block_bytes;       /* as for specgen_kv_tensor_t                      */
+} specgen_kv_export_tensor_t;
+
+/* KV-block export (migration of a suspended prefix out of the serving cache,
+ * Sec. 6.2.3; the reverse of specgen_kv_import): for every tensor and every
+ * i < n, copy pool block src_block_ids[i] to staging block i, byte for byte.
+ * Ids outside [0, num_src_blocks) are skipped (staging block i keeps its
+ * bytes) and, if bad_id_count is not NULL, counted there (device int32,
+ * incremented, not reset).  Repeated source ids are allowed.  Staging and
+ * pool must not overlap.
+ *   tensors: host array of 1..4 descriptors.
+ *   src_block_ids: device int32 [n].  n >= 0 (0 queues nothing). */
+specgen_status_t specgen_kv_export(const specgen_kv_export_tensor_t *tensors, int32_t num_tensors,
+                                   const int32_t *src_block_ids, int64_t n,
+                                   int64_t num_src_blocks, int32_t *bad_id_count,
+                                   hipStream_t stream);
+
+/* One decode step's new K/V token for each of N forks. */
+typedef struct {
+  int32_t num_forks;         /* N >= 0 (0 queues nothing)                        */
+  int32_t num_kv_heads;      /* Hkv >= 1                                         */
+  int32_t head_dim;          /* D: 1..1024                                       */
+  int32_t kv_dtype;          /* SPECGEN_BF16 or SPECGEN_FP8_E4M3 (element size
+                                2 or 1 byte; elements are copied as bits)        */
+  int64_t num_blocks;        /* pool capacity in blocks (>= 1)                   */
+  /* device memory, caller-owned */
+  void *k_pool;              /* [num_blocks][Hkv][16][D]                         */
+  void *v_pool;              /* [num_blocks][Hkv][D][16] (transposed)            */
+  const void *k_new;         /* [N][Hkv][D], the new token's K per kv head       */
+  const void *v_new;         /* [N][Hkv][D]                                      */
+  const int32_t *pos;        /* [N], the suffix position each token takes: the
+                                fork's suffix length before this step            */
+  const int32_t *suffix_table_off; /* [N+1], nondecreasing                       */
+  const int32_t *suffix_table;     /* fork f's ids are
+                                suffix_table[suffix_table_off[f] ..
+                                suffix_table_off[f+1]) in logical order          */
+  int32_t *bad_count;        /* device int32 or NULL: forks skipped              */
+} specgen_kv_append_t;
+
+/* Per-step append (each fork's continuation grows by one token per decode
+ * step after the shared prefix, Sec. 4.2; Sec. 8.7, prefix caching
+ * paragraph): for every fork f, kv head j and dim d,
+ *   b = suffix_table[suffix_table_off[f] + pos[f]/16], t = pos[f] % 16,
+ *   K element (b, j, t, d) = k_new[f][j][d],  V element (b, j, d, t) = v_new[f][j][d]
+ * in the layout of the fork batch.  A position that is a multiple of 16 opens
+ * a fresh block: the caller lists it at the end of the fork's table first
+ * (block allocation is the caller's).  A fork with pos < 0, with no table
+ * entry for pos/16, or whose block id lies outside [0, num_blocks) is skipped
+ * and, if bad_count is not NULL, counted (incremented, not reset).  Only the
+ * listed elements are written.  E4M3 elements are copied as codes: they must
+ * already be encoded with the target block's scale, which the caller owns and
+ * sets for a fresh block.  Two forks writing the same (block, slot) race.
+ * After the call, a fork batch with S_f = pos[f] + 1 attends over the new
+ * token. */
+specgen_status_t specgen_kv_append(const specgen_kv_append_t *a, hipStream_t stream);
 
 /* Log-sum-exp merge of S partial attention results over disjoint key sets:
  *   M = max_s lse[s][r]; w_s = exp(lse[s][r] - M);

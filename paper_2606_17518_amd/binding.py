@@ -26,7 +26,7 @@ PATHS = {"auto": SPECGEN_PATH_AUTO, "dot": SPECGEN_PATH_DOT, "mfma": SPECGEN_PAT
 SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
 
 EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
-            "specgen_kv_import", "specgen_lse_merge", "specgen_last_error")
+            "specgen_kv_import", "specgen_kv_export", "specgen_kv_append", "specgen_lse_merge", "specgen_last_error")
 
 
 class SpecgenError(RuntimeError):
@@ -55,6 +55,20 @@ class KvTensorC(C.Structure):
     _fields_ = [("dst_pool", C.c_void_p), ("src_staging", C.c_void_p), ("block_bytes", C.c_int64)]
 
 
+class KvExportTensorC(C.Structure):
+    _fields_ = [("dst_staging", C.c_void_p), ("src_pool", C.c_void_p), ("block_bytes", C.c_int64)]
+
+
+class KvAppendC(C.Structure):
+    _fields_ = [
+        ("num_forks", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("kv_dtype", C.c_int32),
+        ("num_blocks", C.c_int64),
+        ("k_pool", C.c_void_p), ("v_pool", C.c_void_p), ("k_new", C.c_void_p), ("v_new", C.c_void_p),
+        ("pos", C.c_void_p), ("suffix_table_off", C.c_void_p), ("suffix_table", C.c_void_p),
+        ("bad_count", C.c_void_p),
+    ]
+
+
 _lib = None
 
 
@@ -74,6 +88,10 @@ def lib():
         L.specgen_fork_decode_attn_phase.restype = C.c_int
         L.specgen_kv_import.argtypes = [C.POINTER(KvTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
         L.specgen_kv_import.restype = C.c_int
+        L.specgen_kv_export.argtypes = [C.POINTER(KvExportTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
+        L.specgen_kv_export.restype = C.c_int
+        L.specgen_kv_append.argtypes = [C.POINTER(KvAppendC), P]
+        L.specgen_kv_append.restype = C.c_int
         L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
         L.specgen_lse_merge.restype = C.c_int
         L.specgen_last_error.argtypes = []
@@ -217,6 +235,35 @@ def specgen_kv_import(tensors: Sequence[tuple], dst_block_ids: torch.Tensor, num
         arr[i].block_bytes = int(bb)
     _check(lib().specgen_kv_import(arr, len(tensors), _dptr(dst_block_ids), int(dst_block_ids.numel()),
                                    int(num_dst_blocks), _dptr(bad_id_count), _stream(stream)))
+
+
+def specgen_kv_export(tensors: Sequence[tuple], src_block_ids: torch.Tensor, num_src_blocks: int,
+                      bad_id_count: Optional[torch.Tensor] = None, stream=None) -> None:
+    """tensors: sequence of (dst_staging tensor, src_pool tensor, block_bytes)."""
+    arr = (KvExportTensorC * max(1, len(tensors)))()
+    for i, (dst, src, bb) in enumerate(tensors):
+        arr[i].dst_staging = dst.data_ptr()
+        arr[i].src_pool = src.data_ptr()
+        arr[i].block_bytes = int(bb)
+    _check(lib().specgen_kv_export(arr, len(tensors), _dptr(src_block_ids), int(src_block_ids.numel()),
+                                   int(num_src_blocks), _dptr(bad_id_count), _stream(stream)))
+
+
+def specgen_kv_append(k_pool: torch.Tensor, v_pool: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                      pos: torch.Tensor, suffix_table_off: torch.Tensor, suffix_table: torch.Tensor,
+                      num_kv_heads: int, head_dim: int, kv_dtype: int = SPECGEN_BF16, num_blocks: Optional[int] = None,
+                      bad_count: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Pools: device tensors of 2-byte (bf16) or 1-byte (E4M3) elements; k_new,
+    v_new: [N][Hkv][D] of the same element size; pos, offsets, table: int32."""
+    es = 2 if kv_dtype == SPECGEN_BF16 else 1
+    if num_blocks is None:
+        num_blocks = k_pool.numel() * k_pool.element_size() // (num_kv_heads * 16 * head_dim * es)
+    a = KvAppendC(num_forks=int(pos.numel()), num_kv_heads=int(num_kv_heads), head_dim=int(head_dim),
+                  kv_dtype=int(kv_dtype), num_blocks=int(num_blocks), k_pool=k_pool.data_ptr(),
+                  v_pool=v_pool.data_ptr(), k_new=k_new.data_ptr(), v_new=v_new.data_ptr(), pos=pos.data_ptr(),
+                  suffix_table_off=suffix_table_off.data_ptr(), suffix_table=suffix_table.data_ptr(),
+                  bad_count=None if bad_count is None else bad_count.data_ptr())
+    _check(lib().specgen_kv_append(C.byref(a), _stream(stream)))
 
 
 def specgen_lse_merge(o_parts: torch.Tensor, lse_parts: torch.Tensor, out: torch.Tensor,

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
-SOURCES = ["abi.hip", "attn_bf16.hip", "attn_dot.hip", "merge.hip", "kv_import.hip"]
+SOURCES = ["abi.hip", "attn_bf16.hip", "attn_dot.hip", "merge.hip", "kv_import.hip", "kv_append.hip"]
 # Per-source device flags: the bf16 attention kernel keeps MFMA accumulators in
 # VGPRs and runs without IEEE-mode NaN quieting (masked scores are -inf, never NaN).
 EXTRA_FLAGS = {"attn_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mno-amdgpu-ieee", "-fno-honor-nans"]}

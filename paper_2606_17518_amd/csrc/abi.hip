@@ -180,7 +180,7 @@ specgen_status_t specgen_kv_import(const specgen_kv_tensor_t* tensors, int32_t n
   if (n < 0 || n > INT32_MAX) return fail(SPECGEN_ERR_INVALID_ARG, "n %lld out of range", (long long)n);
   if (num_dst_blocks < 0) return fail(SPECGEN_ERR_INVALID_ARG, "num_dst_blocks must be >= 0");
   if (n > 0 && !dst_block_ids) return fail(SPECGEN_ERR_INVALID_ARG, "dst_block_ids is NULL");
-  ImportArgs a;
+  BlockCopyArgs a;
   std::memset(&a, 0, sizeof a);
   for (int i = 0; i < num_tensors; ++i) {
     const specgen_kv_tensor_t& t = tensors[i];
@@ -191,16 +191,86 @@ specgen_status_t specgen_kv_import(const specgen_kv_tensor_t* tensors, int32_t n
     const uintptr_t al = (t.block_bytes & 15) ? 3 : 15;
     if (((uintptr_t)t.dst_pool & al) || ((uintptr_t)t.src_staging & al))
       return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: pointers must be aligned to the copy vector", i);
-    a.t[i].dst = static_cast<uint8_t*>(t.dst_pool);
-    a.t[i].src = static_cast<const uint8_t*>(t.src_staging);
+    a.t[i].pool = static_cast<uint8_t*>(t.dst_pool);
+    a.t[i].staging = const_cast<uint8_t*>(static_cast<const uint8_t*>(t.src_staging));
     a.t[i].block_bytes = t.block_bytes;
   }
   a.num_tensors = num_tensors;
-  a.dst_ids = dst_block_ids;
+  a.ids = dst_block_ids;
   a.n = n;
-  a.num_dst_blocks = num_dst_blocks;
+  a.num_pool_blocks = num_dst_blocks;
   a.bad_id_count = bad_id_count;
   const hipError_t e = launch_kv_import(a, stream);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+specgen_status_t specgen_kv_export(const specgen_kv_export_tensor_t* tensors, int32_t num_tensors,
+                                   const int32_t* src_block_ids, int64_t n, int64_t num_src_blocks,
+                                   int32_t* bad_id_count, hipStream_t stream) {
+  if (!tensors) return fail(SPECGEN_ERR_INVALID_ARG, "tensors is NULL");
+  if (num_tensors < 1 || num_tensors > 4) return fail(SPECGEN_ERR_INVALID_ARG, "num_tensors %d not in 1..4", num_tensors);
+  if (n < 0 || n > INT32_MAX) return fail(SPECGEN_ERR_INVALID_ARG, "n %lld out of range", (long long)n);
+  if (num_src_blocks < 0) return fail(SPECGEN_ERR_INVALID_ARG, "num_src_blocks must be >= 0");
+  if (n > 0 && !src_block_ids) return fail(SPECGEN_ERR_INVALID_ARG, "src_block_ids is NULL");
+  BlockCopyArgs a;
+  std::memset(&a, 0, sizeof a);
+  for (int i = 0; i < num_tensors; ++i) {
+    const specgen_kv_export_tensor_t& t = tensors[i];
+    if (t.block_bytes <= 0 || (t.block_bytes & 3))
+      return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: block_bytes %lld must be > 0 and a multiple of 4", i,
+                  (long long)t.block_bytes);
+    if (n > 0 && (!t.dst_staging || !t.src_pool)) return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: NULL pointer", i);
+    const uintptr_t al = (t.block_bytes & 15) ? 3 : 15;
+    if (((uintptr_t)t.dst_staging & al) || ((uintptr_t)t.src_pool & al))
+      return fail(SPECGEN_ERR_INVALID_ARG, "tensor %d: pointers must be aligned to the copy vector", i);
+    a.t[i].pool = const_cast<uint8_t*>(static_cast<const uint8_t*>(t.src_pool));
+    a.t[i].staging = static_cast<uint8_t*>(t.dst_staging);
+    a.t[i].block_bytes = t.block_bytes;
+  }
+  a.num_tensors = num_tensors;
+  a.ids = src_block_ids;
+  a.n = n;
+  a.num_pool_blocks = num_src_blocks;
+  a.bad_id_count = bad_id_count;
+  const hipError_t e = launch_kv_export(a, stream);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+specgen_status_t specgen_kv_append(const specgen_kv_append_t* p, hipStream_t stream) {
+  if (!p) return fail(SPECGEN_ERR_INVALID_ARG, "append descriptor is NULL");
+  if (p->num_forks < 0) return fail(SPECGEN_ERR_INVALID_ARG, "num_forks must be >= 0 (got %d)", p->num_forks);
+  if (p->num_kv_heads < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_kv_heads must be >= 1");
+  if (p->head_dim < 1 || p->head_dim > 1024)
+    return fail(SPECGEN_ERR_INVALID_ARG, "head_dim %d not in 1..1024", p->head_dim);
+  if (p->kv_dtype != SPECGEN_BF16 && p->kv_dtype != SPECGEN_FP8_E4M3)
+    return fail(SPECGEN_ERR_UNSUPPORTED, "kv_dtype %d not supported", p->kv_dtype);
+  if (p->num_blocks < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_blocks must be >= 1");
+  if ((int64_t)p->num_forks * p->num_kv_heads > 4LL * INT32_MAX)
+    return fail(SPECGEN_ERR_INVALID_ARG, "num_forks * num_kv_heads too large");
+  const int es = p->kv_dtype == SPECGEN_BF16 ? 2 : 1;
+  if (p->num_forks > 0) {
+    if (!p->k_pool || !p->v_pool || !p->k_new || !p->v_new || !p->pos || !p->suffix_table_off || !p->suffix_table)
+      return fail(SPECGEN_ERR_INVALID_ARG, "NULL pointer in append descriptor");
+    if (es == 2 && (((uintptr_t)p->k_pool | (uintptr_t)p->v_pool | (uintptr_t)p->k_new | (uintptr_t)p->v_new) & 1))
+      return fail(SPECGEN_ERR_INVALID_ARG, "bf16 arrays must be 2-byte aligned");
+  }
+  AppendArgs a;
+  a.k_pool = static_cast<uint8_t*>(p->k_pool);
+  a.v_pool = static_cast<uint8_t*>(p->v_pool);
+  a.k_new = static_cast<const uint8_t*>(p->k_new);
+  a.v_new = static_cast<const uint8_t*>(p->v_new);
+  a.pos = p->pos;
+  a.suffix_table_off = p->suffix_table_off;
+  a.suffix_table = p->suffix_table;
+  a.bad_count = p->bad_count;
+  a.num_blocks = p->num_blocks;
+  a.num_forks = p->num_forks;
+  a.num_kv_heads = p->num_kv_heads;
+  a.head_dim = p->head_dim;
+  a.elem_bytes = es;
+  const hipError_t e = launch_kv_append(a, stream);
   if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -25,20 +25,36 @@ int dot_tile_cap(int D);
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream);
 hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S, int64_t R, int D, void* out,
                             bool out_bf16, float* out_lse, hipStream_t stream);
-// kv_import.hip
-struct ImportTensor {
-  uint8_t* dst;
-  const uint8_t* src;
+// kv_import.hip: whole-block moves between the pool and a staging buffer
+// (import: staging block i -> pool block ids[i]; export: the reverse)
+struct BlockCopyTensor {
+  uint8_t* pool;       // written by import, read by export
+  uint8_t* staging;    // read by import, written by export
   int64_t block_bytes;
 };
-struct ImportArgs {
-  ImportTensor t[4];
+struct BlockCopyArgs {
+  BlockCopyTensor t[4];
   int32_t num_tensors;
-  const int32_t* dst_ids;
+  const int32_t* ids;  // [n] pool block of each staging block
   int64_t n;
-  int64_t num_dst_blocks;
+  int64_t num_pool_blocks;
   int32_t* bad_id_count;
 };
-hipError_t launch_kv_import(const ImportArgs& a, hipStream_t stream);
+hipError_t launch_kv_import(const BlockCopyArgs& a, hipStream_t stream);
+hipError_t launch_kv_export(const BlockCopyArgs& a, hipStream_t stream);
+// kv_append.hip: one new token per fork written into its suffix blocks
+struct AppendArgs {
+  uint8_t* k_pool;
+  uint8_t* v_pool;
+  const uint8_t* k_new;            // [N][Hkv][D] elements of elem_bytes
+  const uint8_t* v_new;
+  const int32_t* pos;              // [N]
+  const int32_t* suffix_table_off; // [N+1]
+  const int32_t* suffix_table;
+  int32_t* bad_count;
+  int64_t num_blocks;
+  int32_t num_forks, num_kv_heads, head_dim, elem_bytes;
+};
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 
 }  // namespace specgen

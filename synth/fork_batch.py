@@ -310,6 +310,7 @@ class AppendCase:
     pos: np.ndarray             # int32 [N], the suffix slot each new token takes
     suffix_table_off: np.ndarray  # int32 [N+1]
     suffix_table: np.ndarray      # int32
+    fresh_blocks: np.ndarray      # int32, the pool blocks opened by this step
 
     @property
     def num_forks(self) -> int:
@@ -361,4 +362,4 @@ def make_append_case(batch: ForkBatch, seed: int = 0, bad_forks: Sequence[int] =
         else:
             table[off[f] + pos[f] // BLOCK] = batch.num_blocks + f
     i32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
-    return AppendCase(Hkv, D, el, k_new, v_new, i32(pos), i32(off), i32(table))
+    return AppendCase(Hkv, D, el, k_new, v_new, i32(pos), i32(off), i32(table), i32(free[:nfree]))

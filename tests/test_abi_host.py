@@ -29,8 +29,8 @@ def L():
 def test_every_declared_symbol_is_exported(L):
     names = _declared()
     assert set(names) == {"specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn",
-                          "specgen_fork_decode_attn_phase", "specgen_kv_import", "specgen_lse_merge",
-                          "specgen_last_error"}
+                          "specgen_fork_decode_attn_phase", "specgen_kv_import", "specgen_kv_export",
+                          "specgen_kv_append", "specgen_lse_merge", "specgen_last_error"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -101,3 +101,57 @@ def test_import_and_merge_argument_errors(L):
     assert L.specgen_lse_merge(P, P, 0, 4, 64, P, 0, None, None) == B.SPECGEN_ERR_INVALID_ARG
     assert L.specgen_lse_merge(P, P, 2, 4, 2000, P, 0, None, None) == B.SPECGEN_ERR_INVALID_ARG
     assert L.specgen_lse_merge(P, P, 2, 4, 64, P, 7, None, None) == B.SPECGEN_ERR_INVALID_ARG
+
+
+def test_export_argument_errors(L):
+    import paper_2606_17518_amd.binding as B
+    t = (B.KvExportTensorC * 1)()
+    t[0].dst_staging, t[0].src_pool, t[0].block_bytes = 0x10000, 0x20000, 6
+    ids = C.c_void_p(0x30000)
+    assert L.specgen_kv_export(t, 1, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    t[0].block_bytes = 64
+    assert L.specgen_kv_export(None, 1, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_export(t, 0, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_export(t, 5, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_export(t, 1, None, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_export(t, 1, ids, -1, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    assert L.specgen_kv_export(t, 1, ids, 4, -1, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    t[0].src_pool = 0x20008      # not 16-byte aligned for a 64-byte block
+    assert L.specgen_kv_export(t, 1, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    t[0].dst_staging = 0
+    assert L.specgen_kv_export(t, 1, ids, 4, 16, None, None) == B.SPECGEN_ERR_INVALID_ARG
+    # n = 0 queues nothing, so it succeeds without touching the device
+    t[0].dst_staging, t[0].src_pool = 0x10000, 0x20000
+    assert L.specgen_kv_export(t, 1, None, 0, 16, None, None) == B.SPECGEN_OK
+
+
+def _append_desc(**kw):
+    import paper_2606_17518_amd.binding as B
+    a = B.KvAppendC(num_forks=2, num_kv_heads=2, head_dim=64, kv_dtype=B.SPECGEN_BF16, num_blocks=8)
+    for f in ("k_pool", "v_pool", "k_new", "v_new", "pos", "suffix_table_off", "suffix_table"):
+        setattr(a, f, 0x10000)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("num_forks", -1, 1), ("num_kv_heads", 0, 1), ("head_dim", 0, 1), ("head_dim", 1025, 1), ("kv_dtype", 2, 2),
+    ("kv_dtype", 7, 2), ("num_blocks", 0, 1), ("k_new", None, 1), ("suffix_table", None, 1), ("pos", None, 1),
+    ("v_pool", 0x10001, 1),
+])
+def test_append_argument_errors(L, field, value, status):
+    a = _append_desc(**{field: value})
+    assert L.specgen_kv_append(C.byref(a), None) == status
+    assert L.specgen_last_error().decode() != ""
+
+
+def test_append_null_and_empty(L):
+    import paper_2606_17518_amd.binding as B
+    assert L.specgen_kv_append(None, None) == B.SPECGEN_ERR_INVALID_ARG
+    # no forks: nothing is queued, pointers are not needed
+    a = B.KvAppendC(num_forks=0, num_kv_heads=1, head_dim=64, kv_dtype=B.SPECGEN_FP8_E4M3, num_blocks=1)
+    assert L.specgen_kv_append(C.byref(a), None) == B.SPECGEN_OK
+    # 1-byte elements need no alignment
+    a = _append_desc(kv_dtype=B.SPECGEN_FP8_E4M3, num_forks=0, v_pool=0x10001)
+    assert L.specgen_kv_append(C.byref(a), None) == B.SPECGEN_OK
