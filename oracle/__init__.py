@@ -50,7 +50,7 @@ class RefBatch(C.Structure):
         ("fork_off", C.c_void_p), ("prefix_len", C.c_void_p),
         ("prefix_table_off", C.c_void_p), ("prefix_table", C.c_void_p),
         ("suffix_len", C.c_void_p), ("suffix_table_off", C.c_void_p),
-        ("suffix_table", C.c_void_p),
+        ("suffix_table", C.c_void_p), ("prefix_parent", C.c_void_p),
     ]
 
 
@@ -160,6 +160,8 @@ def fork_decode_attn(batch, rows=None, nthreads: int = 0):
     rb.suffix_len = hold(b.suffix_len, np.int32)
     rb.suffix_table_off = hold(b.suffix_table_off, np.int32)
     rb.suffix_table = hold(b.suffix_table, np.int32)
+    parent = getattr(b, "prefix_parent", None)
+    rb.prefix_parent = None if parent is None else hold(parent, np.int32)
     D = b.head_dim
     if rows is None:
         out = np.empty((b.num_forks, b.num_q_heads, D), np.float64)

@@ -123,26 +123,15 @@ typedef struct {
   const int32_t *suffix_len;         /* [N]                                   */
   const int32_t *suffix_table_off;   /* [N+1]                                 */
   const int32_t *suffix_table;
+  const int32_t *prefix_parent;      /* [T] parent trace or -1; NULL: all -1  */
 } specgen_ref_batch_t;
 
-/* Element d of kv head j of logical token i of fork f (trace t): tokens
- * 0..P_t-1 come from the trace's prefix blocks, tokens P_t.. from the fork's
- * own suffix blocks; each block holds bs consecutive tokens.  Inside a block,
- * head j's K is bs rows of D elements and its V is D rows of bs elements. */
-static double kv_elem(const specgen_ref_batch_t *b, int is_v, int32_t t,
-                      int32_t f, int64_t i, int32_t j, int32_t d) {
-  const int32_t bs = b->block_size;
-  const int64_t P = b->prefix_len[t];
-  int64_t blk, slot;
-  if (i < P) {
-    blk = b->prefix_table[b->prefix_table_off[t] + i / bs];
-    slot = i % bs;
-  } else {
-    const int64_t s = i - P;
-    blk = b->suffix_table[b->suffix_table_off[f] + s / bs];
-    slot = s % bs;
-  }
-  const int64_t D = b->head_dim;
+/* Element d of kv head j of one cached token: slot `slot` of pool block blk.
+ * Inside a block, head j's K is bs rows of D elements and its V is D rows of
+ * bs elements. */
+static double kv_elem(const specgen_ref_batch_t *b, int is_v, int64_t blk, int64_t slot, int32_t j,
+                      int32_t d) {
+  const int64_t D = b->head_dim, bs = b->block_size;
   const int64_t head = blk * b->num_kv_heads + j;
   const int64_t idx = is_v ? (head * D + d) * bs + slot : (head * bs + slot) * D + d;
   const void *pool = is_v ? b->v_pool : b->k_pool;
@@ -157,26 +146,61 @@ static int32_t trace_of_fork(const specgen_ref_batch_t *b, int32_t f) {
   return -1;
 }
 
+/* The prefix a fork of trace t is conditioned on.  A fork taken at a later
+ * trigger point of the same reasoning trace sees a longer prefix that extends
+ * the one seen by earlier forks (Algorithm 1; Sec. 4.2): trace t's own
+ * prefix tokens then continue its parent's whole prefix.  Writes the chain
+ * root first into chain[] and returns its length (-1 on a cycle). */
+static int32_t prefix_chain(const specgen_ref_batch_t *b, int32_t t, int32_t *chain) {
+  int32_t n = 0;
+  for (int32_t c = t; c >= 0; c = b->prefix_parent ? b->prefix_parent[c] : -1) {
+    if (n == b->num_traces) return -1;
+    chain[n++] = c;
+  }
+  for (int32_t i = 0; i < n / 2; ++i) {
+    const int32_t x = chain[i];
+    chain[i] = chain[n - 1 - i];
+    chain[n - 1 - i] = x;
+  }
+  return n;
+}
+
 /* One output row (fork f, query head h): gather the fork's keys and values in
- * logical order, then apply the dense definition.  q head h reads kv head
- * h / (Hq / Hkv). */
+ * logical order (the prefix tokens of every trace on its chain, root first,
+ * each in its own block table; then the fork's suffix tokens), then apply the
+ * dense definition.  q head h reads kv head h / (Hq / Hkv). */
 static void fork_row(const specgen_ref_batch_t *b, int32_t f, int32_t h,
                      double *out_row, double *lse_out) {
-  const int32_t D = b->head_dim;
+  const int32_t D = b->head_dim, bs = b->block_size;
   const int32_t g = b->num_q_heads / b->num_kv_heads;
   const int32_t j = h / g;
-  const int32_t t = trace_of_fork(b, f);
-  const int64_t n = (int64_t)b->prefix_len[t] + b->suffix_len[f];
+  int32_t chain[64];
+  const int32_t L = prefix_chain(b, trace_of_fork(b, f), chain);
+  int64_t n = b->suffix_len[f];
+  for (int32_t c = 0; c < L; ++c) n += b->prefix_len[chain[c]];
   double *q = (double *)malloc((size_t)D * sizeof(double));
   double *K = (double *)malloc((size_t)(n > 0 ? n : 1) * D * sizeof(double));
   double *V = (double *)malloc((size_t)(n > 0 ? n : 1) * D * sizeof(double));
   for (int32_t d = 0; d < D; ++d)
     q[d] = specgen_ref_bf16_to_f64(b->q[((int64_t)f * b->num_q_heads + h) * D + d]);
-  for (int64_t i = 0; i < n; ++i)
-    for (int32_t d = 0; d < D; ++d) {
-      K[i * D + d] = kv_elem(b, 0, t, f, i, j, d);
-      V[i * D + d] = kv_elem(b, 1, t, f, i, j, d);
+  int64_t i = 0;
+  for (int32_t c = 0; c < L; ++c) {
+    const int32_t t = chain[c];
+    for (int64_t x = 0; x < b->prefix_len[t]; ++x, ++i) {
+      const int64_t blk = b->prefix_table[b->prefix_table_off[t] + x / bs];
+      for (int32_t d = 0; d < D; ++d) {
+        K[i * D + d] = kv_elem(b, 0, blk, x % bs, j, d);
+        V[i * D + d] = kv_elem(b, 1, blk, x % bs, j, d);
+      }
     }
+  }
+  for (int64_t x = 0; x < b->suffix_len[f]; ++x, ++i) {
+    const int64_t blk = b->suffix_table[b->suffix_table_off[f] + x / bs];
+    for (int32_t d = 0; d < D; ++d) {
+      K[i * D + d] = kv_elem(b, 0, blk, x % bs, j, d);
+      V[i * D + d] = kv_elem(b, 1, blk, x % bs, j, d);
+    }
+  }
   specgen_ref_attend_dense(q, K, V, n, D, b->sm_scale, out_row, lse_out);
   free(q);
   free(K);
@@ -190,6 +214,13 @@ int specgen_ref_fork_decode_attn(const specgen_ref_batch_t *b, const int32_t *ro
                                  int64_t nrows, double *out, double *out_lse,
                                  int32_t nthreads) {
   if (!b || b->num_kv_heads <= 0 || b->num_q_heads % b->num_kv_heads != 0) return -1;
+  if (b->prefix_parent) {
+    int32_t chain[64];
+    if (b->num_traces > 64) return -1;
+    for (int32_t t = 0; t < b->num_traces; ++t)
+      if (b->prefix_parent[t] < -1 || b->prefix_parent[t] >= b->num_traces || prefix_chain(b, t, chain) < 0)
+        return -1;
+  }
   const int64_t total = rows ? nrows : (int64_t)b->num_forks * b->num_q_heads;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);

@@ -39,6 +39,15 @@ WORKLOADS = {
         batch=dict(prefix_lens=[131072], forks_per_trace=32, suffix_range=(256, 4096), num_q_heads=128,
                    num_kv_heads=8, head_dim=128, kv_dtype="fp8_e4m3", extra_blocks=0),
         import_prefix=False),
+    # nested fork points on one 32768-token trace (a fork tree): forks taken at
+    # 16384 tokens (4), at 24576 (6) and at 32768 (6) see prefixes that extend
+    # each other, stored once as three segments of 16384, 8192 and 8192 tokens;
+    # suffixes in [128, 1024], keys with the per-kv-head bias of std 0.5
+    "tree_p32k_l3": dict(
+        batch=dict(prefix_lens=[16384, 8192, 8192], prefix_parent=[-1, 0, 1], forks_per_trace=[4, 6, 6],
+                   suffix_range=(128, 1024), num_q_heads=64, num_kv_heads=8, head_dim=128, key_bias_std=0.5,
+                   num_blocks=16384),
+        import_prefix=False),
 }
 WORKLOAD_SEEDS = {name: i + 1 for i, name in enumerate(WORKLOADS)}
 

@@ -69,6 +69,8 @@ class ForkBatch:
     # E4M3 only: per-token scale [len] of the block each logical token sits in
     k_logical_scale: Optional[list] = None
     v_logical_scale: Optional[list] = None
+    # nested prefixes: parent trace of each trace (-1 for a root), or None
+    prefix_parent: Optional[np.ndarray] = None
 
     @property
     def group(self) -> int:
@@ -76,6 +78,17 @@ class ForkBatch:
 
     def trace_of_fork(self, f: int) -> int:
         return int(np.searchsorted(self.fork_off, f, side="right") - 1)
+
+    def prefix_chain(self, t: int) -> list:
+        """Traces whose prefix tokens precede a fork of trace t, root first."""
+        chain = []
+        while t >= 0:
+            chain.append(t)
+            t = -1 if self.prefix_parent is None else int(self.prefix_parent[t])
+        return chain[::-1]
+
+    def keys_of_fork(self, f: int) -> int:
+        return sum(int(self.prefix_len[c]) for c in self.prefix_chain(self.trace_of_fork(f))) + int(self.suffix_len[f])
 
     def kv_elem_bytes(self) -> int:
         return 2 if self.kv_dtype == "bf16" else 1
@@ -103,9 +116,7 @@ class ForkBatch:
 
     def flops(self) -> int:
         """Multiply-adds x2 of QK^T and PV over every (fork, q head) row."""
-        toks = 0
-        for f in range(self.num_forks):
-            toks += int(self.prefix_len[self.trace_of_fork(f)]) + int(self.suffix_len[f])
+        toks = sum(self.keys_of_fork(f) for f in range(self.num_forks))
         return 4 * self.head_dim * self.num_q_heads * toks
 
 
@@ -127,8 +138,12 @@ def make_fork_batch(*, prefix_lens: Sequence[int] | None = None,
                     kv_dtype: str = "bf16", key_bias_std: float = 0.0,
                     num_blocks: int | None = None, extra_blocks: int | None = None,
                     sm_scale: float | None = None, seed: int = 0, name: str = "",
-                    keep_logical: bool = False, identity_table: bool = False) -> ForkBatch:
-    """Draw one fork batch.  Integer ranges are inclusive of both ends."""
+                    keep_logical: bool = False, identity_table: bool = False,
+                    prefix_parent: Sequence[int] | None = None) -> ForkBatch:
+    """Draw one fork batch.  Integer ranges are inclusive of both ends.
+    ``prefix_parent`` makes the traces' prefixes nested: trace t's own prefix
+    tokens follow the whole prefix of trace prefix_parent[t] (-1: a root); the
+    traces must be listed in depth-first order."""
     rng = np.random.default_rng(seed)
     bs = BLOCK
     # 1. lengths
@@ -242,6 +257,7 @@ def make_fork_batch(*, prefix_lens: Sequence[int] | None = None,
         fork_off=i32(fork_off), prefix_len=i32(P), prefix_table_off=i32(prefix_table_off),
         prefix_table=i32(prefix_table), suffix_len=i32(S), suffix_table_off=i32(suffix_table_off),
         suffix_table=i32(suffix_table), seed=seed, name=name,
+        prefix_parent=None if prefix_parent is None else i32(prefix_parent),
         k_logical=logical[0] if keep_logical else None,
         v_logical=logical[1] if keep_logical else None,
         k_logical_scale=logical_sc[0] if keep_logical else None,

@@ -175,10 +175,14 @@ def test_merge_order_independent():
 def _logical_dense(batch, f):
     """fp64 K/V [n][Hkv][D] of fork f in logical order, decoded by torch from the
     generator's pre-paging copies (not via the oracle or the pool)."""
-    t = batch.trace_of_fork(f)
-    segs = [(batch.k_logical[t], batch.v_logical[t], batch.k_logical_scale[t], batch.v_logical_scale[t]),
-            (batch.k_logical[batch.num_traces + f], batch.v_logical[batch.num_traces + f],
-             batch.k_logical_scale[batch.num_traces + f], batch.v_logical_scale[batch.num_traces + f])]
+    t = int(np.searchsorted(batch.fork_off, f, side="right") - 1)
+    chain = [t]     # the traces whose prefixes precede the fork's keys, root first
+    while batch.prefix_parent is not None and batch.prefix_parent[chain[0]] >= 0:
+        chain.insert(0, int(batch.prefix_parent[chain[0]]))
+    segs = [(batch.k_logical[c], batch.v_logical[c], batch.k_logical_scale[c], batch.v_logical_scale[c])
+            for c in chain]
+    segs.append((batch.k_logical[batch.num_traces + f], batch.v_logical[batch.num_traces + f],
+                 batch.k_logical_scale[batch.num_traces + f], batch.v_logical_scale[batch.num_traces + f]))
     Ks, Vs = [], []
     for k, v, ks, vs in segs:
         if batch.kv_dtype == "bf16":
@@ -234,6 +238,56 @@ def test_fork_batch_fp8_matches_sdpa_on_dequantised_kv():
 def test_fork_batch_tiny_workload_matches_sdpa():
     b = synth.workload("tiny_p256_f4", keep_logical=True)
     _check_batch_against_sdpa(b, atol=1e-11)
+
+
+# ---- nested prefixes (fork tree) ------------------------------------------------
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_fork_chain_matches_sdpa_on_concatenated_prefixes(kv):
+    """Forks taken at three nested trigger points of one trace: a fork of
+    level k attends over the level-1..k prefix segments in order, then its
+    suffix (segments of 17, 1 and 31 tokens: block boundaries inside and
+    across segments)."""
+    b = synth.make_fork_batch(prefix_lens=[17, 1, 31], prefix_parent=[-1, 0, 1], forks_per_trace=[2, 1, 3],
+                              suffix_lens=[0, 5, 16, 1, 0, 33], num_q_heads=4, num_kv_heads=2, head_dim=8,
+                              kv_dtype=kv, seed=40, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_tree_with_branches_matches_sdpa():
+    """Two roots; the first has two children, one of which has a child
+    (depth-first order), the second root has none."""
+    b = synth.make_fork_batch(prefix_lens=[20, 16, 9, 3, 40], prefix_parent=[-1, 0, 1, 0, -1],
+                              forks_per_trace=[1, 2, 1, 2, 1], suffix_lens=[3, 0, 17, 4, 16, 1, 2],
+                              num_q_heads=6, num_kv_heads=3, head_dim=16, seed=41, keep_logical=True)
+    _check_batch_against_sdpa(b)
+
+
+def test_fork_tree_root_forks_do_not_see_descendants():
+    """The forks of a root give bit-identical results when the root's
+    descendants (and their forks) are dropped from the batch."""
+    b = synth.make_fork_batch(prefix_lens=[33, 16, 7], prefix_parent=[-1, 0, 0], forks_per_trace=[2, 1, 2],
+                              suffix_lens=[1, 18, 0, 5, 2], num_q_heads=4, num_kv_heads=2, head_dim=16, seed=42)
+    o, l = oracle.fork_decode_attn(b)
+    import copy
+    r = copy.copy(b)
+    r.num_traces, r.num_forks = 1, 2
+    r.fork_off = np.array([0, 2], np.int32)
+    r.prefix_len, r.prefix_table_off = b.prefix_len[:1], b.prefix_table_off[:2]
+    r.suffix_len, r.suffix_table_off = b.suffix_len[:2], b.suffix_table_off[:3]
+    r.q, r.prefix_parent = b.q[:2], None
+    o1, l1 = oracle.fork_decode_attn(r)
+    np.testing.assert_array_equal(o[:2], o1)
+    np.testing.assert_array_equal(l[:2], l1)
+
+
+def test_fork_tree_bad_parent_rejected():
+    b = synth.make_fork_batch(prefix_lens=[4, 4], forks_per_trace=1, suffix_lens=[0, 0], num_q_heads=2,
+                              num_kv_heads=1, head_dim=8, seed=43)
+    for parent in ([1, 0], [-1, 2], [-2, -1]):
+        b.prefix_parent = np.array(parent, np.int32)
+        with pytest.raises(ValueError):
+            oracle.fork_decode_attn(b)
 
 
 def test_paging_invariance():
