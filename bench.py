@@ -257,8 +257,7 @@ def main():
     achieved = kern_bytes / part_s / 1e9
     # matrix work of the partial kernel: S = q K^T and P V over every key of
     # every (fork, q head) row, 2 flops per multiply-add each
-    keys = sum(int(b.prefix_len[t]) * int(b.fork_off[t + 1] - b.fork_off[t]) for t in range(b.num_traces)) \
-        + int(b.suffix_len.sum())
+    keys = sum(b.keys_of_fork(f) for f in range(N))   # prefix chain + suffix of every fork
     kern_flops = 4.0 * D * Hq * keys
     fp8 = b.kv_dtype != "bf16"
     if fp8:   # E4M3 KV: 2r/e flop per byte puts the MFMA path above the ridge

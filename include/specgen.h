@@ -9,7 +9,11 @@
  * Speculative Generation"; Sec. 8.7, prefix caching paragraph).  A fork event
  * launches K forks (Algorithm 1, the line that sets K from the resource
  * capacity), and idle-triggered forking adds more forks on the same prefix
- * (Sec. 6.1.1), so one trace's prefix is shared by F forks.  Suspended
+ * (Sec. 6.1.1), so one trace's prefix is shared by F forks.  Successive
+ * trigger points of one trace fork from ever longer prefixes while the
+ * reasoning generation continues (Algorithm 1), so forks of different
+ * trigger points share the earlier part: nested prefixes, stored once as a
+ * chain of traces (prefix_parent_h).  Suspended
  * prefixes are kept in spare GPU memory and restored into the serving cache
  * instead of being recomputed (Sec. 6.2.3 "Remote Cache of Reasoning
  * Prefixes").
@@ -113,6 +117,14 @@ typedef struct {
   const int32_t *suffix_len_h;
   const int32_t *prefix_table_off_h;
   const int32_t *suffix_table_off_h;
+  /* Nested prefixes (a fork tree), host only, read during the call: [T]
+     parent trace of each trace, or -1 for a root; NULL makes every trace a
+     root.  A fork of trace t attends over the prefix tokens of every trace
+     on the chain root, ..., parent, t (in that order, each with its own
+     block table and P), then its suffix.  Parents come first and traces are
+     in depth-first order: prefix_parent_h[t] is t-1 or an ancestor of t-1.
+     At most 8 traces on a chain.                                              */
+  const int32_t *prefix_parent_h;
 } specgen_fork_batch_t;
 
 /* Workspace bytes that specgen_fork_decode_attn needs for this batch (partial

@@ -48,6 +48,7 @@ class ForkBatchC(C.Structure):
         ("suffix_table", C.c_void_p),
         ("fork_off_h", C.c_void_p), ("prefix_len_h", C.c_void_p), ("suffix_len_h", C.c_void_p),
         ("prefix_table_off_h", C.c_void_p), ("suffix_table_off_h", C.c_void_p),
+        ("prefix_parent_h", C.c_void_p),
     ]
 
 
@@ -147,6 +148,7 @@ class ForkBatchTensors:
     suffix_table_off_h: np.ndarray
     path: int = SPECGEN_PATH_AUTO
     block_size: int = 16
+    prefix_parent_h: Optional[np.ndarray] = None   # nested prefixes: parent trace or -1
 
     @staticmethod
     def from_numpy(b, device="cuda", path: str | int = "auto") -> "ForkBatchTensors":
@@ -173,7 +175,9 @@ class ForkBatchTensors:
             suffix_len_h=np.ascontiguousarray(b.suffix_len, np.int32),
             prefix_table_off_h=np.ascontiguousarray(b.prefix_table_off, np.int32),
             suffix_table_off_h=np.ascontiguousarray(b.suffix_table_off, np.int32),
-            path=PATHS[path] if isinstance(path, str) else int(path))
+            path=PATHS[path] if isinstance(path, str) else int(path),
+            prefix_parent_h=None if getattr(b, "prefix_parent", None) is None
+            else np.ascontiguousarray(b.prefix_parent, np.int32))
 
     def c_struct(self, **overrides) -> ForkBatchC:
         s = ForkBatchC()
@@ -194,6 +198,7 @@ class ForkBatchTensors:
             setattr(s, name, None if t is None else t.data_ptr())
         for name in ("fork_off_h", "prefix_len_h", "suffix_len_h", "prefix_table_off_h", "suffix_table_off_h"):
             setattr(s, name, getattr(self, name).ctypes.data)
+        s.prefix_parent_h = None if self.prefix_parent_h is None else self.prefix_parent_h.ctypes.data
         for k, v in overrides.items():
             setattr(s, k, v)
         return s

@@ -78,6 +78,7 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.D = b->head_dim;
   in.policy = b->path;
   in.fork_off = b->fork_off_h;
+  in.prefix_parent = b->prefix_parent_h;
   in.prefix_len = b->prefix_len_h;
   in.suffix_len = b->suffix_len_h;
   in.prefix_table_off = b->prefix_table_off_h;

@@ -90,51 +90,71 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
 }
 
 // The row (f, h) = (row / Hq, row % Hq) of the output: the parts are the
-// partials of the workers that covered its prefix item and its suffix item.
-// One wavefront per row; `plan` may live in LDS or in the kernel arguments.
-template <int D>
+// partials of the workers that covered its prefix items (one per trace on the
+// fork's prefix chain: its own trace and, with nested prefixes, each ancestor)
+// and its suffix item.  kDepth bounds the chain (1: no nesting).  One
+// wavefront per row; `plan` may live in LDS or in the kernel arguments.
+template <int D, int kDepth>
 __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __restrict__ ws, int64_t row,
                                                uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+  constexpr int kItems = kDepth + 1;   // prefix items nearest trace first, then the suffix item
   const int f = (int)(row / plan.Hq);
   const int h = (int)(row % plan.Hq);
   // The item table (written by the partial kernels' walks) gives each item's
   // first and last worker and its segment index in the first one.  Part i of
   // an item sits in slot (w_lo + i) * kmax + (i == 0 ? k_lo : 0), so relative
   // to part 0 it is i * kmax - k_lo slots further (plain scalars: a lane picks
-  // the prefix or the suffix item by its part index).
-  int Xs[2] = {0, 0}, ords[2] = {0, 0}, rs[2] = {0, 0};
-  bool has[2];
-  prefix_item_of_row(plan, f, h, &Xs[0], &ords[0], &rs[0]);
-  has[0] = true;
-  has[1] = suffix_item_of_row(plan, f, h, &Xs[1], &ords[1], &rs[1]);
-  // both table entries are loaded before either is used
-  int32_t e[2][3];
+  // its part's item by the part index).
+  int Xs[kItems], ords[kItems], rs[kItems];
+  bool has[kItems];
+  int t = trace_of_fork(plan, f);
 #pragma unroll
-  for (int s2 = 0; s2 < 2; ++s2) {
+  for (int i = 0; i < kDepth; ++i) {
+    Xs[i] = ords[i] = rs[i] = 0;
+    has[i] = t >= 0;
+    if (has[i]) {
+      prefix_item_of_row(plan, f, h, t, &Xs[i], &ords[i], &rs[i]);
+      t = plan.parent[t];
+    }
+  }
+  Xs[kDepth] = ords[kDepth] = rs[kDepth] = 0;
+  has[kDepth] = suffix_item_of_row(plan, f, h, &Xs[kDepth], &ords[kDepth], &rs[kDepth]);
+  // every table entry is loaded before any is used
+  int32_t e[kItems][3];
+#pragma unroll
+  for (int s2 = 0; s2 < kItems; ++s2) {
     const int32_t* info = reinterpret_cast<const int32_t*>(ws + plan.part[Xs[s2]].info_base) + 3 * (int64_t)ords[s2];
 #pragma unroll
     for (int c = 0; c < 3; ++c) e[s2][c] = has[s2] ? info[c] : 0;
   }
-  int64_t o0[2] = {0, 0}, l0[2] = {0, 0};
-  int kmax[2] = {1, 1}, klo[2] = {0, 0}, n[2] = {0, 0}, srows[2] = {1, 1};
+  int64_t o0[kItems], l0[kItems];
+  int kmax[kItems], klo[kItems], first[kItems + 1], srows[kItems];
   bool ok = true;
+  first[0] = 0;
 #pragma unroll
-  for (int s2 = 0; s2 < 2; ++s2) {
-    if (!has[s2]) continue;
-    const int X = Xs[s2], ord = ords[s2], r = rs[s2];
-    const PartPlan& pp = plan.part[X];
-    const int w_lo = e[s2][0], w_hi = e[s2][1], k_lo = e[s2][2];
-    if (ord < 0 || ord >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 || k_lo >= pp.kmax) {
-      ok = false;
-      continue;
+  for (int s2 = 0; s2 < kItems; ++s2) {
+    o0[s2] = l0[s2] = 0;
+    kmax[s2] = srows[s2] = 1;
+    klo[s2] = 0;
+    int n = 0;
+    if (has[s2]) {
+      const int X = Xs[s2], ord = ords[s2], r = rs[s2];
+      const PartPlan& pp = plan.part[X];
+      const int w_lo = e[s2][0], w_hi = e[s2][1], k_lo = e[s2][2];
+      if (ord < 0 || ord >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 ||
+          k_lo >= pp.kmax) {
+        ok = false;
+      } else {
+        const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
+        o0[s2] = part_o_off(pp, slot0, r, D);
+        l0[s2] = part_l_off(pp, slot0, r);
+        kmax[s2] = pp.kmax;
+        klo[s2] = k_lo;
+        n = w_hi - w_lo + 1;
+        srows[s2] = pp.slot_rows;
+      }
     }
-    const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
-    o0[s2] = part_o_off(pp, slot0, r, D);
-    l0[s2] = part_l_off(pp, slot0, r);
-    kmax[s2] = pp.kmax;
-    klo[s2] = k_lo;
-    n[s2] = w_hi - w_lo + 1;
-    srows[s2] = pp.slot_rows;
+    first[s2 + 1] = first[s2] + n;   // an absent item holds no parts
   }
   if (!ok) {   // the item table is inconsistent: fail loudly rather than read out of range
     const int lane = threadIdx.x & 63;
@@ -142,23 +162,56 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
     if (out_lse && lane == 0) out_lse[row] = __builtin_nanf("");
     return;
   }
-  const int np = n[0];
-  const int64_t pO0 = o0[0], sO0 = o0[1], pL0 = l0[0], sL0 = l0[1];
-  const int pK = kmax[0], sK = kmax[1], pKlo = klo[0], sKlo = klo[1], pR = srows[0], sR = srows[1];
-  auto rel_slots = [&](int p) -> int64_t {   // slots between part p and its item's part 0
-    const bool pre = p < np;
-    const int i = pre ? p : p - np;
-    return i == 0 ? 0 : (int64_t)i * (pre ? pK : sK) - (pre ? pKlo : sKlo);
+  struct Loc {
+    int64_t slots;   // slots between part p and its item's part 0
+    int64_t o, l;    // the item's part-0 offsets
+    int rows;
+  };
+  // Picking a part's item is a chain of per-lane selects between wave-uniform
+  // values.  Selecting between two elements of one array makes the compiler
+  // index the array in private memory; with one prefix item the values are
+  // named scalars, and deeper chains read them through readfirstlane.
+  const int64_t pO = o0[0], pL = l0[0], sO = o0[kItems - 1], sL = l0[kItems - 1];
+  const int pK = kmax[0], pKlo = klo[0], pR = srows[0], sK = kmax[kItems - 1], sKlo = klo[kItems - 1],
+            sR = srows[kItems - 1], np = first[1];
+  auto u32 = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
+  auto u64 = [](int64_t v) {
+    const uint64_t x = (uint64_t)v;
+    return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x));
+  };
+  auto locate_part = [&](int p) {   // the last item whose first part is <= p owns p
+    if constexpr (kItems == 2) {
+      const bool pre = p < np;
+      const int i = pre ? p : p - np;
+      const int K = pre ? pK : sK, KL = pre ? pKlo : sKlo;
+      return Loc{i == 0 ? 0 : (int64_t)i * K - KL, pre ? pO : sO, pre ? pL : sL, pre ? pR : sR};
+    } else {
+      int64_t o = u64(o0[0]), l = u64(l0[0]);
+      int K = u32(kmax[0]), KL = u32(klo[0]), R = u32(srows[0]), c = 0;
+#pragma unroll
+      for (int s2 = 1; s2 < kItems; ++s2) {
+        const bool in = p >= u32(first[s2]);
+        o = in ? u64(o0[s2]) : o;
+        l = in ? u64(l0[s2]) : l;
+        K = in ? u32(kmax[s2]) : K;
+        KL = in ? u32(klo[s2]) : KL;
+        R = in ? u32(srows[s2]) : R;
+        c = in ? u32(first[s2]) : c;
+      }
+      const int i = p - c;
+      return Loc{i == 0 ? 0 : (int64_t)i * K - KL, o, l, R};
+    }
   };
   auto po = [&](int p) {   // the part's o row: D fp16 values, two per uint32
-    const bool pre = p < np;
-    return reinterpret_cast<const uint32_t*>(ws + (pre ? pO0 : sO0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * (D / 2));
+    const Loc L = locate_part(p);
+    return reinterpret_cast<const uint32_t*>(ws + L.o + L.slots * (int64_t)L.rows * (D / 2));
   };
   auto pl = [&](int p) {   // its (lse, dec) pair
-    const bool pre = p < np;
-    return *reinterpret_cast<const f32x2*>(ws + (pre ? pL0 : sL0) + rel_slots(p) * (int64_t)(pre ? pR : sR) * 2);
+    const Loc L = locate_part(p);
+    return *reinterpret_cast<const f32x2*>(ws + L.l + L.slots * (int64_t)L.rows * 2);
   };
-  merge_row_v4<D>(np + n[1], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
+  merge_row_v4<D>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
 }  // namespace specgen

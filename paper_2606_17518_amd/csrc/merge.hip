@@ -93,25 +93,34 @@ hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S,
 }
 
 // ---- fork merge: the parts of row (f, h) are the partials of the workers that
-// covered its prefix item and its suffix item ---------------------------------
+// covered its prefix items and its suffix item ---------------------------------
 
-template <int D>
+template <int D, int kDepth>
 __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, const float* __restrict__ ws, uint16_t* __restrict__ out,
                                                          float* __restrict__ out_lse) {
   __shared__ Plan splan;
   plan_to_lds<256>(plan_arg, splan);
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= (int64_t)splan.N * splan.Hq) return;
-  fork_merge_row<D>(splan, ws, row, out, out_lse);
+  fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
   const int64_t rows = (int64_t)plan.N * plan.Hq;
   const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-  if (plan.D == 128)
-    hipLaunchKernelGGL(fork_merge_kernel<128>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-  else
-    hipLaunchKernelGGL(fork_merge_kernel<64>, grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  // without nested prefixes a row has one prefix item; otherwise up to kMaxDepth
+  const bool nested = plan.depth > 1;
+  if (plan.D == 128) {
+    if (nested)
+      hipLaunchKernelGGL((fork_merge_kernel<128, kMaxDepth>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    else
+      hipLaunchKernelGGL((fork_merge_kernel<128, 1>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  } else {
+    if (nested)
+      hipLaunchKernelGGL((fork_merge_kernel<64, kMaxDepth>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    else
+      hipLaunchKernelGGL((fork_merge_kernel<64, 1>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  }
   return hipGetLastError();
 }
 

@@ -38,6 +38,7 @@ namespace specgen {
 
 constexpr int kMaxTraces = 32;   // traces per call
 constexpr int kMaxForks = 512;   // forks per call
+constexpr int kMaxDepth = 8;     // traces on one prefix chain (nested prefixes)
 constexpr int kBlock = 16;       // tokens per KV block
 
 enum { kPartMfma = 0, kPartDot = 1 };
@@ -71,16 +72,23 @@ struct PartPlan {
 // The scalar part of the plan.
 struct PlanHead {
   int32_t T, N, Hq, Hkv, g, D;
-  int32_t policy, pad_;
+  int32_t policy;
+  int32_t depth;          // traces on the longest prefix chain (1: no nesting)
   PartPlan part[2];
 };
 
 // The whole plan, computed on the host from the length mirrors and passed to
-// every kernel by value (about 7.4 KB of kernel arguments); each workgroup
+// every kernel by value (about 7.6 KB of kernel arguments); each workgroup
 // copies it into LDS with one vector load per thread (plan_to_lds).
 struct alignas(16) Plan : PlanHead {
   int32_t fork_off[kMaxTraces + 1];
   int32_t prefix_len[kMaxTraces];
+  // Nested prefixes: a fork of trace t attends over the prefix tokens of
+  // every trace on the chain root, ..., parent[t], t.  Traces are in
+  // depth-first order, so the forks of t and its descendants are
+  // [fork_off[t], fork_end[t]): the rows of t's prefix items.
+  int32_t parent[kMaxTraces];       // -1 for a root
+  int32_t fork_end[kMaxTraces];
   int32_t trace_part[kMaxTraces];   // partition of trace t's prefix items
   int32_t trace_pos[kMaxTraces];    // index of t in ptrace
   int32_t ptrace[kMaxTraces];       // traces grouped by partition, ascending within each
@@ -98,7 +106,7 @@ SG_HD int32_t cdiv32(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
 
 
-SG_HD int32_t trace_rows(const Plan& p, int t) { return (p.fork_off[t + 1] - p.fork_off[t]) * p.g; }
+SG_HD int32_t trace_rows(const Plan& p, int t) { return (p.fork_end[t] - p.fork_off[t]) * p.g; }
 
 SG_HD int part_of_trace(int policy, int rows) {
   if (policy == kPolicyDot) return kPartDot;
@@ -407,10 +415,10 @@ SG_HD ItemParts item_parts(const Plan& p, int part, int64_t first_unit, int tile
   return ip;
 }
 
-// The prefix item of row (f, h) and its row inside the item.
-SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h) {
+// The prefix item of trace t (the fork's own trace or one of its ancestors)
+// that holds row (f, h), and the row inside the item.
+SG_HD ItemParts prefix_parts_of_row(const Plan& p, int f, int h, int t) {
   const int g = p.g, j = h / g, hh = h - j * g;
-  const int t = trace_of_fork(p, f);
   const int ri = (f - p.fork_off[t]) * g + hh;
   const int X = p.trace_part[t];
   const PartPlan& pp = p.part[X];
@@ -438,10 +446,10 @@ SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
   return true;
 }
 
-// The prefix item of row (f, h): its partition, ordinal and the row inside it.
-SG_HD void prefix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, int* row) {
+// The prefix item of trace t that holds row (f, h): its partition, ordinal
+// and the row inside it (t is the fork's own trace or one of its ancestors).
+SG_HD void prefix_item_of_row(const Plan& p, int f, int h, int t, int* part, int* ord, int* row) {
   const int g = p.g, j = h / g, hh = h - j * g;
-  const int t = trace_of_fork(p, f);
   const int ri = (f - p.fork_off[t]) * g + hh;
   const int X = p.trace_part[t];
   const PartPlan& pp = p.part[X];

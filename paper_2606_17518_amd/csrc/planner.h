@@ -18,6 +18,7 @@ enum { kPlanOk = 0, kPlanInvalid = 1, kPlanUnsupported = 2 };
 struct PlanInputs {
   int T, N, Hq, Hkv, D, policy;
   const int32_t* fork_off;    // [T+1]
+  const int32_t* prefix_parent;  // [T] parent trace or -1, or NULL (every trace a root)
   const int32_t* prefix_len;  // [T]
   const int32_t* suffix_len;  // [N]
   const int32_t* prefix_table_off;  // [T+1]
@@ -65,6 +66,28 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   }
   for (int f = 0; f < N; ++f)
     if (in.suffix_len[f] < 0) SG_FAIL(kPlanInvalid, "suffix_len[%d] must be >= 0", f);
+  // Nested prefixes: each parent comes earlier, and the traces are in
+  // depth-first order (a trace's parent is the previous trace or one of its
+  // ancestors), so every subtree is a contiguous run of traces and forks.
+  int32_t parent[kMaxTraces], depth[kMaxTraces], sub_end[kMaxTraces];
+  int max_depth = 1;
+  for (int t = 0; t < T; ++t) {
+    const int pa = in.prefix_parent ? in.prefix_parent[t] : -1;
+    if (pa < -1 || pa >= t) SG_FAIL(kPlanInvalid, "prefix_parent[%d] = %d must be -1 or an earlier trace", t, pa);
+    if (pa >= 0) {
+      int a = t - 1;
+      while (a >= 0 && a != pa) a = parent[a];
+      if (a != pa) SG_FAIL(kPlanInvalid, "traces are not in depth-first order at trace %d", t);
+    }
+    parent[t] = pa;
+    depth[t] = pa < 0 ? 1 : depth[pa] + 1;
+    if (depth[t] > kMaxDepth) SG_FAIL(kPlanUnsupported, "prefix chain deeper than %d traces", kMaxDepth);
+    max_depth = std::max(max_depth, depth[t]);
+  }
+  for (int t = T - 1; t >= 0; --t) {   // one past the last trace of t's subtree
+    sub_end[t] = t + 1;
+    while (sub_end[t] < T && depth[sub_end[t]] > depth[t]) sub_end[t] = sub_end[sub_end[t]];
+  }
 
   const int g = Hq / Hkv;
   memset(plan, 0, sizeof(Plan));
@@ -75,7 +98,12 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   plan->g = g;
   plan->D = D;
   plan->policy = in.policy;
+  plan->depth = max_depth;
   for (int t = 0; t <= T; ++t) plan->fork_off[t] = fo[t];
+  for (int t = 0; t < T; ++t) {
+    plan->parent[t] = parent[t];
+    plan->fork_end[t] = fo[sub_end[t]];
+  }
   for (int t = 0; t < T; ++t) plan->prefix_len[t] = in.prefix_len[t];
   for (int t = 0; t <= T; ++t) plan->prefix_table_off[t] = in.prefix_table_off[t];
   for (int f = 0; f < N; ++f) plan->suffix_len[f] = in.suffix_len[f];
@@ -100,7 +128,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     int wt_min = pp.wt_suf;
     int64_t units = 0, items = 0;
     for (int t = 0; t < T; ++t) {
-      const int rows = (fo[t + 1] - fo[t]) * g;
+      const int rows = (plan->fork_end[t] - fo[t]) * g;   // the forks of t and its descendants
       if (part_of_trace(in.policy, rows) != X) continue;
       plan->trace_part[t] = X;
       plan->trace_pos[t] = pos;

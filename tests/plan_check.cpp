@@ -7,7 +7,8 @@
 //   - every tile of every work item is processed exactly once;
 //   - per-worker item count and tile count stay within the kernels' caps;
 //   - each row's merge finds exactly the (worker, segment) pairs that
-//     processed its prefix item and its suffix item, with in-range slots;
+//     processed its prefix items (one per trace on the fork's prefix chain,
+//     for nested prefixes) and its suffix item, with in-range slots;
 //   - each item row maps back to the (fork, q head) it belongs to;
 //   - stepping from an item to the next (next_item) agrees with locate();
 //   - per-worker units and tiles stay within the kernels' caps;
@@ -43,6 +44,19 @@ struct Seg {
 };
 
 static int g_unsupported = 0;
+
+// Forks of trace t and of every trace below it (nested prefixes), counted
+// from the parent array directly: [fork_off[t], fork_off[e]) where e is the
+// first later trace that does not descend from t.
+static int subtree_rows(const PlanInputs& in, int t, int g) {
+  int e = t + 1;
+  for (; e < in.T; ++e) {
+    int a = e;
+    while (a >= 0 && a != t) a = in.prefix_parent ? in.prefix_parent[a] : -1;
+    if (a != t) break;
+  }
+  return (in.fork_off[e] - in.fork_off[t]) * g;
+}
 
 // lib_prices: the library's unit prices, with which every generated shape
 // must plan; with random prices the planner may answer "unsupported" (a
@@ -150,7 +164,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
   };
   for (int X = 0; X < 2; ++X) {
     for (int t = 0; t < in.T; ++t) {
-      const int rows = (in.fork_off[t + 1] - in.fork_off[t]) * g;
+      const int rows = subtree_rows(in, t, g);
       if (part_of_trace(in.policy, rows) != X) continue;
       const int rb = (rows + in.rbs[X] - 1) / in.rbs[X];
       const int tiles = (in.prefix_len[t] + in.tt[X] - 1) / in.tt[X];
@@ -211,33 +225,39 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     int t = 0;
     while (in.fork_off[t + 1] <= f) ++t;
     CHECK(trace_of_fork(plan, f) == t, "trace_of_fork");
+    std::vector<int> chain;   // the fork's own trace, then its ancestors
+    for (int c = t; c >= 0; c = in.prefix_parent ? in.prefix_parent[c] : -1) chain.push_back(c);
+    CHECK((int)chain.size() <= plan.depth, "chain of %zu traces, plan depth %d", chain.size(), plan.depth);
     for (int h = 0; h < in.Hq; ++h) {
       const int j = h / g, hh = h % g;
-      const int ri = (f - in.fork_off[t]) * g + hh;
-      const int X = plan.trace_part[t];
-      const int rbs = in.rbs[X];
-      const int rows = (in.fork_off[t + 1] - in.fork_off[t]) * g;
-      const int rbc = (rows + rbs - 1) / rbs;
-      // prefix item ordinal, counted directly
-      int ord = 0;
-      for (int t2 = 0; t2 < t; ++t2) {
-        const int r2 = (in.fork_off[t2 + 1] - in.fork_off[t2]) * g;
-        if (part_of_trace(in.policy, r2) == X) ord += in.Hkv * ((r2 + rbs - 1) / rbs);
-      }
-      ord += j * rbc + ri / rbs;
-      const ItemParts P = prefix_parts_of_row(plan, f, h);
-      CHECK(P.part == X, "prefix partition");
-      {
-        int xp = -1, op = -1, rp = -1;
-        prefix_item_of_row(plan, f, h, &xp, &op, &rp);
-        CHECK(xp == X && op == ord && rp == P.row, "prefix_item_of_row (%d,%d,%d) vs (%d,%d,%d)", xp, op, rp, X, ord,
-              P.row);
-        CHECK(op < plan.part[X].n_items, "prefix ordinal past the item table");
-      }
-      if (!same(P, ord)) return false;
       int ff, hh2;
-      item_row_fork_head(plan, 0, t, -1, j, (ri / rbs) * rbs, P.row, &ff, &hh2);
-      CHECK(ff == f && hh2 == h, "prefix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
+      for (const int c : chain) {
+        CHECK(plan.fork_off[c] <= f && f < plan.fork_end[c], "fork %d outside the rows of trace %d", f, c);
+        const int ri = (f - in.fork_off[c]) * g + hh;
+        const int X = plan.trace_part[c];
+        const int rbs = in.rbs[X];
+        const int rows = subtree_rows(in, c, g);
+        const int rbc = (rows + rbs - 1) / rbs;
+        // prefix item ordinal, counted directly
+        int ord = 0;
+        for (int t2 = 0; t2 < c; ++t2) {
+          const int r2 = subtree_rows(in, t2, g);
+          if (part_of_trace(in.policy, r2) == X) ord += in.Hkv * ((r2 + rbs - 1) / rbs);
+        }
+        ord += j * rbc + ri / rbs;
+        const ItemParts P = prefix_parts_of_row(plan, f, h, c);
+        CHECK(P.part == X, "prefix partition");
+        {
+          int xp = -1, op = -1, rp = -1;
+          prefix_item_of_row(plan, f, h, c, &xp, &op, &rp);
+          CHECK(xp == X && op == ord && rp == P.row, "prefix_item_of_row (%d,%d,%d) vs (%d,%d,%d)", xp, op, rp, X,
+                ord, P.row);
+          CHECK(op < plan.part[X].n_items, "prefix ordinal past the item table");
+        }
+        if (!same(P, ord)) return false;
+        item_row_fork_head(plan, 0, c, -1, j, (ri / rbs) * rbs, P.row, &ff, &hh2);
+        CHECK(ff == f && hh2 == h, "prefix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
+      }
       ItemParts S;
       const bool has = suffix_parts_of_row(plan, f, h, &S);
       CHECK(has == (in.suffix_len[f] > 0), "suffix presence");
@@ -292,6 +312,22 @@ int main(int argc, char** argv) {
     std::vector<int32_t> pto(in.T + 1, 0), sto(in.N + 1, 0);
     for (int t = 0; t < in.T; ++t) pto[t + 1] = pto[t] + (P[t] + 15) / 16;
     for (int f = 0; f < in.N; ++f) sto[f + 1] = sto[f] + (S[f] + 15) / 16;
+    // nested prefixes in a third of the cases: a random depth-first forest of
+    // depth <= kMaxDepth (each trace's parent is the previous trace or one of
+    // its ancestors)
+    std::vector<int32_t> parent(in.T, -1), depth(in.T, 1);
+    const bool nested = U(0, 2) == 0;
+    if (nested) {
+      for (int t = 1; t < in.T; ++t) {
+        int a = t - 1;
+        const int up = U(0, 3);   // how many levels above the previous trace
+        for (int k = 0; k < up && a >= 0; ++k) a = parent[a];
+        if (a >= 0 && depth[a] >= kMaxDepth) a = parent[a];
+        parent[t] = a;
+        depth[t] = a < 0 ? 1 : depth[a] + 1;
+      }
+    }
+    in.prefix_parent = nested ? parent.data() : nullptr;
     in.fork_off = fo.data();
     in.prefix_len = P.data();
     in.suffix_len = S.data();

@@ -155,3 +155,35 @@ def test_append_null_and_empty(L):
     # 1-byte elements need no alignment
     a = _append_desc(kv_dtype=B.SPECGEN_FP8_E4M3, num_forks=0, v_pool=0x10001)
     assert L.specgen_kv_append(C.byref(a), None) == B.SPECGEN_OK
+
+
+def _tree_batch(parent, forks=1, P=20):
+    """T traces with `forks` forks each (no suffixes) and the given parents."""
+    import paper_2606_17518_amd.binding as B
+    T = len(parent)
+    s, keep = _host_batch()
+    N = T * forks
+    arrs = [np.arange(0, N + 1, forks, dtype=np.int32), np.full(T, P, np.int32), np.zeros(N, np.int32),
+            np.arange(0, T + 1, dtype=np.int32) * ((P + 15) // 16), np.zeros(N + 1, np.int32),
+            np.asarray(parent, np.int32)]
+    keep += arrs
+    s.num_traces, s.num_forks = T, N
+    s.fork_off_h, s.prefix_len_h, s.suffix_len_h, s.prefix_table_off_h, s.suffix_table_off_h, s.prefix_parent_h = \
+        (a.ctypes.data for a in arrs)
+    return s, keep
+
+
+@pytest.mark.parametrize("parent,status", [
+    ([-1, 0, 1], 0), ([-1, 0, 0, 2, -1, 4], 0), ([-1, -1], 0),
+    ([0], 1), ([-1, 1], 1), ([-1, 2, 0], 1), ([-2], 1),
+    ([-1, 0, -1, 1], 1),                    # 1 is not an ancestor of trace 2 (not depth-first)
+    ([-1] + list(range(8)), 2),             # a chain of 9 traces
+    ([-1] + list(range(7)), 0),             # a chain of 8 traces
+])
+def test_nested_prefix_parents_validated(L, parent, status):
+    s, keep = _tree_batch(parent)
+    n = C.c_size_t(0)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status, \
+        L.specgen_last_error().decode()
+    if status == 0:
+        assert n.value > 0
