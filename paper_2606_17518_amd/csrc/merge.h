@@ -94,9 +94,22 @@ __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, 
 // fork's prefix chain: its own trace and, with nested prefixes, each ancestor)
 // and its suffix item.  kDepth bounds the chain (1: no nesting).  One
 // wavefront per row; `plan` may live in LDS or in the kernel arguments.
+struct MergeLoc {
+  int64_t slots;   // slots between a part and its item's part 0
+  int64_t o, l;    // the item's part-0 offsets
+  int rows;
+};
+struct alignas(16) MergeItemLoc {
+  int64_t o, l;
+  int kmax, klo, rows, first;
+};
+
+// loc: kDepth + 1 entries of LDS private to the calling wavefront (unused
+// when kDepth == 1).
 template <int D, int kDepth>
 __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __restrict__ ws, int64_t row,
-                                               uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+                                               uint16_t* __restrict__ out, float* __restrict__ out_lse,
+                                               MergeItemLoc* loc) {
   constexpr int kItems = kDepth + 1;   // prefix items nearest trace first, then the suffix item
   const int f = (int)(row / plan.Hq);
   const int h = (int)(row % plan.Hq);
@@ -162,53 +175,42 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
     if (out_lse && lane == 0) out_lse[row] = __builtin_nanf("");
     return;
   }
-  struct Loc {
-    int64_t slots;   // slots between part p and its item's part 0
-    int64_t o, l;    // the item's part-0 offsets
-    int rows;
-  };
-  // Picking a part's item is a chain of per-lane selects between wave-uniform
-  // values.  Selecting between two elements of one array makes the compiler
-  // index the array in private memory; with one prefix item the values are
-  // named scalars, and deeper chains read them through readfirstlane.
+  // Picking a part's item: with one prefix item, per-lane selects between
+  // named scalars; with a chain, the wave's item table in LDS (`loc`, kItems
+  // entries), indexed by the number of items that start at or before the
+  // part.  (Selecting between elements of a register array would make the
+  // compiler index the array in private memory instead.)
   const int64_t pO = o0[0], pL = l0[0], sO = o0[kItems - 1], sL = l0[kItems - 1];
   const int pK = kmax[0], pKlo = klo[0], pR = srows[0], sK = kmax[kItems - 1], sKlo = klo[kItems - 1],
             sR = srows[kItems - 1], np = first[1];
-  auto u32 = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
-  auto u64 = [](int64_t v) {
-    const uint64_t x = (uint64_t)v;
-    return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
-                     (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x));
-  };
+  if constexpr (kItems > 2) {
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+      for (int s2 = 0; s2 < kItems; ++s2) loc[s2] = MergeItemLoc{o0[s2], l0[s2], kmax[s2], klo[s2], srows[s2], first[s2]};
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
   auto locate_part = [&](int p) {   // the last item whose first part is <= p owns p
     if constexpr (kItems == 2) {
       const bool pre = p < np;
       const int i = pre ? p : p - np;
       const int K = pre ? pK : sK, KL = pre ? pKlo : sKlo;
-      return Loc{i == 0 ? 0 : (int64_t)i * K - KL, pre ? pO : sO, pre ? pL : sL, pre ? pR : sR};
+      return MergeLoc{i == 0 ? 0 : (int64_t)i * K - KL, pre ? pO : sO, pre ? pL : sL, pre ? pR : sR};
     } else {
-      int64_t o = u64(o0[0]), l = u64(l0[0]);
-      int K = u32(kmax[0]), KL = u32(klo[0]), R = u32(srows[0]), c = 0;
+      int k = 0;
 #pragma unroll
-      for (int s2 = 1; s2 < kItems; ++s2) {
-        const bool in = p >= u32(first[s2]);
-        o = in ? u64(o0[s2]) : o;
-        l = in ? u64(l0[s2]) : l;
-        K = in ? u32(kmax[s2]) : K;
-        KL = in ? u32(klo[s2]) : KL;
-        R = in ? u32(srows[s2]) : R;
-        c = in ? u32(first[s2]) : c;
-      }
-      const int i = p - c;
-      return Loc{i == 0 ? 0 : (int64_t)i * K - KL, o, l, R};
+      for (int s2 = 1; s2 < kItems; ++s2) k += p >= first[s2];
+      const MergeItemLoc it = loc[k];
+      const int i = p - it.first;
+      return MergeLoc{i == 0 ? 0 : (int64_t)i * it.kmax - it.klo, it.o, it.l, it.rows};
     }
   };
   auto po = [&](int p) {   // the part's o row: D fp16 values, two per uint32
-    const Loc L = locate_part(p);
+    const MergeLoc L = locate_part(p);
     return reinterpret_cast<const uint32_t*>(ws + L.o + L.slots * (int64_t)L.rows * (D / 2));
   };
   auto pl = [&](int p) {   // its (lse, dec) pair
-    const Loc L = locate_part(p);
+    const MergeLoc L = locate_part(p);
     return *reinterpret_cast<const f32x2*>(ws + L.l + L.slots * (int64_t)L.rows * 2);
   };
   merge_row_v4<D>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);

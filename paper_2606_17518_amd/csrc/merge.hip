@@ -99,10 +99,11 @@ template <int D, int kDepth>
 __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, const float* __restrict__ ws, uint16_t* __restrict__ out,
                                                          float* __restrict__ out_lse) {
   __shared__ Plan splan;
+  __shared__ MergeItemLoc sloc[4][kDepth + 1];   // each wave's item table (nested prefixes)
   plan_to_lds<256>(plan_arg, splan);
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= (int64_t)splan.N * splan.Hq) return;
-  fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse);
+  fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
