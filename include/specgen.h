@@ -73,7 +73,8 @@ typedef enum {
 typedef enum { SPECGEN_BF16 = 0, SPECGEN_FP8_E4M3 = 1, SPECGEN_FP32 = 2 } specgen_dtype_t;
 
 /* Which kernel serves each work item.  AUTO: a prefix item uses the bf16 MFMA
- * kernel when its row count F_t * (Hq/Hkv) is at least 16, else the
+ * kernel when its row count F_t * (Hq/Hkv) is at least 16 (F_t: the forks of
+ * trace t and of every trace nested below it), else the
  * wavefront dot kernel; suffix items use the MFMA kernel.  DOT / MFMA force
  * one kernel for every item (used by tests to cover both paths). */
 typedef enum { SPECGEN_PATH_AUTO = 0, SPECGEN_PATH_DOT = 1, SPECGEN_PATH_MFMA = 2 } specgen_path_t;

@@ -64,6 +64,8 @@ def _load():
             lib.specgen_ref_attend_dense.restype = None
             lib.specgen_ref_fork_decode_attn.argtypes = [C.POINTER(RefBatch), P, C.c_int64, P, P, C.c_int32]
             lib.specgen_ref_fork_decode_attn.restype = C.c_int
+            lib.specgen_ref_fork_prefill_attn.argtypes = [C.POINTER(RefBatch), P, P, C.c_int64, P, P, C.c_int32]
+            lib.specgen_ref_fork_prefill_attn.restype = C.c_int
             lib.specgen_ref_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, P]
             lib.specgen_ref_lse_merge.restype = None
             lib.specgen_ref_kv_import.argtypes = [P, P, C.c_int64, P, C.c_int64, C.c_int64]
@@ -122,15 +124,7 @@ def attend_dense(q, K, V, sm_scale: float):
     return o, float(lse[0])
 
 
-def fork_decode_attn(batch, rows=None, nthreads: int = 0):
-    """Oracle fork-decode attention for a ``synth`` ForkBatch (numpy arrays).
-
-    rows: optional int array [n][2] of (fork, q head) pairs; default all rows.
-    Returns (out, lse): [N][Hq][D] and [N][Hq] (or [n][D], [n]) float64.
-    """
-    b = batch
-    keep = []
-
+def _ref_batch(b, keep):
     def hold(a, dt):
         a = _c(a, dt)
         keep.append(a)
@@ -162,21 +156,54 @@ def fork_decode_attn(batch, rows=None, nthreads: int = 0):
     rb.suffix_table = hold(b.suffix_table, np.int32)
     parent = getattr(b, "prefix_parent", None)
     rb.prefix_parent = None if parent is None else hold(parent, np.int32)
-    D = b.head_dim
+    return rb
+
+
+def _rows_out(rows, n_all, D, keep):
     if rows is None:
-        out = np.empty((b.num_forks, b.num_q_heads, D), np.float64)
-        lse = np.empty((b.num_forks, b.num_q_heads), np.float64)
-        rows_p, n = None, 0
-    else:
-        rows_a = _c(rows, np.int32).reshape(-1, 2)
-        keep.append(rows_a)
-        n = rows_a.shape[0]
-        out = np.empty((n, D), np.float64)
-        lse = np.empty((n,), np.float64)
-        rows_p = _ptr(rows_a)
+        return None, 0, np.empty((n_all, D), np.float64), np.empty((n_all,), np.float64)
+    rows_a = _c(rows, np.int32).reshape(-1, 2)
+    keep.append(rows_a)
+    n = rows_a.shape[0]
+    return _ptr(rows_a), n, np.empty((n, D), np.float64), np.empty((n,), np.float64)
+
+
+def fork_decode_attn(batch, rows=None, nthreads: int = 0):
+    """Oracle fork-decode attention for a ``synth`` ForkBatch (numpy arrays).
+
+    rows: optional int array [n][2] of (fork, q head) pairs; default all rows.
+    Returns (out, lse): [N][Hq][D] and [N][Hq] (or [n][D], [n]) float64.
+    """
+    keep = []
+    rb = _ref_batch(batch, keep)
+    N, Hq, D = batch.num_forks, batch.num_q_heads, batch.head_dim
+    rows_p, n, out, lse = _rows_out(rows, N * Hq, D, keep)
     rc = _load().specgen_ref_fork_decode_attn(C.byref(rb), rows_p, n, _ptr(out), _ptr(lse), int(nthreads))
     if rc != 0:
         raise ValueError("oracle: malformed fork batch")
+    if rows is None:
+        return out.reshape(N, Hq, D), lse.reshape(N, Hq)
+    return out, lse
+
+
+def fork_prefill_attn(batch, q_len, rows=None, nthreads: int = 0):
+    """Oracle multi-token prefill: fork f's last q_len[f] suffix tokens are
+    queries (batch.q is [sum q_len][Hq][D]), causal inside the suffix.
+
+    rows: optional int array [n][2] of (query index, q head) pairs.
+    Returns (out, lse): [sum q_len][Hq][D] and [sum q_len][Hq] (or [n][D], [n])."""
+    keep = []
+    rb = _ref_batch(batch, keep)
+    ql = _c(q_len, np.int32)
+    keep.append(ql)
+    nq, Hq, D = int(ql.sum()), batch.num_q_heads, batch.head_dim
+    rows_p, n, out, lse = _rows_out(rows, nq * Hq, D, keep)
+    rc = _load().specgen_ref_fork_prefill_attn(C.byref(rb), _ptr(ql), rows_p, n, _ptr(out), _ptr(lse),
+                                               int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle: malformed prefill batch")
+    if rows is None:
+        return out.reshape(nq, Hq, D), lse.reshape(nq, Hq)
     return out, lse
 
 

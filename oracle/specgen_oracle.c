@@ -169,20 +169,30 @@ static int32_t prefix_chain(const specgen_ref_batch_t *b, int32_t t, int32_t *ch
  * logical order (the prefix tokens of every trace on its chain, root first,
  * each in its own block table; then the fork's suffix tokens), then apply the
  * dense definition.  q head h reads kv head h / (Hq / Hkv). */
+static void fork_row_upto(const specgen_ref_batch_t *b, int32_t f, int32_t h, int64_t suffix_keys,
+                          const uint16_t *q_row, double *out_row, double *lse_out);
+
 static void fork_row(const specgen_ref_batch_t *b, int32_t f, int32_t h,
                      double *out_row, double *lse_out) {
+  fork_row_upto(b, f, h, b->suffix_len[f], b->q + ((int64_t)f * b->num_q_heads + h) * b->head_dim, out_row,
+                lse_out);
+}
+
+/* The same with the fork's suffix cut to its first suffix_keys tokens and the
+ * query given explicitly (one query of a multi-token prefill). */
+static void fork_row_upto(const specgen_ref_batch_t *b, int32_t f, int32_t h, int64_t suffix_keys,
+                          const uint16_t *q_row, double *out_row, double *lse_out) {
   const int32_t D = b->head_dim, bs = b->block_size;
   const int32_t g = b->num_q_heads / b->num_kv_heads;
   const int32_t j = h / g;
   int32_t chain[64];
   const int32_t L = prefix_chain(b, trace_of_fork(b, f), chain);
-  int64_t n = b->suffix_len[f];
+  int64_t n = suffix_keys;
   for (int32_t c = 0; c < L; ++c) n += b->prefix_len[chain[c]];
   double *q = (double *)malloc((size_t)D * sizeof(double));
   double *K = (double *)malloc((size_t)(n > 0 ? n : 1) * D * sizeof(double));
   double *V = (double *)malloc((size_t)(n > 0 ? n : 1) * D * sizeof(double));
-  for (int32_t d = 0; d < D; ++d)
-    q[d] = specgen_ref_bf16_to_f64(b->q[((int64_t)f * b->num_q_heads + h) * D + d]);
+  for (int32_t d = 0; d < D; ++d) q[d] = specgen_ref_bf16_to_f64(q_row[d]);
   int64_t i = 0;
   for (int32_t c = 0; c < L; ++c) {
     const int32_t t = chain[c];
@@ -194,7 +204,7 @@ static void fork_row(const specgen_ref_batch_t *b, int32_t f, int32_t h,
       }
     }
   }
-  for (int64_t x = 0; x < b->suffix_len[f]; ++x, ++i) {
+  for (int64_t x = 0; x < suffix_keys; ++x, ++i) {
     const int64_t blk = b->suffix_table[b->suffix_table_off[f] + x / bs];
     for (int32_t d = 0; d < D; ++d) {
       K[i * D + d] = kv_elem(b, 0, blk, x % bs, j, d);
@@ -239,6 +249,58 @@ int specgen_ref_fork_decode_attn(const specgen_ref_batch_t *b, const int32_t *ro
     }
     fork_row(b, f, h, out + r * b->head_dim, out_lse + r);
   }
+  return 0;
+}
+
+/* Multi-token prefill of every fork over its cached prefix: the speculative
+ * prompt adds a few tokens per fork (a switch of the chat template to the
+ * non-reasoning mode, Sec. 6.1.1 and Sec. 8.1) that are processed against the
+ * cached reasoning prefix (Sec. 8.7, prefix caching paragraph).  Fork f's last
+ * q_len[f] suffix tokens are queries: query i (0-based) sits at suffix
+ * position S_f - q_len[f] + i and attends to the fork's whole prefix chain
+ * and to suffix tokens 0 .. S_f - q_len[f] + i (causal inside the suffix).
+ * b->q holds the queries [sum q_len][Hq][D], fork by fork.  rows: nrows
+ * (query index, q head) pairs, or NULL for all.  Returns 0, or -1 if the
+ * batch or q_len is malformed. */
+int specgen_ref_fork_prefill_attn(const specgen_ref_batch_t *b, const int32_t *q_len, const int32_t *rows,
+                                  int64_t nrows, double *out, double *out_lse, int32_t nthreads) {
+  if (!b || !q_len || b->num_kv_heads <= 0 || b->num_q_heads % b->num_kv_heads != 0) return -1;
+  int64_t nq = 0;
+  for (int32_t f = 0; f < b->num_forks; ++f) {
+    if (q_len[f] < 1 || q_len[f] > b->suffix_len[f]) return -1;
+    nq += q_len[f];
+  }
+  int32_t *qf = (int32_t *)malloc((size_t)nq * sizeof(int32_t));   /* fork of each query */
+  int64_t *qi = (int64_t *)malloc((size_t)nq * sizeof(int64_t));   /* its index in the fork */
+  for (int32_t f = 0, k = 0; f < b->num_forks; ++f)
+    for (int32_t i = 0; i < q_len[f]; ++i, ++k) {
+      qf[k] = f;
+      qi[k] = i;
+    }
+  const int64_t total = rows ? nrows : nq * b->num_q_heads;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < total; ++r) {
+    int64_t v;
+    int32_t h;
+    if (rows) {
+      v = rows[2 * r];
+      h = rows[2 * r + 1];
+    } else {
+      v = r / b->num_q_heads;
+      h = (int32_t)(r % b->num_q_heads);
+    }
+    const int32_t f = qf[v];
+    const int64_t keys = (int64_t)b->suffix_len[f] - q_len[f] + qi[v] + 1;
+    fork_row_upto(b, f, h, keys, b->q + (v * b->num_q_heads + h) * b->head_dim, out + r * b->head_dim,
+                  out_lse + r);
+  }
+  free(qf);
+  free(qi);
   return 0;
 }
 

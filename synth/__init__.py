@@ -7,7 +7,7 @@ paper's own workloads (LLM reasoning traces over KernelBench tasks) are not
 reproduced; these synthetic tensors have the shapes of such caches.
 """
 from .fork_batch import (BLOCK, AppendCase, ForkBatch, ImportCase, make_append_case, make_fork_batch,
-                         make_import_case, prefix_import_from_batch, SENTINEL)
+                         make_import_case, prefix_import_from_batch, SENTINEL, with_prefill_queries)
 
 # name -> (fork-batch keyword arguments, import description or None)
 WORKLOADS = {

@@ -71,6 +71,8 @@ class ForkBatch:
     v_logical_scale: Optional[list] = None
     # nested prefixes: parent trace of each trace (-1 for a root), or None
     prefix_parent: Optional[np.ndarray] = None
+    # multi-token prefill: queries per fork (q is then [sum q_len][Hq][D]), or None
+    q_len: Optional[np.ndarray] = None
 
     @property
     def group(self) -> int:
@@ -379,3 +381,18 @@ def make_append_case(batch: ForkBatch, seed: int = 0, bad_forks: Sequence[int] =
             table[off[f] + pos[f] // BLOCK] = batch.num_blocks + f
     i32 = lambda a: np.ascontiguousarray(a, dtype=np.int32)
     return AppendCase(Hkv, D, el, k_new, v_new, i32(pos), i32(off), i32(table), i32(free[:nfree]))
+
+
+# ---- multi-token prefill workloads -----------------------------------------------
+
+def with_prefill_queries(batch: ForkBatch, q_len: Sequence[int], seed: int = 0) -> ForkBatch:
+    """A copy of ``batch`` whose forks each carry q_len[f] queries (their last
+    q_len[f] suffix tokens, which the suffix already holds): q becomes
+    [sum q_len][Hq][D] bf16 drawn from N(0, 1), and ``q_len`` is attached."""
+    ql = np.ascontiguousarray(q_len, dtype=np.int32)
+    assert ql.size == batch.num_forks and np.all(ql >= 1) and np.all(ql <= batch.suffix_len)
+    rng = np.random.default_rng(seed)
+    out = dataclasses.replace(batch)
+    out.q = _to_bf16_bits(rng.standard_normal((int(ql.sum()), batch.num_q_heads, batch.head_dim), dtype=np.float32))
+    out.q_len = ql
+    return out

@@ -510,3 +510,74 @@ def test_append_fresh_block_and_bad_forks():
     assert np.array_equal(k[mask], b.k_pool[mask]) and np.array_equal(v[mask], b.v_pool[mask])
     for bid in changed:
         assert (k[bid] != b.k_pool[bid]).sum() <= b.num_kv_heads * b.head_dim
+
+
+# ---- multi-token prefill -----------------------------------------------------------
+
+def test_prefill_of_one_token_is_the_decode_step():
+    b = synth.make_fork_batch(prefix_lens=[30, 9], prefix_parent=[-1, 0], forks_per_trace=[2, 2],
+                              suffix_lens=[1, 16, 3, 40], num_q_heads=4, num_kv_heads=2, head_dim=16, seed=60)
+    p = synth.with_prefill_queries(b, [1, 1, 1, 1], seed=1)
+    b.q = p.q
+    o, l = oracle.fork_decode_attn(b)
+    po, pl = oracle.fork_prefill_attn(p, p.q_len)
+    np.testing.assert_array_equal(po, o)
+    np.testing.assert_array_equal(pl, l)
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_prefill_matches_masked_sdpa(kv):
+    """Each query sees the whole prefix chain and the suffix up to its own
+    position: torch SDPA with an explicit boolean mask on the concatenated
+    logical K/V."""
+    b = synth.make_fork_batch(prefix_lens=[25, 7], prefix_parent=[-1, 0], forks_per_trace=[1, 2],
+                              suffix_lens=[5, 17, 33], num_q_heads=4, num_kv_heads=2, head_dim=8, kv_dtype=kv,
+                              seed=61, keep_logical=True)
+    p = synth.with_prefill_queries(b, [5, 3, 17], seed=2)
+    o, l = oracle.fork_prefill_attn(p, p.q_len)
+    qd = torch.from_numpy(p.q.view(np.int16)).view(torch.bfloat16).to(torch.float64)
+    v = 0
+    for f in range(b.num_forks):
+        K, V = _logical_dense(b, f)
+        n = K.shape[0]
+        S, L = int(b.suffix_len[f]), int(p.q_len[f])
+        for i in range(L):
+            visible = n - S + (S - L + i + 1)
+            for h in range(b.num_q_heads):
+                j = h // b.group
+                mask = torch.zeros(1, 1, 1, n, dtype=torch.bool)
+                mask[..., :visible] = True
+                qt = qd[v, h].reshape(1, 1, 1, -1)
+                kt = torch.from_numpy(K[:, j]).reshape(1, 1, n, -1)
+                vt = torch.from_numpy(V[:, j]).reshape(1, 1, n, -1)
+                ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask,
+                                                                       scale=b.sm_scale).reshape(-1).numpy()
+                s = (kt.reshape(n, -1)[:visible] @ qt.reshape(-1)) * b.sm_scale
+                np.testing.assert_allclose(o[v, h], ref, rtol=0, atol=1e-12)
+                assert abs(l[v, h] - float(torch.logsumexp(s, 0))) < 1e-12
+            v += 1
+
+
+def test_prefill_query_ignores_later_suffix_tokens():
+    """Overwriting the suffix tokens after query i's position (K and V, in the
+    pools) leaves query i's output bit-identical; the last query sees all."""
+    b = synth.make_fork_batch(prefix_lens=[20], forks_per_trace=1, suffix_lens=[12], num_q_heads=2,
+                              num_kv_heads=1, head_dim=16, seed=62)
+    p = synth.with_prefill_queries(b, [6], seed=3)
+    o, _ = oracle.fork_prefill_attn(p, p.q_len)
+    blk = int(b.suffix_table[0])
+    p2 = synth.with_prefill_queries(b, [6], seed=3)
+    p2.k_pool, p2.v_pool = b.k_pool.copy(), b.v_pool.copy()
+    p2.k_pool[blk][:, 11, :] = 0x4000     # suffix token 11: bf16 2.0
+    p2.v_pool[blk][:, :, 11] = 0x4000
+    o2, _ = oracle.fork_prefill_attn(p2, p2.q_len)
+    np.testing.assert_array_equal(o2[:5], o[:5])
+    assert np.abs(o2[5] - o[5]).max() > 0
+
+
+def test_prefill_bad_q_len_rejected():
+    b = synth.make_fork_batch(prefix_lens=[8], forks_per_trace=2, suffix_lens=[3, 0], num_q_heads=2,
+                              num_kv_heads=1, head_dim=8, seed=63)
+    for ql in ([1, 1], [4, 0], [0, 0]):
+        with pytest.raises(ValueError):
+            oracle.fork_prefill_attn(b, np.array(ql, np.int32))
