@@ -71,19 +71,22 @@ def traffic_from_profile(workload: str):
     return d.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline(batch, target_s: float):
+def cpu_baseline(batch, target_s: float, q_len=None, step_bytes=None):
     """The fp64 oracle on the same workload on this host's cores: whole decode
-    steps (every fork and q head) repeated until about target_s of CPU work."""
+    steps (every fork and q head; every query with q_len) repeated until about
+    target_s of CPU work."""
     import oracle
+    run = (lambda: oracle.fork_decode_attn(batch)) if q_len is None else (lambda: oracle.fork_prefill_attn(batch, q_len))
     t0 = time.perf_counter()
-    oracle.fork_decode_attn(batch)
+    run()
     reps = 1
     while time.perf_counter() - t0 < target_s and reps < 64:
-        oracle.fork_decode_attn(batch)
+        run()
         reps += 1
     dt = time.perf_counter() - t0
     step_s = dt / reps
-    return {"value": round(batch.algorithmic_bytes() / step_s / 1e9, 4), "unit": "GB/s",
+    step_bytes = batch.algorithmic_bytes() if step_bytes is None else step_bytes
+    return {"value": round(step_bytes / step_s / 1e9, 4), "unit": "GB/s",
             "fork_tokens_per_s": round(batch.num_forks / step_s, 3), "cores": oracle.max_threads(), "kind": "oracle",
             "sample": f"{reps} whole decode steps ({batch.num_forks} forks x {batch.num_q_heads} q heads) of the same "
                       f"workload, fp64 C oracle, {dt:.1f} s; GB/s = step algorithmic bytes / mean step time"}
@@ -115,6 +118,11 @@ def main():
     spec = synth.WORKLOADS[args.workload]
     log(f"generating {args.workload}")
     b = synth.workload(args.workload)
+    prefill_q = spec.get("prefill_q")
+    q_len = None
+    if prefill_q:   # multi-token prefill: every fork's last prefill_q suffix tokens are queries
+        q_len = np.full(b.num_forks, prefill_q, np.int32)
+        b = synth.with_prefill_queries(b, q_len, seed=1)
     do_import = spec.get("import_prefix", False)
     R = max(2, args.replicas)
     log(f"uploading {R} replicas")
@@ -127,9 +135,10 @@ def main():
                 setattr(fb, name, getattr(reps[0], name))
         reps.append(fb)
     N, Hq, D = b.num_forks, b.num_q_heads, b.head_dim
-    out = torch.empty((N, Hq, D), dtype=torch.bfloat16, device=dev)
-    lse = torch.empty((N, Hq), dtype=torch.float32, device=dev)
-    ws = sg.alloc_workspace(reps[0])
+    Q = N if q_len is None else int(q_len.sum())   # query rows per head
+    out = torch.empty((Q, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((Q, Hq), dtype=torch.float32, device=dev)
+    ws = sg.alloc_workspace(reps[0]) if q_len is None else sg.alloc_prefill_workspace(reps[0], q_len)
     stream = torch.cuda.current_stream()
 
     imp = None
@@ -163,7 +172,10 @@ def main():
         if imp is not None:
             sg.specgen_kv_import(imp[r_imp], ids_d, b.num_blocks, stream=stream)
         evs[1].record(stream)
-        if split:
+        if q_len is not None:   # one entry point, no separate phases
+            sg.specgen_fork_prefill_attn(reps[r_att], q_len, out, lse, ws, stream=stream)
+            evs[2].record(stream)
+        elif split:
             sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_PARTIALS, None, None, ws, stream=stream)
             evs[2].record(stream)
             sg.specgen_fork_decode_attn_phase(reps[r_att], sg.SPECGEN_PHASE_MERGE, out, lse, ws, stream=stream)
@@ -194,7 +206,7 @@ def main():
     attn_ms = np.array([e[1].elapsed_time(e[3]) for e in timed])
     # the same steps again with an event between the two kernels: the partial
     # kernel's own duration (the roofline figure) and the merge's
-    log(f"timing {args.steps} steps with the phases split")
+    log(f"timing {args.steps} steps with the phases split" if q_len is None else f"timing {args.steps} more steps")
     sevents = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda._sleep(SPIN_CYCLES)
     for k in range(args.steps):
@@ -248,8 +260,8 @@ def main():
         moves["append"] = {"forks": N, "fresh_blocks": int(app.fresh_blocks.size), "bytes": int(app_bytes),
                            "us": round(float(app_ms.mean()) * 1e3, 2),
                            "gbps": round(app_bytes / (float(app_ms.mean()) / 1e3) / 1e9, 2)}
-    attn_bytes = b.algorithmic_bytes()
-    out_bytes = N * Hq * (D * 2 + 4)
+    attn_bytes = b.algorithmic_bytes() + (Q - N) * Hq * (D * 2 * 2 + 4)   # extra queries: q in, out and lse out
+    out_bytes = Q * Hq * (D * 2 + 4)
     kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
     attn_s = float(attn_ms.mean()) / 1e3
     part_s = float(part_ms.mean()) / 1e3
@@ -258,11 +270,16 @@ def main():
     # matrix work of the partial kernel: S = q K^T and P V over every key of
     # every (fork, q head) row, 2 flops per multiply-add each
     keys = sum(b.keys_of_fork(f) for f in range(N))   # prefix chain + suffix of every fork
+    if q_len is not None:   # query i of fork f sees its suffix up to its own position
+        keys = sum(int(q_len[f]) * b.keys_of_fork(f) - sum(int(q_len[f]) - 1 - i for i in range(int(q_len[f])))
+                   for f in range(N))
     kern_flops = 4.0 * D * Hq * keys
     fp8 = b.kv_dtype != "bf16"
-    if fp8:   # E4M3 KV: 2r/e flop per byte puts the MFMA path above the ridge
+    if fp8 or q_len is not None:   # E4M3 KV (2r/e flop per byte) or many query rows: above the MFMA ridge
         tflops = kern_flops / part_s / 1e12
-        roofline = {"kernel": partial_kernel(D, True) + " (partials phase)", "bound": "mfma",
+        kname = partial_kernel(D, fp8) + (" (partials phase)" if q_len is None else
+                                          " + merge (the whole prefill call: no separate phases)")
+        roofline = {"kernel": kname, "bound": "mfma",
                     "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload),
                     "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2)}
@@ -278,9 +295,9 @@ def main():
         "config": {"workload": args.workload, "traces": b.num_traces, "forks": N,
                    "prefix_len": [int(x) for x in b.prefix_len[:4]], "suffix_tokens": int(b.suffix_len.sum()),
                    "q_heads": Hq, "kv_heads": b.num_kv_heads, "head_dim": D, "kv_dtype": b.kv_dtype,
-                   "path": args.path, "replicas": R, "import_blocks": int(len(ids)) if imp is not None else 0},
+                   "path": args.path, "replicas": R, "prefill_queries_per_fork": prefill_q or 0, "import_blocks": int(len(ids)) if imp is not None else 0},
         "pct_of_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "fork_tokens_per_s": round(N / attn_s, 1),
+        "fork_tokens_per_s": round(Q / attn_s, 1),
         "attn_us": {"mean": round(float(attn_ms.mean()) * 1e3, 2), "p10": round(float(np.percentile(attn_ms, 10)) * 1e3, 2),
                     "p50": round(float(np.median(attn_ms)) * 1e3, 2), "p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
                     "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2),
@@ -295,7 +312,7 @@ def main():
     res.update(moves)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, q_len, attn_bytes)
     print(json.dumps(res), flush=True)
 
 

@@ -164,6 +164,29 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t *b, i
                                                 float *out_lse, void *workspace, size_t workspace_bytes,
                                                 hipStream_t stream);
 
+/* Multi-token prefill of every fork over its cached prefix: the speculative
+ * prompt appends a few tokens per fork (the chat template's switch to the
+ * non-reasoning mode, Sec. 6.1.1 and Sec. 8.1) that are processed against the
+ * cached reasoning prefix instead of recomputing it (Sec. 8.7, prefix caching
+ * paragraph).  Fork f's last q_len_h[f] suffix tokens are queries (their K/V
+ * already in the suffix, S_f counting them): query i (0-based) attends to
+ * every prefix token of its chain and to suffix tokens 0 .. S_f - q_len_h[f]
+ * + i (causal inside the suffix, one query row per (query, q head)).
+ *   b: a fork batch as for specgen_fork_decode_attn, except that q is
+ *      [Q][Hq][D] bf16 with Q = sum_f q_len_h[f], fork by fork in query order.
+ *   q_len_h: host int32 [N], 1 <= q_len_h[f] <= S_f, read during the call;
+ *      Q <= 512 per call.
+ *   out: [Q][Hq][D] bf16; out_lse: [Q][Hq] fp32 or NULL.
+ *   workspace: at least specgen_fork_prefill_attn_workspace_size bytes.
+ * The work runs as a decode batch in which each query is a fork of its own
+ * (same trace, same block table, its causal suffix length), so the shared
+ * prefix is still read once per row block of 256 query rows per kv head. */
+specgen_status_t specgen_fork_prefill_attn_workspace_size(const specgen_fork_batch_t *b, const int32_t *q_len_h,
+                                                          size_t *bytes);
+specgen_status_t specgen_fork_prefill_attn(const specgen_fork_batch_t *b, const int32_t *q_len_h, void *out,
+                                           float *out_lse, void *workspace, size_t workspace_bytes,
+                                           hipStream_t stream);
+
 /* One tensor of a KV-block import: dst_pool is [num_dst_blocks][block_bytes],
  * src_staging is [n][block_bytes] contiguous (the restored remote copy). */
 typedef struct {

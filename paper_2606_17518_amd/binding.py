@@ -26,6 +26,7 @@ PATHS = {"auto": SPECGEN_PATH_AUTO, "dot": SPECGEN_PATH_DOT, "mfma": SPECGEN_PAT
 SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
 
 EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
+            "specgen_fork_prefill_attn_workspace_size", "specgen_fork_prefill_attn",
             "specgen_kv_import", "specgen_kv_export", "specgen_kv_append", "specgen_lse_merge", "specgen_last_error")
 
 
@@ -87,6 +88,10 @@ def lib():
         L.specgen_fork_decode_attn.restype = C.c_int
         L.specgen_fork_decode_attn_phase.argtypes = [C.POINTER(ForkBatchC), C.c_int32, P, P, P, C.c_size_t, P]
         L.specgen_fork_decode_attn_phase.restype = C.c_int
+        L.specgen_fork_prefill_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), P, C.POINTER(C.c_size_t)]
+        L.specgen_fork_prefill_attn_workspace_size.restype = C.c_int
+        L.specgen_fork_prefill_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, P, C.c_size_t, P]
+        L.specgen_fork_prefill_attn.restype = C.c_int
         L.specgen_kv_import.argtypes = [C.POINTER(KvTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
         L.specgen_kv_import.restype = C.c_int
         L.specgen_kv_export.argtypes = [C.POINTER(KvExportTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
@@ -228,6 +233,33 @@ def specgen_fork_decode_attn_phase(batch, phase: int, out: Optional[torch.Tensor
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
     _check(lib().specgen_fork_decode_attn_phase(C.byref(s), int(phase), _dptr(out), _dptr(out_lse), _dptr(workspace),
                                                 workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def _q_len(q_len) -> np.ndarray:
+    return np.ascontiguousarray(q_len, dtype=np.int32)
+
+
+def specgen_fork_prefill_attn_workspace_size(batch, q_len) -> int:
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    ql = _q_len(q_len)
+    n = C.c_size_t(0)
+    _check(lib().specgen_fork_prefill_attn_workspace_size(C.byref(s), ql.ctypes.data_as(C.c_void_p), C.byref(n)))
+    return n.value
+
+
+def alloc_prefill_workspace(batch, q_len, device="cuda") -> torch.Tensor:
+    n = specgen_fork_prefill_attn_workspace_size(batch, q_len)
+    return torch.empty(max(1, (n + 3) // 4), dtype=torch.float32, device=device)
+
+
+def specgen_fork_prefill_attn(batch, q_len, out: torch.Tensor, out_lse: Optional[torch.Tensor],
+                              workspace: torch.Tensor, stream=None) -> None:
+    """q_len: host int32 [N]; batch.q is [sum q_len][Hq][D]; out [sum q_len][Hq][D] bf16."""
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    ql = _q_len(q_len)
+    _check(lib().specgen_fork_prefill_attn(C.byref(s), ql.ctypes.data_as(C.c_void_p), _dptr(out), _dptr(out_lse),
+                                           _dptr(workspace), workspace.numel() * workspace.element_size(),
+                                           _stream(stream)))
 
 
 def specgen_kv_import(tensors: Sequence[tuple], dst_block_ids: torch.Tensor, num_dst_blocks: int,

@@ -117,23 +117,9 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   return ok();
 }
 
-}  // namespace
-
-extern "C" {
-
-specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batch_t* b, size_t* bytes) {
-  if (!bytes) return fail(SPECGEN_ERR_INVALID_ARG, "bytes is NULL");
-  Plan plan;
-  int64_t wsf = 0;
-  const specgen_status_t st = build_plan(b, &plan, &wsf);
-  if (st != SPECGEN_OK) return st;
-  *bytes = (size_t)(wsf * 4);
-  return ok();
-}
-
-specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, int32_t phase, void* out,
-                                                float* out_lse, void* workspace, size_t workspace_bytes,
-                                                hipStream_t stream) {
+// One call of the split attention for a checked batch (both phases or one).
+specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* out, float* out_lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
   if (phase != SPECGEN_PHASE_ALL && phase != SPECGEN_PHASE_PARTIALS && phase != SPECGEN_PHASE_MERGE)
     return fail(SPECGEN_ERR_INVALID_ARG, "phase %d unknown", phase);
   Plan plan;
@@ -166,6 +152,94 @@ specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, i
   if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);
   if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+// Multi-token prefill as a decode batch of virtual forks: query i of fork f
+// becomes a fork of the same trace whose suffix ends at that query's own
+// position (S_f - q_len[f] + i + 1 tokens) and reads f's block table; the
+// host mirrors change, the device arrays are shared.
+struct PrefillBatch {
+  specgen_fork_batch_t b;
+  std::vector<int32_t> fork_off, suffix_len, suffix_table_off;
+};
+
+specgen_status_t expand_prefill(const specgen_fork_batch_t* b, const int32_t* q_len_h, PrefillBatch* x) {
+  Plan plan;
+  int64_t wsf = 0;
+  const specgen_status_t st = build_plan(b, &plan, &wsf);   // checks the batch as given
+  if (st != SPECGEN_OK) return st;
+  if (!q_len_h) return fail(SPECGEN_ERR_INVALID_ARG, "q_len is NULL");
+  const int T = b->num_traces, N = b->num_forks;
+  int64_t nq = 0;
+  for (int f = 0; f < N; ++f) {
+    if (q_len_h[f] < 1 || q_len_h[f] > b->suffix_len_h[f])
+      return fail(SPECGEN_ERR_INVALID_ARG, "q_len[%d] = %d must be in 1..S_f = %d", f, q_len_h[f], b->suffix_len_h[f]);
+    nq += q_len_h[f];
+  }
+  if (nq > kMaxForks) return fail(SPECGEN_ERR_UNSUPPORTED, "%lld queries exceed %d per call", (long long)nq, kMaxForks);
+  x->b = *b;
+  x->fork_off.assign(T + 1, 0);
+  x->suffix_len.clear();
+  x->suffix_table_off.clear();
+  for (int t = 0; t < T; ++t) {
+    int64_t n = 0;
+    for (int f = b->fork_off_h[t]; f < b->fork_off_h[t + 1]; ++f) n += q_len_h[f];
+    x->fork_off[t + 1] = x->fork_off[t] + (int32_t)n;
+  }
+  for (int f = 0; f < N; ++f)
+    for (int i = 0; i < q_len_h[f]; ++i) {
+      x->suffix_len.push_back(b->suffix_len_h[f] - q_len_h[f] + i + 1);
+      x->suffix_table_off.push_back(b->suffix_table_off_h[f]);
+    }
+  x->suffix_table_off.push_back(b->suffix_table_off_h[N]);
+  x->b.num_forks = (int32_t)nq;
+  x->b.fork_off_h = x->fork_off.data();
+  x->b.suffix_len_h = x->suffix_len.data();
+  x->b.suffix_table_off_h = x->suffix_table_off.data();
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batch_t* b, size_t* bytes) {
+  if (!bytes) return fail(SPECGEN_ERR_INVALID_ARG, "bytes is NULL");
+  Plan plan;
+  int64_t wsf = 0;
+  const specgen_status_t st = build_plan(b, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  *bytes = (size_t)(wsf * 4);
+  return ok();
+}
+
+specgen_status_t specgen_fork_decode_attn_phase(const specgen_fork_batch_t* b, int32_t phase, void* out,
+                                                float* out_lse, void* workspace, size_t workspace_bytes,
+                                                hipStream_t stream) {
+  return run_batch(b, phase, out, out_lse, workspace, workspace_bytes, stream);
+}
+
+specgen_status_t specgen_fork_prefill_attn_workspace_size(const specgen_fork_batch_t* b, const int32_t* q_len_h,
+                                                          size_t* bytes) {
+  if (!bytes) return fail(SPECGEN_ERR_INVALID_ARG, "bytes is NULL");
+  PrefillBatch x;
+  specgen_status_t st = expand_prefill(b, q_len_h, &x);
+  if (st != SPECGEN_OK) return st;
+  Plan plan;
+  int64_t wsf = 0;
+  st = build_plan(&x.b, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  *bytes = (size_t)(wsf * 4);
+  return ok();
+}
+
+specgen_status_t specgen_fork_prefill_attn(const specgen_fork_batch_t* b, const int32_t* q_len_h, void* out,
+                                           float* out_lse, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream) {
+  PrefillBatch x;
+  const specgen_status_t st = expand_prefill(b, q_len_h, &x);
+  if (st != SPECGEN_OK) return st;
+  return run_batch(&x.b, SPECGEN_PHASE_ALL, out, out_lse, workspace, workspace_bytes, stream);
 }
 
 specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t* b, void* out, float* out_lse,

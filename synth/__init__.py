@@ -48,6 +48,12 @@ WORKLOADS = {
                    suffix_range=(128, 1024), num_q_heads=64, num_kv_heads=8, head_dim=128, key_bias_std=0.5,
                    num_blocks=16384),
         import_prefix=False),
+    # multi-token prefill over the P=32768 trace of trace_p32k_f16: each of its
+    # 16 forks processes its last 16 suffix tokens as queries (256 queries)
+    "prefill_p32k_f16_q16": dict(
+        batch=dict(prefix_lens=[32768], forks_per_trace=16, suffix_range=(128, 1024), num_q_heads=64,
+                   num_kv_heads=8, head_dim=128, key_bias_std=0.5, num_blocks=16384),
+        import_prefix=False, prefill_q=16),
 }
 WORKLOAD_SEEDS = {name: i + 1 for i, name in enumerate(WORKLOADS)}
 

@@ -29,7 +29,8 @@ def L():
 def test_every_declared_symbol_is_exported(L):
     names = _declared()
     assert set(names) == {"specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn",
-                          "specgen_fork_decode_attn_phase", "specgen_kv_import", "specgen_kv_export",
+                          "specgen_fork_decode_attn_phase", "specgen_fork_prefill_attn_workspace_size",
+                          "specgen_fork_prefill_attn", "specgen_kv_import", "specgen_kv_export",
                           "specgen_kv_append", "specgen_lse_merge", "specgen_last_error"}
     for n in names:
         assert hasattr(L, n), n
@@ -187,3 +188,28 @@ def test_nested_prefix_parents_validated(L, parent, status):
         L.specgen_last_error().decode()
     if status == 0:
         assert n.value > 0
+
+
+def test_prefill_q_len_validated(L):
+    import paper_2606_17518_amd.binding as B
+    s, keep = _host_batch()             # suffix lengths 3 and 0
+    n = C.c_size_t(7)
+    for ql, status in (([1, 1], 1), ([0, 0], 1), ([4, 0], 1), (None, 1)):
+        arr = None if ql is None else np.array(ql, np.int32)
+        p = None if arr is None else arr.ctypes.data_as(C.c_void_p)
+        assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s), p, C.byref(n)) == status
+        assert L.specgen_fork_prefill_attn(C.byref(s), p, C.c_void_p(0x10000), None, None, 0, None) == status
+    assert n.value == 7
+    s2, keep2 = _host_batch(suffix_len_h=np.array([3, 2], np.int32).ctypes.data)
+    keep2.append(s2)
+    ql = np.array([3, 2], np.int32)
+    suf = np.array([3, 2], np.int32)
+    s2.suffix_len_h = suf.ctypes.data
+    assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s2), ql.ctypes.data_as(C.c_void_p), C.byref(n)) == 0
+    assert n.value > 0
+    # more than 512 queries in one call
+    s3, keep3 = _host_batch()
+    big = np.array([600, 1], np.int32)
+    s3.suffix_len_h = big.ctypes.data
+    ql3 = np.array([600, 1], np.int32)
+    assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s3), ql3.ctypes.data_as(C.c_void_p), C.byref(n)) == 2
