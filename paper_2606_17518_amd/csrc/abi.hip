@@ -45,7 +45,9 @@ int device_cus() {
 }
 
 // Checks the batch and builds the plan; `ws_floats` receives the workspace size.
-specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* ws_floats) {
+// `ptab_sel` (internal, [T] or NULL): traces whose prefix ids index the suffix table.
+specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* ws_floats,
+                            const int32_t* ptab_sel = nullptr) {
   if (!b) return fail(SPECGEN_ERR_INVALID_ARG, "batch is NULL");
   if (b->reserved != 0) return fail(SPECGEN_ERR_INVALID_ARG, "reserved field must be 0");
   if (b->num_traces < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_traces must be >= 1 (got %d)", b->num_traces);
@@ -79,6 +81,7 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.policy = b->path;
   in.fork_off = b->fork_off_h;
   in.prefix_parent = b->prefix_parent_h;
+  in.prefix_in_suffix_table = ptab_sel;
   in.prefix_len = b->prefix_len_h;
   in.suffix_len = b->suffix_len_h;
   in.prefix_table_off = b->prefix_table_off_h;
@@ -119,12 +122,12 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
 
 // One call of the split attention for a checked batch (both phases or one).
 specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* out, float* out_lse, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+                           size_t workspace_bytes, hipStream_t stream, const int32_t* ptab_sel = nullptr) {
   if (phase != SPECGEN_PHASE_ALL && phase != SPECGEN_PHASE_PARTIALS && phase != SPECGEN_PHASE_MERGE)
     return fail(SPECGEN_ERR_INVALID_ARG, "phase %d unknown", phase);
   Plan plan;
   int64_t wsf = 0;
-  specgen_status_t st = build_plan(b, &plan, &wsf);
+  specgen_status_t st = build_plan(b, &plan, &wsf, ptab_sel);
   if (st != SPECGEN_OK) return st;
   if (!out && phase != SPECGEN_PHASE_PARTIALS) return fail(SPECGEN_ERR_INVALID_ARG, "out is NULL");
   if ((size_t)(wsf * 4) > workspace_bytes || (wsf > 0 && !workspace))
@@ -155,12 +158,16 @@ specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* o
 }
 
 // Multi-token prefill as a decode batch of virtual forks: query i of fork f
-// becomes a fork of the same trace whose suffix ends at that query's own
-// position (S_f - q_len[f] + i + 1 tokens) and reads f's block table; the
-// host mirrors change, the device arrays are shared.
+// becomes a fork whose suffix ends at that query's own position (S_f -
+// q_len[f] + i + 1 tokens).  Where every fork of a trace has at least one
+// whole block of suffix before its first query, each such fork also becomes a
+// trace nested under its own trace: its prefix is those whole blocks (listed
+// in the suffix table), shared by the fork's queries, and each query keeps
+// only the tokens from the next block on.  The host mirrors change; the
+// device arrays are shared.
 struct PrefillBatch {
   specgen_fork_batch_t b;
-  std::vector<int32_t> fork_off, suffix_len, suffix_table_off;
+  std::vector<int32_t> fork_off, prefix_len, prefix_table_off, parent, sel, suffix_len, suffix_table_off;
 };
 
 specgen_status_t expand_prefill(const specgen_fork_batch_t* b, const int32_t* q_len_h, PrefillBatch* x) {
@@ -177,23 +184,67 @@ specgen_status_t expand_prefill(const specgen_fork_batch_t* b, const int32_t* q_
     nq += q_len_h[f];
   }
   if (nq > kMaxForks) return fail(SPECGEN_ERR_UNSUPPORTED, "%lld queries exceed %d per call", (long long)nq, kMaxForks);
+  // whole suffix blocks before each fork's first query
+  auto shared = [&](int f) { return (b->suffix_len_h[f] - q_len_h[f] + 1) / kBlock * kBlock; };
+  // traces whose forks all get a nested trace, within the trace and depth limits
+  std::vector<char> nest(T, 0);
+  int budget = kMaxTraces - T;
+  for (int t = 0; t < T; ++t) {
+    bool ok = plan.fork_off[t + 1] - plan.fork_off[t] <= budget;
+    int d = 1;
+    for (int a = plan.parent[t]; a >= 0; a = plan.parent[a]) ++d;
+    ok = ok && d < kMaxDepth && plan.fork_off[t + 1] > plan.fork_off[t];
+    for (int f = plan.fork_off[t]; ok && f < plan.fork_off[t + 1]; ++f) ok = shared(f) >= kBlock;
+    if (ok) {
+      nest[t] = 1;
+      budget -= plan.fork_off[t + 1] - plan.fork_off[t];
+    }
+  }
   x->b = *b;
-  x->fork_off.assign(T + 1, 0);
+  x->fork_off.assign(1, 0);
+  x->prefix_len.clear();
+  x->prefix_table_off.clear();
+  x->parent.clear();
+  x->sel.clear();
   x->suffix_len.clear();
   x->suffix_table_off.clear();
-  for (int t = 0; t < T; ++t) {
-    int64_t n = 0;
-    for (int f = b->fork_off_h[t]; f < b->fork_off_h[t + 1]; ++f) n += q_len_h[f];
-    x->fork_off[t + 1] = x->fork_off[t] + (int32_t)n;
-  }
-  for (int f = 0; f < N; ++f)
+  std::vector<int32_t> pos(T, -1);   // index of each original trace in the new list
+  int nv = 0;                        // virtual forks so far
+  auto add_queries = [&](int f, int skip) {   // fork f's queries, each suffix starting after `skip` tokens
     for (int i = 0; i < q_len_h[f]; ++i) {
-      x->suffix_len.push_back(b->suffix_len_h[f] - q_len_h[f] + i + 1);
-      x->suffix_table_off.push_back(b->suffix_table_off_h[f]);
+      x->suffix_len.push_back(b->suffix_len_h[f] - q_len_h[f] + i + 1 - skip);
+      x->suffix_table_off.push_back(b->suffix_table_off_h[f] + skip / kBlock);
+      ++nv;
     }
+  };
+  for (int t = 0; t < T; ++t) {
+    pos[t] = (int)x->prefix_len.size();
+    x->prefix_len.push_back(b->prefix_len_h[t]);
+    x->prefix_table_off.push_back(b->prefix_table_off_h[t]);
+    x->parent.push_back(plan.parent[t] < 0 ? -1 : pos[plan.parent[t]]);
+    x->sel.push_back(0);
+    if (!nest[t])
+      for (int f = plan.fork_off[t]; f < plan.fork_off[t + 1]; ++f) add_queries(f, 0);
+    x->fork_off.push_back(nv);
+    if (nest[t]) {
+      for (int f = plan.fork_off[t]; f < plan.fork_off[t + 1]; ++f) {
+        x->prefix_len.push_back(shared(f));
+        x->prefix_table_off.push_back(b->suffix_table_off_h[f]);
+        x->parent.push_back(pos[t]);
+        x->sel.push_back(1);
+        add_queries(f, shared(f));
+        x->fork_off.push_back(nv);
+      }
+    }
+  }
+  x->prefix_table_off.push_back(b->prefix_table_off_h[T]);
   x->suffix_table_off.push_back(b->suffix_table_off_h[N]);
+  x->b.num_traces = (int32_t)x->prefix_len.size();
   x->b.num_forks = (int32_t)nq;
   x->b.fork_off_h = x->fork_off.data();
+  x->b.prefix_len_h = x->prefix_len.data();
+  x->b.prefix_table_off_h = x->prefix_table_off.data();
+  x->b.prefix_parent_h = x->parent.data();
   x->b.suffix_len_h = x->suffix_len.data();
   x->b.suffix_table_off_h = x->suffix_table_off.data();
   return ok();
@@ -227,7 +278,7 @@ specgen_status_t specgen_fork_prefill_attn_workspace_size(const specgen_fork_bat
   if (st != SPECGEN_OK) return st;
   Plan plan;
   int64_t wsf = 0;
-  st = build_plan(&x.b, &plan, &wsf);
+  st = build_plan(&x.b, &plan, &wsf, x.sel.data());
   if (st != SPECGEN_OK) return st;
   *bytes = (size_t)(wsf * 4);
   return ok();
@@ -239,7 +290,7 @@ specgen_status_t specgen_fork_prefill_attn(const specgen_fork_batch_t* b, const 
   PrefillBatch x;
   const specgen_status_t st = expand_prefill(b, q_len_h, &x);
   if (st != SPECGEN_OK) return st;
-  return run_batch(&x.b, SPECGEN_PHASE_ALL, out, out_lse, workspace, workspace_bytes, stream);
+  return run_batch(&x.b, SPECGEN_PHASE_ALL, out, out_lse, workspace, workspace_bytes, stream, x.sel.data());
 }
 
 specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t* b, void* out, float* out_lse,

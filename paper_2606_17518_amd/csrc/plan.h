@@ -78,7 +78,7 @@ struct PlanHead {
 };
 
 // The whole plan, computed on the host from the length mirrors and passed to
-// every kernel by value (about 7.6 KB of kernel arguments); each workgroup
+// every kernel by value (about 7.8 KB of kernel arguments); each workgroup
 // copies it into LDS with one vector load per thread (plan_to_lds).
 struct alignas(16) Plan : PlanHead {
   int32_t fork_off[kMaxTraces + 1];
@@ -89,6 +89,9 @@ struct alignas(16) Plan : PlanHead {
   // [fork_off[t], fork_end[t]): the rows of t's prefix items.
   int32_t parent[kMaxTraces];       // -1 for a root
   int32_t fork_end[kMaxTraces];
+  // 1: trace t's prefix blocks are listed in the suffix table (a prefill
+  // shares the whole blocks before a fork's first query as a nested prefix)
+  int32_t ptab_sel[kMaxTraces];
   int32_t trace_part[kMaxTraces];   // partition of trace t's prefix items
   int32_t trace_pos[kMaxTraces];    // index of t in ptrace
   int32_t ptrace[kMaxTraces];       // traces grouped by partition, ascending within each

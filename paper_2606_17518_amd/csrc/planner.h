@@ -19,6 +19,7 @@ struct PlanInputs {
   int T, N, Hq, Hkv, D, policy;
   const int32_t* fork_off;    // [T+1]
   const int32_t* prefix_parent;  // [T] parent trace or -1, or NULL (every trace a root)
+  const int32_t* prefix_in_suffix_table;  // [T] 1: trace t's prefix ids index the suffix table; or NULL
   const int32_t* prefix_len;  // [T]
   const int32_t* suffix_len;  // [N]
   const int32_t* prefix_table_off;  // [T+1]
@@ -61,7 +62,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   const int32_t* fo = in.fork_off;
   if (fo[0] != 0 || fo[T] != N) SG_FAIL(kPlanInvalid, "fork_off must start at 0 and end at num_forks");
   for (int t = 0; t < T; ++t) {
-    if (fo[t + 1] <= fo[t]) SG_FAIL(kPlanInvalid, "trace %d has no forks", t);
+    if (fo[t + 1] < fo[t]) SG_FAIL(kPlanInvalid, "fork_off must be nondecreasing (trace %d)", t);
     if (in.prefix_len[t] < 1) SG_FAIL(kPlanInvalid, "prefix_len[%d] must be >= 1", t);
   }
   for (int f = 0; f < N; ++f)
@@ -87,6 +88,8 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   for (int t = T - 1; t >= 0; --t) {   // one past the last trace of t's subtree
     sub_end[t] = t + 1;
     while (sub_end[t] < T && depth[sub_end[t]] > depth[t]) sub_end[t] = sub_end[sub_end[t]];
+    // a trace may have no forks of its own only if traces nested below it have some
+    if (fo[sub_end[t]] <= fo[t]) SG_FAIL(kPlanInvalid, "trace %d has no forks", t);
   }
 
   const int g = Hq / Hkv;
@@ -103,6 +106,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
   for (int t = 0; t < T; ++t) {
     plan->parent[t] = parent[t];
     plan->fork_end[t] = fo[sub_end[t]];
+    plan->ptab_sel[t] = in.prefix_in_suffix_table ? (in.prefix_in_suffix_table[t] != 0) : 0;
   }
   for (int t = 0; t < T; ++t) plan->prefix_len[t] = in.prefix_len[t];
   for (int t = 0; t <= T; ++t) plan->prefix_table_off[t] = in.prefix_table_off[t];

@@ -91,7 +91,8 @@ __device__ WorkerRange worker_walk_tiles(const AttnArgs& a, const Plan& plan, in
       const ItemRef& it = tr.it;
       const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
       const int lastblk = (nv - 1) / 16;
-      const int32_t* tab = it.kind == 0 ? a.prefix_table + plan.prefix_table_off[it.t]
+      const int32_t* tab = it.kind == 0 ? (plan.ptab_sel[it.t] ? a.suffix_table : a.prefix_table) +
+                                              plan.prefix_table_off[it.t]
                                         : a.suffix_table + plan.suffix_table_off[it.f];
 #pragma unroll
       for (int b = 0; b < kIdsPerTile; ++b) {
@@ -181,7 +182,7 @@ __device__ WorkerRange worker_prepass(const AttnArgs& a, const Plan& plan, int p
     const int32_t* d = items + ii * kItemInts;
     int bi = (d[IT_TILE0] + (r - d[IT_RTILE0])) * kIdsPerTile + b;
     if (bi > d[IT_LASTBLK]) bi = d[IT_LASTBLK];
-    const int32_t* tab = d[IT_KIND] == 0 ? a.prefix_table : a.suffix_table;
+    const int32_t* tab = (d[IT_KIND] == 0 && !plan.ptab_sel[d[IT_T]]) ? a.prefix_table : a.suffix_table;
     const int id = tab[d[IT_TABOFF] + bi];
     ids[e] = id;
     if (scales) {

@@ -328,6 +328,7 @@ int main(int argc, char** argv) {
       }
     }
     in.prefix_parent = nested ? parent.data() : nullptr;
+    in.prefix_in_suffix_table = nullptr;
     in.fork_off = fo.data();
     in.prefix_len = P.data();
     in.suffix_len = S.data();

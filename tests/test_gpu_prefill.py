@@ -32,6 +32,14 @@ CASES = {
     "chain": dict(batch=dict(prefix_lens=[100, 33], prefix_parent=[-1, 0], forks_per_trace=[2, 2],
                              suffix_lens=[20, 8, 64, 2], num_q_heads=8, num_kv_heads=1, head_dim=64),
                   q_len=[4, 8, 30, 2]),
+    # every fork has whole suffix blocks before its first query: they become a
+    # nested prefix shared by the fork's queries (a trace with no forks of its own)
+    "nest_single": dict(batch=dict(prefix_lens=[300], forks_per_trace=4, suffix_lens=[40, 21, 100, 33],
+                                   num_q_heads=8, num_kv_heads=2, head_dim=64), q_len=[5, 5, 17, 1]),
+    # one trace nests its forks' blocks, the trace below it cannot (a fork with 3 suffix tokens)
+    "nest_mixed": dict(batch=dict(prefix_lens=[100, 50], prefix_parent=[-1, 0], forks_per_trace=[2, 2],
+                                  suffix_lens=[40, 70, 3, 64], num_q_heads=16, num_kv_heads=2, head_dim=128),
+                       q_len=[3, 10, 2, 20]),
     # many queries: 16 forks x 16 queries over an 8-head GQA group (2048 rows per kv head)
     "gqa8_q16": dict(batch=dict(prefix_lens=[1500], forks_per_trace=16, suffix_range=(16, 100), num_q_heads=64,
                                 num_kv_heads=8, head_dim=128), q_len=[16] * 16),
