@@ -109,18 +109,18 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
   const int64_t rows = (int64_t)plan.N * plan.Hq;
   const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-  // without nested prefixes a row has one prefix item; otherwise up to kMaxDepth
-  const bool nested = plan.depth > 1;
-  if (plan.D == 128) {
-    if (nested)
-      hipLaunchKernelGGL((fork_merge_kernel<128, kMaxDepth>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-    else
-      hipLaunchKernelGGL((fork_merge_kernel<128, 1>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-  } else {
-    if (nested)
-      hipLaunchKernelGGL((fork_merge_kernel<64, kMaxDepth>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-    else
-      hipLaunchKernelGGL((fork_merge_kernel<64, 1>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+  // the merge walks as many prefix items per row as the longest chain needs,
+  // rounded up to 1, 2, 4 or kMaxDepth
+  const int dep = plan.depth <= 1 ? 1 : plan.depth <= 2 ? 2 : plan.depth <= 4 ? 4 : kMaxDepth;
+  switch (dep * 1000 + plan.D) {
+#define SG_CASE(DEP, DD)                                                                                  \
+  case DEP * 1000 + DD:                                                                                   \
+    hipLaunchKernelGGL((fork_merge_kernel<DD, DEP>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse); \
+    break;
+    SG_CASE(1, 128) SG_CASE(2, 128) SG_CASE(4, 128) SG_CASE(kMaxDepth, 128)
+    SG_CASE(1, 64) SG_CASE(2, 64) SG_CASE(4, 64) SG_CASE(kMaxDepth, 64)
+#undef SG_CASE
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
