@@ -99,8 +99,9 @@ typedef struct {
   const float *k_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
   const float *v_scale;      /* [num_blocks] fp32 for E4M3, else NULL            */
   const int32_t *fork_off;   /* [T+1], fork_off[0] = 0, nondecreasing, [T] = N;
-                                forks of trace t are [fork_off[t], fork_off[t+1]),
-                                each trace has at least one fork                */
+                                forks of trace t are [fork_off[t], fork_off[t+1]);
+                                a trace has at least one fork of its own or in a
+                                trace nested below it (prefix_parent_h)          */
   const int32_t *prefix_len; /* [T], P_t >= 1                                    */
   const int32_t *prefix_table_off; /* [T+1]; trace t's ids are
                                 prefix_table[prefix_table_off[t] ..], at least

@@ -6,6 +6,8 @@
 // One wavefront merges one output row: lane p first takes part p's lse to
 // find the running max and weights (chunks of 64 parts, rescaled between
 // chunks), then all lanes sweep the parts over the head dimension.
+#include <algorithm>
+
 #include "merge.h"
 
 namespace specgen {
@@ -101,14 +103,17 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
   __shared__ Plan splan;
   __shared__ MergeItemLoc sloc[4][kDepth + 1];   // each wave's item table (nested prefixes)
   plan_to_lds<256>(plan_arg, splan);
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= (int64_t)splan.N * splan.Hq) return;
-  fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
+  // a wave per row; with more rows than the grid holds, waves take every
+  // (4 * gridDim.x)-th row, so fewer workgroups copy the plan
+  const int64_t rows = (int64_t)splan.N * splan.Hq;
+  for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < rows; row += (int64_t)gridDim.x * 4)
+    fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
   const int64_t rows = (int64_t)plan.N * plan.Hq;
-  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  constexpr int64_t kMaxMergeBlocks = 2048;   // 8 per CU; beyond that waves loop over rows
+  const dim3 grid((unsigned)std::min<int64_t>((rows + 3) / 4, kMaxMergeBlocks)), block(256);
   // the merge walks as many prefix items per row as the longest chain needs,
   // rounded up to 1, 2, 4 or kMaxDepth
   const int dep = plan.depth <= 1 ? 1 : plan.depth <= 2 ? 2 : plan.depth <= 4 ? 4 : kMaxDepth;
