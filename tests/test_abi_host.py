@@ -213,3 +213,18 @@ def test_prefill_q_len_validated(L):
     s3.suffix_len_h = big.ctypes.data
     ql3 = np.array([600, 1], np.int32)
     assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s3), ql3.ctypes.data_as(C.c_void_p), C.byref(n)) == 2
+
+
+@pytest.mark.parametrize("fork_off,parent,status", [
+    ([0, 0, 2], [-1, 0], 0),        # the root has no forks of its own, its child has two
+    ([0, 2, 2], [-1, 0], 1),        # an empty leaf
+    ([0, 0, 2], [-1, -1], 1),       # an empty root with nothing below it
+])
+def test_trace_without_own_forks(L, fork_off, parent, status):
+    s, keep = _tree_batch(parent, forks=1)
+    fo = np.array(fork_off, np.int32)
+    keep.append(fo)
+    s.fork_off_h = fo.ctypes.data
+    n = C.c_size_t(0)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status, \
+        L.specgen_last_error().decode()

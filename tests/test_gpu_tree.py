@@ -20,6 +20,9 @@ CASES = {
     # a chain of the maximum depth (8 traces), one fork per level
     "chain8": dict(prefix_lens=[100, 33, 16, 1, 250, 7, 64, 90], prefix_parent=[-1, 0, 1, 2, 3, 4, 5, 6],
                    forks_per_trace=1, suffix_range=(0, 40), num_q_heads=8, num_kv_heads=1, head_dim=64),
+    # a root with no forks of its own: its prefix serves only the forks of the trace below it
+    "empty_root": dict(prefix_lens=[64, 40], prefix_parent=[-1, 0], forks_per_trace=[0, 3],
+                       suffix_lens=[0, 9, 33], num_q_heads=8, num_kv_heads=2, head_dim=128),
     # the shape of the nested workload, scaled down: 4 / 6 / 6 forks at three levels
     "chain3_gqa8": dict(prefix_lens=[2048, 1024, 1000], prefix_parent=[-1, 0, 1], forks_per_trace=[4, 6, 6],
                         suffix_range=(10, 200), num_q_heads=64, num_kv_heads=8, head_dim=128, key_bias_std=0.5),
