@@ -49,7 +49,10 @@
  * thread's most recent non-OK status.
  * Streams: all work is asynchronous on `stream` (0 = the null stream) of the
  * current HIP device.  Results are deterministic: the work split depends only
- * on the lengths, and no floating-point atomics are used.
+ * on the lengths, and no floating-point atomics are used.  A call queues
+ * kernel launches only (no allocation, copy or memset), so it can be captured
+ * into a HIP graph; a replay uses the lengths of the captured call and the
+ * device buffers' contents at replay time.
  */
 #ifndef SPECGEN_H
 #define SPECGEN_H
