@@ -274,7 +274,13 @@ typedef struct {
  * token. */
 specgen_status_t specgen_kv_append(const specgen_kv_append_t *a, hipStream_t stream);
 
-/* Log-sum-exp merge of S partial attention results over disjoint key sets:
+/* Log-sum-exp merge of S partial attention results over disjoint key sets.
+ * No passage of the paper defines this step: it serves through an inference
+ * engine and gives no attention arithmetic.  The merge is the identity that
+ * softmax attention over a union of disjoint key sets satisfies, which lets
+ * the key axis of the fork-decode step (the shared prefix of Sec. 4.2 and
+ * Sec. 8.7 plus each fork's suffix) be split across workgroups; the same
+ * identity is how partial results from several devices would be combined.
  *   M = max_s lse[s][r]; w_s = exp(lse[s][r] - M);
  *   out[r] = sum_s w_s o[s][r] / sum_s w_s; out_lse[r] = M + ln sum_s w_s.
  * A part with lse = -inf is empty and its o is ignored; a row with only empty

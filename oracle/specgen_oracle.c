@@ -22,9 +22,10 @@
  * directions, and an element copy of each fork's new token into the paged
  * layout.
  * The conventions it fixes where the paper is silent (GQA grouping, natural
- * log LSE, paged layout [block][slot][kv_head][dim], OCP E4M3 decode, a
- * block-wide fp32 dequantisation scale) are listed with the header that
- * declares the GPU entry points.
+ * log LSE, OCP E4M3 decode, a block-wide fp32 dequantisation scale, and the
+ * paged layout: K pool [block][kv_head][slot][dim], V pool transposed as
+ * [block][kv_head][dim][slot]) are listed with the header that declares the
+ * GPU entry points.
  */
 #include <math.h>
 #include <stdint.h>

@@ -44,6 +44,22 @@ int device_cus() {
   return cus;
 }
 
+// A block-table offset mirror off[0..n] for lengths len[0..n-1]: off[0] >= 0,
+// and range i, [off[i], off[i+1]), holds at least ceil(len[i] / 16) ids.
+specgen_status_t check_table_offsets(const char* what, const int32_t* off, const int32_t* len, int n) {
+  if (n > kMaxForks) n = kMaxForks;   // the planner rejects larger batches
+  if (off[0] < 0) return fail(SPECGEN_ERR_INVALID_ARG, "%s_table_off[0] = %d must be >= 0", what, off[0]);
+  for (int i = 0; i < n; ++i) {
+    if (off[i + 1] < off[i])
+      return fail(SPECGEN_ERR_INVALID_ARG, "%s_table_off must be nondecreasing (index %d)", what, i);
+    const int64_t need = len[i] > 0 ? ((int64_t)len[i] + kBlock - 1) / kBlock : 0;
+    if ((int64_t)off[i + 1] - off[i] < need)
+      return fail(SPECGEN_ERR_INVALID_ARG, "%s_table_off gives %d ids to entry %d, which needs %lld", what,
+                  off[i + 1] - off[i], i, (long long)need);
+  }
+  return ok();
+}
+
 // Checks the batch and builds the plan; `ws_floats` receives the workspace size.
 // `ptab_sel` (internal, [T] or NULL): traces whose prefix ids index the suffix table.
 specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* ws_floats,
@@ -70,6 +86,16 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   if (!b->suffix_table) {   // only a batch without suffix tokens may omit the suffix table
     for (int f = 0; f < b->num_forks; ++f)
       if (b->suffix_len_h[f] > 0) return fail(SPECGEN_ERR_INVALID_ARG, "suffix_table is NULL but fork %d has suffix tokens", f);
+  }
+  if (!ptab_sel) {
+    // The caller's table offsets: non-negative, nondecreasing, and each range
+    // long enough for its length (the kernels read ceil(len/16) ids from the
+    // start of a range, with no bound of their own).  Internal batches
+    // (ptab_sel set) derive their offsets from a batch checked here.
+    specgen_status_t st = check_table_offsets("prefix", b->prefix_table_off_h, b->prefix_len_h, b->num_traces);
+    if (st != SPECGEN_OK) return st;
+    st = check_table_offsets("suffix", b->suffix_table_off_h, b->suffix_len_h, b->num_forks);
+    if (st != SPECGEN_OK) return st;
   }
   const bool fp8 = b->kv_dtype == SPECGEN_FP8_E4M3;
   PlanInputs in;

@@ -8,20 +8,15 @@
 namespace specgen {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #define SG_LDS __attribute__((address_space(3)))
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
@@ -46,30 +41,6 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
 __device__ __forceinline__ f32x2 unpack_f16x2(uint32_t w) {
   typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
   return __builtin_convertvector(__builtin_bit_cast(f16x2_t, w), f32x2);
-}
-
-__device__ __forceinline__ float wave_max_xor(float v, int mask) {
-  return fmaxf(v, __shfl_xor(v, mask, 64));
-}
-
-// acc *= alpha for an MFMA accumulator that lives in AGPRs: read, scale and
-// write back inside one asm block so the compiler keeps the accumulator in
-// AGPRs instead of shuttling every accumulator through VGPRs around the
-// (rare) rescale branch.  alpha usually comes straight from v_exp_f32, and a
-// VALU read of a transcendental result needs wait states the compiler cannot
-// insert inside an asm block, hence the leading s_nop.
-__device__ __forceinline__ void scale_acc(f32x4& acc, float alpha) {
-  float x0 = acc[0], x1 = acc[1], x2 = acc[2], x3 = acc[3];
-  float t;
-  asm volatile(
-      "s_nop 4\n\t"
-      "v_accvgpr_read_b32 %4, %0\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %0, %4\n\t"
-      "v_accvgpr_read_b32 %4, %1\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %1, %4\n\t"
-      "v_accvgpr_read_b32 %4, %2\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %2, %4\n\t"
-      "v_accvgpr_read_b32 %4, %3\n\tv_mul_f32 %4, %4, %5\n\tv_accvgpr_write_b32 %3, %4"
-      : "+a"(x0), "+a"(x1), "+a"(x2), "+a"(x3), "=&v"(t)
-      : "v"(alpha));
-  acc = f32x4{x0, x1, x2, x3};
 }
 
 // Max / sum over the four 16-lane rows of a wave (lanes l, l^16, l^32, l^48)
@@ -119,13 +90,10 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // so the compiler does not place that wait inside the hot loop instead.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// LDS swizzles: K chunks are XOR-ed so a 16-key MFMA operand read hits
-// distinct banks; V chunks are XOR-ed by even values (8-byte halves stay
-// together) so the 4 keys of a transposing read hit distinct 32-byte groups.
+// LDS swizzle of K chunks: XOR-ed so a 16-key MFMA operand read hits
+// distinct banks.
 template <int CPR>
 __device__ __forceinline__ int swz_k(int tok) { return ((tok & 3) | ((tok >> 1) & 12)) & (CPR - 1); }
-template <int CPR>
-__device__ __forceinline__ int swz_v(int tok) { return (2 * ((tok & 3) | ((tok >> 1) & 4))) & (CPR - 1); }
 
 // Partial-result and plan arguments shared by the attention kernels.
 struct AttnArgs {

@@ -200,17 +200,19 @@ def test_prefill_q_len_validated(L):
         assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s), p, C.byref(n)) == status
         assert L.specgen_fork_prefill_attn(C.byref(s), p, C.c_void_p(0x10000), None, None, 0, None) == status
     assert n.value == 7
-    s2, keep2 = _host_batch(suffix_len_h=np.array([3, 2], np.int32).ctypes.data)
-    keep2.append(s2)
+    s2, keep2 = _host_batch()
     ql = np.array([3, 2], np.int32)
     suf = np.array([3, 2], np.int32)
-    s2.suffix_len_h = suf.ctypes.data
+    soff = np.array([0, 1, 2], np.int32)
+    keep2 += [suf, soff]
+    s2.suffix_len_h, s2.suffix_table_off_h = suf.ctypes.data, soff.ctypes.data
     assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s2), ql.ctypes.data_as(C.c_void_p), C.byref(n)) == 0
     assert n.value > 0
     # more than 512 queries in one call
     s3, keep3 = _host_batch()
     big = np.array([600, 1], np.int32)
-    s3.suffix_len_h = big.ctypes.data
+    boff = np.array([0, 38, 39], np.int32)
+    s3.suffix_len_h, s3.suffix_table_off_h = big.ctypes.data, boff.ctypes.data
     ql3 = np.array([600, 1], np.int32)
     assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s3), ql3.ctypes.data_as(C.c_void_p), C.byref(n)) == 2
 
@@ -228,3 +230,37 @@ def test_trace_without_own_forks(L, fork_off, parent, status):
     n = C.c_size_t(0)
     assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status, \
         L.specgen_last_error().decode()
+
+
+@pytest.mark.parametrize("which,off,lens,status", [
+    ("prefix", [-100000, 2], None, 1),           # negative start
+    ("prefix", [0, 1], None, 1),                 # 20 prefix tokens need 2 ids
+    ("prefix", [3, 5], None, 0),                 # any start, enough ids
+    ("suffix", [0, 0, 0], None, 1),              # fork 0 has 3 tokens and no id
+    ("suffix", [0, 1, 0], None, 1),              # decreasing
+    ("suffix", [-1, 0, 0], None, 1),             # negative start
+    ("suffix", [4, 5, 5], None, 0),
+    ("suffix", [0, 1, 1], [17, 0], 1),           # 17 tokens need 2 ids
+    ("suffix", [0, 2, 2], [17, 0], 0),
+    ("suffix", [0, 2, 2], [17, 1], 1),           # fork 1's one token needs one id
+])
+def test_table_offsets_validated(L, which, off, lens, status):
+    """Offset mirrors that would make the kernels read past a fork's or trace's
+    ids are rejected before any launch (decode and prefill entry points)."""
+    s, keep = _host_batch()
+    o = np.array(off, np.int32)
+    keep.append(o)
+    setattr(s, f"{which}_table_off_h", o.ctypes.data)
+    if lens is not None:
+        ln = np.array(lens, np.int32)
+        keep.append(ln)
+        s.suffix_len_h = ln.ctypes.data
+    n = C.c_size_t(5)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status, L.specgen_last_error().decode()
+    if status:
+        assert n.value == 5
+        assert "table_off" in L.specgen_last_error().decode()
+        assert L.specgen_fork_decode_attn(C.byref(s), C.c_void_p(0x10000), None, None, 0, None) == status
+        ql = np.ones(2, np.int32)
+        assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s), ql.ctypes.data_as(C.c_void_p),
+                                                          C.byref(n)) == status
