@@ -12,11 +12,16 @@ was restored R-1 steps earlier.
 
 Prints one JSON line.  `value` is the attention call's achieved HBM rate in
 GB/s: algorithmic bytes (each valid prefix token's K/V once per kv head, each
-suffix token's K/V once, q in, out/lse out, index arrays) over the average
-attention time measured with HIP events on the launch stream.  The export of
-the same prefix blocks (specgen_kv_export) and the per-step append of every
-fork's next token (specgen_kv_append) are timed on their own and reported
-beside the import; they are not part of `value`.
+suffix token's K/V once, q in, out/lse out, index arrays) over the median
+attention time measured with HIP events on the launch stream, cold (the
+replica it reads was last touched three steps earlier).  Beside it: the same
+call warm (one replica, repeated), and replayed from HIP graphs (one captured
+call per replica, replayed in rotation, so still cold); the partial kernel's
+own time (the roofline figure); the streaming read and copy rates a plain
+kernel reaches on this GPU (the practical ceilings); the export of the same
+prefix blocks (specgen_kv_export) and the per-step append of every fork's next
+token (specgen_kv_append), timed on their own; and the oracle on the host's
+cores (all of them, and one).
 """
 from __future__ import annotations
 
@@ -71,10 +76,22 @@ def traffic_from_profile(workload: str):
     return d.get("traffic_bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(batch, target_s: float, q_len=None, step_bytes=None):
     """The fp64 oracle on the same workload on this host's cores: whole decode
     steps (every fork and q head; every query with q_len) repeated until about
-    target_s of CPU work."""
+    target_s of CPU work on all threads; then one thread on a sample of rows
+    (about target_s / 3), scaled to a whole step by the fraction of rows."""
     import oracle
     run = (lambda: oracle.fork_decode_attn(batch)) if q_len is None else (lambda: oracle.fork_prefill_attn(batch, q_len))
     t0 = time.perf_counter()
@@ -86,10 +103,67 @@ def cpu_baseline(batch, target_s: float, q_len=None, step_bytes=None):
     dt = time.perf_counter() - t0
     step_s = dt / reps
     step_bytes = batch.algorithmic_bytes() if step_bytes is None else step_bytes
+    # one thread, on the first rows of the step (rows cost alike: every row
+    # of a fork reads the same keys)
+    cores = oracle.max_threads()
+    nq = batch.num_forks if q_len is None else int(np.sum(q_len))
+    total_rows = nq * batch.num_q_heads
+    n1 = max(1, min(total_rows, int(total_rows * (target_s / 3) / (step_s * cores))))
+    rows = np.stack(np.divmod(np.arange(n1), batch.num_q_heads), axis=1).astype(np.int32)
+    t1 = time.perf_counter()
+    if q_len is None:
+        oracle.fork_decode_attn(batch, rows=rows, nthreads=1)
+    else:
+        oracle.fork_prefill_attn(batch, q_len, rows=rows, nthreads=1)
+    dt1 = time.perf_counter() - t1
+    step1_s = dt1 * total_rows / n1
+    oracle.fork_decode_attn(batch, rows=rows[:1], nthreads=cores)   # back to every thread
     return {"value": round(step_bytes / step_s / 1e9, 4), "unit": "GB/s",
-            "fork_tokens_per_s": round(batch.num_forks / step_s, 3), "cores": oracle.max_threads(), "kind": "oracle",
+            "fork_tokens_per_s": round(batch.num_forks / step_s, 3), "cores": cores, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "one_thread": {"value": round(step_bytes / step1_s / 1e9, 5), "unit": "GB/s",
+                           "sample": f"{n1} of {total_rows} rows on 1 thread in {dt1:.1f} s, scaled to the step"},
             "sample": f"{reps} whole decode steps ({batch.num_forks} forks x {batch.num_q_heads} q heads) of the same "
                       f"workload, fp64 C oracle, {dt:.1f} s; GB/s = step algorithmic bytes / mean step time"}
+
+
+def stream_ceilings(dev, stream, reps: int = 10):
+    """Streaming read (1 GiB) and copy (512 MiB -> 512 MiB) rates of the plain
+    probe kernels (libspecgen_probe.so): medians over `reps` launches, each
+    timed with HIP events on the launch stream."""
+    import ctypes as C
+    import torch
+    from paper_2606_17518_amd.build import PROBE_LIB_PATH
+    lib = C.CDLL(PROBE_LIB_PATH)
+    lib.specgen_probe_stream_read.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
+    lib.specgen_probe_stream_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.int32, device=dev).random_(0, 1 << 30)
+    half = torch.empty(nbytes // 8, dtype=torch.int32, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    sp = C.c_void_p(stream.cuda_stream)
+
+    def timed(fn):
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            assert fn() == 0
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return float(np.median(ms))
+    read_ms = timed(lambda: lib.specgen_probe_stream_read(src.data_ptr(), nbytes, sink.data_ptr(), sp))
+    copy_ms = timed(lambda: lib.specgen_probe_stream_copy(half.data_ptr(), src.data_ptr(), nbytes // 2, sp))
+    del src, half
+    return {"read_gbps": round(nbytes / (read_ms / 1e3) / 1e9, 1),
+            "copy_gbps": round(nbytes / (copy_ms / 1e3) / 1e9, 1),
+            "note": "plain nontemporal 16-byte streams over every CU: 1 GiB read; 512 MiB copied (1 GiB of "
+                    "traffic); median of 10 launches between HIP events"}
+
+
+def pct(a, q):
+    return round(float(np.percentile(a, q)) * 1e3, 2)
 
 
 def main():
@@ -214,6 +288,58 @@ def main():
     torch.cuda.synchronize()
     part_ms = np.array([e[1].elapsed_time(e[2]) for e in sevents])
     merge_ms = np.array([e[2].elapsed_time(e[3]) for e in sevents])
+
+    def call(fb, st):   # the attention call alone
+        if q_len is not None:
+            sg.specgen_fork_prefill_attn(fb, q_len, out, lse, ws, stream=st)
+        else:
+            sg.specgen_fork_decode_attn(fb, out, lse, ws, stream=st)
+
+    def pairs(n):
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+
+    # warm: the call repeated on one replica, whose data the caches keep as far
+    # as they hold it (172 MB of the 32k-prefix step fits the 256 MB MALL)
+    log(f"timing {args.steps} warm calls")
+    for _ in range(3):
+        call(reps[1], stream)
+    wev = pairs(args.steps)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(SPIN_CYCLES)
+    for k in range(args.steps):
+        wev[k][0].record(stream)
+        call(reps[1], stream)
+        wev[k][1].record(stream)
+    torch.cuda.synchronize()
+    warm_ms = np.array([e[0].elapsed_time(e[1]) for e in wev])
+    # HIP graphs: one captured call per replica, replayed in rotation (cold, like
+    # the eager steps; no host work between the kernels of a call)
+    log(f"timing {args.steps} graph replays")
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graphs = []
+    with torch.cuda.stream(side):
+        for fb in reps:   # library and module set-up outside the capture
+            call(fb, side)
+    for fb in reps:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            call(fb, side)
+        graphs.append(g)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    gev = pairs(args.steps)
+    for k in range(R):
+        graphs[k].replay()
+    torch.cuda.synchronize()
+    torch.cuda._sleep(SPIN_CYCLES)
+    for k in range(args.steps):
+        gev[k][0].record(stream)
+        graphs[(k + 1) % R].replay()
+        gev[k][1].record(stream)
+    torch.cuda.synchronize()
+    graph_ms = np.array([e[0].elapsed_time(e[1]) for e in gev])
+    del graphs
     # the steps on either side of the restore, each timed on its own: export
     # (the prefix blocks migrate out to staging, the reverse of the import)
     # and append (every fork's next token written into its suffix blocks at
@@ -263,8 +389,8 @@ def main():
     attn_bytes = b.algorithmic_bytes() + (Q - N) * Hq * (D * 2 * 2 + 4)   # extra queries: q in, out and lse out
     out_bytes = Q * Hq * (D * 2 + 4)
     kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
-    attn_s = float(attn_ms.mean()) / 1e3
-    part_s = float(part_ms.mean()) / 1e3
+    attn_s = float(np.median(attn_ms)) / 1e3
+    part_s = float(np.median(part_ms)) / 1e3
     value = attn_bytes / attn_s / 1e9
     achieved = kern_bytes / part_s / 1e9
     # matrix work of the partial kernel: S = q K^T and P V over every key of
@@ -298,11 +424,14 @@ def main():
                    "path": args.path, "replicas": R, "prefill_queries_per_fork": prefill_q or 0, "import_blocks": int(len(ids)) if imp is not None else 0},
         "pct_of_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "fork_tokens_per_s": round(Q / attn_s, 1),
-        "attn_us": {"mean": round(float(attn_ms.mean()) * 1e3, 2), "p10": round(float(np.percentile(attn_ms, 10)) * 1e3, 2),
-                    "p50": round(float(np.median(attn_ms)) * 1e3, 2), "p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
-                    "partials": round(part_s * 1e6, 2), "merge": round(float(merge_ms.mean()) * 1e3, 2),
-                    "note": "mean/p10/p50/p90: whole call between two events; partials/merge: the kernels "
-                            "timed separately in a second run of the same steps"},
+        "attn_us": {"p50": pct(attn_ms, 50), "p10": pct(attn_ms, 10), "p90": pct(attn_ms, 90),
+                    "mean": round(float(attn_ms.mean()) * 1e3, 2),
+                    "partials_p50": round(part_s * 1e6, 2), "merge_p50": pct(merge_ms, 50),
+                    "warm_p50": pct(warm_ms, 50), "graph_p50": pct(graph_ms, 50), "graph_p10": pct(graph_ms, 10),
+                    "graph_p90": pct(graph_ms, 90),
+                    "note": "whole call between two events, cold (value uses p50); partials/merge: the kernels "
+                            "timed separately in a second run of the same steps; warm: the call repeated on one "
+                            "replica; graph: one captured call per replica replayed in rotation (cold)"},
         "attn_algorithmic_bytes": int(attn_bytes),
         "roofline": roofline,
     }
@@ -310,6 +439,9 @@ def main():
         res["import"] = {"blocks": int(len(ids)), "bytes": int(import_bytes), "us": round(float(imp_ms.mean()) * 1e3, 2),
                          "gbps": round(import_bytes / (float(imp_ms.mean()) / 1e3) / 1e9, 2)}
     res.update(moves)
+    log("streaming ceilings")
+    res["stream_ceiling"] = stream_ceilings(dev, stream)
+    res["stream_ceiling"]["attn_frac_of_read"] = round(value / res["stream_ceiling"]["read_gbps"], 4)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, q_len, attn_bytes)

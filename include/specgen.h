@@ -155,6 +155,39 @@ specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t *b, void *o
                                           void *workspace, size_t workspace_bytes,
                                           hipStream_t stream);
 
+/* How specgen_fork_decode_attn splits the key axis of a batch, for callers
+ * that analyse load balance or place test inputs relative to the split.  Host
+ * only: it runs the same planner as the call (on the current device's compute
+ * unit count, 256 where no device is present) and launches nothing.  One
+ * segment per (work item, workgroup) pair: the keys [first_token, first_token
+ * + num_tokens) of the item that one workgroup processes and leaves as one
+ * partial result.  A prefix item is (trace, kv head, row block) over the
+ * trace's own P_t prefix tokens (token 0 = the trace's first own token); a
+ * suffix item is (fork, kv head, row block) over the fork's S_f suffix tokens.
+ *   b: as for the call; its device pointers are not read and may be NULL.
+ *   segs: host array of cap entries (may be NULL when cap is 0); *count
+ *   receives the number of segments, which may exceed cap (then only cap are
+ *   written).  Validates the host mirrors like the call itself. */
+typedef struct {
+  int32_t kind;         /* 0: prefix item, 1: suffix item                      */
+  int32_t trace;        /* trace of a prefix item; the fork's trace otherwise  */
+  int32_t fork;         /* fork of a suffix item, -1 for a prefix item        */
+  int32_t kv_head;
+  int32_t row_block;    /* row block of the item                               */
+  int32_t first_row;    /* the item's rows: [first_row, first_row + num_rows)
+                           of its trace's rows (fork f - fork_off[t], q head
+                           h % (Hq/Hkv) is row (f - fork_off[t]) * (Hq/Hkv)
+                           + h % (Hq/Hkv)) for a prefix item, of the group's
+                           q heads for a suffix item                          */
+  int32_t num_rows;
+  int32_t kernel;       /* 0: MFMA kernel, 1: dot kernel                       */
+  int32_t worker;       /* workgroup index in that kernel's launch             */
+  int32_t first_token;  /* first key of the segment within the item's keys    */
+  int32_t num_tokens;   /* keys in the segment                                 */
+} specgen_split_segment_t;
+specgen_status_t specgen_fork_decode_attn_split(const specgen_fork_batch_t *b, specgen_split_segment_t *segs,
+                                                int64_t cap, int64_t *count);
+
 /* The two phases of specgen_fork_decode_attn, for callers that want to place
  * work or timing events between them.  SPECGEN_PHASE_PARTIALS runs the split
  * attention kernels, which leave one partial (o, lse) per worker and item in

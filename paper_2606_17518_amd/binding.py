@@ -27,7 +27,8 @@ SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
 
 EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
             "specgen_fork_prefill_attn_workspace_size", "specgen_fork_prefill_attn",
-            "specgen_kv_import", "specgen_kv_export", "specgen_kv_append", "specgen_lse_merge", "specgen_last_error")
+            "specgen_kv_import", "specgen_kv_export", "specgen_kv_append", "specgen_lse_merge", "specgen_last_error",
+            "specgen_fork_decode_attn_split")
 
 
 class SpecgenError(RuntimeError):
@@ -51,6 +52,11 @@ class ForkBatchC(C.Structure):
         ("prefix_table_off_h", C.c_void_p), ("suffix_table_off_h", C.c_void_p),
         ("prefix_parent_h", C.c_void_p),
     ]
+
+
+class SplitSegmentC(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in ("kind", "trace", "fork", "kv_head", "row_block", "first_row", "num_rows",
+                                         "kernel", "worker", "first_token", "num_tokens")]
 
 
 class KvTensorC(C.Structure):
@@ -100,6 +106,8 @@ def lib():
         L.specgen_kv_append.restype = C.c_int
         L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
         L.specgen_lse_merge.restype = C.c_int
+        L.specgen_fork_decode_attn_split.argtypes = [C.POINTER(ForkBatchC), P, C.c_int64, C.POINTER(C.c_int64)]
+        L.specgen_fork_decode_attn_split.restype = C.c_int
         L.specgen_last_error.argtypes = []
         L.specgen_last_error.restype = C.c_char_p
         _lib = L
@@ -310,3 +318,45 @@ def specgen_lse_merge(o_parts: torch.Tensor, lse_parts: torch.Tensor, out: torch
     dt = SPECGEN_BF16 if out.dtype == torch.bfloat16 else SPECGEN_FP32
     _check(lib().specgen_lse_merge(_dptr(o_parts), _dptr(lse_parts), S, R, D, _dptr(out), dt, _dptr(out_lse),
                                    _stream(stream)))
+
+
+def host_batch_struct(b, path: str | int = "auto"):
+    """A ForkBatchC for the host-only queries from an object with a fork
+    batch's numpy fields: the host mirrors are set, the device pointers NULL.
+    Returns (struct, arrays the struct points into, to be kept alive)."""
+    keep = [np.ascontiguousarray(a, np.int32) for a in
+            (b.fork_off, b.prefix_len, b.suffix_len, b.prefix_table_off, b.suffix_table_off)]
+    s = ForkBatchC()
+    s.num_traces, s.num_forks, s.num_q_heads, s.num_kv_heads = b.num_traces, b.num_forks, b.num_q_heads, b.num_kv_heads
+    s.head_dim, s.block_size, s.num_blocks, s.sm_scale = b.head_dim, 16, b.num_blocks, float(b.sm_scale)
+    s.kv_dtype = SPECGEN_BF16 if b.kv_dtype == "bf16" else SPECGEN_FP8_E4M3
+    s.path = PATHS[path] if isinstance(path, str) else int(path)
+    s.reserved = 0
+    s.fork_off_h, s.prefix_len_h, s.suffix_len_h, s.prefix_table_off_h, s.suffix_table_off_h = \
+        (a.ctypes.data for a in keep)
+    if getattr(b, "prefix_parent", None) is not None:
+        keep.append(np.ascontiguousarray(b.prefix_parent, np.int32))
+        s.prefix_parent_h = keep[-1].ctypes.data
+    return s, keep
+
+
+def specgen_fork_decode_attn_split(batch, path: str | int = "auto") -> dict:
+    """The key-axis split of a batch (host only).  `batch` is a ForkBatchC, a
+    ForkBatchTensors, or an object with a fork batch's numpy fields.  Returns a
+    dict of int32 arrays, one entry per segment, keyed by the fields of
+    specgen_split_segment_t."""
+    keep = None
+    if isinstance(batch, ForkBatchC):
+        s = batch
+    elif isinstance(batch, ForkBatchTensors):
+        s = batch.c_struct()
+    else:
+        s, keep = host_batch_struct(batch, path)
+    n = C.c_int64(0)
+    _check(lib().specgen_fork_decode_attn_split(C.byref(s), None, 0, C.byref(n)))
+    arr = (SplitSegmentC * max(1, n.value))()
+    _check(lib().specgen_fork_decode_attn_split(C.byref(s), arr, n.value, C.byref(n)))
+    del keep
+    names = [f for f, _ in SplitSegmentC._fields_]
+    raw = np.frombuffer(arr, dtype=np.int32, count=n.value * len(names)).reshape(n.value, len(names))
+    return {name: raw[:, i].copy() for i, name in enumerate(names)}

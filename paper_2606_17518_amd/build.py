@@ -1,7 +1,8 @@
 """Compile the HIP sources under csrc/ into libspecgen.so for gfx950.
 
 Objects are built in parallel under _build/ at the repository root and linked
-into paper_2606_17518_amd/libspecgen.so.  Packed-FP32 instruction selection is
+into paper_2606_17518_amd/libspecgen.so, and the benchmark's memory-ceiling
+kernels into libspecgen_probe.so.  Packed-FP32 instruction selection is
 switched off on every device compile.
 """
 from __future__ import annotations
@@ -17,6 +18,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
 SOURCES = ["abi.hip", "attn_bf16.hip", "attn_dot.hip", "merge.hip", "kv_import.hip", "kv_append.hip"]
+# the benchmark's memory-ceiling kernels, linked into a library of their own
+PROBE_SOURCES = ["probe.hip"]
+PROBE_LIB_PATH = os.path.join(PKG, "libspecgen_probe.so")
 # Per-source device flags: the bf16 attention kernel keeps MFMA accumulators in
 # VGPRs and runs without IEEE-mode NaN quieting (masked scores are -inf, never NaN).
 EXTRA_FLAGS = {"attn_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mno-amdgpu-ieee", "-fno-honor-nans"]}
@@ -52,13 +56,14 @@ def build(verbose: bool = False) -> str:
         return obj
 
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(one, SOURCES))
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
-    r = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs],
-                       capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB_PATH)
+        objs = list(ex.map(one, SOURCES + PROBE_SOURCES))
+    for lib_path, lib_objs in ((LIB_PATH, objs[:-len(PROBE_SOURCES)]), (PROBE_LIB_PATH, objs[-len(PROBE_SOURCES):])):
+        tmp = lib_path + ".tmp%d" % os.getpid()
+        r = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *lib_objs],
+                           capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"link failed:\n{r.stderr}")
+        os.replace(tmp, lib_path)
     return LIB_PATH
 
 

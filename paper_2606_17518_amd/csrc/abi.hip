@@ -146,15 +146,10 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   return ok();
 }
 
-// One call of the split attention for a checked batch (both phases or one).
-specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* out, float* out_lse, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream, const int32_t* ptab_sel = nullptr) {
-  if (phase != SPECGEN_PHASE_ALL && phase != SPECGEN_PHASE_PARTIALS && phase != SPECGEN_PHASE_MERGE)
-    return fail(SPECGEN_ERR_INVALID_ARG, "phase %d unknown", phase);
-  Plan plan;
-  int64_t wsf = 0;
-  specgen_status_t st = build_plan(b, &plan, &wsf, ptab_sel);
-  if (st != SPECGEN_OK) return st;
+// Queues one call of the split attention (both phases or one) for a checked
+// batch and its plan.
+specgen_status_t run_plan(const specgen_fork_batch_t* b, const Plan& plan, int64_t wsf, int32_t phase, void* out,
+                          float* out_lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!out && phase != SPECGEN_PHASE_PARTIALS) return fail(SPECGEN_ERR_INVALID_ARG, "out is NULL");
   if ((size_t)(wsf * 4) > workspace_bytes || (wsf > 0 && !workspace))
     return fail(SPECGEN_ERR_WORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes, (long long)(wsf * 4));
@@ -181,6 +176,18 @@ specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* o
   if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);
   if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+// One call of the split attention (both phases or one).
+specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* out, float* out_lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream, const int32_t* ptab_sel = nullptr) {
+  if (phase != SPECGEN_PHASE_ALL && phase != SPECGEN_PHASE_PARTIALS && phase != SPECGEN_PHASE_MERGE)
+    return fail(SPECGEN_ERR_INVALID_ARG, "phase %d unknown", phase);
+  Plan plan;
+  int64_t wsf = 0;
+  const specgen_status_t st = build_plan(b, &plan, &wsf, ptab_sel);
+  if (st != SPECGEN_OK) return st;
+  return run_plan(b, plan, wsf, phase, out, out_lse, workspace, workspace_bytes, stream);
 }
 
 // Multi-token prefill as a decode batch of virtual forks: query i of fork f
@@ -287,6 +294,56 @@ specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batc
   const specgen_status_t st = build_plan(b, &plan, &wsf);
   if (st != SPECGEN_OK) return st;
   *bytes = (size_t)(wsf * 4);
+  return ok();
+}
+
+specgen_status_t specgen_fork_decode_attn_split(const specgen_fork_batch_t* b, specgen_split_segment_t* segs,
+                                                int64_t cap, int64_t* count) {
+  if (!count) return fail(SPECGEN_ERR_INVALID_ARG, "count is NULL");
+  if (cap < 0 || (cap > 0 && !segs)) return fail(SPECGEN_ERR_INVALID_ARG, "segs is NULL or cap < 0");
+  if (!b) return fail(SPECGEN_ERR_INVALID_ARG, "batch is NULL");
+  // Device arrays are not read here: stand-ins let the shared checks pass.
+  specgen_fork_batch_t hb = *b;
+  const void* stand_in = reinterpret_cast<const void*>(uintptr_t{256});
+  if (!hb.q) hb.q = stand_in;
+  if (!hb.k_pool) hb.k_pool = stand_in;
+  if (!hb.v_pool) hb.v_pool = stand_in;
+  if (!hb.k_scale) hb.k_scale = static_cast<const float*>(stand_in);
+  if (!hb.v_scale) hb.v_scale = static_cast<const float*>(stand_in);
+  for (const int32_t** a : {&hb.fork_off, &hb.prefix_len, &hb.prefix_table_off, &hb.prefix_table, &hb.suffix_len,
+                            &hb.suffix_table_off, &hb.suffix_table})
+    if (!*a) *a = static_cast<const int32_t*>(stand_in);
+  Plan plan;
+  int64_t wsf = 0;
+  const specgen_status_t st = build_plan(&hb, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  int64_t n = 0;
+  for (int X = 0; X < 2; ++X) {
+    const PartPlan& pp = plan.part[X];
+    for (int w = 0; w < pp.workers; ++w) {
+      walk_range(plan, X, w, INT32_MAX, [&](const ItemRef& it, int nt, int, int, int) {
+        if (n < cap) {
+          specgen_split_segment_t& s = segs[n];
+          const int nv = it.kind == 0 ? plan.prefix_len[it.t] : plan.suffix_len[it.f];
+          s.kind = it.kind;
+          s.trace = it.kind == 0 ? it.t : trace_of_fork(plan, it.f);
+          s.fork = it.kind == 0 ? -1 : it.f;
+          s.kv_head = it.j;
+          s.row_block = it.rb;
+          const int rows = it.kind == 0 ? trace_rows(plan, it.t) : plan.g;
+          s.first_row = it.rb * pp.rbs;
+          s.num_rows = rows - s.first_row < pp.rbs ? rows - s.first_row : pp.rbs;
+          s.kernel = X;
+          s.worker = w;
+          s.first_token = it.tile * pp.tt;
+          const int end = (it.tile + nt) * pp.tt;
+          s.num_tokens = (end < nv ? end : nv) - s.first_token;
+        }
+        ++n;
+      });
+    }
+  }
+  *count = n;
   return ok();
 }
 

@@ -56,9 +56,9 @@
 namespace specgen {
 namespace bf16k {
 
-// l + the sum of the 8 bf16 probabilities packed in pk: the denominator adds
-// exactly the weights the PV product uses (one dot2 with (1, 1) per pair).
-// The elements are copied to scalars first: __builtin_bit_cast applied to an
+// l + the sum of the 8 bf16 probabilities packed in pk (one dot2 with (1, 1)
+// per pair): the sum of exactly the weights the PV product uses.  The
+// elements are copied to scalars first: __builtin_bit_cast applied to an
 // element of an ext_vector_type value reads element 0 whatever the index.
 __device__ __forceinline__ float row_sum_bf16(const u32x4 pk, float l) {
   const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
@@ -94,7 +94,7 @@ struct Cfg {
   static constexpr int kQRows = 128;                  // q rows per slot: an item takes 1 or 2 q slots
   static constexpr int kOffItems = kStages * kStageB;
   static constexpr int kOffML = kOffItems + kItemCap * kItemInts * 4;
-  static constexpr int kMLBytes = kWaves * 2 * 64 * 2 * 4;   // [wave][nt][lane] (m, l)
+  static constexpr int kMLBytes = kWaves * 2 * 16 * 4 * 4;   // [wave][nt][row] (m, l, lf, -)
   static constexpr int kOffIds = kOffML + kMLBytes;
   static constexpr int kIdCap = 2560;                 // block ids of a worker's range
   static constexpr int kIdsPerTile = kTT / 16;
@@ -375,7 +375,12 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   const int v_lane_off = (G >> 1) * C::kSliceB + 32 * ln + 16 * ((G & 1) ^ ((ln >> 3) & 1));
   bf16x8 qop[2][KS];
   f32x4 acc[2][DT];
-  float m_run[2], l_run[2];
+  // Per row (each lane: its share of it): the running max, and two sums of
+  // the probabilities: l_run of the bf16 weights the PV product uses (the
+  // output's normaliser, so a dominant key's rounding cancels out of the
+  // output) and lf_run of the unrounded fp32 ones (the lse, which would
+  // otherwise carry that rounding, up to 2^-8 relative).
+  float m_run[2], l_run[2], lf_run[2];
   constexpr int NT = 2;   // 16-row MFMA tiles per row group
   int RG = 1, TG = 1, rg = 0, tg = 0, tpg = TT;   // tpg: tokens of a tile per token group
   bool active = false;
@@ -407,6 +412,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       }
       m_run[nt] = -INFINITY;
       l_run[nt] = 0.f;
+      lf_run[nt] = 0.f;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -457,7 +463,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
     // (all in block (sb + 8G) / 16 of the tile)
-    float vsc = 1.f;
+    float vsc = 1.f, inv_vsc = 1.f;
     if constexpr (FP8) {
       // the slab's two blocks (ids[idb + sb/16] and the next): lanes G < 2 hold
       // keys of the first
@@ -474,6 +480,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       const float k0 = sload(ks, id0), k1 = sload(ks, id1), v0 = sload(vs, id0), v1 = sload(vs, id1);
       const float ksc = G < 2 ? k0 : k1;
       vsc = G < 2 ? v0 : v1;
+      inv_vsc = __builtin_amdgcn_rcpf(vsc);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -507,6 +514,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         const float alpha = __builtin_amdgcn_exp2f((m_run[nt] - m_new) * a.c_log2);
         m_run[nt] = m_new;
         l_run[nt] *= alpha;
+        lf_run[nt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) acc[nt][dt] *= alpha;
       }
@@ -527,8 +535,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], a.c_log2, -mc0));
       p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], a.c_log2, -mc0));
     }
-    if constexpr (FP8) {   // the row sum excludes the value scale, which P carries into PV
-      l_run[0] += ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
+    lf_run[0] += ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
+    if constexpr (FP8) {   // P carries the value scale into PV
 #pragma unroll
       for (int e = 0; e < 8; ++e) p0[e] *= vsc;
     }
@@ -537,7 +545,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     pk0[1] = pack_bf16x2(p0[2], p0[3]);
     pk0[2] = pack_bf16x2(p0[4], p0[5]);
     pk0[3] = pack_bf16x2(p0[6], p0[7]);
-    if constexpr (!FP8) l_run[0] = row_sum_bf16(pk0, l_run[0]);
+    // the normaliser adds the weights PV uses, without the value scale
+    if constexpr (FP8) l_run[0] = fmaf(row_sum_bf16(pk0, 0.f), inv_vsc, l_run[0]);
+    else l_run[0] = row_sum_bf16(pk0, l_run[0]);
     const bf16x8 pop0 = __builtin_bit_cast(bf16x8, pk0);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -547,8 +557,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int e = DT; e < 8; ++e)   // D = 64: fewer PV MFMAs than exponentials
       p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], a.c_log2, -mc1));
+    lf_run[1] += ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
     if constexpr (FP8) {
-      l_run[1] += ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
 #pragma unroll
       for (int e = 0; e < 8; ++e) p1[e] *= vsc;
     }
@@ -557,7 +567,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     pk1[1] = pack_bf16x2(p1[2], p1[3]);
     pk1[2] = pack_bf16x2(p1[4], p1[5]);
     pk1[3] = pack_bf16x2(p1[6], p1[7]);
-    if constexpr (!FP8) l_run[1] = row_sum_bf16(pk1, l_run[1]);
+    if constexpr (FP8) l_run[1] = fmaf(row_sum_bf16(pk1, 0.f), inv_vsc, l_run[1]);
+    else l_run[1] = row_sum_bf16(pk1, l_run[1]);
     const bf16x8 pop1 = __builtin_bit_cast(bf16x8, pk1);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop1, acc[1][dt], 0, 0, 0);
@@ -587,9 +598,12 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   // write token group 0's normalised partial.  Every wave calls this (it has
   // barriers); returns the number of vector-memory stores this wave issued.
   auto finish_item = [&](const Desc& d, int stage) -> int {
-    float lrow[2];
+    float lrow[2], lfrow[2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) lrow[nt] = rows4_sum(l_run[nt]);
+    for (int nt = 0; nt < 2; ++nt) {
+      lrow[nt] = rows4_sum(l_run[nt]);
+      lfrow[nt] = rows4_sum(lf_run[nt]);
+    }
     if (TG > 1) {
       float* cb = reinterpret_cast<float*>(lds + stage * C::kStageB);
       constexpr int wave_bytes = NT * DT * 64 * 16;
@@ -606,8 +620,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
               *reinterpret_cast<f32x4*>(dst + ((nt * DT + dt) * 64 + lane) * 4) = acc[nt][dt];
-            ml[((wave * 2 + nt) * 64 + lane) * 2 + 0] = m_run[nt];
-            ml[((wave * 2 + nt) * 64 + lane) * 2 + 1] = lrow[nt];
+            // a row's m and sums are the same on its four lanes: lane group 0 writes them
+            if (G == 0)
+              *reinterpret_cast<f32x4*>(ml + ((wave * 2 + nt) * 16 + ln) * 4) = f32x4{m_run[nt], lrow[nt], lfrow[nt], 0.f};
           }
         }
         lds_barrier();
@@ -620,8 +635,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
               // a token group that saw no token of the item has m = -inf, l = 0, acc = 0
-              const float m1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 0];
-              const float l1 = ml[((pw * 2 + nt) * 64 + lane) * 2 + 1];
+              const f32x4 ml1 = *reinterpret_cast<const f32x4*>(ml + ((pw * 2 + nt) * 16 + ln) * 4);
+              const float m1 = ml1[0], l1 = ml1[1], lf1 = ml1[2];
               const float m = fmaxf(m_run[nt], m1);
               const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
               const float a0 = __builtin_amdgcn_exp2f(m_run[nt] * a.c_log2 - mc);
@@ -632,6 +647,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
                 acc[nt][dt] = acc[nt][dt] * a0 + o1 * a1;
               }
               lrow[nt] = lrow[nt] * a0 + l1 * a1;
+              lfrow[nt] = lfrow[nt] * a0 + lf1 * a1;
               m_run[nt] = m;
             }
           }
@@ -677,7 +693,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         // of the caches' retention
         __builtin_nontemporal_store(chunk, reinterpret_cast<u32x4*>(orow + dim0 / 2));
       }
-      const f32x2 ld = {m_run[nt] * a.sm_scale + __logf(lrow[nt]), dec};
+      const f32x2 ld = {m_run[nt] * a.sm_scale + __logf(lfrow[nt]), dec};
       __builtin_nontemporal_store(ld, reinterpret_cast<f32x2*>(a.ws + part_l_off(pp, slot, row)));
       stores += DT / 2 + 1;
     }

@@ -58,7 +58,7 @@ struct PartPlan {
   int32_t kmax;           // max items touched by one worker
   int32_t tt;             // tokens per tile
   int32_t rbs;            // rows per row block
-  int32_t slot_rows;      // rows reserved per partial slot (== rbs)
+  int32_t slot_rows;      // rows reserved per partial slot: the largest item's, rounded up to 16
   int32_t n_prefix_items; // prefix items in the partition
   int32_t has_suffix;     // suffix items belong to this partition
   int32_t suffix_rb;      // row blocks per suffix (fork, head): ceil(g / rbs)

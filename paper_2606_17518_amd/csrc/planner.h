@@ -212,6 +212,12 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     }
     if (pp.kmax > in.item_cap[X] || tmax > in.tile_cap[X] || (pp.units + pp.workers - 1) / pp.workers > unit_cap[X])
       SG_FAIL(kPlanUnsupported, "work split exceeds the kernel's per-worker capacity");
+    // Rows per slot: the partition's largest item, rounded up to 16 rows (an
+    // MFMA N-tile stores all its 16 rows), at most the row-block size.
+    int max_rows = pp.has_suffix ? std::min(g, pp.rbs) : 1;
+    for (int i = pp.trace_begin; i < pp.trace_begin + pp.n_traces; ++i)
+      max_rows = std::max(max_rows, std::min(trace_rows(*plan, plan->ptrace[i]), pp.rbs));
+    pp.slot_rows = std::min(pp.rbs, (max_rows + 15) / 16 * 16);
     const int64_t slots = (int64_t)pp.workers * pp.kmax;
     // o: fp16 [slots][slot_rows][D] (D is even); lse: (lse, dec) float pairs
     pp.o_base = off;

@@ -396,3 +396,50 @@ def with_prefill_queries(batch: ForkBatch, q_len: Sequence[int], seed: int = 0) 
     out.q = _to_bf16_bits(rng.standard_normal((int(ql.sum()), batch.num_q_heads, batch.head_dim), dtype=np.float32))
     out.q_len = ql
     return out
+
+
+# ---- peaked queries -------------------------------------------------------------
+
+def logical_key(batch: ForkBatch, f: int, j: int, i: int) -> np.ndarray:
+    """The value of key i (0-based, logical order: the prefix chain of fork
+    f's trace, root first, then f's suffix) of kv head j as float32: the bf16
+    bits widened, or the E4M3 code decoded and multiplied by its block scale.
+    This reads back the generator's own placement."""
+    bs = batch.block_size
+    blk = slot = None
+    for t in batch.prefix_chain(batch.trace_of_fork(f)):
+        n = int(batch.prefix_len[t])
+        if i < n:
+            blk = int(batch.prefix_table[batch.prefix_table_off[t] + i // bs])
+            slot = i % bs
+            break
+        i -= n
+    if blk is None:
+        assert 0 <= i < int(batch.suffix_len[f]), "key index past the fork's keys"
+        blk = int(batch.suffix_table[batch.suffix_table_off[f] + i // bs])
+        slot = i % bs
+    row = batch.k_pool[blk, j, slot]
+    if batch.kv_dtype == "bf16":
+        return (row.astype(np.uint32) << 16).view(np.float32)
+    dec = torch.from_numpy(np.ascontiguousarray(row)).view(torch.float8_e4m3fn).to(torch.float32).numpy()
+    return dec * batch.k_scale[blk]
+
+
+def with_peaked_queries(batch: ForkBatch, key_index: np.ndarray, weight: np.ndarray, q_scale: float) -> ForkBatch:
+    """A copy of ``batch`` whose queries make attention peaked:
+    q[f][h] = q_scale * q0[f][h] + weight[f][h] * k, rounded to bf16, where q0
+    is the batch's own query and k the logical key key_index[f][h] of the
+    fork's kv head for h (no key where key_index < 0).  With N(0, 1) keys and
+    scale 1/sqrt(D), the scores of a row spread with standard deviation about
+    sqrt(q_scale^2 + weight^2) and the chosen key scores about weight * |k|^2
+    / sqrt(D) above zero, so it dominates its row for weight >= 2."""
+    N, Hq, D, g = batch.num_forks, batch.num_q_heads, batch.head_dim, batch.group
+    q0 = (batch.q.astype(np.uint32) << 16).view(np.float32).reshape(N, Hq, D)
+    q = q_scale * q0
+    for f in range(N):
+        for h in range(Hq):
+            if key_index[f, h] >= 0:
+                q[f, h] += np.float32(weight[f, h]) * logical_key(batch, f, h // g, int(key_index[f, h]))
+    out = dataclasses.replace(batch)
+    out.q = _to_bf16_bits(q)
+    return out

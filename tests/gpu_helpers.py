@@ -12,6 +12,12 @@ import paper_2606_17518_amd as sg
 ATTN_MAX_ABS = 1e-2
 ATTN_MEAN_ABS = 1e-3
 LSE_MAX_ABS = 1e-3
+# Beside them, on the full-size decode workloads (tens of thousands of keys per
+# row): an lse bound that resolves one 16-token KV block.  Dropping one block
+# out of ~33k keys moves a row's lse by about 16/33k = 5e-4 (the oracle shows
+# 2e-4 to 1e-3 on the 32k-prefix workload), while fp32 accumulation of the
+# split softmax keeps the kernels' lse within about 1e-5.
+LSE_FULL_SIZE_MAX_ABS = 1e-4
 
 
 def say(msg):
@@ -34,15 +40,55 @@ def run_attn(batch, path="auto", with_lse=True, fb=None):
     return o, l
 
 
-def check_attn(out, ref, lse=None, ref_lse=None, what=""):
+def bf16_half_ulp(x):
+    """Half a unit in the last place of bf16 (8 significant bits) at |x|: the
+    most that rounding to nearest bf16 can move a value of that size."""
+    ax = np.maximum(np.abs(x), 2.0 ** -126)
+    return np.exp2(np.floor(np.log2(ax)) - 8)
+
+
+def check_attn_excess(out, ref, lse, ref_lse, what=""):
+    """The tolerances applied to the error beyond the bf16 output's own rounding.
+
+    Where a few keys dominate a row, the output is about one value row, with
+    elements up to ~4 in size, and the bf16 output format alone rounds such
+    values by up to 7.8e-3 (in [2, 4)) or 1.6e-2 (in [4, 8)): no bf16-output
+    computation can meet an absolute 1e-2 there.  So each element's error is
+    reduced by half a bf16 ulp of its size (of the larger of the two values,
+    the binade the rounding happened in) and the max abs 1e-2 / mean abs 1e-3
+    bars apply to what remains: the computation's own error.  |d lse| <= 1e-3."""
+    assert np.isfinite(out).all(), f"{what}: non-finite output"
+    err = np.abs(out - ref)
+    excess = np.maximum(0.0, err - bf16_half_ulp(np.maximum(np.abs(out), np.abs(ref))))
+    rmx, rmean = rel_err(out, ref)
+    le = float(np.abs(lse - ref_lse).max())
+    say(f"{what}: max abs {err.max():.2e} mean abs {err.mean():.2e} | beyond bf16 output rounding: max "
+        f"{excess.max():.2e} mean {excess.mean():.2e} | rel to rms(out): max {rmx:.2e} mean {rmean:.2e} | "
+        f"lse max abs {le:.2e} | max |ref| {np.abs(ref).max():.2f}")
+    assert excess.max() <= ATTN_MAX_ABS, f"{what}: max error beyond rounding {excess.max():.3e}"
+    assert excess.mean() <= ATTN_MEAN_ABS, f"{what}: mean error beyond rounding {excess.mean():.3e}"
+    assert le <= LSE_MAX_ABS, f"{what}: lse max abs err {le:.3e}"
+
+
+def rel_err(out, ref):
+    """Error relative to the size of the output: (max |d|, mean |d|) / rms(ref)."""
+    rms = float(np.sqrt(np.mean(np.square(ref))))
+    err = np.abs(out - ref)
+    return float(err.max()) / rms, float(err.mean()) / rms
+
+
+def check_attn(out, ref, lse=None, ref_lse=None, what="", lse_max=LSE_MAX_ABS):
     assert np.isfinite(out).all(), f"{what}: non-finite output"
     err = np.abs(out - ref)
     mx, mean = float(err.max()), float(err.mean())
+    rmx, rmean = rel_err(out, ref)
+    le = float(np.abs(lse - ref_lse).max()) if lse is not None else float("nan")
+    say(f"{what}: max abs {mx:.2e} mean abs {mean:.2e} | rel to rms(out): max {rmx:.2e} mean {rmean:.2e} | "
+        f"lse max abs {le:.2e}")
     assert mx <= ATTN_MAX_ABS, f"{what}: max abs err {mx:.3e}"
     assert mean <= ATTN_MEAN_ABS, f"{what}: mean abs err {mean:.3e}"
     if lse is not None:
-        le = float(np.abs(lse - ref_lse).max())
-        assert le <= LSE_MAX_ABS, f"{what}: lse max abs err {le:.3e}"
+        assert le <= lse_max, f"{what}: lse max abs err {le:.3e} (bound {lse_max:.0e})"
     return mx, mean
 
 

@@ -17,6 +17,7 @@
 // Built and run by tests/test_plan.py with g++ (no GPU involved).
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <map>
 #include <random>
 #include <set>
@@ -97,6 +98,11 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
             at + (int64_t)(n - 1) * it.w >= x1 || (it.tile > 0 && at - it.w >= x0) || rt != data || k < 0 ||
             k >= pp.kmax || it.ord >= pp.n_items)
           fine = false;
+        // the MFMA kernel stores whole 16-row N-tiles of an item's rows: the
+        // rounded row count must fit the slot
+        const int item_rows = std::min(it.kind == 0 ? trace_rows(plan, it.t) - it.rb * pp.rbs : plan.g - it.rb * pp.rbs,
+                                       pp.rbs);
+        if (item_rows < 1 || (X == kPartMfma ? (item_rows + 15) / 16 * 16 : item_rows) > pp.slot_rows) fine = false;
         segs[{X, it.ord}].push_back(Seg{w, k, at, n});
         if (it.ord >= 0 && it.ord < pp.n_items) record_item(tables[X].data(), it, n, w, k);
         x = at + (int64_t)(n - 1) * it.w + 1;

@@ -31,7 +31,8 @@ def test_every_declared_symbol_is_exported(L):
     assert set(names) == {"specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn",
                           "specgen_fork_decode_attn_phase", "specgen_fork_prefill_attn_workspace_size",
                           "specgen_fork_prefill_attn", "specgen_kv_import", "specgen_kv_export",
-                          "specgen_kv_append", "specgen_lse_merge", "specgen_last_error"}
+                          "specgen_kv_append", "specgen_lse_merge", "specgen_last_error",
+                          "specgen_fork_decode_attn_split"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -264,3 +265,45 @@ def test_table_offsets_validated(L, which, off, lens, status):
         ql = np.ones(2, np.int32)
         assert L.specgen_fork_prefill_attn_workspace_size(C.byref(s), ql.ctypes.data_as(C.c_void_p),
                                                           C.byref(n)) == status
+
+
+@pytest.mark.parametrize("path", ["auto", "mfma", "dot"])
+def test_split_query_tiles_every_item_once(L, path):
+    """specgen_fork_decode_attn_split (host only): the segments of every work
+    item cover its keys exactly once, in worker order, and its rows are the
+    trace's (or group's) rows cut into row blocks."""
+    import synth
+    import paper_2606_17518_amd as sg
+    b = synth.make_fork_batch(prefix_lens=[5000, 37], forks_per_trace=[20, 3], suffix_range=(0, 700),
+                              num_q_heads=16, num_kv_heads=2, head_dim=128, seed=3)
+    sp = sg.specgen_fork_decode_attn_split(b, path)
+    g = b.group
+    items = {}
+    for k in range(len(sp["kind"])):
+        key = (int(sp["kind"][k]), int(sp["trace"][k]), int(sp["fork"][k]), int(sp["kv_head"][k]), int(sp["row_block"][k]))
+        items.setdefault(key, []).append((int(sp["kernel"][k]), int(sp["worker"][k]), int(sp["first_token"][k]),
+                                          int(sp["num_tokens"][k]), int(sp["first_row"][k]), int(sp["num_rows"][k])))
+    rows_seen = {}
+    for (kind, t, f, j, rb), segs in items.items():
+        segs.sort(key=lambda s: s[1])
+        assert len({s[0] for s in segs}) == 1                      # one kernel per item
+        n = int(b.prefix_len[t]) if kind == 0 else int(b.suffix_len[f])
+        pos = 0
+        for s in segs:
+            assert s[2] == pos and s[3] > 0
+            pos += s[3]
+        assert pos == n
+        assert len({(s[4], s[5]) for s in segs}) == 1
+        r0, nr = segs[0][4], segs[0][5]
+        rows_seen.setdefault((kind, t, f, j), []).append((r0, nr))
+        if path == "dot" or (path == "auto" and kind == 0 and (b.fork_off[t + 1] - b.fork_off[t]) * g < 16):
+            assert segs[0][0] == 1
+    for (kind, t, f, j), blocks in rows_seen.items():
+        total = (b.fork_off[t + 1] - b.fork_off[t]) * g if kind == 0 else g
+        blocks.sort()
+        assert blocks[0][0] == 0 and sum(nr for _, nr in blocks) == total
+    # every prefix item and every non-empty suffix item appears
+    assert {(k[1], k[3]) for k in items if k[0] == 0} == {(t, j) for t in range(2) for j in range(2)}
+    assert {(k[2], k[3]) for k in items if k[0] == 1} == {(f, j) for f in range(b.num_forks) if b.suffix_len[f] > 0
+                                                         for j in range(2)}
+

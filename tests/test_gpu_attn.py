@@ -2,15 +2,17 @@
 
 Tolerance (bf16 inputs, fp32 accumulation, bf16 output): max abs <= 1e-2 and
 mean abs <= 1e-3 over all compared elements; natural-log LSE within 1e-3.
-Small shapes are compared on every row; the long workloads on sampled rows
-(the oracle computes each sampled row by definition over its full key set).
+Small shapes and the 32k-prefix workload are compared on every row; the other
+long workloads on sampled rows (the oracle computes each sampled row by
+definition over its full key set).  The full-size workloads also meet an lse
+bound of 1e-4, which a single dropped 16-token block would break.
 """
 import numpy as np
 import pytest
 
 import oracle
 import synth
-from gpu_helpers import check_attn, run_attn, sample_rows, say
+from gpu_helpers import LSE_FULL_SIZE_MAX_ABS, check_attn, run_attn, sample_rows, say
 
 pytestmark = pytest.mark.gpu
 
@@ -69,17 +71,22 @@ def test_trace_8k_all_rows():
     check_attn(out, ref, lse, ref_l, what="p8k")
 
 
-@pytest.mark.parametrize("name,nrows", [("trace_p32k_f16", 96), ("ragged_t32_f8", 96), ("fp8_p128k_f32", 48)])
-def test_full_size_workloads_sampled_rows(name, nrows):
+@pytest.mark.parametrize("name,nrows", [("trace_p32k_f16", None), ("ragged_t32_f8", 1024), ("fp8_p128k_f32", 256)])
+def test_full_size_workloads(name, nrows):
+    """Full-size decode workloads: every row of the 32k-prefix workload, sampled
+    rows of the others (the oracle computes each by definition over all its
+    keys); the benchmark spec's tolerances, and beside them the lse bound that
+    resolves a single 16-token block."""
     say(f"{name}: generating")
     b = synth.workload(name)
-    rows = sample_rows(b, nrows, seed=7)
-    say(f"{name}: oracle on {len(rows)} rows")
+    rows = None if nrows is None else sample_rows(b, nrows, seed=7)
+    say(f"{name}: oracle on {'all' if rows is None else len(rows)} rows")
     ref, ref_l = oracle.fork_decode_attn(b, rows=rows)
     say(f"{name}: gpu")
     out, lse = run_attn(b)
-    got = out[rows[:, 0], rows[:, 1]]
-    got_l = lse[rows[:, 0], rows[:, 1]]
-    mx, mean = check_attn(got, ref, got_l, ref_l, what=name)
-    say(f"{name}: max abs {mx:.2e} mean abs {mean:.2e}")
     assert np.isfinite(out).all()
+    if rows is None:
+        got, got_l = out, lse
+    else:
+        got, got_l = out[rows[:, 0], rows[:, 1]], lse[rows[:, 0], rows[:, 1]]
+    check_attn(got, ref, got_l, ref_l, what=name, lse_max=LSE_FULL_SIZE_MAX_ABS)
