@@ -307,3 +307,21 @@ def test_split_query_tiles_every_item_once(L, path):
     assert {(k[2], k[3]) for k in items if k[0] == 1} == {(f, j) for f in range(b.num_forks) if b.suffix_len[f] > 0
                                                          for j in range(2)}
 
+
+
+def test_probe_library_exports_its_header():
+    """libspecgen_probe.so (the benchmark's memory ceilings) exports every call
+    include/specgen_probe.h declares, and rejects bad sizes without a launch."""
+    import ctypes
+    from paper_2606_17518_amd.build import PROBE_LIB_PATH
+    src = open(os.path.join(ROOT, "include", "specgen_probe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = sorted(set(re.findall(r"\b(specgen_probe_\w+)\s*\(", src)))
+    assert names == ["specgen_probe_stream_copy", "specgen_probe_stream_read"]
+    lib = ctypes.CDLL(PROBE_LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    lib.specgen_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.specgen_probe_stream_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    assert lib.specgen_probe_stream_read(0x10000, 24, 0x20000, None) == 1      # not a multiple of 16
+    assert lib.specgen_probe_stream_copy(0x10000, None, 64, None) == 1
