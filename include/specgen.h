@@ -155,6 +155,24 @@ specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t *b, void *o
                                           void *workspace, size_t workspace_bytes,
                                           hipStream_t stream);
 
+/* specgen_fork_decode_attn for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  It takes no workspace: the partial results live in a scratch
+ * array of the library, SPECGEN_NOALLOC_SCRATCH_BYTES of device memory per
+ * GPU, which each GPU the library runs on holds from the first call there
+ * until the process ends.  The call allocates nothing.
+ *   Arguments, results and errors as for specgen_fork_decode_attn; a batch
+ *   whose workspace (specgen_fork_decode_attn_workspace_size) exceeds the
+ *   scratch is rejected with SPECGEN_ERR_WORKSPACE before anything is queued.
+ * All calls on one GPU share its scratch, which keeps the last call's
+ * contents (none of which a later call reads: nothing needs clearing).  Calls
+ * that overlap on one GPU -- on different streams, or from threads without
+ * ordering -- race on it and give undefined results; calls ordered on one
+ * stream are safe. */
+#define SPECGEN_NOALLOC_SCRATCH_BYTES (64ull << 20)
+specgen_status_t specgen_fork_decode_attn_noalloc(const specgen_fork_batch_t *b, void *out, float *out_lse,
+                                                  hipStream_t stream);
+
 /* How specgen_fork_decode_attn splits the key axis of a batch, for callers
  * that analyse load balance or place test inputs relative to the split.  Host
  * only: it runs the same planner as the call (on the current device's compute

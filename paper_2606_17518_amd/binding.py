@@ -28,7 +28,7 @@ SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
 EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
             "specgen_fork_prefill_attn_workspace_size", "specgen_fork_prefill_attn",
             "specgen_kv_import", "specgen_kv_export", "specgen_kv_append", "specgen_lse_merge", "specgen_last_error",
-            "specgen_fork_decode_attn_split")
+            "specgen_fork_decode_attn_split", "specgen_fork_decode_attn_noalloc")
 
 
 class SpecgenError(RuntimeError):
@@ -106,6 +106,8 @@ def lib():
         L.specgen_kv_append.restype = C.c_int
         L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
         L.specgen_lse_merge.restype = C.c_int
+        L.specgen_fork_decode_attn_noalloc.argtypes = [C.POINTER(ForkBatchC), P, P, P]
+        L.specgen_fork_decode_attn_noalloc.restype = C.c_int
         L.specgen_fork_decode_attn_split.argtypes = [C.POINTER(ForkBatchC), P, C.c_int64, C.POINTER(C.c_int64)]
         L.specgen_fork_decode_attn_split.restype = C.c_int
         L.specgen_last_error.argtypes = []
@@ -234,6 +236,16 @@ def specgen_fork_decode_attn(batch, out: torch.Tensor, out_lse: Optional[torch.T
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
     _check(lib().specgen_fork_decode_attn(C.byref(s), _dptr(out), _dptr(out_lse), _dptr(workspace),
                                           workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+SPECGEN_NOALLOC_SCRATCH_BYTES = 64 << 20   # the library's per-GPU scratch of the no-allocation call
+
+
+def specgen_fork_decode_attn_noalloc(batch, out: torch.Tensor, out_lse: Optional[torch.Tensor], stream=None) -> None:
+    """specgen_fork_decode_attn without a workspace: the partials live in the
+    library's per-GPU scratch (calls that overlap on one GPU race)."""
+    s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _check(lib().specgen_fork_decode_attn_noalloc(C.byref(s), _dptr(out), _dptr(out_lse), _stream(stream)))
 
 
 def specgen_fork_decode_attn_phase(batch, phase: int, out: Optional[torch.Tensor], out_lse: Optional[torch.Tensor],

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -188,6 +189,33 @@ specgen_status_t run_batch(const specgen_fork_batch_t* b, int32_t phase, void* o
   const specgen_status_t st = build_plan(b, &plan, &wsf, ptab_sel);
   if (st != SPECGEN_OK) return st;
   return run_plan(b, plan, wsf, phase, out, out_lse, workspace, workspace_bytes, stream);
+}
+
+// Scratch of specgen_fork_decode_attn_noalloc: the workspace of a call, in a
+// device array of the library (one per GPU, held until the process ends).  In
+// host code `scratch` names a host-side stand-in, not device memory: host code
+// uses only the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[SPECGEN_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, looked up once per device.
+specgen_status_t scratch_of_current_device(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPECGEN_ERR_DEVICE, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SPECGEN_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SPECGEN_ERR_DEVICE, "scratch address of device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return ok();
 }
 
 // Multi-token prefill as a decode batch of virtual forks: query i of fork f
@@ -379,6 +407,23 @@ specgen_status_t specgen_fork_prefill_attn(const specgen_fork_batch_t* b, const 
 specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t* b, void* out, float* out_lse,
                                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return specgen_fork_decode_attn_phase(b, SPECGEN_PHASE_ALL, out, out_lse, workspace, workspace_bytes, stream);
+}
+
+specgen_status_t specgen_fork_decode_attn_noalloc(const specgen_fork_batch_t* b, void* out, float* out_lse,
+                                                  hipStream_t stream) {
+  Plan plan;
+  int64_t wsf = 0;
+  specgen_status_t st = build_plan(b, &plan, &wsf);
+  if (st != SPECGEN_OK) return st;
+  if ((uint64_t)wsf * 4 > (uint64_t)SPECGEN_NOALLOC_SCRATCH_BYTES)
+    return fail(SPECGEN_ERR_WORKSPACE,
+                "batch needs %lld bytes of workspace, above the %llu-byte scratch of the no-allocation entry point "
+                "(use specgen_fork_decode_attn with a workspace)",
+                (long long)(wsf * 4), (unsigned long long)SPECGEN_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
+  if (st != SPECGEN_OK) return st;
+  return run_plan(b, plan, wsf, SPECGEN_PHASE_ALL, out, out_lse, ws, SPECGEN_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 specgen_status_t specgen_kv_import(const specgen_kv_tensor_t* tensors, int32_t num_tensors,

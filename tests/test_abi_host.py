@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported(L):
                           "specgen_fork_decode_attn_phase", "specgen_fork_prefill_attn_workspace_size",
                           "specgen_fork_prefill_attn", "specgen_kv_import", "specgen_kv_export",
                           "specgen_kv_append", "specgen_lse_merge", "specgen_last_error",
-                          "specgen_fork_decode_attn_split"}
+                          "specgen_fork_decode_attn_split", "specgen_fork_decode_attn_noalloc"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -325,3 +325,31 @@ def test_probe_library_exports_its_header():
     lib.specgen_probe_stream_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     assert lib.specgen_probe_stream_read(0x10000, 24, 0x20000, None) == 1      # not a multiple of 16
     assert lib.specgen_probe_stream_copy(0x10000, None, 64, None) == 1
+
+
+def test_noalloc_scratch_size_and_rejection(L):
+    """The no-allocation entry point's scratch size is the header's, and a batch
+    needing more workspace is rejected during argument checking (no device
+    work: this runs without a GPU)."""
+    import re
+    import types
+    import paper_2606_17518_amd as sg
+    hdr = open(os.path.join(ROOT, "include", "specgen.h")).read()
+    m = re.search(r"#define SPECGEN_NOALLOC_SCRATCH_BYTES \((\d+)ull << (\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == sg.SPECGEN_NOALLOC_SCRATCH_BYTES
+    P, N = 131072, 32
+    o = types.SimpleNamespace(num_traces=1, num_forks=N, num_q_heads=128, num_kv_heads=8, head_dim=128,
+                              num_blocks=10 ** 6, sm_scale=0.1, kv_dtype="fp8_e4m3", fork_off=[0, N], prefix_len=[P],
+                              suffix_len=[300] * N, prefix_table_off=[0, P // 16],
+                              suffix_table_off=list(range(0, 19 * (N + 1), 19)))
+    s, keep = sg.host_batch_struct(o)
+    for f in ("q", "k_pool", "v_pool", "k_scale", "v_scale", "fork_off", "prefix_len", "prefix_table_off",
+              "prefix_table", "suffix_len", "suffix_table_off", "suffix_table"):
+        setattr(s, f, 0x10000)
+    n = C.c_size_t(0)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 0
+    assert n.value > sg.SPECGEN_NOALLOC_SCRATCH_BYTES
+    assert L.specgen_fork_decode_attn_noalloc(C.byref(s), C.c_void_p(0x10000), None, None) == 3
+    assert "scratch" in L.specgen_last_error().decode()
+    bad, keep2 = sg.host_batch_struct(o)   # NULL device pointers: rejected first
+    assert L.specgen_fork_decode_attn_noalloc(C.byref(bad), C.c_void_p(0x10000), None, None) == 1
