@@ -122,21 +122,22 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.tile_cap[0] = mfma_tile_cap(in.D == 64 ? 64 : 128, fp8);
   in.tile_cap[1] = dot_tile_cap(in.D);
   // Unit prices of the split, from per-worker timelines of the MFMA kernel on
-  // MI355X: a tile of an item of 1, 2, 4 or 8 groups of 32 rows took
-  // 1.16-1.20, 1.20, 1.48 and about 2.5 us with bf16 KV, and 1.56-1.60, 1.96
-  // and 2.96 us for 1, 4 and 8 groups with E4M3 (which adds the decode of each
-  // tile); an item's fixed cost (q slot, token-group combine, partial stores)
-  // is about two tiles of 4 groups.  Prices in eighths of that tile, the item
-  // charge 16.  Items of 5-8 groups run one token group per wave (each wave
-  // takes both 32-token slabs of a tile).  The dot path prices every tile
-  // alike and an item at one tile.
-  const int mfma_rg_bf16[9] = {0, 6, 6, 7, 8, 10, 11, 12, 13};
+  // MI355X, in eighths of a tile of an item of 4 groups of 32 rows.  bf16 KV: a
+  // tile of 1 or 4 groups took 1.20 and 1.32 us, and an item's fixed cost (its
+  // q slot, about 1 us, and its end: token-group combine and partial stores,
+  // about 2.5 us) about 2.5 such tiles; the item charge is 20 (workers whose
+  // range holds two items ended last at a charge of 16).  E4M3 KV (which adds
+  // the decode of each tile): 1.56-1.60, 1.96 and 2.96 us for 1, 4 and 8
+  // groups, charge 16.  Items of 5-8 groups run one token group per wave
+  // (each wave takes both 32-token slabs of a tile).  The dot path prices
+  // every tile alike and an item at one tile.
+  const int mfma_rg_bf16[9] = {0, 7, 7, 7, 8, 10, 11, 12, 13};
   const int mfma_rg_e4m3[9] = {0, 6, 6, 7, 8, 9, 10, 10, 11};
   for (int r = 0; r < 9; ++r) {
     in.wt_rg[0][r] = fp8 ? mfma_rg_e4m3[r] : mfma_rg_bf16[r];
     in.wt_rg[1][r] = 1;
   }
-  in.charge[0] = 16;
+  in.charge[0] = fp8 ? 16 : 20;
   in.charge[1] = 1;
   in.walk_threads[0] = mfma_walk_threads();
   in.walk_threads[1] = 0;   // the dot kernel walks serially

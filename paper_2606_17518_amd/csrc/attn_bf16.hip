@@ -750,11 +750,21 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   if (issued < S) mk2 = issue_next();
   Desc cp_d = load_desc(0);
   int cp_ii = 0, cp_k = -q_slots(cp_d.nrows);
+  // bf16 KV: waves 0-3 queue their share of the next slot's DMAs after their
+  // compute, waves 4-7 before it.  Issuing a slot's 32 DMA instructions stalls
+  // the issuing waves for hundreds of cycles; with all eight issuing at once
+  // after the barrier, the two waves of each SIMD (w and w + 4) then run every
+  // phase of the slab (score MFMAs, softmax, PV MFMAs) in step and contend for
+  // the same unit.  Staggered, one wave's matrix work overlaps the other's
+  // vector work: 1.32 instead of 1.52 us per 32 KiB prefix slot on the 32k-prefix
+  // workload.  (E4M3 KV keeps the single issue point: there every wave
+  // converts the next tile right after the barrier, and the split gained 2%.)
+  const bool late_dma = !FP8 && wave < 4;
   for (int s = 0; s < S; ++s) {
     // E4M3 converts the next tile during this iteration, so it waits for that slot
     vm_wait_le(uniform(ops - ((FP8 && s + 1 < S) ? mk1 : mk0)));
     lds_barrier();
-    if (issued < S) mk3 = issue_next();
+    if (!late_dma && issued < S) mk3 = issue_next();
     const int stage = s & 3;
     if constexpr (FP8) {
       if (s + 1 < S && cp_k + 1 >= 0 && cp_k + 1 < cp_d.ntile) convert_tile((s + 1) & 3);   // slot s + 1 is a tile
@@ -767,6 +777,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       if (cp_k == cp_d.ntile - 1) st0 = uniform(finish_item(cp_d, stage));
     }
     ops += st0;
+    // the slot goes into the stage consumed last iteration, which no wave reads
+    // again before it lands: late issue only shortens its lead
+    if (late_dma && issued < S) mk3 = issue_next();
     mk0 = mk1;
     mk1 = mk2;
     mk2 = mk3;

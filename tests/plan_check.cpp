@@ -345,13 +345,15 @@ int main(int argc, char** argv) {
     in.rbs[0] = 256;
     in.rbs[1] = 16;
     in.item_cap[0] = in.item_cap[1] = 64;
-    // unit prices: the library's (MFMA 8 / 6 / 16, dot 1 / 1 / 1) or random;
-    // any positive prices must give a valid split
+    // unit prices: the library's (bf16 or E4M3 MFMA prices and charges, dot
+    // 1 / 1) or random; any positive prices must give a valid split
     const bool lib_prices = U(0, 1) != 0;
     if (lib_prices) {
-      const int mfma_rg[9] = {0, 6, 6, 7, 8, 11, 12, 12, 13};
-      for (int r = 0; r < 9; ++r) { in.wt_rg[0][r] = mfma_rg[r]; in.wt_rg[1][r] = 1; }
-      in.charge[0] = 16;
+      const bool e4m3 = U(0, 1) != 0;
+      const int rg_bf16[9] = {0, 7, 7, 7, 8, 10, 11, 12, 13};
+      const int rg_e4m3[9] = {0, 6, 6, 7, 8, 9, 10, 10, 11};
+      for (int r = 0; r < 9; ++r) { in.wt_rg[0][r] = e4m3 ? rg_e4m3[r] : rg_bf16[r]; in.wt_rg[1][r] = 1; }
+      in.charge[0] = e4m3 ? 16 : 20;
       in.charge[1] = 1;
     } else {
       for (int X = 0; X < 2; ++X) {
