@@ -48,8 +48,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of the MI355X
 
 
 # the partial kernel of the MFMA path (bf16 or E4M3 KV), and the sources it includes
-def partial_kernel(D: int, fp8: bool) -> str:
-    return f"attn_bf16_kernel<{D}, {'true' if fp8 else 'false'}>"
+def partial_kernel(D: int, fp8: bool, qk8: bool = False) -> str:
+    return f"attn_bf16_kernel<{D}, {'true' if fp8 else 'false'}, {'true' if qk8 else 'false'}>"
 
 
 PARTIAL_SOURCES = ("attn_bf16.hip", "worker.h", "common.h", "plan.h")
@@ -174,6 +174,8 @@ def main():
     ap.add_argument("--workload", default="trace_p32k_f16")
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--path", default="auto", choices=["auto", "mfma", "dot"])
+    ap.add_argument("--fp8-scores", action="store_true",
+                    help="E4M3 KV: scores on the fp8 matrix cores (SPECGEN_FLAG_FP8_SCORES)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -202,7 +204,8 @@ def main():
     log(f"uploading {R} replicas")
     reps = []
     for r in range(R):
-        fb = sg.ForkBatchTensors.from_numpy(b, dev, args.path)
+        fb = sg.ForkBatchTensors.from_numpy(b, dev, args.path,
+                                            flags=sg.SPECGEN_FLAG_FP8_SCORES if args.fp8_scores else 0)
         if r > 0:   # index arrays are shared; only q and the pools are replicated
             for name in ("fork_off", "prefix_len", "prefix_table_off", "prefix_table", "suffix_len",
                          "suffix_table_off", "suffix_table"):
@@ -403,14 +406,14 @@ def main():
     fp8 = b.kv_dtype != "bf16"
     if fp8 or q_len is not None:   # E4M3 KV (2r/e flop per byte) or many query rows: above the MFMA ridge
         tflops = kern_flops / part_s / 1e12
-        kname = partial_kernel(D, fp8) + (" (partials phase)" if q_len is None else
+        kname = partial_kernel(D, fp8, args.fp8_scores) + (" (partials phase)" if q_len is None else
                                           " + merge (the whole prefill call: no separate phases)")
         roofline = {"kernel": kname, "bound": "mfma",
                     "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload),
                     "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2)}
     else:
-        roofline = {"kernel": partial_kernel(D, False) + " (partials phase)", "bound": "hbm",
+        roofline = {"kernel": partial_kernel(D, False, False) + " (partials phase)", "bound": "hbm",
                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profile(args.workload),
                     "algorithmic_bytes_per_launch": int(kern_bytes)}
@@ -421,7 +424,7 @@ def main():
         "config": {"workload": args.workload, "traces": b.num_traces, "forks": N,
                    "prefix_len": [int(x) for x in b.prefix_len[:4]], "suffix_tokens": int(b.suffix_len.sum()),
                    "q_heads": Hq, "kv_heads": b.num_kv_heads, "head_dim": D, "kv_dtype": b.kv_dtype,
-                   "path": args.path, "replicas": R, "prefill_queries_per_fork": prefill_q or 0, "import_blocks": int(len(ids)) if imp is not None else 0},
+                   "path": args.path, "fp8_scores": bool(args.fp8_scores), "replicas": R, "prefill_queries_per_fork": prefill_q or 0, "import_blocks": int(len(ids)) if imp is not None else 0},
         "pct_of_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "fork_tokens_per_s": round(Q / attn_s, 1),
         "attn_us": {"p50": pct(attn_ms, 50), "p10": pct(attn_ms, 10), "p90": pct(attn_ms, 90),

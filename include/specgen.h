@@ -82,6 +82,17 @@ typedef enum { SPECGEN_BF16 = 0, SPECGEN_FP8_E4M3 = 1, SPECGEN_FP32 = 2 } specge
  * one kernel for every item (used by tests to cover both paths). */
 typedef enum { SPECGEN_PATH_AUTO = 0, SPECGEN_PATH_DOT = 1, SPECGEN_PATH_MFMA = 2 } specgen_path_t;
 
+/* Options of a fork batch (the flags field).
+ * SPECGEN_FLAG_FP8_SCORES: with E4M3 KV and head_dim 128, the MFMA kernel
+ * computes the scores q . k on the fp8 matrix cores straight from the K codes
+ * (no decode of K), with each query row held as two E4M3 terms,
+ * q = 2^e (hi + lo/16), e from the row's largest |q|: the scores stay within
+ * the accuracy of bf16 queries.  Values and probabilities stay bf16.  Items
+ * on the dot path are unaffected.  With bf16 KV the flag is rejected
+ * (SPECGEN_ERR_INVALID_ARG); with head_dim 64, SPECGEN_ERR_UNSUPPORTED.
+ * Other bits must be 0. */
+#define SPECGEN_FLAG_FP8_SCORES 1
+
 /* One decode step for every fork of T traces. */
 typedef struct {
   int32_t num_traces;        /* T >= 1                                           */
@@ -94,7 +105,7 @@ typedef struct {
   float sm_scale;            /* > 0 and finite, e.g. 1/sqrt(D)                   */
   int32_t kv_dtype;          /* specgen_dtype_t: SPECGEN_BF16 or SPECGEN_FP8_E4M3 */
   int32_t path;              /* specgen_path_t                                   */
-  int32_t reserved;          /* must be 0                                        */
+  int32_t flags;             /* 0, or SPECGEN_FLAG_FP8_SCORES                    */
   /* device memory, caller-owned */
   const void *q;             /* [N][Hq][D] bf16                                  */
   const void *k_pool;        /* [num_blocks][Hkv][16][D] kv_dtype                */

@@ -24,6 +24,7 @@ SPECGEN_PATH_AUTO, SPECGEN_PATH_DOT, SPECGEN_PATH_MFMA = 0, 1, 2
 PATHS = {"auto": SPECGEN_PATH_AUTO, "dot": SPECGEN_PATH_DOT, "mfma": SPECGEN_PATH_MFMA}
 
 SPECGEN_PHASE_ALL, SPECGEN_PHASE_PARTIALS, SPECGEN_PHASE_MERGE = 0, 1, 2
+SPECGEN_FLAG_FP8_SCORES = 1
 
 EXPORTED = ("specgen_fork_decode_attn_workspace_size", "specgen_fork_decode_attn", "specgen_fork_decode_attn_phase",
             "specgen_fork_prefill_attn_workspace_size", "specgen_fork_prefill_attn",
@@ -42,7 +43,7 @@ class ForkBatchC(C.Structure):
         ("num_traces", C.c_int32), ("num_forks", C.c_int32), ("num_q_heads", C.c_int32),
         ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("block_size", C.c_int32),
         ("num_blocks", C.c_int64), ("sm_scale", C.c_float), ("kv_dtype", C.c_int32),
-        ("path", C.c_int32), ("reserved", C.c_int32),
+        ("path", C.c_int32), ("flags", C.c_int32),
         ("q", C.c_void_p), ("k_pool", C.c_void_p), ("v_pool", C.c_void_p),
         ("k_scale", C.c_void_p), ("v_scale", C.c_void_p),
         ("fork_off", C.c_void_p), ("prefix_len", C.c_void_p), ("prefix_table_off", C.c_void_p),
@@ -162,11 +163,12 @@ class ForkBatchTensors:
     prefix_table_off_h: np.ndarray
     suffix_table_off_h: np.ndarray
     path: int = SPECGEN_PATH_AUTO
+    flags: int = 0                                 # SPECGEN_FLAG_FP8_SCORES or 0
     block_size: int = 16
     prefix_parent_h: Optional[np.ndarray] = None   # nested prefixes: parent trace or -1
 
     @staticmethod
-    def from_numpy(b, device="cuda", path: str | int = "auto") -> "ForkBatchTensors":
+    def from_numpy(b, device="cuda", path: str | int = "auto", flags: int = 0) -> "ForkBatchTensors":
         """Upload an object with the numpy fields of a fork batch (q, pools,
         scales, index arrays) and keep int32 host mirrors of the lengths and
         table offsets."""
@@ -190,7 +192,7 @@ class ForkBatchTensors:
             suffix_len_h=np.ascontiguousarray(b.suffix_len, np.int32),
             prefix_table_off_h=np.ascontiguousarray(b.prefix_table_off, np.int32),
             suffix_table_off_h=np.ascontiguousarray(b.suffix_table_off, np.int32),
-            path=PATHS[path] if isinstance(path, str) else int(path),
+            path=PATHS[path] if isinstance(path, str) else int(path), flags=int(flags),
             prefix_parent_h=None if getattr(b, "prefix_parent", None) is None
             else np.ascontiguousarray(b.prefix_parent, np.int32))
 
@@ -206,7 +208,7 @@ class ForkBatchTensors:
         s.sm_scale = self.sm_scale
         s.kv_dtype = self.kv_dtype
         s.path = self.path
-        s.reserved = 0
+        s.flags = self.flags
         for name in ("q", "k_pool", "v_pool", "k_scale", "v_scale", "fork_off", "prefix_len", "prefix_table_off",
                      "prefix_table", "suffix_len", "suffix_table_off", "suffix_table"):
             t = getattr(self, name)
@@ -343,7 +345,7 @@ def host_batch_struct(b, path: str | int = "auto"):
     s.head_dim, s.block_size, s.num_blocks, s.sm_scale = b.head_dim, 16, b.num_blocks, float(b.sm_scale)
     s.kv_dtype = SPECGEN_BF16 if b.kv_dtype == "bf16" else SPECGEN_FP8_E4M3
     s.path = PATHS[path] if isinstance(path, str) else int(path)
-    s.reserved = 0
+    s.flags = 0
     s.fork_off_h, s.prefix_len_h, s.suffix_len_h, s.prefix_table_off_h, s.suffix_table_off_h = \
         (a.ctypes.data for a in keep)
     if getattr(b, "prefix_parent", None) is not None:

@@ -66,7 +66,7 @@ specgen_status_t check_table_offsets(const char* what, const int32_t* off, const
 specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* ws_floats,
                             const int32_t* ptab_sel = nullptr) {
   if (!b) return fail(SPECGEN_ERR_INVALID_ARG, "batch is NULL");
-  if (b->reserved != 0) return fail(SPECGEN_ERR_INVALID_ARG, "reserved field must be 0");
+  if (b->flags & ~SPECGEN_FLAG_FP8_SCORES) return fail(SPECGEN_ERR_INVALID_ARG, "unknown flags 0x%x", b->flags);
   if (b->num_traces < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_traces must be >= 1 (got %d)", b->num_traces);
   if (b->num_forks < 1) return fail(SPECGEN_ERR_INVALID_ARG, "num_forks must be >= 1 (got %d)", b->num_forks);
   if (b->block_size != 16) return fail(SPECGEN_ERR_UNSUPPORTED, "block_size %d must be 16", b->block_size);
@@ -80,6 +80,10 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   if (!b->q || !b->k_pool || !b->v_pool || !b->fork_off || !b->prefix_len || !b->prefix_table_off ||
       !b->prefix_table || !b->suffix_len || !b->suffix_table_off)
     return fail(SPECGEN_ERR_INVALID_ARG, "a device pointer of the batch is NULL");
+  if ((b->flags & SPECGEN_FLAG_FP8_SCORES) && b->kv_dtype != SPECGEN_FP8_E4M3)
+    return fail(SPECGEN_ERR_INVALID_ARG, "fp8 scores need E4M3 KV");
+  if ((b->flags & SPECGEN_FLAG_FP8_SCORES) && b->head_dim != 128)
+    return fail(SPECGEN_ERR_UNSUPPORTED, "fp8 scores need head_dim 128");
   if (b->kv_dtype == SPECGEN_FP8_E4M3 && (!b->k_scale || !b->v_scale))
     return fail(SPECGEN_ERR_INVALID_ARG, "E4M3 KV needs k_scale and v_scale");
   if (!b->fork_off_h || !b->prefix_len_h || !b->suffix_len_h || !b->prefix_table_off_h || !b->suffix_table_off_h)
@@ -172,7 +176,8 @@ specgen_status_t run_plan(const specgen_fork_batch_t* b, const Plan& plan, int64
   const bool fp8 = b->kv_dtype == SPECGEN_FP8_E4M3;
   hipError_t e = hipSuccess;
   if (phase != SPECGEN_PHASE_MERGE) {
-    if (plan.part[kPartMfma].workers > 0) e = launch_attn_mfma_any(a, plan, fp8, stream);
+    const bool qk8 = (b->flags & SPECGEN_FLAG_FP8_SCORES) != 0;
+    if (plan.part[kPartMfma].workers > 0) e = launch_attn_mfma_any(a, plan, fp8, qk8, stream);
     if (e == hipSuccess && plan.part[kPartDot].workers > 0) e = launch_attn_dot_any(a, plan, fp8, stream);
   }
   if (e == hipSuccess && phase != SPECGEN_PHASE_PARTIALS) e = launch_fork_merge(plan, a.ws, out, out_lse, stream);

@@ -45,6 +45,18 @@
 // with lazy rescaling; O^T += V^T P^T, where the A operand (16 dims x 32
 // tokens) is one 16-byte LDS read per lane because V is stored transposed.
 //
+// E4M3 KV with fp8 scores (QK8): S^T = K Q^T runs on gfx950's fp8 matrix cores
+// (v_mfma_scale_f32_16x16x128_f8f6f4: all 128 dims of 16 keys x 16 rows in one
+// instruction) straight from the K codes in LDS, which are then never decoded;
+// each query row is held as two E4M3 terms, q = 2^e (hi + lo / 16), whose
+// power-of-two scale rides in the instruction's per-row E8M0 scale operand, so
+// the score is the hi product accumulated onto the lo product.  A single E4M3
+// term would double the score rate but moves peaked scores by several percent;
+// with two terms the scores are as close as with bf16 queries at the same
+// matrix time (the fp8 instruction runs at twice the bf16 rate).  The PV
+// product stays on bf16 operands (V codes are decoded in LDS, and P in E4M3
+// would be as coarse as a one-term query).
+//
 // The accumulators live in VGPRs: this file is compiled with MFMA operands and
 // results in VGPRs (-amdgpu-mfma-vgpr-form), which leaves the whole 256-register
 // budget of a two-waves-per-SIMD kernel to one register file.  It is also
@@ -148,6 +160,24 @@ __device__ __forceinline__ u32x2 e4m3x4_to_bf16x4(uint32_t w) {
   return r;
 }
 
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// fp8 scores: the XOR swizzle of the 16-byte chunks of K code row t (bit 0 from
+// bit 1 of t, bits 1-2 from bits 3-4): the 16 rows an operand read touches in
+// one lane group spread over all bank groups.
+__device__ __forceinline__ int k8_swz(int t) { return ((t >> 1) & 1) | ((t >> 2) & 6); }
+
+// The smallest e with amax * 2^-e <= 448 (E4M3's largest finite value), from
+// the bits of amax, kept in [-123, 120] so that 127 + e and 127 + e - 4 are
+// valid E8M0 scales and 2^-e is a normal float; 0 for a zero row.
+__device__ __forceinline__ int q8_exponent(float amax) {
+  const uint32_t b = __float_as_uint(amax);
+  if (amax == 0.f) return 0;
+  const int ex = (int)((b >> 23) & 0xFF) - 127;          // amax = 1.m x 2^ex
+  int e = ex - 8 + ((b & 0x7FFFFFu) > 0x600000u ? 1 : 0);   // 448 = 1.75 x 2^8
+  return e < -123 ? -123 : (e > 120 ? 120 : e);
+}
+
 template <int N>
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
@@ -173,10 +203,11 @@ __device__ __forceinline__ void vm_wait_le(int n) {
 
 }  // namespace bf16k
 
-template <int D, bool FP8>
+template <int D, bool FP8, bool QK8>
 __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, const Plan plan_arg) {
   using namespace bf16k;
   using C = Cfg<D, FP8>;
+  static_assert(!QK8 || (FP8 && D == 128), "fp8 scores: E4M3 KV with 128 dims (one 128-deep MFMA per key tile)");
   constexpr int TT = C::kTT;
   constexpr int CPR = C::kCPR;
   constexpr int KS = D / 32;   // k-steps of S^T
@@ -293,9 +324,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         const int kb = wq * NB + b;
         const uint8_t* sb = pool + (int64_t)id[b] * blk8 + (int64_t)d.j * C::kF8Slice;
 #pragma unroll
-        for (int i = 0; i < NI8; ++i)
-          dma16(sb, (uint32_t)(1024 * i + 16 * lane),
-                st + (uint32_t)((is_v ? C::kTileB : 0) + 2048 * (kb * NI8 + i)));
+        for (int i = 0; i < NI8; ++i) {
+          uint32_t src = (uint32_t)(1024 * i + 16 * lane);
+          if (QK8 && !is_v) {
+            // K codes stay codes: 16-byte chunk c of tile row t lands at chunk
+            // c ^ k8_swz(t) of its LDS row, so the score reads hit distinct banks
+            const int t = 8 * (kb * NI8 + i) + lane / 8;
+            src = (uint32_t)(1024 * i + 128 * (lane / 8) + 16 * ((lane % 8) ^ k8_swz(t)));
+          }
+          dma16(sb, src, st + (uint32_t)((is_v ? C::kTileB : 0) + 2048 * (kb * NI8 + i)));
+        }
       }
     } else {
       const int tile = d.tile0 + k;
@@ -338,8 +376,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     const u32x4 ck = *reinterpret_cast<const u32x4*>(st8 + 2048 * wave + 16 * lane);
     const u32x4 cv = *reinterpret_cast<const u32x4*>(st8 + C::kTileB + 2048 * wave + 16 * lane);
     const int o = tid * 16;   // byte of the chunk within the tile's codes of one tensor
-    // K chunk: 16 dims of one token row of block slice kb
-    {
+    // K chunk: 16 dims of one token row of block slice kb (fp8 scores read the codes as they are)
+    if constexpr (!QK8) {
       const int kb = o / C::kF8Slice;
       const int tok = (o % C::kF8Slice) / D;
       const int c8 = (o % D) / 8;                  // first bf16 chunk of the 16 dims
@@ -374,6 +412,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   // tile, row d = 16 dt + ln, half G & 1 -> LDS position 2d + (half ^ bit 3 of d)
   const int v_lane_off = (G >> 1) * C::kSliceB + 32 * ln + 16 * ((G & 1) ^ ((ln >> 3) & 1));
   bf16x8 qop[2][KS];
+  // QK8: per N-tile, the E4M3 codes of the lane's 32 dims of its row (dims
+  // 16G .. 16G+15 in bytes 0-15, 64+16G .. +15 in bytes 16-31, the operand
+  // layout of the 128-deep fp8 MFMA) for both terms, and their E8M0 scales
+  i32x8 q8h[2], q8l[2];
+  int q8sh[2], q8sl[2];
   f32x4 acc[2][DT];
   // Per row (each lane: its share of it): the running max, and two sums of
   // the probabilities: l_run of the bf16 weights the PV product uses (the
@@ -403,7 +446,53 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int row = rg * RS + nt * 16 + ln - qi * C::kQRows;   // row within the slot
-      if (mine) {
+      if (QK8 && mine) {
+        // the row's largest |q| over its 4 lanes (the 4 lane groups hold a
+        // quarter of its dims each) sets e; every lane computes it (`mine` is
+        // wave-uniform: only the waves whose rows are in this slot read it)
+        const SG_LDS uint8_t* qr = qb + row * C::kRowB;
+        u32x4 c4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ch = (i < 2 ? 2 * G + i : 8 + 2 * G + (i - 2)) ^ swz_q<D>(row);
+          c4[i] = *reinterpret_cast<const SG_LDS u32x4*>(qr + ch * 16);
+        }
+        float x[32];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t w0 = c4[i].x, w1 = c4[i].y, w2 = c4[i].z, w3 = c4[i].w;
+          const uint32_t ww[4] = {w0, w1, w2, w3};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            x[8 * i + 2 * j] = __uint_as_float(ww[j] << 16);
+            x[8 * i + 2 * j + 1] = __uint_as_float(ww[j] & 0xFFFF0000u);
+          }
+        }
+        float amax = 0.f;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) amax = fmaxf(amax, fabsf(x[i]));
+        amax = rows4_max(amax);
+        const int e = q8_exponent(amax);
+        const float inv = __uint_as_float((uint32_t)(127 - e) << 23);   // 2^-e, exact
+        uint32_t hw[8], lw[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          // four values: codes of x * 2^-e (RNE), then of the remainder times 16
+          const float y0 = x[4 * k] * inv, y1 = x[4 * k + 1] * inv, y2 = x[4 * k + 2] * inv, y3 = x[4 * k + 3] * inv;
+          uint32_t h = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false);
+          h = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, (int)h, true);
+          const f32x2 d01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)h, false);
+          const f32x2 d23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)h, true);
+          uint32_t l = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32((y0 - d01[0]) * 16.f, (y1 - d01[1]) * 16.f, 0, false);
+          l = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32((y2 - d23[0]) * 16.f, (y3 - d23[1]) * 16.f, (int)l, true);
+          hw[k] = h;
+          lw[k] = l;
+        }
+        q8h[nt] = i32x8{(int)hw[0], (int)hw[1], (int)hw[2], (int)hw[3], (int)hw[4], (int)hw[5], (int)hw[6], (int)hw[7]};
+        q8l[nt] = i32x8{(int)lw[0], (int)lw[1], (int)lw[2], (int)lw[3], (int)lw[4], (int)lw[5], (int)lw[6], (int)lw[7]};
+        q8sh[nt] = 127 + e;
+        q8sl[nt] = 127 + e - 4;
+      } else if (!QK8 && mine) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int slot = (ks * 4 + G) ^ swz_q<D>(row);
@@ -440,25 +529,51 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) s[u][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
-    const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
-    bf16x8 ka[KS], kbo[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int cho = (((4 * ks + G) ^ k_lane_swz) << 4);
-      ka[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
-      kbo[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
-    }
     const SG_LDS uint8_t* vrow = vb + (sb >> 4) * C::kSliceB + v_lane_off;
     u32x4 vraw[DT];
+    if constexpr (QK8) {
+      // A operand: key row t's codes, dims 16G .. +15 and 64+16G .. +15 (chunks G
+      // and 4+G, swizzled), for the keys {8G' + e} (u = 0) and {8G' + 4 + e} (u = 1)
+      i32x8 k8[2];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vraw[dt] = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
+      for (int u = 0; u < 2; ++u) {
+        const int t = sb + k_lane_tok + 4 * u;
+        const SG_LDS uint8_t* krow = kb + (t >> 3) * 2048 + (t & 7) * 128;
+        const int sw = k8_swz(t);
+        const u32x4 lo = *reinterpret_cast<const SG_LDS u32x4*>(krow + ((G ^ sw) << 4));
+        const u32x4 hi = *reinterpret_cast<const SG_LDS u32x4*>(krow + (((4 + G) ^ sw) << 4));
+        k8[u] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+      }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+      for (int dt = 0; dt < DT; ++dt) vraw[dt] = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qop[nt][ks], s[0][nt], 0, 0, 0);
-        s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kbo[ks], qop[nt][ks], s[1][nt], 0, 0, 0);
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          s[u][nt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(k8[u], q8l[nt], s[u][nt], 0, 0, 0, 127, 0,
+                                                                       q8sl[nt]);
+          s[u][nt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(k8[u], q8h[nt], s[u][nt], 0, 0, 0, 127, 0,
+                                                                       q8sh[nt]);
+        }
+    } else {
+      const SG_LDS uint8_t* ka_row = kb + (sb + k_lane_tok) * C::kRowB;
+      const SG_LDS uint8_t* kb_row = ka_row + 4 * C::kRowB;
+      bf16x8 ka[KS], kbo[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int cho = (((4 * ks + G) ^ k_lane_swz) << 4);
+        ka[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(ka_row + cho));
+        kbo[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const SG_LDS u32x4*>(kb_row + cho));
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vraw[dt] = *reinterpret_cast<const SG_LDS u32x4*>(vrow + dt * 512);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          s[0][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qop[nt][ks], s[0][nt], 0, 0, 0);
+          s[1][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kbo[ks], qop[nt][ks], s[1][nt], 0, 0, 0);
+        }
       }
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
@@ -788,16 +903,18 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 }
 
 // Partial kernel of the MFMA partition: bf16 KV, or E4M3 KV decoded exactly to
-// bf16 in LDS.
-hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream) {
+// bf16 in LDS, or (qk8, D = 128 only) E4M3 KV with fp8 scores.
+hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, bool qk8, hipStream_t stream) {
   const int W = plan.part[kPartMfma].workers;
   if (W <= 0) return hipSuccess;
+  if (qk8 && (!fp8 || plan.D != 128)) return hipErrorInvalidValue;
   if (plan.D == 128) {
-    if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(W), dim3(512), 0, stream, a, plan);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(W), dim3(512), 0, stream, a, plan);
+    if (qk8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(W), dim3(512), 0, stream, a, plan);
+    else if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, false>), dim3(W), dim3(512), 0, stream, a, plan);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, false, false>), dim3(W), dim3(512), 0, stream, a, plan);
   } else {
-    if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(W), dim3(512), 0, stream, a, plan);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(W), dim3(512), 0, stream, a, plan);
+    if (fp8) hipLaunchKernelGGL((attn_bf16_kernel<64, true, false>), dim3(W), dim3(512), 0, stream, a, plan);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, false, false>), dim3(W), dim3(512), 0, stream, a, plan);
   }
   return hipGetLastError();
 }

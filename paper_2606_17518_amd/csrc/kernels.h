@@ -9,7 +9,7 @@
 namespace specgen {
 
 // attn_bf16.hip (MFMA partition: bf16 or E4M3 KV)
-hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, hipStream_t stream);
+hipError_t launch_attn_mfma_any(const AttnArgs& a, const Plan& plan, bool fp8, bool qk8, hipStream_t stream);
 int mfma_tile_tokens(int D, bool fp8);
 int mfma_item_cap();
 int mfma_tile_cap(int D, bool fp8);

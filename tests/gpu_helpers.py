@@ -25,9 +25,9 @@ def say(msg):
     sys.stdout.flush()
 
 
-def run_attn(batch, path="auto", with_lse=True, fb=None):
+def run_attn(batch, path="auto", with_lse=True, fb=None, flags=0):
     if fb is None:
-        fb = sg.ForkBatchTensors.from_numpy(batch, "cuda", path)
+        fb = sg.ForkBatchTensors.from_numpy(batch, "cuda", path, flags=flags)
     N, Hq, D = batch.num_forks, batch.num_q_heads, batch.head_dim
     out = torch.full((N, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
     lse = torch.full((N, Hq), float("nan"), dtype=torch.float32, device="cuda") if with_lse else None

@@ -41,7 +41,7 @@ def _host_batch(**kw):
     import paper_2606_17518_amd.binding as B
     s = B.ForkBatchC()
     s.num_traces, s.num_forks, s.num_q_heads, s.num_kv_heads, s.head_dim, s.block_size = 1, 2, 8, 2, 64, 16
-    s.num_blocks, s.sm_scale, s.kv_dtype, s.path, s.reserved = 8, 0.125, 0, 0, 0
+    s.num_blocks, s.sm_scale, s.kv_dtype, s.path, s.flags = 8, 0.125, 0, 0, 0
     fake = 0x10000   # never dereferenced: every call below fails argument checks first
     for f in ("q", "k_pool", "v_pool", "fork_off", "prefix_len", "prefix_table_off", "prefix_table",
               "suffix_len", "suffix_table_off", "suffix_table"):
@@ -58,7 +58,7 @@ def _host_batch(**kw):
 @pytest.mark.parametrize("field,value,status", [
     ("num_traces", 0, 1), ("num_forks", 0, 1), ("num_q_heads", 7, 1), ("head_dim", 96, 2),
     ("block_size", 32, 2), ("sm_scale", 0.0, 1), ("sm_scale", float("nan"), 1), ("kv_dtype", 5, 2),
-    ("path", 9, 1), ("reserved", 1, 1), ("q", None, 1), ("suffix_len_h", None, 1), ("num_blocks", 0, 1),
+    ("path", 9, 1), ("flags", 2, 1), ("flags", 1, 1), ("q", None, 1), ("suffix_len_h", None, 1), ("num_blocks", 0, 1),
     ("suffix_table_off_h", None, 1), ("prefix_table_off_h", None, 1),
 ])
 def test_bad_batch_rejected_without_launch(L, field, value, status):
@@ -353,3 +353,16 @@ def test_noalloc_scratch_size_and_rejection(L):
     assert "scratch" in L.specgen_last_error().decode()
     bad, keep2 = sg.host_batch_struct(o)   # NULL device pointers: rejected first
     assert L.specgen_fork_decode_attn_noalloc(C.byref(bad), C.c_void_p(0x10000), None, None) == 1
+
+
+def test_fp8_scores_flag_validated(L):
+    """SPECGEN_FLAG_FP8_SCORES: E4M3 KV with head_dim 128 only."""
+    import paper_2606_17518_amd.binding as B
+    n = C.c_size_t(0)
+    s, keep = _host_batch(flags=B.SPECGEN_FLAG_FP8_SCORES, kv_dtype=B.SPECGEN_FP8_E4M3, k_scale=0x10000, v_scale=0x10000)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_UNSUPPORTED   # D = 64
+    s.head_dim = 128
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 0
+    s.kv_dtype = B.SPECGEN_BF16
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
+    assert "E4M3" in L.specgen_last_error().decode()

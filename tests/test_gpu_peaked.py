@@ -42,12 +42,12 @@ def _base(name, kv):
     return _cache[key]
 
 
-def _check(b, path, rows, what):
+def _check(b, path, rows, what, flags=0):
     pb, case = peaked_batch(b, path)
     say(f"{what}: oracle on {'all' if rows is None else len(rows)} rows")
     ref, ref_l = oracle.fork_decode_attn(pb, rows=rows)
     say(f"{what}: gpu")
-    out, lse = run_attn(pb, path)
+    out, lse = run_attn(pb, path, flags=flags)
     if rows is not None:
         out, lse = out[rows[:, 0], rows[:, 1]], lse[rows[:, 0], rows[:, 1]]
         case = case[rows[:, 0], rows[:, 1]]
