@@ -161,7 +161,15 @@ specgen_status_t specgen_fork_decode_attn_workspace_size(const specgen_fork_batc
  *   workspace: device, at least specgen_fork_decode_attn_workspace_size bytes,
  *   256-byte aligned; its contents on entry do not matter.
  * Block ids must lie in [0, num_blocks); an out-of-range id is undefined
- * behaviour (the kernels do not check it). */
+ * behaviour (the kernels do not check it).  The library built with
+ * SPECGEN_DEBUG_CHECKS defined (libspecgen_debug.so) checks every id the call
+ * will read before anything is launched -- ceil(P_t/16) entries per trace and
+ * ceil(S_f/16) per fork -- by copying the read part of each block table to
+ * the host and synchronising `stream`; an id out of range returns
+ * SPECGEN_ERR_INVALID_ARG naming the table entry.  That build is for testing:
+ * its calls block and copy, so they cannot be captured into a graph.  The same
+ * check guards specgen_fork_decode_attn_phase (PARTIALS and ALL),
+ * specgen_fork_decode_attn_noalloc and specgen_fork_prefill_attn there. */
 specgen_status_t specgen_fork_decode_attn(const specgen_fork_batch_t *b, void *out, float *out_lse,
                                           void *workspace, size_t workspace_bytes,
                                           hipStream_t stream);

@@ -16,7 +16,7 @@ from typing import Optional, Sequence
 import numpy as np
 import torch
 
-from .build import LIB_PATH
+from .build import DEBUG_LIB_PATH, LIB_PATH
 
 SPECGEN_OK, SPECGEN_ERR_INVALID_ARG, SPECGEN_ERR_UNSUPPORTED, SPECGEN_ERR_WORKSPACE, SPECGEN_ERR_DEVICE = range(5)
 SPECGEN_BF16, SPECGEN_FP8_E4M3, SPECGEN_FP32 = 0, 1, 2
@@ -79,42 +79,58 @@ class KvAppendC(C.Structure):
 
 
 _lib = None
+_debug_lib = None
+
+
+def load(path: str):
+    """Loads a build of the library at `path` and declares its entry points."""
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2606_17518_amd.build.build()")
+    L = C.CDLL(path)
+    P = C.c_void_p
+    L.specgen_fork_decode_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), C.POINTER(C.c_size_t)]
+    L.specgen_fork_decode_attn_workspace_size.restype = C.c_int
+    L.specgen_fork_decode_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, C.c_size_t, P]
+    L.specgen_fork_decode_attn.restype = C.c_int
+    L.specgen_fork_decode_attn_phase.argtypes = [C.POINTER(ForkBatchC), C.c_int32, P, P, P, C.c_size_t, P]
+    L.specgen_fork_decode_attn_phase.restype = C.c_int
+    L.specgen_fork_prefill_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), P, C.POINTER(C.c_size_t)]
+    L.specgen_fork_prefill_attn_workspace_size.restype = C.c_int
+    L.specgen_fork_prefill_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, P, C.c_size_t, P]
+    L.specgen_fork_prefill_attn.restype = C.c_int
+    L.specgen_kv_import.argtypes = [C.POINTER(KvTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
+    L.specgen_kv_import.restype = C.c_int
+    L.specgen_kv_export.argtypes = [C.POINTER(KvExportTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
+    L.specgen_kv_export.restype = C.c_int
+    L.specgen_kv_append.argtypes = [C.POINTER(KvAppendC), P]
+    L.specgen_kv_append.restype = C.c_int
+    L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
+    L.specgen_lse_merge.restype = C.c_int
+    L.specgen_fork_decode_attn_noalloc.argtypes = [C.POINTER(ForkBatchC), P, P, P]
+    L.specgen_fork_decode_attn_noalloc.restype = C.c_int
+    L.specgen_fork_decode_attn_split.argtypes = [C.POINTER(ForkBatchC), P, C.c_int64, C.POINTER(C.c_int64)]
+    L.specgen_fork_decode_attn_split.restype = C.c_int
+    L.specgen_last_error.argtypes = []
+    L.specgen_last_error.restype = C.c_char_p
+    return L
 
 
 def lib():
     """The loaded library; raises if it was never built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2606_17518_amd.build.build()")
-        L = C.CDLL(LIB_PATH)
-        P = C.c_void_p
-        L.specgen_fork_decode_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), C.POINTER(C.c_size_t)]
-        L.specgen_fork_decode_attn_workspace_size.restype = C.c_int
-        L.specgen_fork_decode_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, C.c_size_t, P]
-        L.specgen_fork_decode_attn.restype = C.c_int
-        L.specgen_fork_decode_attn_phase.argtypes = [C.POINTER(ForkBatchC), C.c_int32, P, P, P, C.c_size_t, P]
-        L.specgen_fork_decode_attn_phase.restype = C.c_int
-        L.specgen_fork_prefill_attn_workspace_size.argtypes = [C.POINTER(ForkBatchC), P, C.POINTER(C.c_size_t)]
-        L.specgen_fork_prefill_attn_workspace_size.restype = C.c_int
-        L.specgen_fork_prefill_attn.argtypes = [C.POINTER(ForkBatchC), P, P, P, P, C.c_size_t, P]
-        L.specgen_fork_prefill_attn.restype = C.c_int
-        L.specgen_kv_import.argtypes = [C.POINTER(KvTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
-        L.specgen_kv_import.restype = C.c_int
-        L.specgen_kv_export.argtypes = [C.POINTER(KvExportTensorC), C.c_int32, P, C.c_int64, C.c_int64, P, P]
-        L.specgen_kv_export.restype = C.c_int
-        L.specgen_kv_append.argtypes = [C.POINTER(KvAppendC), P]
-        L.specgen_kv_append.restype = C.c_int
-        L.specgen_lse_merge.argtypes = [P, P, C.c_int32, C.c_int64, C.c_int32, P, C.c_int32, P, P]
-        L.specgen_lse_merge.restype = C.c_int
-        L.specgen_fork_decode_attn_noalloc.argtypes = [C.POINTER(ForkBatchC), P, P, P]
-        L.specgen_fork_decode_attn_noalloc.restype = C.c_int
-        L.specgen_fork_decode_attn_split.argtypes = [C.POINTER(ForkBatchC), P, C.c_int64, C.POINTER(C.c_int64)]
-        L.specgen_fork_decode_attn_split.restype = C.c_int
-        L.specgen_last_error.argtypes = []
-        L.specgen_last_error.restype = C.c_char_p
-        _lib = L
+        _lib = load(LIB_PATH)
     return _lib
+
+
+def debug_lib():
+    """The build with SPECGEN_DEBUG_CHECKS (attention block ids checked on the
+    host before every launch: a table copy and a stream synchronisation per
+    call), with the same entry points."""
+    global _debug_lib
+    if _debug_lib is None:
+        _debug_lib = load(DEBUG_LIB_PATH)
+    return _debug_lib
 
 
 def _check(status: int):

@@ -1,9 +1,11 @@
 """Compile the HIP sources under csrc/ into libspecgen.so for gfx950.
 
 Objects are built in parallel under _build/ at the repository root and linked
-into paper_2606_17518_amd/libspecgen.so, and the benchmark's memory-ceiling
-kernels into libspecgen_probe.so.  Packed-FP32 instruction selection is
-switched off on every device compile.
+into paper_2606_17518_amd/libspecgen.so; the same kernels with the entry
+points built under SPECGEN_DEBUG_CHECKS (every attention block id checked on
+the host before launch) into libspecgen_debug.so; and the benchmark's
+memory-ceiling kernels into libspecgen_probe.so.  Packed-FP32 instruction
+selection is switched off on every device compile.
 """
 from __future__ import annotations
 
@@ -17,6 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
+DEBUG_LIB_PATH = os.path.join(PKG, "libspecgen_debug.so")
 SOURCES = ["abi.hip", "attn_bf16.hip", "attn_dot.hip", "merge.hip", "kv_import.hip", "kv_append.hip"]
 # the benchmark's memory-ceiling kernels, linked into a library of their own
 PROBE_SOURCES = ["probe.hip"]
@@ -45,9 +48,10 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     flags = compile_flags()
 
-    def one(src: str) -> str:
-        obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
-        cmd = [hipcc, *flags, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+    def one(job: tuple) -> str:
+        src, tag, defs = job
+        obj = os.path.join(BUILD_DIR, src.replace(".hip", tag + ".o"))
+        cmd = [hipcc, *flags, *defs, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
@@ -55,9 +59,13 @@ def build(verbose: bool = False) -> str:
             print(r.stderr)
         return obj
 
-    with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(one, SOURCES + PROBE_SOURCES))
-    for lib_path, lib_objs in ((LIB_PATH, objs[:-len(PROBE_SOURCES)]), (PROBE_LIB_PATH, objs[-len(PROBE_SOURCES):])):
+    jobs = [(s, "", []) for s in SOURCES + PROBE_SOURCES] + [("abi.hip", "_debug", ["-DSPECGEN_DEBUG_CHECKS"])]
+    with cf.ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 4)) as ex:
+        objs = dict(zip([j[0] + j[1] for j in jobs], ex.map(one, jobs)))
+    kernels = [objs[s] for s in SOURCES if s != "abi.hip"]
+    for lib_path, lib_objs in ((LIB_PATH, [objs["abi.hip"], *kernels]),
+                               (DEBUG_LIB_PATH, [objs["abi.hip_debug"], *kernels]),
+                               (PROBE_LIB_PATH, [objs[s] for s in PROBE_SOURCES])):
         tmp = lib_path + ".tmp%d" % os.getpid()
         r = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *lib_objs],
                            capture_output=True, text=True)

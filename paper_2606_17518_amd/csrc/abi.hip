@@ -14,6 +14,7 @@
 #include "../../include/specgen.h"
 #include "kernels.h"
 #include "planner.h"
+#include "table_check.h"
 
 
 using namespace specgen;
@@ -152,6 +153,29 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   return ok();
 }
 
+#ifdef SPECGEN_DEBUG_CHECKS
+// The debug build's check of every block id the partial kernels will read
+// (table_check.h): the read part of each block table is copied to the host
+// on `stream`, which is then synchronised, before anything is launched.
+specgen_status_t debug_check_block_ids(const specgen_fork_batch_t* b, const Plan& plan, hipStream_t stream) {
+  auto fetch = [&](int table, int64_t first, int64_t count, int32_t* dst) {
+    const int32_t* src = table == 0 ? b->prefix_table : b->suffix_table;
+    if (!src) return false;
+    return hipMemcpyAsync(dst, src + first, (size_t)count * sizeof(int32_t), hipMemcpyDeviceToHost, stream) ==
+               hipSuccess &&
+           hipStreamSynchronize(stream) == hipSuccess;
+  };
+  BadBlockId bad;
+  const int rc = check_block_ids(plan, b->num_blocks, fetch, &bad);
+  if (rc == kTableFetchFailed) return fail(SPECGEN_ERR_DEVICE, "debug check: the block tables could not be read back");
+  if (rc == kTableBadId)
+    return fail(SPECGEN_ERR_INVALID_ARG, "debug check: %s_table[%lld] = %d, read by %s %d, is outside [0, %lld)",
+                bad.table == 0 ? "prefix" : "suffix", (long long)bad.entry, bad.id,
+                bad.kind == 0 ? "the prefix of trace" : "the suffix of fork", bad.owner, (long long)b->num_blocks);
+  return ok();
+}
+#endif
+
 // Queues one call of the split attention (both phases or one) for a checked
 // batch and its plan.
 specgen_status_t run_plan(const specgen_fork_batch_t* b, const Plan& plan, int64_t wsf, int32_t phase, void* out,
@@ -174,6 +198,12 @@ specgen_status_t run_plan(const specgen_fork_batch_t* b, const Plan& plan, int64
   a.sm_scale = b->sm_scale;
   a.c_log2 = b->sm_scale * kLog2e;
   const bool fp8 = b->kv_dtype == SPECGEN_FP8_E4M3;
+#ifdef SPECGEN_DEBUG_CHECKS
+  if (phase != SPECGEN_PHASE_MERGE) {
+    const specgen_status_t st = debug_check_block_ids(b, plan, stream);
+    if (st != SPECGEN_OK) return st;
+  }
+#endif
   hipError_t e = hipSuccess;
   if (phase != SPECGEN_PHASE_MERGE) {
     const bool qk8 = (b->flags & SPECGEN_FLAG_FP8_SCORES) != 0;

@@ -366,3 +366,30 @@ def test_fp8_scores_flag_validated(L):
     s.kv_dtype = B.SPECGEN_BF16
     assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
     assert "E4M3" in L.specgen_last_error().decode()
+
+
+def test_debug_library_exports_the_same_entry_points(L):
+    """libspecgen_debug.so (SPECGEN_DEBUG_CHECKS) is a drop-in build of the
+    library: every declared entry point, and the same argument checks."""
+    import paper_2606_17518_amd.binding as B
+    D = B.debug_lib()
+    for n in _declared():
+        assert hasattr(D, n), n
+    s, keep = _host_batch(num_traces=0)
+    n = C.c_size_t(0)
+    assert D.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 1
+    assert b"num_traces" in D.specgen_last_error()
+
+
+def test_debug_block_id_check_on_host_tables(tmp_path):
+    """The debug build's block-id check (csrc/table_check.h), driven with host
+    tables by a g++ harness: ids past ceil(len/16) are never read, -1 and
+    num_blocks are caught in either table, prefill traces whose prefix lives in
+    the suffix table are checked there, and empty suffixes read nothing."""
+    import subprocess
+    exe = str(tmp_path / "table_check")
+    subprocess.run(["g++", "-O1", "-std=c++17", "-Wall", "-Werror", "-o", exe,
+                    os.path.join(ROOT, "tests", "table_check_driver.cpp")], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all table checks passed" in r.stdout

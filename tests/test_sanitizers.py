@@ -1,10 +1,11 @@
 """Host code under AddressSanitizer and UndefinedBehaviorSanitizer (CPU only).
 
-Two programs are built with gcc/g++ and the sanitizers and run to completion:
+Three programs are built with gcc/g++ and the sanitizers and run to completion:
   - tests/sanitize_driver.c: every entry point of the fp64 oracle on small
     random batches whose buffers are allocated to their exact sizes;
   - tests/plan_check.cpp: the host planner's work split and its replay of
-    every worker walk and merge lookup.
+    every worker walk and merge lookup;
+  - tests/table_check_driver.cpp: the debug build's block-id check.
 Any out-of-bounds access, leak or undefined operation aborts the program
 (-fno-sanitize-recover), which fails the test.
 """
@@ -42,3 +43,12 @@ def test_planner_under_asan_ubsan(tmp_path):
     r = subprocess.run([exe, "150", "3"], capture_output=True, text=True, timeout=600, env=_env())
     assert r.returncode == 0, r.stderr[-4000:]
     assert r.stdout.startswith("OK"), r.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not found")
+def test_block_id_check_under_asan_ubsan(tmp_path):
+    exe = str(tmp_path / "table_check")
+    subprocess.run(["g++", *SAN, "-std=c++17", "-o", exe, os.path.join(HERE, "table_check_driver.cpp")], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120, env=_env())
+    assert r.returncode == 0, r.stdout + r.stderr[-4000:]
+    assert "all table checks passed" in r.stdout
