@@ -38,7 +38,9 @@
  *    log-sum-exp of the scaled scores, fp32.
  *  - E4M3 KV is the OCP 8-bit "E4M3FN" format (bias 7, max 448, no inf,
  *    0x7F/0xFF NaN) with one fp32 scale per physical block and tensor: the
- *    value of a stored code c in block b is decode(c) * scale[b].
+ *    value of a stored code c in block b is decode(c) * scale[b].  Scales are
+ *    quantisation scales (e.g. the block's largest |value| / 448): finite and
+ *    >= 0; a negative scale gives unspecified results.
  *
  * Ownership: the caller allocates every buffer and keeps it alive until the
  * work queued on `stream` has finished.  The library keeps no pointer after a

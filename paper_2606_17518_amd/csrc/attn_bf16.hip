@@ -578,7 +578,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     }
     // lane (G, ln) holds, for row ln of each N-tile, the scores of keys sb+8G+0..7
     // (all in block (sb + 8G) / 16 of the tile)
-    float vsc = 1.f, inv_vsc = 1.f;
+    // E4M3: the key scale multiplies a slab's scores only where the slab is
+    // masked; elsewhere it rides in the exponent's scale factor, cl, and in the
+    // row maxima (scales are non-negative, so scaling commutes with max)
+    float vsc = 1.f, inv_vsc = 1.f, ksc = 1.f;
     if constexpr (FP8) {
       // the slab's two blocks (ids[idb + sb/16] and the next): lanes G < 2 hold
       // keys of the first
@@ -593,13 +596,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       // into one per-lane load of a selected address)
       auto sload = [](cfp p, int i) { return __int_as_float(uniform(__float_as_int(p[i]))); };
       const float k0 = sload(ks, id0), k1 = sload(ks, id1), v0 = sload(vs, id0), v1 = sload(vs, id1);
-      const float ksc = G < 2 ? k0 : k1;
+      ksc = G < 2 ? k0 : k1;
       vsc = G < 2 ? v0 : v1;
       inv_vsc = __builtin_amdgcn_rcpf(vsc);
+      if constexpr (kMask) {   // scaled before the -inf masking (a zero scale times -inf would be NaN)
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) s[u][nt] *= ksc;
+          for (int nt = 0; nt < NT; ++nt) s[u][nt] *= ksc;
+        ksc = 1.f;
+      }
     }
     if constexpr (kMask) {
 #pragma unroll
@@ -616,8 +622,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     float mx[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
-      mx[nt] = fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
-                     fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
+      mx[nt] = ksc * fmaxf(fmaxf(fmaxf(s[0][nt][0], s[0][nt][1]), fmaxf(s[0][nt][2], s[0][nt][3])),
+                           fmaxf(fmaxf(s[1][nt][0], s[1][nt][1]), fmaxf(s[1][nt][2], s[1][nt][3])));
     // Lazy rescaling: the reference max only moves when a score exceeds it by
     // more than 2^kRescaleLog2 in probability (one wave-uniform decision for
     // both N-tiles; m_run is the same on the 4 lanes of a row).
@@ -644,11 +650,12 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     // P = exp2(S - m) in bf16, then O^T += V^T P^T; the exponentials of N-tile 1
     // are interleaved with the PV MFMAs of N-tile 0
     const float mc0 = m_run[0] * a.c_log2, mc1 = m_run[1] * a.c_log2;
+    const float cl = a.c_log2 * ksc;
     float p0[8], p1[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], a.c_log2, -mc0));
-      p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], a.c_log2, -mc0));
+      p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], cl, -mc0));
+      p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], cl, -mc0));
     }
     lf_run[0] += ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
     if constexpr (FP8) {   // P carries the value scale into PV
@@ -667,11 +674,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop0, acc[0][dt], 0, 0, 0);
-      if (dt < 8) p1[dt] = __builtin_amdgcn_exp2f(fmaf(s[dt >> 2][1][dt & 3], a.c_log2, -mc1));
+      if (dt < 8) p1[dt] = __builtin_amdgcn_exp2f(fmaf(s[dt >> 2][1][dt & 3], cl, -mc1));
     }
 #pragma unroll
     for (int e = DT; e < 8; ++e)   // D = 64: fewer PV MFMAs than exponentials
-      p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], a.c_log2, -mc1));
+      p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], cl, -mc1));
     lf_run[1] += ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
     if constexpr (FP8) {
 #pragma unroll
