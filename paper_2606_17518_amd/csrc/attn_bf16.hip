@@ -717,8 +717,18 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   };
 
   // Combine the token groups of the item through the stage just consumed and
-  // write token group 0's normalised partial.  Every wave calls this (it has
-  // barriers); returns the number of vector-memory stores this wave issued.
+  // write the normalised partial (o, lse) of each row.  Every wave calls this
+  // (it has barriers); returns the number of vector-memory stores this wave
+  // issued.
+  //   Two token groups (every D = 128 item of up to 128 rows): the waves of a
+  // row-group pair swap halves -- token group 0 keeps N-tile 0 and sends
+  // N-tile 1, token group 1 the reverse -- so each wave combines and stores
+  // one N-tile.  The sent half travels normalised by its row sum, as fp16
+  // with the per-row power-of-two scale of the stored partials (4 KiB per
+  // wave: 32 KiB, one stage, for eight waves), and its (m, l, lf, scale)
+  // through the ML area.
+  //   More token groups (D = 64): token group 0 gathers the others' fp32
+  // accumulators in rounds that fit the stage and stores both N-tiles.
   auto finish_item = [&](const Desc& d, int stage) -> int {
     float lrow[2], lfrow[2];
 #pragma unroll
@@ -726,7 +736,66 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       lrow[nt] = rows4_sum(l_run[nt]);
       lfrow[nt] = rows4_sum(lf_run[nt]);
     }
-    if (TG > 1) {
+    int nt_lo = 0;   // this wave stores N-tiles nt_lo .. NT - 1 (TG = 2: only nt_lo)
+    bool stores = active && tg == 0;
+    // (keep is a compile-time constant in each call, so the accumulator arrays
+    // are indexed statically and stay in registers)
+    auto swap_halves = [&](auto keep_c) {
+      constexpr int keep = decltype(keep_c)::value, send = 1 - keep;
+      uint32_t* cb = reinterpret_cast<uint32_t*>(lds + stage * C::kStageB);
+      lds_barrier();   // every wave is done with the stage's K and V
+      if (active) {
+        const float inv_l = lrow[send] > 0.f ? 1.f / lrow[send] : 0.f;
+        float amax = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) amax = fmaxf(amax, fabsf(acc[send][dt][e]));
+        amax = rows4_max(amax);
+        const uint32_t kexp = (uint32_t)part_row_k(__float_as_uint(amax * inv_l));
+        const float mul = inv_l * __uint_as_float((254u - kexp) << 23);
+        // chunk c (d-tiles 2c, 2c + 1) of lane L at 1 KiB * c + 16 B * L of the wave's region
+#pragma unroll
+        for (int c = 0; c < DT / 2; ++c) {
+          const f32x4 x = acc[send][2 * c] * mul, y = acc[send][2 * c + 1] * mul;
+          const u32x4 ch = {pack_f16x2(x[0], x[1]), pack_f16x2(x[2], x[3]), pack_f16x2(y[0], y[1]),
+                            pack_f16x2(y[2], y[3])};
+          *reinterpret_cast<u32x4*>(cb + (wave * (DT / 2) + c) * 256 + lane * 4) = ch;
+        }
+        if (G == 0)
+          *reinterpret_cast<f32x4*>(ml + ((wave * 2 + send) * 16 + ln) * 4) =
+              f32x4{m_run[send], lrow[send], lfrow[send], __uint_as_float(kexp << 23)};
+      }
+      lds_barrier();
+      if (active) {
+        const int pw = rg + (1 - tg) * RG;   // the partner wave (same row group)
+        const f32x4 ml1 = *reinterpret_cast<const f32x4*>(ml + ((pw * 2 + keep) * 16 + ln) * 4);
+        const float m1 = ml1[0], l1 = ml1[1], lf1 = ml1[2];
+        // a token group that saw no token of the item has m = -inf, l = 0 and sent zeros
+        const float m = fmaxf(m_run[keep], m1);
+        const float mc = (m == -INFINITY) ? 0.f : m * a.c_log2;
+        const float a0 = __builtin_amdgcn_exp2f(m_run[keep] * a.c_log2 - mc);
+        const float a1 = __builtin_amdgcn_exp2f(m1 * a.c_log2 - mc);
+        const float w1 = a1 * l1 * ml1[3];   // the partner's accumulator is o1 * l1 * scale
+#pragma unroll
+        for (int c = 0; c < DT / 2; ++c) {
+          const u32x4 ch = *reinterpret_cast<const u32x4*>(cb + (pw * (DT / 2) + c) * 256 + lane * 4);
+          const f32x2 x01 = unpack_f16x2(ch[0]), x23 = unpack_f16x2(ch[1]);
+          const f32x2 y01 = unpack_f16x2(ch[2]), y23 = unpack_f16x2(ch[3]);
+          acc[keep][2 * c] = acc[keep][2 * c] * a0 + f32x4{x01[0], x01[1], x23[0], x23[1]} * w1;
+          acc[keep][2 * c + 1] = acc[keep][2 * c + 1] * a0 + f32x4{y01[0], y01[1], y23[0], y23[1]} * w1;
+        }
+        lrow[keep] = lrow[keep] * a0 + l1 * a1;
+        lfrow[keep] = lfrow[keep] * a0 + lf1 * a1;
+        m_run[keep] = m;
+      }
+    };
+    if (TG == 2) {
+      if (tg == 0) swap_halves(std::integral_constant<int, 0>());
+      else swap_halves(std::integral_constant<int, 1>());
+      nt_lo = tg;
+      stores = active;
+    } else if (TG > 2) {
       float* cb = reinterpret_cast<float*>(lds + stage * C::kStageB);
       constexpr int wave_bytes = NT * DT * 64 * 16;
       const int per_round = C::kStageB / wave_bytes;      // writers whose accumulators fit at once
@@ -776,16 +845,17 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         }
       }
     }
-    if (!(active && tg == 0)) return 0;
+    if (!stores) return 0;
     const int kseg = d.ord - first_ord;
     const int64_t slot = slot_of(pp, w, kseg);
     if (slot < 0) return 0;
     constexpr int RS = 16 * NT;
-    int stores = 0;
+    int nst = 0;
     // every lane of an N-tile that holds rows of the item stores (rows past the
     // item's end land in unused rows of the slot), so the count is wave-uniform
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      if (nt < nt_lo || (TG == 2 && nt > nt_lo)) continue;
       if (rg * RS + nt * 16 >= d.nrows) break;
       const int row = rg * RS + nt * 16 + ln;
       // the row's largest |o| (its 4 lanes hold 32 dims each) sets its fp16 scale
@@ -817,9 +887,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       }
       const f32x2 ld = {m_run[nt] * a.sm_scale + __logf(lfrow[nt]), dec};
       __builtin_nontemporal_store(ld, reinterpret_cast<f32x2*>(a.ws + part_l_off(pp, slot, row)));
-      stores += DT / 2 + 1;
+      nst += DT / 2 + 1;
     }
-    return stores;
+    return nst;
   };
 
   // ---- the slot loop -------------------------------------------------------------
