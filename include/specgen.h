@@ -40,7 +40,9 @@
  *    0x7F/0xFF NaN) with one fp32 scale per physical block and tensor: the
  *    value of a stored code c in block b is decode(c) * scale[b].  Scales are
  *    quantisation scales (e.g. the block's largest |value| / 448): finite and
- *    >= 0; a negative scale gives unspecified results.
+ *    >= 0 (0: every value of the block is 0, as for an all-zero block); a
+ *    negative scale gives unspecified results, and positive scales below
+ *    2^-96 lose accuracy.
  *
  * Ownership: the caller allocates every buffer and keeps it alive until the
  * work queued on `stream` has finished.  The library keeps no pointer after a

@@ -149,14 +149,12 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
 }
 
-// Four E4M3 codes -> four bf16 (exact: every E4M3 value, NaN included, has a
-// bf16 encoding; the hardware converts to fp32 and the upper halves are kept).
+// Four E4M3 codes -> four bf16, one gfx950 scaled conversion per pair with
+// scale 1: exact (every E4M3 value, NaN included, has a bf16 encoding).
 __device__ __forceinline__ u32x2 e4m3x4_to_bf16x4(uint32_t w) {
-  const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
-  const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(w, true);
   u32x2 r;
-  r[0] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
-  r[1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+  r[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, false));
+  r[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, true));
   return r;
 }
 
@@ -580,8 +578,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     // (all in block (sb + 8G) / 16 of the tile)
     // E4M3: the key scale multiplies a slab's scores only where the slab is
     // masked; elsewhere it rides in the exponent's scale factor, cl, and in the
-    // row maxima (scales are non-negative, so scaling commutes with max)
-    float vsc = 1.f, inv_vsc = 1.f, ksc = 1.f;
+    // row maxima (scales are non-negative, so scaling commutes with max).  The
+    // value scale rides in the exponent's offset (log2 vsc): the exponentials
+    // give P times the value scale, which the PV product takes as it is.
+    float inv_vsc = 1.f, lvs = 0.f, ksc = 1.f;
     if constexpr (FP8) {
       // the slab's two blocks (ids[idb + sb/16] and the next): lanes G < 2 hold
       // keys of the first
@@ -597,8 +597,18 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       auto sload = [](cfp p, int i) { return __int_as_float(uniform(__float_as_int(p[i]))); };
       const float k0 = sload(ks, id0), k1 = sload(ks, id1), v0 = sload(vs, id0), v1 = sload(vs, id1);
       ksc = G < 2 ? k0 : k1;
-      vsc = G < 2 ? v0 : v1;
+      // A block whose value scale is 0 holds zero values: its lanes zero their
+      // V operands and take scale 1 for P, so its keys still count in the sums.
+      if (v0 == 0.f || v1 == 0.f) {
+        const bool zv = (G < 2 ? v0 : v1) == 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          if (zv) vraw[dt] = u32x4{0u, 0u, 0u, 0u};
+      }
+      const float ve = G < 2 ? v0 : v1;
+      const float vsc = ve > 0.f ? ve : 1.f;
       inv_vsc = __builtin_amdgcn_rcpf(vsc);
+      lvs = __builtin_amdgcn_logf(vsc);
       if constexpr (kMask) {   // scaled before the -inf masking (a zero scale times -inf would be NaN)
 #pragma unroll
         for (int u = 0; u < 2; ++u)
@@ -649,7 +659,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     }
     // P = exp2(S - m) in bf16, then O^T += V^T P^T; the exponentials of N-tile 1
     // are interleaved with the PV MFMAs of N-tile 0
-    const float mc0 = m_run[0] * a.c_log2, mc1 = m_run[1] * a.c_log2;
+    const float mc0 = m_run[0] * a.c_log2 - lvs, mc1 = m_run[1] * a.c_log2 - lvs;
     const float cl = a.c_log2 * ksc;
     float p0[8], p1[8];
 #pragma unroll
@@ -657,11 +667,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       p0[e] = __builtin_amdgcn_exp2f(fmaf(s[0][0][e], cl, -mc0));
       p0[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][0][e], cl, -mc0));
     }
-    lf_run[0] += ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
-    if constexpr (FP8) {   // P carries the value scale into PV
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p0[e] *= vsc;
-    }
+    // the sums take P without the value scale
+    const float sp0 = ((p0[0] + p0[1]) + (p0[2] + p0[3])) + ((p0[4] + p0[5]) + (p0[6] + p0[7]));
+    if constexpr (FP8) lf_run[0] = fmaf(sp0, inv_vsc, lf_run[0]);
+    else lf_run[0] += sp0;
     u32x4 pk0;
     pk0[0] = pack_bf16x2(p0[0], p0[1]);
     pk0[1] = pack_bf16x2(p0[2], p0[3]);
@@ -679,11 +688,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int e = DT; e < 8; ++e)   // D = 64: fewer PV MFMAs than exponentials
       p1[e] = __builtin_amdgcn_exp2f(fmaf(s[e >> 2][1][e & 3], cl, -mc1));
-    lf_run[1] += ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
-    if constexpr (FP8) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p1[e] *= vsc;
-    }
+    const float sp1 = ((p1[0] + p1[1]) + (p1[2] + p1[3])) + ((p1[4] + p1[5]) + (p1[6] + p1[7]));
+    if constexpr (FP8) lf_run[1] = fmaf(sp1, inv_vsc, lf_run[1]);
+    else lf_run[1] += sp1;
     u32x4 pk1;
     pk1[0] = pack_bf16x2(p1[0], p1[1]);
     pk1[1] = pack_bf16x2(p1[2], p1[3]);

@@ -71,3 +71,28 @@ def test_peaked_mid_size_all_rows():
     b = synth.make_fork_batch(prefix_lens=[3000, 900], forks_per_trace=[5, 2], suffix_range=(0, 300), num_q_heads=32,
                               num_kv_heads=4, head_dim=128, kv_dtype="fp8_e4m3", seed=410)
     peaked_check(b, "auto", None, "fp8 scores peaked mid", flags=F8)
+
+
+@pytest.mark.parametrize("flags", [0, F8])
+@pytest.mark.parametrize("path", ["auto", "mfma", "dot"])
+def test_zero_scale_blocks(path, flags):
+    """Blocks whose K or V scale is 0 (all-zero blocks quantise to scale 0):
+    their values are 0 and their keys score 0, yet those keys still take part
+    in the softmax.  Some prefix and suffix blocks get a zero V scale, some a
+    zero K scale, one both; all rows against the oracle."""
+    if path == "dot" and flags:
+        pytest.skip("fp8 scores are an MFMA-kernel option")
+    b = synth.make_fork_batch(prefix_lens=[700], forks_per_trace=8, suffix_lens=[0, 5, 16, 40, 90, 1, 33, 64],
+                              num_q_heads=32, num_kv_heads=4, head_dim=128, kv_dtype="fp8_e4m3", seed=470)
+    pre = b.prefix_table[b.prefix_table_off[0]:b.prefix_table_off[0] + (700 + 15) // 16]
+    suf = np.concatenate([b.suffix_table[b.suffix_table_off[f]:b.suffix_table_off[f] + (int(b.suffix_len[f]) + 15) // 16]
+                          for f in range(b.num_forks)])
+    b.v_scale[pre[[0, 5, 6, 43]]] = 0.0
+    b.k_scale[pre[[2, 6, 20]]] = 0.0
+    b.v_scale[suf[[1, 4]]] = 0.0
+    b.k_scale[suf[[3]]] = 0.0
+    ref, ref_l = oracle.fork_decode_attn(b)
+    assert np.isfinite(ref).all() and np.isfinite(ref_l).all()
+    say(f"zero scales: path {path} flags {flags}")
+    o, l = run_attn(b, path, flags=flags)
+    check_attn(o, ref, l, ref_l, what=f"zero-scale blocks, {path}, flags {flags}")
