@@ -410,12 +410,12 @@ def main():
                                           " + merge (the whole prefill call: no separate phases)")
         roofline = {"kernel": kname, "bound": "mfma",
                     "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload),
+                    "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload + ("_fp8scores" if args.fp8_scores else "")),
                     "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2)}
     else:
         roofline = {"kernel": partial_kernel(D, False, False) + " (partials phase)", "bound": "hbm",
                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profile(args.workload),
+                    "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profile(args.workload + ("_fp8scores" if args.fp8_scores else "")),
                     "algorithmic_bytes_per_launch": int(kern_bytes)}
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
