@@ -14,17 +14,19 @@ namespace specgen {
 // Row merge for D in {64, 128} over partial rows stored as fp16 with a
 // per-row power-of-two scale (plan.h, part_row_k): lanes read 16 bytes (8
 // dims) each, so one load instruction covers PPI = 64 / (D/8) parts.  A batch
-// is up to 64 parts: each lane loads one part's (lse, dec) pair and the wave
-// issues the o loads of every part of the batch before it waits for any of
-// them, so a row of up to 64 parts costs one memory round trip.
-template <int D, typename PO, typename PL>
+// is U load instructions, PPI * U parts (at most 64): each lane loads one
+// part's (lse, dec) pair and the wave issues the o loads of every part of the
+// batch before it waits for any of them, so a row of up to PPI * U parts costs
+// one memory round trip.  The o registers of a batch set the kernel's register
+// count, and with it how many waves a compute unit holds, so the launch takes
+// the smallest U that covers the plan's rows.
+template <int D, int U, typename PO, typename PL>
 __device__ __forceinline__ void merge_row_v4(int nparts, PO part_o, PL part_ld, uint16_t* out_row,
                                              float* out_lse_p) {
   constexpr int LPP = D / 8;       // lanes per part
   constexpr int PPI = 64 / LPP;    // parts per load instruction
-  constexpr int U = 64 / PPI;      // load instructions per batch
   constexpr int kBatch = PPI * U;  // parts per batch: one (lse, dec) per lane
-  static_assert(kBatch == 64 && (LPP == 16 || LPP == 8), "one part per lane; lane groups of 16 or 8");
+  static_assert(kBatch <= 64 && (LPP == 16 || LPP == 8), "at most one part per lane; lane groups of 16 or 8");
   const int lane = threadIdx.x & 63;
   const int gsl = lane / LPP;      // part slot of this lane within an instruction
   const int c8 = (lane % LPP) * 8; // first of the 8 dims this lane owns
@@ -106,7 +108,7 @@ struct alignas(16) MergeItemLoc {
 
 // loc: kDepth + 1 entries of LDS private to the calling wavefront (unused
 // when kDepth == 1).
-template <int D, int kDepth>
+template <int D, int kDepth, int kU>
 __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __restrict__ ws, int64_t row,
                                                uint16_t* __restrict__ out, float* __restrict__ out_lse,
                                                MergeItemLoc* loc) {
@@ -213,7 +215,7 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
     const MergeLoc L = locate_part(p);
     return *reinterpret_cast<const f32x2*>(ws + L.l + L.slots * (int64_t)L.rows * 2);
   };
-  merge_row_v4<D>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
+  merge_row_v4<D, kU>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
 }  // namespace specgen

@@ -97,7 +97,7 @@ hipError_t launch_lse_merge(const float* o_parts, const float* lse_parts, int S,
 // ---- fork merge: the parts of row (f, h) are the partials of the workers that
 // covered its prefix items and its suffix item ---------------------------------
 
-template <int D, int kDepth>
+template <int D, int kDepth, int kU>
 __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, const float* __restrict__ ws, uint16_t* __restrict__ out,
                                                          float* __restrict__ out_lse) {
   __shared__ Plan splan;
@@ -107,7 +107,7 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
   // (4 * gridDim.x)-th row, so fewer workgroups copy the plan
   const int64_t rows = (int64_t)splan.N * splan.Hq;
   for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < rows; row += (int64_t)gridDim.x * 4)
-    fork_merge_row<D, kDepth>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
+    fork_merge_row<D, kDepth, kU>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
 }
 
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
@@ -117,10 +117,24 @@ hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float
   // the merge walks as many prefix items per row as the longest chain needs,
   // rounded up to 1, 2, 4 or kMaxDepth
   const int dep = plan.depth <= 1 ? 1 : plan.depth <= 2 ? 2 : plan.depth <= 4 ? 4 : kMaxDepth;
-  switch (dep * 1000 + plan.D) {
-#define SG_CASE(DEP, DD)                                                                                  \
-  case DEP * 1000 + DD:                                                                                   \
-    hipLaunchKernelGGL((fork_merge_kernel<DD, DEP>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse); \
+  // parts per batch: the fewest load instructions per batch (2, 8 or all 64
+  // parts) that cover every row of the plan in one batch.  A kernel holding 8
+  // parts per batch needs about 60 registers, one holding 64 about 150, and a
+  // compute unit holds correspondingly fewer waves of the larger one.
+  const int ppi = 64 / (plan.D / 8);   // parts per load instruction
+  const int mp = max_parts_per_row(plan);
+  const int tier = mp <= 2 * ppi ? 1 : mp <= 8 * ppi ? 2 : 0;
+  switch (dep * 1000 + plan.D + tier) {
+#define SG_CASE(DEP, DD)                                                                                          \
+  case DEP * 1000 + DD:                                                                                           \
+    hipLaunchKernelGGL((fork_merge_kernel<DD, DEP, 64 / (64 / (DD / 8))>), grid, block, 0, stream, plan, ws,     \
+                       (uint16_t*)out, out_lse);                                                                  \
+    break;                                                                                                        \
+  case DEP * 1000 + DD + 1:                                                                                       \
+    hipLaunchKernelGGL((fork_merge_kernel<DD, DEP, 2>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse); \
+    break;                                                                                                        \
+  case DEP * 1000 + DD + 2:                                                                                       \
+    hipLaunchKernelGGL((fork_merge_kernel<DD, DEP, 8>), grid, block, 0, stream, plan, ws, (uint16_t*)out, out_lse); \
     break;
     SG_CASE(1, 128) SG_CASE(2, 128) SG_CASE(4, 128) SG_CASE(kMaxDepth, 128)
     SG_CASE(1, 64) SG_CASE(2, 64) SG_CASE(4, 64) SG_CASE(kMaxDepth, 64)

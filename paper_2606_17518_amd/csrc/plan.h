@@ -476,6 +476,30 @@ SG_HD bool suffix_item_of_row(const Plan& p, int f, int h, int* part, int* ord, 
   return true;
 }
 
+// The most partial results any output row merges (host): over the chain of
+// prefix items a row can see (at most `depth`) and its suffix item, the
+// workers each item's tiles span.
+inline int max_parts_per_row(const Plan& p) {
+  int mp = 0, ms = 0;
+  for (int t = 0; t < p.T; ++t) {
+    const PartPlan& pp = p.part[p.trace_part[t]];
+    const int rows = trace_rows(p, t);
+    for (int j = 0; j < p.Hkv; ++j)
+      for (int r0 = 0; r0 < rows; r0 += pp.rbs) {   // one row of each row block
+        const ItemParts P = prefix_parts_of_row(p, p.fork_off[t] + r0 / p.g, j * p.g + r0 % p.g, t);
+        mp = mp > P.w_hi - P.w_lo + 1 ? mp : P.w_hi - P.w_lo + 1;
+      }
+  }
+  const PartPlan& ps = p.part[part_of_suffix(p.policy)];
+  for (int f = 0; f < p.N; ++f)
+    for (int j = 0; j < p.Hkv; ++j)
+      for (int hh = 0; hh < p.g; hh += ps.rbs) {
+        ItemParts S;
+        if (suffix_parts_of_row(p, f, j * p.g + hh, &S)) ms = ms > S.w_hi - S.w_lo + 1 ? ms : S.w_hi - S.w_lo + 1;
+      }
+  return p.depth * mp + ms;
+}
+
 // Storage of one partial row.  The normalised partial output o (a convex
 // combination of value rows) is kept as fp16 times a power of two chosen per
 // row: with mx = max_d |o_d| and e its biased fp32 exponent, k = clamp(e - 14,

@@ -227,6 +227,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     }
     return true;
   };
+  const int parts_bound = max_parts_per_row(plan);   // what the merge launch sizes its batch for
   for (int f = 0; f < in.N; ++f) {
     int t = 0;
     while (in.fork_off[t + 1] <= f) ++t;
@@ -237,6 +238,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     for (int h = 0; h < in.Hq; ++h) {
       const int j = h / g, hh = h % g;
       int ff, hh2;
+      int row_parts = 0;   // partials this row merges
       for (const int c : chain) {
         CHECK(plan.fork_off[c] <= f && f < plan.fork_end[c], "fork %d outside the rows of trace %d", f, c);
         const int ri = (f - in.fork_off[c]) * g + hh;
@@ -261,6 +263,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
           CHECK(op < plan.part[X].n_items, "prefix ordinal past the item table");
         }
         if (!same(P, ord)) return false;
+        row_parts += P.w_hi - P.w_lo + 1;
         item_row_fork_head(plan, 0, c, -1, j, (ri / rbs) * rbs, P.row, &ff, &hh2);
         CHECK(ff == f && hh2 == h, "prefix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
       }
@@ -285,7 +288,10 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
         CHECK(plan.part[Xs].info_base + 3 * (int64_t)plan.part[Xs].n_items <= wsf, "item table past workspace");
         item_row_fork_head(plan, 1, t, f, j, (hh / rbss) * rbss, S.row, &ff, &hh2);
         CHECK(ff == f && hh2 == h, "suffix row maps to (%d,%d) not (%d,%d)", ff, hh2, f, h);
+        row_parts += S.w_hi - S.w_lo + 1;
       }
+      CHECK(row_parts <= parts_bound, "row (%d,%d) merges %d parts, above the plan's bound %d", f, h, row_parts,
+            parts_bound);
     }
   }
   return true;
