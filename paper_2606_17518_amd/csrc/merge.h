@@ -218,4 +218,133 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
   merge_row_v4<D, kU>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
+// Rows of few parts (the plan bounds every row by kParts): one row per group
+// of D/8 lanes -- four rows per wave at D = 128, eight at D = 64 -- each lane
+// holding 8 dims of its row.  A row's item table entries take one memory round
+// trip and all its parts one more, and a wave carries four or eight rows
+// through them at once, where the one-row-per-wave merge leaves most lanes
+// idle on rows of a handful of parts.  kDepth <= 2 (the per-lane item
+// selection below is a pair of comparisons).
+template <int D, int kDepth, int kParts>
+__device__ __forceinline__ void fork_merge_rows_grouped(const Plan& plan, const float* __restrict__ ws, int64_t row,
+                                                        uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+  static_assert(kDepth <= 2, "per-lane item selection covers a prefix chain of at most two traces");
+  constexpr int LPP = D / 8;           // lanes per row
+  constexpr int kItems = kDepth + 1;   // prefix items nearest trace first, then the suffix item
+  const int lane = threadIdx.x & 63;
+  const int c8 = (lane % LPP) * 8;     // first of the 8 dims this lane owns
+  const bool live = row < (int64_t)plan.N * plan.Hq;
+  const int64_t rw = live ? row : 0;   // the spare groups of a last wave read row 0 and store nothing
+  const int f = (int)(rw / plan.Hq);
+  const int h = (int)(rw % plan.Hq);
+  int Xs[kItems], ords[kItems], rs[kItems];
+  bool has[kItems];
+  int t = trace_of_fork(plan, f);
+#pragma unroll
+  for (int i = 0; i < kDepth; ++i) {
+    Xs[i] = ords[i] = rs[i] = 0;
+    has[i] = t >= 0;
+    if (has[i]) {
+      prefix_item_of_row(plan, f, h, t, &Xs[i], &ords[i], &rs[i]);
+      t = plan.parent[t];
+    }
+  }
+  Xs[kDepth] = ords[kDepth] = rs[kDepth] = 0;
+  has[kDepth] = suffix_item_of_row(plan, f, h, &Xs[kDepth], &ords[kDepth], &rs[kDepth]);
+  int32_t e[kItems][3];
+#pragma unroll
+  for (int s2 = 0; s2 < kItems; ++s2) {
+    const int32_t* info = reinterpret_cast<const int32_t*>(ws + plan.part[Xs[s2]].info_base) + 3 * (int64_t)ords[s2];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) e[s2][c] = has[s2] ? info[c] : 0;
+  }
+  int64_t o0[kItems], l0[kItems];
+  int kmax[kItems], klo[kItems], first[kItems + 1], srows[kItems];
+  bool ok = true;
+  first[0] = 0;
+#pragma unroll
+  for (int s2 = 0; s2 < kItems; ++s2) {
+    o0[s2] = l0[s2] = 0;
+    kmax[s2] = srows[s2] = 1;
+    klo[s2] = 0;
+    int n = 0;
+    if (has[s2]) {
+      const PartPlan& pp = plan.part[Xs[s2]];
+      const int w_lo = e[s2][0], w_hi = e[s2][1], k_lo = e[s2][2];
+      if (ords[s2] < 0 || ords[s2] >= pp.n_items || w_lo < 0 || w_hi < w_lo || w_hi >= pp.workers || k_lo < 0 ||
+          k_lo >= pp.kmax) {
+        ok = false;
+      } else {
+        const int64_t slot0 = (int64_t)w_lo * pp.kmax + k_lo;
+        o0[s2] = part_o_off(pp, slot0, rs[s2], D);
+        l0[s2] = part_l_off(pp, slot0, rs[s2]);
+        kmax[s2] = pp.kmax;
+        klo[s2] = k_lo;
+        n = w_hi - w_lo + 1;
+        srows[s2] = pp.slot_rows;
+      }
+    }
+    first[s2 + 1] = first[s2] + n;
+  }
+  const int np = first[kItems];
+  if (!ok || np > kParts) {   // an inconsistent item table, or more parts than the launch sized for: fail loudly
+    if (live) {
+      *reinterpret_cast<u32x4*>(out + row * D + c8) = u32x4{0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
+      if (out_lse && lane % LPP == 0) out_lse[row] = __builtin_nanf("");
+    }
+    return;
+  }
+  // every part's (lse, dec) and this lane's 8 dims of its o, all loaded before any is used
+  f32x2 ld[kParts];
+  u32x4 v[kParts];
+#pragma unroll
+  for (int p = 0; p < kParts; ++p) {
+    ld[p] = f32x2{-INFINITY, 0.f};
+    v[p] = u32x4{0u, 0u, 0u, 0u};
+    if (p < np) {
+      const int s2 = kItems == 2 ? (p >= first[1] ? 1 : 0) : (p >= first[2] ? 2 : (p >= first[1] ? 1 : 0));
+      const int i = p - (s2 == 0 ? 0 : s2 == 1 ? first[1] : first[kItems - 1]);
+      const int K = s2 == 0 ? kmax[0] : s2 == 1 ? kmax[1] : kmax[kItems - 1];
+      const int KL = s2 == 0 ? klo[0] : s2 == 1 ? klo[1] : klo[kItems - 1];
+      const int R = s2 == 0 ? srows[0] : s2 == 1 ? srows[1] : srows[kItems - 1];
+      const int64_t O = s2 == 0 ? o0[0] : s2 == 1 ? o0[1] : o0[kItems - 1];
+      const int64_t L = s2 == 0 ? l0[0] : s2 == 1 ? l0[1] : l0[kItems - 1];
+      const int64_t slots = i == 0 ? 0 : (int64_t)i * K - KL;
+      ld[p] = *reinterpret_cast<const f32x2*>(ws + L + slots * R * 2);
+      v[p] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint32_t*>(ws + O + slots * (int64_t)R * (D / 2)) +
+                                             c8 / 2);
+    }
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < kParts; ++p) M = fmaxf(M, ld[p][0]);
+  float z = 0.f, acc[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int p = 0; p < kParts; ++p) {
+      const float w = ld[p][0] == -INFINITY ? 0.f : __expf(ld[p][0] - M);
+      z += w;
+      const float wo = w * ld[p][1];   // the weight of the stored (scaled) values
+      if (wo != 0.f) {                 // an empty part's o may be garbage
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x2 x = unpack_f16x2(v[p][q]);
+          acc[2 * q] = fmaf(wo, x[0], acc[2 * q]);
+          acc[2 * q + 1] = fmaf(wo, x[1], acc[2 * q + 1]);
+        }
+      }
+    }
+  }
+  if (!live) return;
+  const bool empty = M == -INFINITY;
+  const float inv = empty ? 0.f : 1.f / z;
+  u32x4 pk;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) pk[q] = pack_bf16x2(acc[2 * q] * inv, acc[2 * q + 1] * inv);
+  *reinterpret_cast<u32x4*>(out + row * D + c8) = pk;
+  if (out_lse && lane % LPP == 0) out_lse[row] = empty ? -INFINITY : M + __logf(z);
+}
+
 }  // namespace specgen

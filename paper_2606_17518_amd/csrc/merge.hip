@@ -110,6 +110,20 @@ __global__ void __launch_bounds__(256) fork_merge_kernel(const Plan plan_arg, co
     fork_merge_row<D, kDepth, kU>(splan, ws, row, out, out_lse, sloc[threadIdx.x >> 6]);
 }
 
+// Rows of at most kParts parts each, several rows per wave (merge.h).
+template <int D, int kDepth, int kParts>
+__global__ void __launch_bounds__(256) fork_merge_grouped_kernel(const Plan plan_arg, const float* __restrict__ ws,
+                                                                 uint16_t* __restrict__ out, float* __restrict__ out_lse) {
+  __shared__ Plan splan;
+  plan_to_lds<256>(plan_arg, splan);
+  constexpr int kRowsPerWave = 64 / (D / 8);
+  const int64_t rows = (int64_t)splan.N * splan.Hq;
+  const int grp = (threadIdx.x & 63) / (D / 8);
+  for (int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kRowsPerWave; r0 < rows;
+       r0 += (int64_t)gridDim.x * 4 * kRowsPerWave)
+    fork_merge_rows_grouped<D, kDepth, kParts>(splan, ws, r0 + grp, out, out_lse);
+}
+
 hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float* out_lse, hipStream_t stream) {
   const int64_t rows = (int64_t)plan.N * plan.Hq;
   constexpr int64_t kMaxMergeBlocks = 2048;   // 8 per CU; beyond that waves loop over rows
@@ -123,6 +137,19 @@ hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float
   // compute unit holds correspondingly fewer waves of the larger one.
   const int ppi = 64 / (plan.D / 8);   // parts per load instruction
   const int mp = max_parts_per_row(plan);
+  constexpr int kGroupedParts = 8;
+  if (dep <= 2 && mp <= kGroupedParts) {   // rows of a handful of parts: several rows per wave
+    const int64_t per_block = 4 * (64 / (plan.D / 8));
+    const dim3 g2((unsigned)std::min<int64_t>((rows + per_block - 1) / per_block, kMaxMergeBlocks));
+    if (plan.D == 128) {
+      if (dep == 1) hipLaunchKernelGGL((fork_merge_grouped_kernel<128, 1, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+      else hipLaunchKernelGGL((fork_merge_grouped_kernel<128, 2, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    } else {
+      if (dep == 1) hipLaunchKernelGGL((fork_merge_grouped_kernel<64, 1, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+      else hipLaunchKernelGGL((fork_merge_grouped_kernel<64, 2, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    }
+    return hipGetLastError();
+  }
   const int tier = mp <= 2 * ppi ? 1 : mp <= 8 * ppi ? 2 : 0;
   switch (dep * 1000 + plan.D + tier) {
 #define SG_CASE(DEP, DD)                                                                                          \
