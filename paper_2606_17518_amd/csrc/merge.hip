@@ -137,16 +137,20 @@ hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float
   // compute unit holds correspondingly fewer waves of the larger one.
   const int ppi = 64 / (plan.D / 8);   // parts per load instruction
   const int mp = max_parts_per_row(plan);
-  constexpr int kGroupedParts = 8;
-  if (dep <= 2 && mp <= kGroupedParts) {   // rows of a handful of parts: several rows per wave
+  if (dep <= 2 && mp <= 16) {   // rows of a handful of parts: several rows per wave
     const int64_t per_block = 4 * (64 / (plan.D / 8));
     const dim3 g2((unsigned)std::min<int64_t>((rows + per_block - 1) / per_block, kMaxMergeBlocks));
-    if (plan.D == 128) {
-      if (dep == 1) hipLaunchKernelGGL((fork_merge_grouped_kernel<128, 1, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-      else hipLaunchKernelGGL((fork_merge_grouped_kernel<128, 2, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-    } else {
-      if (dep == 1) hipLaunchKernelGGL((fork_merge_grouped_kernel<64, 1, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
-      else hipLaunchKernelGGL((fork_merge_grouped_kernel<64, 2, kGroupedParts>), g2, block, 0, stream, plan, ws, (uint16_t*)out, out_lse);
+    const int key = (plan.D == 128 ? 100 : 0) + dep * 10 + (mp <= 8 ? 8 : 16);
+    switch (key) {
+#define SG_GROUPED(DD, DEP, NP)                                                                          \
+  case (DD == 128 ? 100 : 0) + DEP * 10 + NP:                                                              \
+    hipLaunchKernelGGL((fork_merge_grouped_kernel<DD, DEP, NP>), g2, block, 0, stream, plan, ws,          \
+                       (uint16_t*)out, out_lse);                                                         \
+    break;
+      SG_GROUPED(128, 1, 8) SG_GROUPED(128, 2, 8) SG_GROUPED(128, 1, 16) SG_GROUPED(128, 2, 16)
+      SG_GROUPED(64, 1, 8) SG_GROUPED(64, 2, 8) SG_GROUPED(64, 1, 16) SG_GROUPED(64, 2, 16)
+#undef SG_GROUPED
+      default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
   }
