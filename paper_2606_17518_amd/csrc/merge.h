@@ -218,12 +218,12 @@ __device__ __forceinline__ void fork_merge_row(const Plan& plan, const float* __
   merge_row_v4<D, kU>(first[kItems], po, pl, out + row * D, out_lse ? out_lse + row : nullptr);
 }
 
-// Rows of few parts (the plan bounds every row by kParts): one row per group
-// of D/8 lanes -- four rows per wave at D = 128, eight at D = 64 -- each lane
-// holding 8 dims of its row.  A row's item table entries take one memory round
-// trip and all its parts one more, and a wave carries four or eight rows
-// through them at once, where the one-row-per-wave merge leaves most lanes
-// idle on rows of a handful of parts.  kDepth <= 2 (the per-lane item
+// Several rows per wave: one row per group of D/8 lanes -- four rows per wave
+// at D = 128, eight at D = 64 -- each lane holding 8 dims of its row.  A row's
+// item table entries take one memory round trip and its parts one more per
+// batch of kParts, and a wave carries four or eight rows through them at once,
+// where the one-row-per-wave merge leaves most lanes idle on rows of a handful
+// of parts and holds fewer rows in flight.  kDepth <= 2 (the per-lane item
 // selection below is a pair of comparisons).
 template <int D, int kDepth, int kParts>
 __device__ __forceinline__ void fork_merge_rows_grouped(const Plan& plan, const float* __restrict__ ws, int64_t row,
@@ -287,50 +287,58 @@ __device__ __forceinline__ void fork_merge_rows_grouped(const Plan& plan, const 
     first[s2 + 1] = first[s2] + n;
   }
   const int np = first[kItems];
-  if (!ok || np > kParts) {   // an inconsistent item table, or more parts than the launch sized for: fail loudly
+  if (!ok) {   // the item table is inconsistent: fail loudly rather than read out of range
     if (live) {
       *reinterpret_cast<u32x4*>(out + row * D + c8) = u32x4{0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
       if (out_lse && lane % LPP == 0) out_lse[row] = __builtin_nanf("");
     }
     return;
   }
-  // every part's (lse, dec) and this lane's 8 dims of its o, all loaded before any is used
-  f32x2 ld[kParts];
-  u32x4 v[kParts];
-#pragma unroll
-  for (int p = 0; p < kParts; ++p) {
-    ld[p] = f32x2{-INFINITY, 0.f};
-    v[p] = u32x4{0u, 0u, 0u, 0u};
-    if (p < np) {
-      const int s2 = kItems == 2 ? (p >= first[1] ? 1 : 0) : (p >= first[2] ? 2 : (p >= first[1] ? 1 : 0));
-      const int i = p - (s2 == 0 ? 0 : s2 == 1 ? first[1] : first[kItems - 1]);
-      const int K = s2 == 0 ? kmax[0] : s2 == 1 ? kmax[1] : kmax[kItems - 1];
-      const int KL = s2 == 0 ? klo[0] : s2 == 1 ? klo[1] : klo[kItems - 1];
-      const int R = s2 == 0 ? srows[0] : s2 == 1 ? srows[1] : srows[kItems - 1];
-      const int64_t O = s2 == 0 ? o0[0] : s2 == 1 ? o0[1] : o0[kItems - 1];
-      const int64_t L = s2 == 0 ? l0[0] : s2 == 1 ? l0[1] : l0[kItems - 1];
-      const int64_t slots = i == 0 ? 0 : (int64_t)i * K - KL;
-      ld[p] = *reinterpret_cast<const f32x2*>(ws + L + slots * R * 2);
-      v[p] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint32_t*>(ws + O + slots * (int64_t)R * (D / 2)) +
-                                             c8 / 2);
-    }
-  }
-  float M = -INFINITY;
-#pragma unroll
-  for (int p = 0; p < kParts; ++p) M = fmaxf(M, ld[p][0]);
-  float z = 0.f, acc[8];
+  float M = -INFINITY, z = 0.f, acc[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) acc[q] = 0.f;
-  if (M != -INFINITY) {
+  // batches of kParts parts: every part's (lse, dec) and this lane's 8 dims of
+  // its o loaded before any is used; running max and sums carried across batches
+  for (int p0 = 0; p0 < np; p0 += kParts) {
+    f32x2 ld[kParts];
+    u32x4 v[kParts];
 #pragma unroll
-    for (int p = 0; p < kParts; ++p) {
-      const float w = ld[p][0] == -INFINITY ? 0.f : __expf(ld[p][0] - M);
+    for (int pi = 0; pi < kParts; ++pi) {
+      const int p = p0 + pi;
+      ld[pi] = f32x2{-INFINITY, 0.f};
+      v[pi] = u32x4{0u, 0u, 0u, 0u};
+      if (p < np) {
+        const int s2 = kItems == 2 ? (p >= first[1] ? 1 : 0) : (p >= first[2] ? 2 : (p >= first[1] ? 1 : 0));
+        const int i = p - (s2 == 0 ? 0 : s2 == 1 ? first[1] : first[kItems - 1]);
+        const int K = s2 == 0 ? kmax[0] : s2 == 1 ? kmax[1] : kmax[kItems - 1];
+        const int KL = s2 == 0 ? klo[0] : s2 == 1 ? klo[1] : klo[kItems - 1];
+        const int R = s2 == 0 ? srows[0] : s2 == 1 ? srows[1] : srows[kItems - 1];
+        const int64_t O = s2 == 0 ? o0[0] : s2 == 1 ? o0[1] : o0[kItems - 1];
+        const int64_t L = s2 == 0 ? l0[0] : s2 == 1 ? l0[1] : l0[kItems - 1];
+        const int64_t slots = i == 0 ? 0 : (int64_t)i * K - KL;
+        ld[pi] = *reinterpret_cast<const f32x2*>(ws + L + slots * R * 2);
+        v[pi] = *reinterpret_cast<const u32x4*>(
+            reinterpret_cast<const uint32_t*>(ws + O + slots * (int64_t)R * (D / 2)) + c8 / 2);
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int pi = 0; pi < kParts; ++pi) Mn = fmaxf(Mn, ld[pi][0]);
+    if (Mn == -INFINITY) continue;   // every part so far empty
+    const float rescale = __expf(M - Mn);   // M = -inf -> 0
+    z *= rescale;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] *= rescale;
+    M = Mn;
+#pragma unroll
+    for (int pi = 0; pi < kParts; ++pi) {
+      const float w = ld[pi][0] == -INFINITY ? 0.f : __expf(ld[pi][0] - M);
       z += w;
-      const float wo = w * ld[p][1];   // the weight of the stored (scaled) values
-      if (wo != 0.f) {                 // an empty part's o may be garbage
+      const float wo = w * ld[pi][1];   // the weight of the stored (scaled) values
+      if (wo != 0.f) {                  // an empty part's o may be garbage
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const f32x2 x = unpack_f16x2(v[p][q]);
+          const f32x2 x = unpack_f16x2(v[pi][q]);
           acc[2 * q] = fmaf(wo, x[0], acc[2 * q]);
           acc[2 * q + 1] = fmaf(wo, x[1], acc[2 * q + 1]);
         }

@@ -137,7 +137,10 @@ hipError_t launch_fork_merge(const Plan& plan, const float* ws, void* out, float
   // compute unit holds correspondingly fewer waves of the larger one.
   const int ppi = 64 / (plan.D / 8);   // parts per load instruction
   const int mp = max_parts_per_row(plan);
-  if (dep <= 2 && mp <= 16) {   // rows of a handful of parts: several rows per wave
+  // Several rows per wave where every row has at most 16 parts (one batch), or
+  // where there are so many rows that holding more of them in flight beats one
+  // batch per row (a wave of the one-row layout holds one row, 3-7 waves per SIMD).
+  if (dep <= 2 && (mp <= 16 || rows >= 8192)) {
     const int64_t per_block = 4 * (64 / (plan.D / 8));
     const dim3 g2((unsigned)std::min<int64_t>((rows + per_block - 1) / per_block, kMaxMergeBlocks));
     const int key = (plan.D == 128 ? 100 : 0) + dep * 10 + (mp <= 8 ? 8 : 16);
