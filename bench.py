@@ -181,7 +181,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: the fork-decode path has no multi-GPU part in this build "
+        print("bench.py measures one GPU: the fork-decode path here has no multi-GPU part "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 

@@ -72,7 +72,7 @@ extern "C" {
 typedef enum {
   SPECGEN_OK = 0,
   SPECGEN_ERR_INVALID_ARG = 1, /* a null pointer, size or shape out of range */
-  SPECGEN_ERR_UNSUPPORTED = 2, /* a valid request this build does not serve */
+  SPECGEN_ERR_UNSUPPORTED = 2, /* a valid request the library does not serve */
   SPECGEN_ERR_WORKSPACE = 3,   /* workspace missing or too small            */
   SPECGEN_ERR_DEVICE = 4       /* a HIP call or kernel launch failed        */
 } specgen_status_t;

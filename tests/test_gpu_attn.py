@@ -75,7 +75,7 @@ def test_trace_8k_all_rows():
 def test_full_size_workloads(name, nrows):
     """Full-size decode workloads: every row of the 32k-prefix workload, sampled
     rows of the others (the oracle computes each by definition over all its
-    keys); the benchmark spec's tolerances, and beside them the lse bound that
+    keys); the attention tolerances, and beside them the lse bound that
     resolves a single 16-token block."""
     say(f"{name}: generating")
     b = synth.workload(name)

@@ -11,7 +11,7 @@ differ by many nats, and the per-row fp16 scaling of partial outputs.
 
 Shapes: the 32k-prefix workload (all rows) and the 128k-prefix workload (256
 sampled rows), each with bf16 and with E4M3 KV, on both kernels; plus mid-size
-batches on every path, all rows.  Tolerances: the spec ones (max abs
+batches on every path, all rows.  Tolerances: the attention ones (max abs
 1e-2, mean abs 1e-3) on the error beyond the bf16 output's own rounding (a
 dominated row's output is about one value row, with elements up to ~4, where
 bf16 itself rounds by up to 1.6e-2; gpu_helpers.check_attn_excess), and

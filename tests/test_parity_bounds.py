@@ -1,7 +1,7 @@
 """The full-size lse bound can see a lost KV block (CPU only, oracle only).
 
 The GPU parity tests bound |d lse| by 1e-4 on the full-size decode workloads,
-beside the spec output tolerances.  Here the oracle shows why both are
+beside the output tolerances.  Here the oracle shows why both are
 needed: on rows shaped like the 32k-prefix workload (one kv head of it: a
 32768-token prefix, 16 forks with 128-1024 suffix tokens, GQA group of 8,
 D = 128, keys N(0, 1) plus a per-head bias of std 0.5), removing a single
