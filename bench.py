@@ -127,10 +127,15 @@ def cpu_baseline(batch, target_s: float, q_len=None, step_bytes=None):
                       f"workload, fp64 C oracle, {dt:.1f} s; GB/s = step algorithmic bytes / mean step time"}
 
 
-def stream_ceilings(dev, stream, reps: int = 10):
+def stream_ceilings(dev, stream, reps: int = 10, batch=None, fb=None):
     """Streaming read (1 GiB) and copy (512 MiB -> 512 MiB) rates of the plain
-    probe kernels (libspecgen_probe.so): medians over `reps` launches, each
-    timed with HIP events on the launch stream."""
+    probe kernels (libspecgen_probe.so), and the rate of the bf16 partial
+    kernel's own access pattern with no arithmetic (the slice-ring probe: 4 KiB
+    kv-head slices of random pool blocks through the same eight-wave LDS-DMA
+    ring, 1 GiB; and, for a bf16 head_dim-128 workload, the workload's own
+    first prefix on 256 workgroups as the partial kernel launches them):
+    medians over `reps` launches, each timed with HIP events on the launch
+    stream."""
     import ctypes as C
     import torch
     from paper_2606_17518_amd.build import PROBE_LIB_PATH
@@ -155,11 +160,45 @@ def stream_ceilings(dev, stream, reps: int = 10):
         return float(np.median(ms))
     read_ms = timed(lambda: lib.specgen_probe_stream_read(src.data_ptr(), nbytes, sink.data_ptr(), sp))
     copy_ms = timed(lambda: lib.specgen_probe_stream_copy(half.data_ptr(), src.data_ptr(), nbytes // 2, sp))
+    out = {"read_gbps": round(nbytes / (read_ms / 1e3) / 1e9, 1),
+           "copy_gbps": round(nbytes / (copy_ms / 1e3) / 1e9, 1)}
+    # slice ring over the 1 GiB buffer as two 512 MiB pools of 16384 blocks x 8 kv heads
+    ring = lib.specgen_probe_slice_ring
+    ring.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int, C.c_void_p, C.c_int, C.c_int, C.c_void_p,
+                     C.c_void_p]
+    hkv, nblk = 8, (nbytes // 2) // (8 * 4096)
+    tph = nblk // 4
+    perm = torch.from_numpy(np.random.default_rng(7).permutation(nblk).astype(np.int32)).to(dev)
+    kp, vp = src.data_ptr(), src.data_ptr() + nbytes // 2
+    ring_ms = timed(lambda: ring(kp, vp, nblk, hkv, perm.data_ptr(), tph, 256, sink.data_ptr(), sp))
+    out["slice_ring_gbps"] = round(hkv * tph * 32768 / (ring_ms / 1e3) / 1e9, 1)
+    note = ("plain nontemporal 16-byte streams over every CU: 1 GiB read; 512 MiB copied (1 GiB of traffic); "
+            "slice ring: the bf16 partial kernel's tiles (4 KiB K and V slices of one kv head from each of four "
+            "random 16-token blocks per 32 KiB tile, eight waves, four LDS stages, LDS-DMA) with no arithmetic, "
+            "8 kv heads x 4096 tiles = 1 GiB on 256 workgroups")
+    if batch is not None and fb and batch.kv_dtype == "bf16" and batch.head_dim == 128:
+        P0 = int(batch.prefix_len[0])
+        tiles = -(-P0 // 64)
+        o = int(batch.prefix_table_off[0])
+        ids = np.asarray(batch.prefix_table[o:o + -(-P0 // 16)], np.int32)
+        tab = np.concatenate([ids, np.full(4 * tiles - ids.size, ids[-1], np.int32)])
+        tab_d = torch.from_numpy(tab).to(dev)
+        turn = [0]
+
+        def prefix_ring():   # the replicas in rotation, as the timed steps read them
+            r = fb[turn[0] % len(fb)]
+            turn[0] += 1
+            return ring(r.k_pool.data_ptr(), r.v_pool.data_ptr(), batch.num_blocks, batch.num_kv_heads,
+                        tab_d.data_ptr(), tiles, 256, sink.data_ptr(), sp)
+        pms = timed(prefix_ring)
+        out["slice_ring_prefix_gbps"] = round(batch.num_kv_heads * tiles * 32768 / (pms / 1e3) / 1e9, 1)
+        out["slice_ring_prefix_us"] = round(pms * 1e3, 2)
+        note += (f"; slice_ring_prefix: the same ring over trace 0's {P0}-token prefix in this workload's pools "
+                 f"({batch.num_kv_heads} kv heads x {tiles} tiles; the replicas in rotation), launch and ramp "
+                 f"included")
+    out["note"] = note + "; median of 10 launches between HIP events"
     del src, half
-    return {"read_gbps": round(nbytes / (read_ms / 1e3) / 1e9, 1),
-            "copy_gbps": round(nbytes / (copy_ms / 1e3) / 1e9, 1),
-            "note": "plain nontemporal 16-byte streams over every CU: 1 GiB read; 512 MiB copied (1 GiB of "
-                    "traffic); median of 10 launches between HIP events"}
+    return out
 
 
 def pct(a, q):
@@ -443,8 +482,11 @@ def main():
                          "gbps": round(import_bytes / (float(imp_ms.mean()) / 1e3) / 1e9, 2)}
     res.update(moves)
     log("streaming ceilings")
-    res["stream_ceiling"] = stream_ceilings(dev, stream)
+    res["stream_ceiling"] = stream_ceilings(dev, stream, batch=b, fb=reps)
     res["stream_ceiling"]["attn_frac_of_read"] = round(value / res["stream_ceiling"]["read_gbps"], 4)
+    if roofline["bound"] == "hbm":
+        res["stream_ceiling"]["partials_frac_of_slice_ring"] = round(
+            achieved / res["stream_ceiling"]["slice_ring_gbps"], 4)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, q_len, attn_bytes)

@@ -317,7 +317,7 @@ def test_probe_library_exports_its_header():
     src = open(os.path.join(ROOT, "include", "specgen_probe.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     names = sorted(set(re.findall(r"\b(specgen_probe_\w+)\s*\(", src)))
-    assert names == ["specgen_probe_stream_copy", "specgen_probe_stream_read"]
+    assert names == ["specgen_probe_slice_ring", "specgen_probe_stream_copy", "specgen_probe_stream_read"]
     lib = ctypes.CDLL(PROBE_LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -325,6 +325,16 @@ def test_probe_library_exports_its_header():
     lib.specgen_probe_stream_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     assert lib.specgen_probe_stream_read(0x10000, 24, 0x20000, None) == 1      # not a multiple of 16
     assert lib.specgen_probe_stream_copy(0x10000, None, 64, None) == 1
+    ring = lib.specgen_probe_slice_ring
+    ring.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                     ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    ok = (0x10000, 0x20000, 64, 8, 0x30000, 16, 4, 0x40000, None)
+    for i, bad in [(0, None), (1, 0x20008), (2, 0), (3, 0), (4, None), (5, 0), (6, 0), (7, None)]:
+        args = list(ok)
+        args[i] = bad
+        assert ring(*args) == 1, (i, bad)
+    # a share of more than 1024 tiles per workgroup: 8 heads x 2048 tiles on 8 workgroups
+    assert ring(0x10000, 0x20000, 64, 8, 0x30000, 2048, 8, 0x40000, None) == 1
 
 
 def test_noalloc_scratch_size_and_rejection(L):
