@@ -201,6 +201,79 @@ def stream_ceilings(dev, stream, reps: int = 10, batch=None, fb=None):
     return out
 
 
+def timeline_report(args, b, step, q_len):
+    """Per-workgroup timeline of the partial kernel (libspecgen_timeline.so):
+    `warmup` steps, then `steps` steps each read back on its own (stamps
+    cleared before it; the attention call queued behind the step's import as
+    in the timed run).  Prints medians over the steps of per-step percentiles
+    over the workgroups, in microseconds from the first workgroup's start."""
+    import ctypes as C
+    import torch
+    from paper_2606_17518_amd import binding
+    T = binding.timeline_lib()
+    W, S = C.c_int(0), C.c_int(0)
+    assert T.specgen_timeline_shape(C.byref(W), C.byref(S)) == 0
+    W, S = W.value, S.value
+    stamps = np.zeros((W, S), np.uint64)
+    kinds = np.zeros((W, S), np.int32)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for k in range(args.warmup):
+        step(k, evs, q_len is None)
+    torch.cuda.synchronize()
+    rows = []
+    for k in range(args.steps):
+        assert T.specgen_timeline_clear() == 0
+        step(args.warmup + k, evs, q_len is None)
+        torch.cuda.synchronize()
+        assert T.specgen_timeline_read(stamps.ctypes.data, kinds.ctypes.data) == 0
+        live = np.nonzero(stamps[:, 0])[0]
+        if live.size == 0:
+            print("no workgroup of the MFMA partial kernel ran (the dot path is not stamped)")
+            return
+        st = stamps[live].astype(np.int64)
+        kd = kinds[live]
+        t0 = st[:, 0].min()
+        us = lambda col: (st[:, col] - t0) * 0.01   # 100 MHz clock
+        end = us(S - 1)
+        nslot = kd[:, S - 1]
+        inter = {-1: [], 0: [], 1: []}
+        last = []
+        nq = np.zeros(len(live), np.int32)     # q slots: items (or 128-row halves) the worker starts
+        nsuf = np.zeros(len(live), np.int32)   # suffix tiles
+        for i in range(len(live)):
+            n = min(int(nslot[i]), S - 5)
+            ts = (st[i, 4:4 + n] - t0) * 0.01
+            for s in range(1, n):
+                inter[int(kd[i, 4 + s - 1])].append(ts[s] - ts[s - 1])
+            if 0 < nslot[i] <= S - 5:   # the whole range was stamped
+                last.append(end[i] - ts[n - 1])
+            nq[i] = int(np.sum(kd[i, 4:4 + n] == -1))
+            nsuf[i] = int(np.sum(kd[i, 4:4 + n] == 1))
+        xcd = [float(np.median(end[live % 8 == x])) if np.any(live % 8 == x) else float("nan") for x in range(8)]
+        by_q = {q: float(np.median(end[nq == q])) if np.any(nq == q) else float("nan") for q in (1, 2, 3)}
+        rows.append({
+            "workers": len(live), "start_max": us(0).max(), "plan_p50": np.median(us(1)),
+            "walk_p50": np.median(us(2)), "walk_max": us(2).max(),
+            "slot0_p50": np.median(us(4)), "slot0_max": us(4).max(),
+            "end_min": end.min(), "end_p50": np.median(end), "end_max": end.max(),
+            "slots_p50": np.median(nslot), "slots_max": nslot.max(),
+            "q_slot_interval_p50": np.median(inter[-1]) if inter[-1] else float("nan"),
+            "prefix_tile_interval_p50": np.median(inter[0]) if inter[0] else float("nan"),
+            "prefix_tile_interval_p90": np.percentile(inter[0], 90) if inter[0] else float("nan"),
+            "suffix_tile_interval_p50": np.median(inter[1]) if inter[1] else float("nan"),
+            "last_slot_to_end_p50": np.median(last) if last else float("nan"),
+            **{f"end_p50_xcd{x}": xcd[x] for x in range(8)},
+            **{f"end_p50_workers_with_{q}_q_slots": by_q[q] for q in (1, 2, 3)},
+            "end_p50_workers_with_suffix_tiles": float(np.median(end[nsuf > 0])) if np.any(nsuf > 0) else float("nan"),
+            "end_p50_workers_without": float(np.median(end[nsuf == 0])) if np.any(nsuf == 0) else float("nan"),
+        })
+    print(f"timeline of the partial kernel, {args.workload}: medians over {args.steps} steps of per-step figures "
+          f"(us from the first workgroup's start; stamps of thread 0 of each workgroup)")
+    for key in rows[0]:
+        v = float(np.nanmedian([r[key] for r in rows])) if any(np.isfinite(r[key]) for r in rows) else float("nan")
+        print(f"  {key:36s} {v:9.2f}")
+
+
 def pct(a, q):
     return round(float(np.percentile(a, q)) * 1e3, 2)
 
@@ -217,6 +290,9 @@ def main():
                     help="E4M3 KV: scores on the fp8 matrix cores (SPECGEN_FLAG_FP8_SCORES)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--timeline", action="store_true",
+                    help="instead of the JSON line: run the steps on libspecgen_timeline.so and print the partial "
+                         "kernel's per-workgroup timeline (medians over --steps steps)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -227,6 +303,9 @@ def main():
     import torch
     import paper_2606_17518_amd as sg
     import synth
+    if args.timeline:   # every library call of the run goes to the stamping build
+        from paper_2606_17518_amd import binding
+        binding._lib = binding.timeline_lib()
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -299,6 +378,9 @@ def main():
             sg.specgen_fork_decode_attn(reps[r_att], out, lse, ws, stream=stream)
         evs[3].record(stream)
 
+    if args.timeline:
+        timeline_report(args, b, step, q_len)
+        return
     total = args.warmup + args.steps
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
     log(f"warmup {args.warmup}")

@@ -16,7 +16,7 @@ from typing import Optional, Sequence
 import numpy as np
 import torch
 
-from .build import DEBUG_LIB_PATH, LIB_PATH
+from .build import DEBUG_LIB_PATH, LIB_PATH, TIMELINE_LIB_PATH
 
 SPECGEN_OK, SPECGEN_ERR_INVALID_ARG, SPECGEN_ERR_UNSUPPORTED, SPECGEN_ERR_WORKSPACE, SPECGEN_ERR_DEVICE = range(5)
 SPECGEN_BF16, SPECGEN_FP8_E4M3, SPECGEN_FP32 = 0, 1, 2
@@ -80,6 +80,7 @@ class KvAppendC(C.Structure):
 
 _lib = None
 _debug_lib = None
+_timeline_lib = None
 
 
 def load(path: str):
@@ -131,6 +132,19 @@ def debug_lib():
     if _debug_lib is None:
         _debug_lib = load(DEBUG_LIB_PATH)
     return _debug_lib
+
+
+def timeline_lib():
+    """The build whose partial kernel stamps a per-workgroup timeline
+    (include/specgen_timeline.h), with every entry point of the library."""
+    global _timeline_lib
+    if _timeline_lib is None:
+        L = load(TIMELINE_LIB_PATH)
+        L.specgen_timeline_shape.argtypes = [C.POINTER(C.c_int), C.POINTER(C.c_int)]
+        L.specgen_timeline_read.argtypes = [C.c_void_p, C.c_void_p]
+        L.specgen_timeline_clear.argtypes = []
+        _timeline_lib = L
+    return _timeline_lib
 
 
 def _check(status: int):

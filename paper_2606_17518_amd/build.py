@@ -3,8 +3,11 @@
 Objects are built in parallel under _build/ at the repository root and linked
 into paper_2606_17518_amd/libspecgen.so; the same kernels with the entry
 points built under SPECGEN_DEBUG_CHECKS (every attention block id checked on
-the host before launch) into libspecgen_debug.so; and the benchmark's
-memory-ceiling kernels into libspecgen_probe.so.  Packed-FP32 instruction
+the host before launch) into libspecgen_debug.so; the same library with the
+bf16 partial kernel built under SPECGEN_TIMELINE (per-slot clock stamps of
+every workgroup, for the benchmark's --timeline report) into
+libspecgen_timeline.so; and the benchmark's memory-ceiling kernels into
+libspecgen_probe.so.  Packed-FP32 instruction
 selection is switched off on every device compile.
 """
 from __future__ import annotations
@@ -20,6 +23,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspecgen.so")
 DEBUG_LIB_PATH = os.path.join(PKG, "libspecgen_debug.so")
+TIMELINE_LIB_PATH = os.path.join(PKG, "libspecgen_timeline.so")
 SOURCES = ["abi.hip", "attn_bf16.hip", "attn_dot.hip", "merge.hip", "kv_import.hip", "kv_append.hip"]
 # the benchmark's memory-ceiling kernels, linked into a library of their own
 PROBE_SOURCES = ["probe.hip"]
@@ -59,12 +63,15 @@ def build(verbose: bool = False) -> str:
             print(r.stderr)
         return obj
 
-    jobs = [(s, "", []) for s in SOURCES + PROBE_SOURCES] + [("abi.hip", "_debug", ["-DSPECGEN_DEBUG_CHECKS"])]
+    jobs = [(s, "", []) for s in SOURCES + PROBE_SOURCES] + [("abi.hip", "_debug", ["-DSPECGEN_DEBUG_CHECKS"]),
+                                                             ("attn_bf16.hip", "_timeline", ["-DSPECGEN_TIMELINE"])]
     with cf.ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 4)) as ex:
         objs = dict(zip([j[0] + j[1] for j in jobs], ex.map(one, jobs)))
     kernels = [objs[s] for s in SOURCES if s != "abi.hip"]
     for lib_path, lib_objs in ((LIB_PATH, [objs["abi.hip"], *kernels]),
                                (DEBUG_LIB_PATH, [objs["abi.hip_debug"], *kernels]),
+                               (TIMELINE_LIB_PATH, [objs["abi.hip"], objs["attn_bf16.hip_timeline"],
+                                                    *[k for k in kernels if k != objs["attn_bf16.hip"]]]),
                                (PROBE_LIB_PATH, [objs[s] for s in PROBE_SOURCES])):
         tmp = lib_path + ".tmp%d" % os.getpid()
         r = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *lib_objs],

@@ -66,6 +66,20 @@
 #include "worker.h"
 
 namespace specgen {
+
+#ifdef SPECGEN_TIMELINE
+// Timeline build (libspecgen_timeline.so only): thread 0 of every workgroup
+// stamps the GPU's constant 100 MHz clock at fixed points of its run into LDS
+// (kernel start, plan in LDS, walk done, every slot landed, end) and wave 0
+// writes the stamps out when the workgroup ends.  Nothing is stored to global
+// memory inside the slot loop, so the DMA accounting of the ring is untouched;
+// each stamp costs thread 0 a clock read.
+constexpr int kTlWorkers = 2048;   // workgroups recorded
+constexpr int kTlSlots = 128;      // 0 start, 1 plan, 2 walk, 4 + s slot s landed, 127 end
+__device__ uint64_t g_tl_stamp[kTlWorkers][kTlSlots];
+__device__ int32_t g_tl_kind[kTlWorkers][kTlSlots];
+#endif
+
 namespace bf16k {
 
 // l + the sum of the 8 bf16 probabilities packed in pk (one dot2 with (1, 1)
@@ -212,7 +226,35 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   constexpr int DT = D / 16;   // d-tiles of O^T
   __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLdsBytes];
   __shared__ Plan splan;
+#ifdef SPECGEN_TIMELINE
+  __shared__ uint64_t tl_t[kTlSlots];
+  __shared__ int32_t tl_k[kTlSlots];
+#define SG_TL(i, k)                                          \
+  do {                                                       \
+    if (threadIdx.x == 0) {                                  \
+      tl_t[(i)] = __builtin_amdgcn_s_memrealtime();          \
+      tl_k[(i)] = (k);                                       \
+    }                                                        \
+  } while (0)
+  // wave 0 writes the stamps of slots 0 .. n - 1 and the end stamp out
+  auto tl_flush = [&](int n) {
+    if (threadIdx.x < 64 && blockIdx.x < kTlWorkers) {
+      for (int i = threadIdx.x; i < kTlSlots; i += 64) {
+        if (i < 3 || (i >= 4 && i < 4 + n) || i == kTlSlots - 1) {
+          g_tl_stamp[blockIdx.x][i] = tl_t[i];
+          g_tl_kind[blockIdx.x][i] = tl_k[i];
+        }
+      }
+    }
+  };
+#else
+#define SG_TL(i, k) \
+  do {              \
+  } while (0)
+#endif
+  SG_TL(0, 100);
   plan_to_lds<512>(plan_arg, splan);
+  SG_TL(1, 101);
   const Plan& plan = splan;
   int32_t* items = reinterpret_cast<int32_t*>(lds + C::kOffItems);
   float* ml = reinterpret_cast<float*>(lds + C::kOffML);
@@ -226,13 +268,20 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   // (the ML area is free until the first item ends)
   const WorkerRange wr = worker_walk_tiles<C::kThreads, C::kItemCap, C::kIdsPerTile>(
       a, plan, kPartMfma, w, items, reinterpret_cast<int32_t*>(lds + C::kOffIds), reinterpret_cast<int32_t*>(ml));
+  SG_TL(2, 102);
   // The walk reads LDS, so the compiler cannot prove its results uniform;
   // without these readfirstlanes every loop-carried value of the slot loop
   // would live in VGPRs under exec masks.
   const int R = uniform(wr.R);
   const int first_ord = uniform(wr.first_ord);
   const int nitems = uniform(wr.nitems);
-  if (R <= 0) return;
+  if (R <= 0) {
+#ifdef SPECGEN_TIMELINE
+    SG_TL(kTlSlots - 1, 0);
+    tl_flush(0);
+#endif
+    return;
+  }
   const uint32_t lds_base = (uint32_t)(size_t)((SG_LDS uint8_t*)lds);
 
   // Item descriptors are read from LDS once per item and kept in scalar registers.
@@ -963,6 +1012,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     // E4M3 converts the next tile during this iteration, so it waits for that slot
     vm_wait_le(uniform(ops - ((FP8 && s + 1 < S) ? mk1 : mk0)));
     lds_barrier();
+#ifdef SPECGEN_TIMELINE
+    if (s < kTlSlots - 5) SG_TL(4 + s, cp_k < 0 ? -1 : cp_d.kind);
+#endif
     if (!late_dma && issued < S) mk3 = issue_next();
     const int stage = s & 3;
     if constexpr (FP8) {
@@ -984,6 +1036,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     mk2 = mk3;
     advance(cp_ii, cp_k, cp_d);
   }
+#ifdef SPECGEN_TIMELINE
+  SG_TL(kTlSlots - 1, S);
+  tl_flush(S < kTlSlots - 5 ? S : kTlSlots - 5);
+#endif
+#undef SG_TL
 }
 
 // Partial kernel of the MFMA partition: bf16 KV, or E4M3 KV decoded exactly to
@@ -1016,3 +1073,31 @@ int mfma_walk_threads() { return bf16k::Cfg<128, false>::kThreads; }
 int mfma_rows() { return bf16k::Cfg<128, false>::kMaxRows; }
 
 }  // namespace specgen
+
+#ifdef SPECGEN_TIMELINE
+// The stamps of the last partial-kernel launches on the current device
+// (include/specgen_timeline.h).
+extern "C" int specgen_timeline_shape(int* workers, int* slots) {
+  if (!workers || !slots) return 1;
+  *workers = specgen::kTlWorkers;
+  *slots = specgen::kTlSlots;
+  return 0;
+}
+extern "C" int specgen_timeline_read(uint64_t* stamps, int32_t* kinds) {
+  if (!stamps || !kinds) return 1;
+  if (hipMemcpyFromSymbol(stamps, HIP_SYMBOL(specgen::g_tl_stamp), sizeof(specgen::g_tl_stamp)) != hipSuccess)
+    return 2;
+  if (hipMemcpyFromSymbol(kinds, HIP_SYMBOL(specgen::g_tl_kind), sizeof(specgen::g_tl_kind)) != hipSuccess) return 2;
+  return 0;
+}
+extern "C" int specgen_timeline_clear(void) {
+  void* p = nullptr;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(specgen::g_tl_stamp)) != hipSuccess ||
+      hipMemset(p, 0, sizeof(specgen::g_tl_stamp)) != hipSuccess)
+    return 2;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(specgen::g_tl_kind)) != hipSuccess ||
+      hipMemset(p, 0, sizeof(specgen::g_tl_kind)) != hipSuccess)
+    return 2;
+  return hipDeviceSynchronize() == hipSuccess ? 0 : 2;
+}
+#endif

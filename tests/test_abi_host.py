@@ -391,6 +391,31 @@ def test_debug_library_exports_the_same_entry_points(L):
     assert b"num_traces" in D.specgen_last_error()
 
 
+def test_timeline_library_exports_its_header_and_the_entry_points(L):
+    """libspecgen_timeline.so (the partial kernel built with per-slot clock
+    stamps) is a drop-in build of the library that also exports every call of
+    include/specgen_timeline.h, which the release library does not."""
+    import paper_2606_17518_amd.binding as B
+    T = B.timeline_lib()
+    for n in _declared():
+        assert hasattr(T, n), n
+    src = open(os.path.join(ROOT, "include", "specgen_timeline.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = sorted(set(re.findall(r"\b(specgen_timeline_\w+)\s*\(", src)))
+    assert names == ["specgen_timeline_clear", "specgen_timeline_read", "specgen_timeline_shape"]
+    for n in names:
+        assert hasattr(T, n), n
+        assert not hasattr(L, n), n
+    w, k = C.c_int(0), C.c_int(0)
+    assert T.specgen_timeline_shape(C.byref(w), C.byref(k)) == 0
+    assert (w.value, k.value) == (2048, 128)
+    assert T.specgen_timeline_shape(None, C.byref(k)) == 1
+    assert T.specgen_timeline_read(None, None) == 1
+    s, keep = _host_batch(num_traces=0)
+    n = C.c_size_t(0)
+    assert T.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 1
+
+
 def test_debug_block_id_check_on_host_tables(tmp_path):
     """The debug build's block-id check (csrc/table_check.h), driven with host
     tables by a g++ harness: ids past ceil(len/16) are never read, -1 and
