@@ -128,10 +128,13 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   in.tile_cap[1] = dot_tile_cap(in.D);
   // Unit prices of the split, from per-worker timelines of the MFMA kernel on
   // MI355X, in eighths of a tile of an item of 4 groups of 32 rows.  bf16 KV: a
-  // tile of 1 or 4 groups took 1.20 and 1.32 us, and an item's fixed cost (its
-  // q slot, about 1 us, and its end: token-group combine and partial stores,
-  // about 2.5 us) about 2.5 such tiles; the item charge is 20 (workers whose
-  // range holds two items ended last at a charge of 16).  E4M3 KV (which adds
+  // tile of 1 or 4 groups took 1.20 and 1.32-1.36 us, and a prefix item's
+  // fixed cost (its q slot, about 1 us, and its end: token-group combine and
+  // partial stores, about 2.5 us) about 2.5 such tiles; the prefix-item charge
+  // is 20 (workers whose range holds two items ended last at a charge of 16).
+  // A suffix item (g rows) ends with far less to combine and store: at a charge
+  // of 20 the workers holding suffix items ended 2.5-3 us before the others on
+  // the 32k-prefix workload, at 12 with them.  E4M3 KV (which adds
   // the decode of each tile): 1.56-1.60, 1.96 and 2.96 us for 1, 4 and 8
   // groups, charge 16.  Items of 5-8 groups run one token group per wave
   // (each wave takes both 32-token slabs of a tile).  The dot path prices
@@ -144,6 +147,8 @@ specgen_status_t build_plan(const specgen_fork_batch_t* b, Plan* plan, int64_t* 
   }
   in.charge[0] = fp8 ? 16 : 20;
   in.charge[1] = 1;
+  in.charge_suf[0] = fp8 ? 16 : 12;
+  in.charge_suf[1] = 1;
   in.walk_threads[0] = mfma_walk_threads();
   in.walk_threads[1] = 0;   // the dot kernel walks serially
   char err[256];

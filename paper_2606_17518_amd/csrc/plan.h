@@ -16,10 +16,11 @@
 // `tt` tokens.
 //
 // Units.  The split is made over a sequence of units that prices the work:
-// every item takes `charge` units for its fixed cost in a worker (its query
-// rows and its end), then a price per tile that grows with the rows the item
-// computes: wtP[] for the prefix items of each trace, wt_suf for suffix items
-// (g rows of one fork).  The sequence is split evenly over W
+// every item first takes units for its fixed cost in a worker (its query rows
+// and its end: `charge` for a prefix item, `charge_suf` for a suffix item),
+// then a price per tile that grows with the rows the item computes: wtP[] for
+// the prefix items of each trace, wt_suf for suffix items (g rows of one
+// fork).  The sequence is split evenly over W
 // workers (workgroups): worker w takes units [start(w), start(w+1)) and
 // processes the tiles whose first unit lies there.  A worker emits one partial
 // (o, lse) per item it touches, into slot w * kmax + k where k is the item's
@@ -64,7 +65,8 @@ struct PartPlan {
   int32_t suffix_rb;      // row blocks per suffix (fork, head): ceil(g / rbs)
   int32_t n_traces;       // traces whose prefix items are in the partition
   int32_t trace_begin;    // their positions in Plan::ptrace: [trace_begin, +n_traces)
-  int32_t charge;         // units in front of every item (its fixed cost)
+  int32_t charge;         // units in front of every prefix item (its fixed cost)
+  int32_t charge_suf;     // units in front of every suffix item
   int32_t wt_suf;         // units per tile of a suffix item
   int32_t wt_max;         // the largest tile price of the partition
 };
@@ -161,7 +163,7 @@ struct ItemRef {
   int32_t ord;       // ordinal of the item in the partition
 };
 
-// Units taken by one suffix item of fork f (0 if S_f = 0): its charge plus
+// Units taken by one suffix item of fork f (0 if S_f = 0): charge_suf plus
 // ceil(S_f / tt) tiles of wt_suf units; unitS holds their per-fork prefix sums.
 SG_HD int32_t suffix_span(const Plan& p, const PartPlan& pp, int f) {
   return (p.unitS[f + 1] - p.unitS[f]) / (p.Hkv * pp.suffix_rb);
@@ -176,7 +178,7 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
   r.w = 1;
   r.first = 0;
   if (x < 0 || x >= pp.units) return r;
-  int local, span, item;
+  int local, span, item, charge;
   if (x < pp.prefix_units) {
     // largest position i in the partition's trace list with unitP[i] <= x
     int lo = pp.trace_begin, hi = pp.trace_begin + pp.n_traces - 1;
@@ -188,7 +190,8 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
     const int rb_count = cdiv32(trace_rows(p, t), pp.rbs);
     r.tiles = cdiv32(p.prefix_len[t], pp.tt);
     r.w = p.wtP[lo];
-    span = r.tiles * r.w + pp.charge;
+    charge = pp.charge;
+    span = r.tiles * r.w + charge;
     local = (int)(x - p.unitP[lo]);   // unit counts fit in int32 (the planner checks)
     item = local / span;
     r.kind = 0;
@@ -206,7 +209,8 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
     const int f = lo;
     span = suffix_span(p, pp, f);
     r.w = pp.wt_suf;
-    r.tiles = (span - pp.charge) / r.w;
+    charge = pp.charge_suf;
+    r.tiles = (span - charge) / r.w;
     local = xs - p.unitS[f];
     item = local / span;
     r.kind = 1;
@@ -215,22 +219,22 @@ SG_HD ItemRef locate(const Plan& p, int part, int64_t x) {
     r.rb = item % pp.suffix_rb;
     r.ord = pp.n_prefix_items + (f * p.Hkv + r.j) * pp.suffix_rb + r.rb;
   }
-  r.off = local - item * span - pp.charge;
+  r.off = local - item * span - charge;
   r.tile = r.off >= 0 ? r.off / r.w : -1;
   r.first = x - r.off;
   return r;
 }
 
 // The item that follows `cur` in partition `part` (cur must not be the last
-// one), with x at its tile 0: equal to locate(p, part, cur.first +
-// cur.tiles * cur.w + charge).  Steps within a trace or fork in O(1) and falls
-// back to locate() where it would have to skip over forks without suffix
-// tokens or cross into the suffix items.
+// one), with x at its tile 0: equal to locate(p, part, x) for x = cur.first +
+// cur.tiles * cur.w + the next item's charge.  Steps within a trace or fork
+// in O(1) and falls back to locate() where it would have to skip over forks
+// without suffix tokens or cross into the suffix items.
 SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
   const PartPlan& pp = p.part[part];
-  const int64_t x = cur.first + (int64_t)cur.tiles * cur.w + pp.charge;
+  const int64_t end = cur.first + (int64_t)cur.tiles * cur.w;   // where the next item's charge starts
   ItemRef r = cur;
-  r.first = x;
+  r.first = end + (cur.kind == 0 ? pp.charge : pp.charge_suf);
   r.tile = 0;
   r.off = 0;
   r.ord = cur.ord + 1;
@@ -254,29 +258,28 @@ SG_HD ItemRef next_item(const Plan& p, int part, const ItemRef& cur) {
       r.w = p.wtP[pos];
       return r;
     }
-    return locate(p, part, x);
-  }
-  if (cur.rb + 1 < pp.suffix_rb) {
+  } else if (cur.rb + 1 < pp.suffix_rb) {
     r.rb = cur.rb + 1;
     return r;
-  }
-  if (cur.j + 1 < p.Hkv) {
+  } else if (cur.j + 1 < p.Hkv) {
     r.j = cur.j + 1;
     r.rb = 0;
     return r;
-  }
-  const int f = cur.f + 1;
-  if (f < p.N) {
+  } else if (cur.f + 1 < p.N) {
+    const int f = cur.f + 1;
     const int span = suffix_span(p, pp, f);
     if (span > 0) {
       r.f = f;
       r.j = 0;
       r.rb = 0;
-      r.tiles = (span - pp.charge) / pp.wt_suf;
+      r.tiles = (span - pp.charge_suf) / pp.wt_suf;
       return r;
     }
   }
-  return locate(p, part, x);
+  r = locate(p, part, end);   // at the first unit of the next item's charge
+  r.tile = 0;
+  r.off = 0;
+  return r;
 }
 
 // The items of worker w's range, in order.  For each one with tiles in the
@@ -320,7 +323,7 @@ SG_HD WorkerRange walk_range(const Plan& p, int part, int64_t w, int item_cap, V
       if (t + n < it.tiles) break;   // the range ends inside this item
     }
     const int64_t end = it.first + (int64_t)it.tiles * it.w;   // where the next item's charge starts
-    if (end >= pp.units || end + pp.charge >= x1) break;
+    if (end >= pp.units || end + (end >= pp.prefix_units ? pp.charge_suf : pp.charge) >= x1) break;
     it = next_item(p, part, it);
     t = 0;
   }
@@ -444,8 +447,9 @@ SG_HD bool suffix_parts_of_row(const Plan& p, int f, int h, ItemParts* out) {
   if (span <= 0) return false;
   const int rb = hh / pp.rbs;
   const int item = j * pp.suffix_rb + rb;
-  *out = item_parts(p, X, pp.prefix_units + p.unitS[f] + (int64_t)item * span + pp.charge,
-                    (span - pp.charge) / pp.wt_suf, pp.wt_suf, pp.n_prefix_items + f * per_fork + item, hh - rb * pp.rbs);
+  *out = item_parts(p, X, pp.prefix_units + p.unitS[f] + (int64_t)item * span + pp.charge_suf,
+                    (span - pp.charge_suf) / pp.wt_suf, pp.wt_suf, pp.n_prefix_items + f * per_fork + item,
+                    hh - rb * pp.rbs);
   return true;
 }
 

@@ -29,7 +29,8 @@ struct PlanInputs {
   int item_cap[2];            // max items per worker
   int tile_cap[2];            // max tiles per worker
   int walk_threads[2];        // threads of a parallel walk (0: serial walk, no unit limit)
-  int charge[2];              // units in front of every item
+  int charge[2];              // units in front of every prefix item
+  int charge_suf[2];          // units in front of every suffix item
   int wt_rg[2][9];            // units per tile of an item of 1..8 row groups of 32 rows ([0] unused)
 };
 
@@ -124,9 +125,10 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     pp.slot_rows = in.rbs[X];
     pp.trace_begin = pos;
     pp.charge = in.charge[X];
+    pp.charge_suf = in.charge_suf[X];
     for (int r = 1; r <= 8; ++r)
       if (in.wt_rg[X][r] < 1) SG_FAIL(kPlanInvalid, "unit prices must be positive");
-    if (pp.charge < 0) SG_FAIL(kPlanInvalid, "unit prices must be positive");
+    if (pp.charge < 0 || pp.charge_suf < 0) SG_FAIL(kPlanInvalid, "unit prices must be positive");
     pp.wt_suf = in.wt_rg[X][row_groups(std::min(g, pp.rbs))];
     pp.wt_max = pp.wt_suf;
     int wt_min = pp.wt_suf;
@@ -150,10 +152,11 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
       ++pos;
     }
     pp.n_traces = pos - pp.trace_begin;
-    // a parallel walk examines chunks of at most min(price, charge) units per
+    // a parallel walk examines chunks of at most min(price, charges) units per
     // thread, so that a chunk holds at most one tile start
-    unit_cap[X] = in.walk_threads[X] > 0 ? (int64_t)in.walk_threads[X] * std::max(1, std::min(wt_min, pp.charge))
-                                         : INT64_MAX;
+    unit_cap[X] = in.walk_threads[X] > 0
+                      ? (int64_t)in.walk_threads[X] * std::max(1, std::min(wt_min, std::min(pp.charge, pp.charge_suf)))
+                      : INT64_MAX;
     pp.prefix_units = units;
     pp.n_prefix_items = (int32_t)items;
     pp.units = units;
@@ -167,7 +170,7 @@ int plan_build(const PlanInputs& in, CusFn cus_fn, Plan* plan, int64_t* ws_float
     for (int f = 0; f < N; ++f) {
       plan->unitS[f] = (int32_t)acc;
       if (in.suffix_len[f] > 0)
-        acc += (int64_t)Hkv * pp.suffix_rb * ((int64_t)cdiv(in.suffix_len[f], pp.tt) * pp.wt_suf + pp.charge);
+        acc += (int64_t)Hkv * pp.suffix_rb * ((int64_t)cdiv(in.suffix_len[f], pp.tt) * pp.wt_suf + pp.charge_suf);
       if (acc > INT32_MAX) SG_FAIL(kPlanUnsupported, "batch too large");
     }
     plan->unitS[N] = (int32_t)acc;

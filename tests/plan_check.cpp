@@ -149,7 +149,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
   const int g = in.Hq / in.Hkv;
   int64_t ptile[2] = {0, 0};
   int pord[2] = {0, 0};
-  auto cover = [&](int X, int ord, int tiles, int wt) -> bool {
+  auto cover = [&](int X, int ord, int tiles, int wt, int charge) -> bool {
     auto itv = segs.find({X, ord});
     if (tiles == 0) {
       CHECK(itv == segs.end(), "empty item has segments");
@@ -157,7 +157,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     }
     CHECK(itv != segs.end(), "item (%d, %d) never processed", X, ord);
     // an item takes `charge` units, then its tiles of wt units each
-    int64_t expect = ptile[X] + in.charge[X];
+    int64_t expect = ptile[X] + charge;
     int total = 0;
     for (const Seg& s : itv->second) {
       CHECK(s.first == expect, "item tiles not contiguous");
@@ -165,7 +165,7 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
       total += s.n;
     }
     CHECK(total == tiles, "item covered %d of %d tiles", total, tiles);
-    ptile[X] += in.charge[X] + (int64_t)tiles * wt;
+    ptile[X] += charge + (int64_t)tiles * wt;
     return true;
   };
   for (int X = 0; X < 2; ++X) {
@@ -175,7 +175,8 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
       const int rb = (rows + in.rbs[X] - 1) / in.rbs[X];
       const int tiles = (in.prefix_len[t] + in.tt[X] - 1) / in.tt[X];
       for (int i = 0; i < in.Hkv * rb; ++i)
-        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(rows, in.rbs[X]))])) return false;
+        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(rows, in.rbs[X]))], in.charge[X]))
+          return false;
     }
   }
   {
@@ -184,7 +185,8 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     for (int f = 0; f < in.N; ++f) {
       const int tiles = (in.suffix_len[f] + in.tt[X] - 1) / in.tt[X];
       for (int i = 0; i < in.Hkv * rb; ++i)
-        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(g, in.rbs[X]))])) return false;
+        if (!cover(X, pord[X]++, tiles, in.wt_rg[X][row_groups(std::min(g, in.rbs[X]))], in.charge_suf[X]))
+          return false;
     }
   }
   for (int X = 0; X < 2; ++X) CHECK(ptile[X] == plan.part[X].units, "partition %d unit total", X);
@@ -194,11 +196,12 @@ static bool check_plan(const PlanInputs& in, int cus, uint64_t case_id, bool lib
     int64_t x = 0;
     while (x < pp.units) {
       const ItemRef it = locate(plan, X, x);
-      CHECK(it.off == -pp.charge, "an item starts with its charge");
+      CHECK(it.off == -(it.kind == 0 ? pp.charge : pp.charge_suf), "an item starts with its charge");
       const int64_t nx = it.first + (int64_t)it.tiles * it.w;
       if (nx < pp.units) {
         const ItemRef a = next_item(plan, X, it);
-        const ItemRef b = locate(plan, X, nx + pp.charge);
+        const int nc = nx >= pp.prefix_units ? pp.charge_suf : pp.charge;   // the next item's charge
+        const ItemRef b = locate(plan, X, nx + nc);
         CHECK(a.kind == b.kind && a.t == b.t && a.f == b.f && a.j == b.j && a.rb == b.rb && a.tiles == b.tiles &&
                   a.tile == b.tile && a.off == b.off && a.w == b.w && a.first == b.first && a.ord == b.ord,
               "next_item differs from locate at unit %lld of partition %d", (long long)nx, X);
@@ -361,10 +364,13 @@ int main(int argc, char** argv) {
       for (int r = 0; r < 9; ++r) { in.wt_rg[0][r] = e4m3 ? rg_e4m3[r] : rg_bf16[r]; in.wt_rg[1][r] = 1; }
       in.charge[0] = e4m3 ? 16 : 20;
       in.charge[1] = 1;
+      in.charge_suf[0] = e4m3 ? 16 : 12;
+      in.charge_suf[1] = 1;
     } else {
       for (int X = 0; X < 2; ++X) {
         for (int r = 0; r < 9; ++r) in.wt_rg[X][r] = U(1, 16);
         in.charge[X] = U(0, 20);
+        in.charge_suf[X] = U(0, 20);
       }
     }
     in.tile_cap[0] = 2560 / (in.tt[0] / 16);
