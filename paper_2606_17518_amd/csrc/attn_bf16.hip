@@ -17,7 +17,8 @@
 // tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
 // stages with three slots in flight.  Every wave moves exactly four 1 KiB
 // pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no VGPR
-// staging; nontemporal, the KV is read once): waves 0-3 the K block slices of
+// staging; tiles nontemporal, the KV is read once; q slots through the caches,
+// since every worker of a prefix item reads the same q rows): waves 0-3 the K block slices of
 // a tile, waves 4-7 its V slices.  So the number of vector-memory operations
 // a wave has in flight is known exactly and the wait for slot s is
 // "vmcnt <= 4 x (slots issued after s) + partial stores issued since".  These
@@ -161,6 +162,16 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
   const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
   const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(gu), "s"(l) : "m0");
+}
+
+// The same, through the caches (for rows several workgroups read).
+__device__ __forceinline__ void dma16_cached(const void* gbase, uint32_t voff, uint32_t lds_addr) {
+  const uint64_t g = reinterpret_cast<uint64_t>(gbase);
+  const uint32_t glo = __builtin_amdgcn_readfirstlane((uint32_t)g);
+  const uint32_t ghi = __builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+  const void* gu = reinterpret_cast<const void*>(((uint64_t)ghi << 32) | glo);
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gu), "s"(l) : "m0");
 }
 
 // Four E4M3 codes -> four bf16, one gfx950 scaled conversion per pair with
@@ -358,7 +369,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
         item_row_fork_head(plan, d.kind, d.t, d.f, d.j, d.row0, rr, &fork, &hq);
         const int chunk = (lane % CPR) ^ swz_q<D>(row);
         const uint32_t voff = (uint32_t)(((int64_t)fork * plan.Hq + hq) * head_stride) + (uint32_t)(chunk * 16);
-        dma16(a.q, voff, st + (uint32_t)(n * 1024));
+        dma16_cached(a.q, voff, st + (uint32_t)(n * 1024));
       }
     } else if constexpr (FP8) {
       // this wave's block slices of the tile's K (waves 0-3) or V (waves 4-7)
