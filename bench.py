@@ -254,6 +254,7 @@ def timeline_report(args, b, step, q_len):
         rows.append({
             "workers": len(live), "start_max": us(0).max(), "plan_p50": np.median(us(1)),
             "walk_p50": np.median(us(2)), "walk_max": us(2).max(),
+            "first_slots_issued_p50": np.median(us(3)[nslot > 0]) if np.any(nslot > 0) else float("nan"),
             "slot0_p50": np.median(us(4)), "slot0_max": us(4).max(),
             "end_min": end.min(), "end_p50": np.median(end), "end_max": end.max(),
             "slots_p50": np.median(nslot), "slots_max": nslot.max(),

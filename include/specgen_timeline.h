@@ -31,7 +31,9 @@ int specgen_timeline_shape(int *workers, int *slots);
 /* Copies the array to host memory: stamps (uint64 clock ticks of 10 ns, 0 =
  * not stamped) and kinds (int32), each workers x slots, row-major by
  * workgroup.  Slot 0: workgroup start (kind 100); 1: plan in LDS (101); 2:
- * walk done, block ids gathered (102); 4 + s: ring slot s has landed and the
+ * walk done, block ids gathered (102); 3: the first three slots of the ring
+ * issued (103; not stamped for a workgroup with no tiles); 4 + s: ring slot
+ * s has landed and the
  * workgroup starts on it (kind -1 a q slot, 0 a prefix tile, 1 a suffix tile),
  * for the first slots - 5 slots; slots - 1: end (kind = the workgroup's slot
  * count). */

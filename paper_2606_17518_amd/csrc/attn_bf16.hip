@@ -76,7 +76,7 @@ namespace specgen {
 // memory inside the slot loop, so the DMA accounting of the ring is untouched;
 // each stamp costs thread 0 a clock read.
 constexpr int kTlWorkers = 2048;   // workgroups recorded
-constexpr int kTlSlots = 128;      // 0 start, 1 plan, 2 walk, 4 + s slot s landed, 127 end
+constexpr int kTlSlots = 128;      // 0 start, 1 plan, 2 walk, 3 first slots issued, 4 + s slot s landed, 127 end
 __device__ uint64_t g_tl_stamp[kTlWorkers][kTlSlots];
 __device__ int32_t g_tl_kind[kTlWorkers][kTlSlots];
 #endif
@@ -247,11 +247,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
       tl_k[(i)] = (k);                                       \
     }                                                        \
   } while (0)
-  // wave 0 writes the stamps of slots 0 .. n - 1 and the end stamp out
-  auto tl_flush = [&](int n) {
+  // wave 0 writes stamps 0 .. lead - 1 and the end stamp out
+  auto tl_flush = [&](int lead) {
     if (threadIdx.x < 64 && blockIdx.x < kTlWorkers) {
       for (int i = threadIdx.x; i < kTlSlots; i += 64) {
-        if (i < 3 || (i >= 4 && i < 4 + n) || i == kTlSlots - 1) {
+        if (i < lead || i == kTlSlots - 1) {
           g_tl_stamp[blockIdx.x][i] = tl_t[i];
           g_tl_kind[blockIdx.x][i] = tl_k[i];
         }
@@ -289,7 +289,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   if (R <= 0) {
 #ifdef SPECGEN_TIMELINE
     SG_TL(kTlSlots - 1, 0);
-    tl_flush(0);
+    tl_flush(3);
 #endif
     return;
   }
@@ -1007,6 +1007,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   if (issued < S) mk0 = issue_next();
   if (issued < S) mk1 = issue_next();
   if (issued < S) mk2 = issue_next();
+  SG_TL(3, 103);
   Desc cp_d = load_desc(0);
   int cp_ii = 0, cp_k = -q_slots(cp_d.nrows);
   // bf16 KV: waves 0-3 queue their share of the next slot's DMAs after their
@@ -1049,7 +1050,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   }
 #ifdef SPECGEN_TIMELINE
   SG_TL(kTlSlots - 1, S);
-  tl_flush(S < kTlSlots - 5 ? S : kTlSlots - 5);
+  tl_flush(4 + (S < kTlSlots - 5 ? S : kTlSlots - 5));
 #endif
 #undef SG_TL
 }

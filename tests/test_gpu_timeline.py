@@ -51,12 +51,14 @@ def test_timeline_build_bits_and_stamps(name):
     for w in live:
         n = int(kd[w, S - 1])
         assert n >= 0
-        seq = [st[w, 0], st[w, 1], st[w, 2]] + [st[w, 4 + s] for s in range(min(n, S - 5))] + [st[w, S - 1]]
+        seq = [st[w, 0], st[w, 1], st[w, 2], st[w, 3]] + [st[w, 4 + s] for s in range(min(n, S - 5))] + [st[w, S - 1]]
         if n == 0:   # a worker with no tiles ends after its walk
             seq = [st[w, 0], st[w, 1], st[w, 2], st[w, S - 1]]
         assert all(x > 0 for x in seq), (w, seq)
         assert all(a <= c for a, c in zip(seq, seq[1:])), (w, seq)
         assert list(kd[w, :3]) == [100, 101, 102]
+        if n > 0:
+            assert kd[w, 3] == 103
         if n > 0:
             assert kd[w, 4] == -1   # every range starts with its first item's q slot
             assert set(kd[w, 4:4 + min(n, S - 5)]) <= {-1, 0, 1}
