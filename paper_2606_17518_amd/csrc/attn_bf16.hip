@@ -143,6 +143,27 @@ struct Cfg {
   static_assert(!FP8 || kSlicesPerWave * (kF8Slice / 1024) == kTileDma, "E4M3 code instructions per wave");
 };
 
+// V^T slices in LDS: the 16-byte half h (8 tokens) of dim row d of the slice
+// of tile block kb sits at byte 512 (d / 16) + 256 (d & 1) + 32 ((d & 15) / 2)
+// + 16 (h ^ (d & 1)) of the slice, with bit 5 flipped in odd blocks.  An
+// operand read (64 lanes: dims 16 dt + ln, half G & 1, block G / 2) and the
+// E4M3 decode's writes (64 consecutive dims, one half) then take no bank-
+// conflict cycles under gfx950's 128-bit lane grouping; the plain placement
+// 2d + (h ^ bit 3 of d) took two passes per read (measured with the LDS
+// bank-conflict counter: 8 instead of 4 cycles per 1 KiB read).
+__device__ __forceinline__ int v_pos(int d, int h, int kb) {
+  return (512 * (d >> 4) + 256 * (d & 1) + 32 * ((d & 15) >> 1) + 16 * (h ^ (d & 1))) ^ (32 * (kb & 1));
+}
+
+// E4M3 K decode at head_dim 128: lane L of a wave converts token row
+// kdec_row(L) of its 8-row code piece, bf16 chunks c0 and c0 + 1 with c0 =
+// kdec_c0(L).  Each 8 consecutive lanes (one pass of a 16-byte LDS write)
+// take half of each of two adjacent rows, whose K swizzles differ in bit 0, so
+// their writes fall on distinct bank groups (one row per 8 lanes took two
+// passes per write).
+__device__ __forceinline__ int kdec_row(int L) { return 2 * ((L >> 3) & 3) + ((L & 7) >> 2); }
+__device__ __forceinline__ int kdec_c0(int L) { return 2 * (L & 3) + 8 * (((L & 7) >> 2) ^ (L >> 5)); }
+
 // q slots of an item of `nrows` rows (128 rows per slot)
 __device__ __forceinline__ int q_slots(int nrows) { return nrows > 128 ? 2 : 1; }
 
@@ -331,9 +352,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   // Lane constants for piece i of slice b of this wave (tile block
   // kb = wq * kSlicesPerWave + b).  K: LDS chunk p of tile token row tt holds
   // source chunk p ^ swz_k(tt).  V: the slice is D rows of 32 bytes (16 tokens);
-  // LDS position 2d + (h ^ bit 3 of d) holds the 16-byte half h of row d, so a
-  // 16-lane read of 16 consecutive rows hits distinct banks.  One instruction
-  // moves 1 KiB of the slice; for V, lanes with bit 4 set swap their halves.
+  // lane L of piece i gathers the half that v_pos places at 1024 i + 16 L (a
+  // permutation inside the piece's 32 rows).  One instruction moves 1 KiB of
+  // the slice.
   constexpr int NB = C::kSlicesPerWave, NI = C::kPiecesPerSlice;
   uint32_t src_off[NB][NI];   // byte offset in the block slice, full tile
   int ptok[NI];               // K: token row of the slice this lane moves
@@ -344,7 +365,13 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       if (is_v) {
-        src_off[b][i] = (uint32_t)(1024 * i + 16 * (lane ^ ((lane >> 4) & 1)));
+        // invert v_pos for LDS byte 1024 i + 16 lane of the slice of block kb
+        const int kb = wq * NB + b;
+        const int o = (16 * lane) ^ (32 * (kb & 1));
+        const int w = (o >> 8) & 1;
+        const int d = 32 * i + 16 * (o >> 9) + 2 * ((o >> 5) & 7) + w;
+        const int h = ((o >> 4) & 1) ^ w;
+        src_off[b][i] = (uint32_t)(32 * d + 16 * h);
       } else {
         const int tt = (wq * NB + b) * 16 + ptok[i];
         src_off[b][i] = (uint32_t)(ptok[i] * C::kRowB + (((lane % CPR) ^ swz_k<CPR>(tt)) << 4));
@@ -384,7 +411,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
         for (int i = 0; i < NI8; ++i) {
           uint32_t src = (uint32_t)(1024 * i + 16 * lane);
-          if (QK8 && !is_v) {
+          if (!QK8 && !is_v && D == 128) {
+            // K codes of the row and dims this slot's converting lane takes
+            src = (uint32_t)(1024 * i + 128 * kdec_row(lane) + 8 * kdec_c0(lane));
+          } else if (QK8 && !is_v) {
             // K codes stay codes: 16-byte chunk c of tile row t lands at chunk
             // c ^ k8_swz(t) of its LDS row, so the score reads hit distinct banks
             const int t = 8 * (kb * NI8 + i) + lane / 8;
@@ -423,7 +453,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   // E4M3: once a tile slot has landed (one iteration before it is computed),
   // every wave turns its K code piece and V code piece (lane: one 16-byte chunk
   // of each) into the bf16 layout the MFMA path reads -- K rows swizzled, V^T
-  // slices with halves swapped on bit 3 of the row -- inside the 2 KiB runs
+  // halves placed by v_pos -- inside the 2 KiB runs
   // that hold them: it reads its codes before it writes (one wave's LDS
   // operations run in order), and no other wave touches those runs, so no
   // barrier; the next iteration's barrier publishes the tile.  Codes of tokens
@@ -437,8 +467,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     // K chunk: 16 dims of one token row of block slice kb (fp8 scores read the codes as they are)
     if constexpr (!QK8) {
       const int kb = o / C::kF8Slice;
-      const int tok = (o % C::kF8Slice) / D;
-      const int c8 = (o % D) / 8;                  // first bf16 chunk of the 16 dims
+      const int tok = D == 128 ? 8 * (wave & 1) + kdec_row(lane) : (o % C::kF8Slice) / D;
+      const int c8 = D == 128 ? kdec_c0(lane) : (o % D) / 8;   // first bf16 chunk of the 16 dims
       const int tt = kb * 16 + tok;
       const u32x2 b0 = e4m3x4_to_bf16x4(ck[0]), b1 = e4m3x4_to_bf16x4(ck[1]);
       const u32x2 b2 = e4m3x4_to_bf16x4(ck[2]), b3 = e4m3x4_to_bf16x4(ck[3]);
@@ -450,12 +480,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     {
       const int kb = o / C::kF8Slice;
       const int dd = (o % C::kF8Slice) / 16;
-      const int sw = (dd >> 3) & 1;
       uint8_t* vs = st8 + C::kTileB + kb * C::kSliceB;
       const u32x2 b0 = e4m3x4_to_bf16x4(cv[0]), b1 = e4m3x4_to_bf16x4(cv[1]);
       const u32x2 b2 = e4m3x4_to_bf16x4(cv[2]), b3 = e4m3x4_to_bf16x4(cv[3]);
-      *reinterpret_cast<u32x4*>(vs + (2 * dd + sw) * 16) = u32x4{b0[0], b0[1], b1[0], b1[1]};
-      *reinterpret_cast<u32x4*>(vs + (2 * dd + (1 ^ sw)) * 16) = u32x4{b2[0], b2[1], b3[0], b3[1]};
+      *reinterpret_cast<u32x4*>(vs + v_pos(dd, 0, kb)) = u32x4{b0[0], b0[1], b1[0], b1[1]};
+      *reinterpret_cast<u32x4*>(vs + v_pos(dd, 1, kb)) = u32x4{b2[0], b2[1], b3[0], b3[1]};
     }
   };
   static_assert(!FP8 || C::kTT * D == 16 * C::kThreads, "one K and one V code chunk per thread");
@@ -467,8 +496,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
   const int k_lane_tok = 8 * (ln >> 2) + (ln & 3);
   const int k_lane_swz = swz_k<CPR>(k_lane_tok);
   // V^T operand of d-tile dt for a slab at token sb: block sb/16 + G/2 of the
-  // tile, row d = 16 dt + ln, half G & 1 -> LDS position 2d + (half ^ bit 3 of d)
-  const int v_lane_off = (G >> 1) * C::kSliceB + 32 * ln + 16 * ((G & 1) ^ ((ln >> 3) & 1));
+  // tile (sb/16 is even, so the block's parity is that of G/2), row d = 16 dt +
+  // ln, half G & 1, at v_pos(ln, G & 1, G / 2) + 512 dt of the slice
+  static_assert(TT % 32 == 0, "slabs start at even blocks");
+  const int v_lane_off = (G >> 1) * C::kSliceB + v_pos(ln, G & 1, G >> 1);
   bf16x8 qop[2][KS];
   // QK8: per N-tile, the E4M3 codes of the lane's 32 dims of its row (dims
   // 16G .. 16G+15 in bytes 0-15, 64+16G .. +15 in bytes 16-31, the operand
