@@ -65,6 +65,7 @@
 // the row maxima would otherwise cost three instructions per element.  Masked
 // scores are -inf, never NaN, and infinities keep their meaning.
 #include "worker.h"
+#include "lds_layout.h"
 
 namespace specgen {
 
@@ -142,27 +143,6 @@ struct Cfg {
   static_assert(kMLBytes >= (2 * kWaves + 1) * 4, "the walk's scratch fits the ML area");
   static_assert(!FP8 || kSlicesPerWave * (kF8Slice / 1024) == kTileDma, "E4M3 code instructions per wave");
 };
-
-// V^T slices in LDS: the 16-byte half h (8 tokens) of dim row d of the slice
-// of tile block kb sits at byte 512 (d / 16) + 256 (d & 1) + 32 ((d & 15) / 2)
-// + 16 (h ^ (d & 1)) of the slice, with bit 5 flipped in odd blocks.  An
-// operand read (64 lanes: dims 16 dt + ln, half G & 1, block G / 2) and the
-// E4M3 decode's writes (64 consecutive dims, one half) then take no bank-
-// conflict cycles under gfx950's 128-bit lane grouping; the plain placement
-// 2d + (h ^ bit 3 of d) took two passes per read (measured with the LDS
-// bank-conflict counter: 8 instead of 4 cycles per 1 KiB read).
-__device__ __forceinline__ int v_pos(int d, int h, int kb) {
-  return (512 * (d >> 4) + 256 * (d & 1) + 32 * ((d & 15) >> 1) + 16 * (h ^ (d & 1))) ^ (32 * (kb & 1));
-}
-
-// E4M3 K decode at head_dim 128: lane L of a wave converts token row
-// kdec_row(L) of its 8-row code piece, bf16 chunks c0 and c0 + 1 with c0 =
-// kdec_c0(L).  Each 8 consecutive lanes (one pass of a 16-byte LDS write)
-// take half of each of two adjacent rows, whose K swizzles differ in bit 0, so
-// their writes fall on distinct bank groups (one row per 8 lanes took two
-// passes per write).
-__device__ __forceinline__ int kdec_row(int L) { return 2 * ((L >> 3) & 3) + ((L & 7) >> 2); }
-__device__ __forceinline__ int kdec_c0(int L) { return 2 * (L & 3) + 8 * (((L & 7) >> 2) ^ (L >> 5)); }
 
 // q slots of an item of `nrows` rows (128 rows per slot)
 __device__ __forceinline__ int q_slots(int nrows) { return nrows > 128 ? 2 : 1; }
@@ -365,12 +345,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       if (is_v) {
-        // invert v_pos for LDS byte 1024 i + 16 lane of the slice of block kb
-        const int kb = wq * NB + b;
-        const int o = (16 * lane) ^ (32 * (kb & 1));
-        const int w = (o >> 8) & 1;
-        const int d = 32 * i + 16 * (o >> 9) + 2 * ((o >> 5) & 7) + w;
-        const int h = ((o >> 4) & 1) ^ w;
+        int d = 0, h = 0;
+        v_slot_source(i, lane, wq * NB + b, &d, &h);
         src_off[b][i] = (uint32_t)(32 * d + 16 * h);
       } else {
         const int tt = (wq * NB + b) * 16 + ptok[i];

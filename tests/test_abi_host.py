@@ -416,6 +416,21 @@ def test_timeline_library_exports_its_header_and_the_entry_points(L):
     assert T.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 1
 
 
+def test_lds_layouts_of_the_partial_kernel(tmp_path):
+    """The partial kernel's LDS placements (csrc/lds_layout.h), driven by a g++
+    harness: the V^T placement fills every slot once and its DMA inverse stays
+    inside each 1 KiB piece; operand reads are conflict-free under every lane
+    grouping that fits the LDS measurements; the E4M3 K decode covers each
+    (row, chunk pair) once on distinct bank groups per write pass."""
+    import subprocess
+    exe = str(tmp_path / "lds_layout_check")
+    subprocess.run(["g++", "-O1", "-std=c++17", "-Wall", "-Werror", "-o", exe,
+                    os.path.join(ROOT, "tests", "lds_layout_check.cpp")], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all layout checks passed" in r.stdout
+
+
 def test_debug_block_id_check_on_host_tables(tmp_path):
     """The debug build's block-id check (csrc/table_check.h), driven with host
     tables by a g++ harness: ids past ceil(len/16) are never read, -1 and
