@@ -52,7 +52,7 @@ def partial_kernel(D: int, fp8: bool, qk8: bool = False) -> str:
     return f"attn_bf16_kernel<{D}, {'true' if fp8 else 'false'}, {'true' if qk8 else 'false'}>"
 
 
-PARTIAL_SOURCES = ("attn_bf16.hip", "worker.h", "common.h", "plan.h")
+PARTIAL_SOURCES = ("attn_bf16.hip", "worker.h", "common.h", "plan.h", "lds_layout.h")
 
 
 def source_hash() -> str:
