@@ -413,6 +413,27 @@ def main():
     torch.cuda.synchronize()
     part_ms = np.array([e[1].elapsed_time(e[2]) for e in sevents])
     merge_ms = np.array([e[2].elapsed_time(e[3]) for e in sevents])
+    # The partial kernel's average launch duration (the roofline figure):
+    # `steps` launches back to back between one event pair, the replicas in
+    # rotation (cold).  An event right before a launch delays the kernel's
+    # start by several microseconds of dispatch, which the per-step split
+    # above includes; back to back the launches follow each other as the
+    # kernel trace shows them.
+    b2b_ms = None
+    if q_len is None:
+        log(f"timing {args.steps} partial-kernel launches back to back")
+        for k in range(R):
+            sg.specgen_fork_decode_attn_phase(reps[k], sg.SPECGEN_PHASE_PARTIALS, None, None, ws, stream=stream)
+        bev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(SPIN_CYCLES)
+        bev[0].record(stream)
+        for k in range(args.steps):
+            sg.specgen_fork_decode_attn_phase(reps[(k + 1) % R], sg.SPECGEN_PHASE_PARTIALS, None, None, ws,
+                                              stream=stream)
+        bev[1].record(stream)
+        torch.cuda.synchronize()
+        b2b_ms = bev[0].elapsed_time(bev[1]) / args.steps
 
     def call(fb, st):   # the attention call alone
         if q_len is not None:
@@ -515,7 +536,7 @@ def main():
     out_bytes = Q * Hq * (D * 2 + 4)
     kern_bytes = attn_bytes - out_bytes      # the partial kernel reads everything but writes no output
     attn_s = float(np.median(attn_ms)) / 1e3
-    part_s = float(np.median(part_ms)) / 1e3
+    part_s = (b2b_ms if b2b_ms is not None else float(np.median(part_ms))) / 1e3
     value = attn_bytes / attn_s / 1e9
     achieved = kern_bytes / part_s / 1e9
     # matrix work of the partial kernel: S = q K^T and P V over every key of
@@ -533,12 +554,13 @@ def main():
         roofline = {"kernel": kname, "bound": "mfma",
                     "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic_from_profile(args.workload + ("_fp8scores" if args.fp8_scores else "")),
-                    "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2)}
+                    "algorithmic_flops_per_launch": int(kern_flops), "hbm_gbps": round(achieved, 2),
+                    "launch_us": round(part_s * 1e6, 2)}
     else:
         roofline = {"kernel": partial_kernel(D, False, False) + " (partials phase)", "bound": "hbm",
                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profile(args.workload + ("_fp8scores" if args.fp8_scores else "")),
-                    "algorithmic_bytes_per_launch": int(kern_bytes)}
+                    "algorithmic_bytes_per_launch": int(kern_bytes), "launch_us": round(part_s * 1e6, 2)}
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True,
@@ -551,12 +573,16 @@ def main():
         "fork_tokens_per_s": round(Q / attn_s, 1),
         "attn_us": {"p50": pct(attn_ms, 50), "p10": pct(attn_ms, 10), "p90": pct(attn_ms, 90),
                     "mean": round(float(attn_ms.mean()) * 1e3, 2),
-                    "partials_p50": round(part_s * 1e6, 2), "merge_p50": pct(merge_ms, 50),
+                    "partials_p50": pct(part_ms, 50), "merge_p50": pct(merge_ms, 50),
+                    "partials_back_to_back": round(b2b_ms * 1e3, 2) if b2b_ms is not None else None,
                     "warm_p50": pct(warm_ms, 50), "graph_p50": pct(graph_ms, 50), "graph_p10": pct(graph_ms, 10),
                     "graph_p90": pct(graph_ms, 90),
                     "note": "whole call between two events, cold (value uses p50); partials/merge: the kernels "
-                            "timed separately in a second run of the same steps; warm: the call repeated on one "
-                            "replica; graph: one captured call per replica replayed in rotation (cold)"},
+                            "timed separately in a second run of the same steps (an event before each kernel); "
+                            "partials_back_to_back: the partial kernel's mean launch duration over `steps` "
+                            "launches between one event pair, replicas in rotation (the roofline figure); warm: "
+                            "the call repeated on one replica; graph: one captured call per replica replayed in "
+                            "rotation (cold)"},
         "attn_algorithmic_bytes": int(attn_bytes),
         "roofline": roofline,
     }
