@@ -434,6 +434,19 @@ def main():
         bev[1].record(stream)
         torch.cuda.synchronize()
         b2b_ms = bev[0].elapsed_time(bev[1]) / args.steps
+    # whole calls back to back the same way (no import or event between them)
+    cev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(SPIN_CYCLES)
+    cev[0].record(stream)
+    for k in range(args.steps):
+        if q_len is not None:
+            sg.specgen_fork_prefill_attn(reps[(k + 1) % R], q_len, out, lse, ws, stream=stream)
+        else:
+            sg.specgen_fork_decode_attn(reps[(k + 1) % R], out, lse, ws, stream=stream)
+    cev[1].record(stream)
+    torch.cuda.synchronize()
+    calls_b2b_ms = cev[0].elapsed_time(cev[1]) / args.steps
 
     def call(fb, st):   # the attention call alone
         if q_len is not None:
@@ -571,16 +584,19 @@ def main():
                    "path": args.path, "fp8_scores": bool(args.fp8_scores), "replicas": R, "prefill_queries_per_fork": prefill_q or 0, "import_blocks": int(len(ids)) if imp is not None else 0},
         "pct_of_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "fork_tokens_per_s": round(Q / attn_s, 1),
+        "gbps_back_to_back": round(attn_bytes / (calls_b2b_ms / 1e3) / 1e9, 2),
         "attn_us": {"p50": pct(attn_ms, 50), "p10": pct(attn_ms, 10), "p90": pct(attn_ms, 90),
                     "mean": round(float(attn_ms.mean()) * 1e3, 2),
                     "partials_p50": pct(part_ms, 50), "merge_p50": pct(merge_ms, 50),
                     "partials_back_to_back": round(b2b_ms * 1e3, 2) if b2b_ms is not None else None,
+                    "calls_back_to_back": round(calls_b2b_ms * 1e3, 2),
                     "warm_p50": pct(warm_ms, 50), "graph_p50": pct(graph_ms, 50), "graph_p10": pct(graph_ms, 10),
                     "graph_p90": pct(graph_ms, 90),
                     "note": "whole call between two events, cold (value uses p50); partials/merge: the kernels "
                             "timed separately in a second run of the same steps (an event before each kernel); "
                             "partials_back_to_back: the partial kernel's mean launch duration over `steps` "
-                            "launches between one event pair, replicas in rotation (the roofline figure); warm: "
+                            "launches between one event pair, replicas in rotation (the roofline figure); "
+                            "calls_back_to_back: the whole call the same way; warm: "
                             "the call repeated on one replica; graph: one captured call per replica replayed in "
                             "rotation (cold)"},
         "attn_algorithmic_bytes": int(attn_bytes),
