@@ -99,8 +99,10 @@ typedef enum { SPECGEN_PATH_AUTO = 0, SPECGEN_PATH_DOT = 1, SPECGEN_PATH_MFMA = 
 
 /* One decode step for every fork of T traces. */
 typedef struct {
-  int32_t num_traces;        /* T >= 1                                           */
-  int32_t num_forks;         /* N = sum_t F_t >= 1; forks are grouped by trace   */
+  int32_t num_traces;        /* 1 <= T <= 32 per call                            */
+  int32_t num_forks;         /* N = sum_t F_t, 1 <= N <= 512 per call; forks are
+                                grouped by trace.  Larger batches are
+                                SPECGEN_ERR_UNSUPPORTED: split them over calls */
   int32_t num_q_heads;       /* Hq >= 1                                          */
   int32_t num_kv_heads;      /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 128         */
   int32_t head_dim;          /* D: 64 or 128                                     */

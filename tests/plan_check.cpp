@@ -314,9 +314,13 @@ int main(int argc, char** argv) {
     const int g = gs[U(0, 6)];
     in.Hkv = U(1, 3) == 1 ? 8 : U(1, 4);
     in.Hq = g * in.Hkv;
-    in.T = U(1, 12);
+    // up to the per-call limits: a fifth of the cases have 13-32 traces, and a
+    // tenth exactly 512 forks spread over the traces
+    in.T = U(0, 4) == 0 ? U(13, kMaxTraces) : U(1, 12);
     std::vector<int32_t> fo(in.T + 1, 0), P(in.T);
-    for (int t = 0; t < in.T; ++t) fo[t + 1] = fo[t] + U(1, U(0, 3) == 0 ? 40 : 6);
+    const bool most_forks = U(0, 9) == 0;
+    for (int t = 0; t < in.T; ++t)
+      fo[t + 1] = most_forks ? (int32_t)((t + 1) * (int64_t)kMaxForks / in.T) : fo[t] + U(1, U(0, 3) == 0 ? 40 : 6);
     in.N = fo[in.T];
     if (in.N > kMaxForks) continue;
     const int pmax = U(0, 4) == 0 ? 140000 : (U(0, 1) ? 3000 : 300);

@@ -267,6 +267,30 @@ def test_table_offsets_validated(L, which, off, lens, status):
                                                           C.byref(n)) == status
 
 
+@pytest.mark.parametrize("T,N,status", [(32, 512, 0), (33, 33, 2), (1, 513, 2), (32, 513, 2)])
+def test_traces_and_forks_per_call(L, T, N, status):
+    """At most 32 traces and 512 forks per call; a larger batch is
+    SPECGEN_ERR_UNSUPPORTED before any launch (forks spread over the traces as
+    evenly as they go, 20 prefix tokens per trace, 3 suffix tokens per fork)."""
+    fork_off = np.array([(t * N) // T for t in range(T + 1)], np.int32)
+    plen = np.full(T, 20, np.int32)
+    pto = np.arange(T + 1, dtype=np.int32) * 2
+    slen = np.full(N, 3, np.int32)
+    sto = np.arange(N + 1, dtype=np.int32)
+    s, keep = _host_batch(num_traces=T, num_forks=N)
+    keep += [fork_off, plen, pto, slen, sto]
+    s.fork_off_h, s.prefix_len_h, s.prefix_table_off_h = fork_off.ctypes.data, plen.ctypes.data, pto.ctypes.data
+    s.suffix_len_h, s.suffix_table_off_h = slen.ctypes.data, sto.ctypes.data
+    n = C.c_size_t(7)
+    assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == status, L.specgen_last_error().decode()
+    if status:
+        assert n.value == 7
+        assert "per call" in L.specgen_last_error().decode()
+        assert L.specgen_fork_decode_attn(C.byref(s), C.c_void_p(0x10000), None, None, 0, None) == status
+    else:
+        assert n.value > 0
+
+
 @pytest.mark.parametrize("path", ["auto", "mfma", "dot"])
 def test_split_query_tiles_every_item_once(L, path):
     """specgen_fork_decode_attn_split (host only): the segments of every work
