@@ -43,6 +43,11 @@ CASES = {
     # many queries: 16 forks x 16 queries over an 8-head GQA group (2048 rows per kv head)
     "gqa8_q16": dict(batch=dict(prefix_lens=[1500], forks_per_trace=16, suffix_range=(16, 100), num_q_heads=64,
                                 num_kv_heads=8, head_dim=128), q_len=[16] * 16),
+    # the most queries one call takes: 4 traces x 8 forks x 16 queries = 512; forks
+    # with 32 or more suffix tokens have a whole block before their first query,
+    # so some traces nest their forks' blocks and others cannot
+    "most_queries": dict(batch=dict(prefix_lens=[200, 90, 400, 33], forks_per_trace=8, suffix_range=(16, 80),
+                                    num_q_heads=8, num_kv_heads=2, head_dim=64), q_len=[16] * 32),
 }
 
 
