@@ -15,13 +15,15 @@
 // Slots.  The worker's range is a sequence of 32 KiB slots: for each item one
 // "q slot" per 128 query rows (128 x D bf16 each) followed by its tiles (TT
 // tokens of K, then TT tokens of V).  Slots go through a ring of four LDS
-// stages with three slots in flight.  Every wave moves exactly four 1 KiB
-// pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no VGPR
-// staging; tiles nontemporal, the KV is read once; q slots through the caches,
-// since every worker of a prefix item reads the same q rows): waves 0-3 the K block slices of
-// a tile, waves 4-7 its V slices.  So the number of vector-memory operations
-// a wave has in flight is known exactly and the wait for slot s is
-// "vmcnt <= 4 x (slots issued after s) + partial stores issued since".  These
+// stages with three slots in flight.  Every wave moves the same number of
+// 1 KiB pieces of every slot with global_load_lds_dwordx4 (64 lanes x 16 B, no
+// VGPR staging; tiles nontemporal, the KV is read once; q slots through the
+// caches, since every worker of a prefix item reads the same q rows): four of a
+// bf16 slot (waves 0-3 the K block slices of a tile, waves 4-7 its V slices),
+// two of an E4M3 tile (one of its K codes, one of its V codes).  So the number
+// of vector-memory operations a wave has in flight is known exactly and the
+// wait for slot s is "vmcnt <= (pieces per slot) x (slots issued after s) +
+// partial stores issued since".  These
 // loads are issued from inline asm: the compiler does not see them, so it
 // neither drains them (vmcnt(0)) before LDS reads nor reorders them across
 // the LDS barriers.
@@ -29,9 +31,10 @@
 // Rows and tokens.  An item with r <= 256 rows uses RG = ceil(r / 32) row
 // groups of 32 rows and splits each tile's tokens over TG = min(TT/32, 8/RG)
 // token groups: wave w computes row group w % RG over token group w / RG (two
-// waves per SIMD for the 128-row prefix items, so one wave's softmax overlaps
-// the other's MFMAs; one token group for 5-8 row groups, where each wave runs
-// both slabs of a tile).  An item of more than 128 rows has two q slots, and a
+// token groups for the 128-row prefix items, the two waves of a SIMD, whose
+// vector and matrix work can overlap when they do not run in step: the slot
+// loop staggers their DMA issue for that; one token group for 5-8 row groups,
+// where each wave runs both slabs of a tile).  An item of more than 128 rows has two q slots, and a
 // wave reads its Q^T from the one holding its rows.  Items with fewer rows pad
 // their last row group; they are bound by their K/V bytes, not by the matrix
 // cores (one wave's dependent chain through a 32-token slab takes about 0.9
@@ -651,9 +654,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a, con
     float inv_vsc = 1.f, lvs = 0.f, ksc = 1.f;
     if constexpr (FP8) {
       // the slab's two blocks (ids[idb + sb/16] and the next): lanes G < 2 hold
-      // keys of the first
-      // of the first.  Scalar loads (the constant address space): a vector load
-      // would sit in the vmcnt queue behind the slots in flight.
+      // keys of the first, lanes G >= 2 keys of the second.  Scalar loads (the
+      // constant address space): a vector load would sit in the vmcnt queue
+      // behind the slots in flight.
       typedef const __attribute__((address_space(4))) float* cfp;
       const int id0 = uniform(ids[idb + (sb >> 4)]);
       const int id1 = uniform(ids[idb + (sb >> 4) + 1]);

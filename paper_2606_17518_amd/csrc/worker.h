@@ -52,14 +52,6 @@ __device__ WorkerRange worker_walk(const Plan& plan, int part, int w, int32_t* i
   });
 }
 
-// The walk only, ending with a barrier so `items` is visible to every thread.
-template <int kItemCap>
-__device__ WorkerRange worker_items(const Plan& plan, int part, int w, int32_t* items, int32_t* info) {
-  const WorkerRange wr = worker_walk<kItemCap>(plan, part, w, items, info);
-  __syncthreads();
-  return wr;
-}
-
 // The walk and the block-id gather in one pass: thread i examines the chunk
 // of c = ceil((x1 - x0) / kThreads) units at x0 + i * c (tile_in_chunk; the
 // planner keeps c within every tile price and the charge); a chunk where a
