@@ -467,3 +467,49 @@ def test_debug_block_id_check_on_host_tables(tmp_path):
     r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "all table checks passed" in r.stdout
+
+
+def test_concurrent_host_calls(L):
+    """The host side is reentrant: eight threads plan different batches at
+    once (ctypes releases the GIL around each call), every size equals the
+    serial one, and each thread's specgen_last_error is its own call's."""
+    import threading
+    import paper_2606_17518_amd.binding as B
+    import synth
+    batches = [synth.make_fork_batch(prefix_lens=[100 + 37 * i, 50], forks_per_trace=[1 + i % 5, 2],
+                                     suffix_range=(0, 90), num_q_heads=16, num_kv_heads=2,
+                                     head_dim=64 if i % 2 else 128, seed=600 + i) for i in range(8)]
+    structs = []
+    for b in batches:
+        s, keep = B.host_batch_struct(b)
+        for f in ("q", "k_pool", "v_pool", "fork_off", "prefix_len", "prefix_table_off", "prefix_table",
+                  "suffix_len", "suffix_table_off", "suffix_table"):
+            setattr(s, f, 0x10000)   # never dereferenced: the size query reads the host mirrors only
+        structs.append((s, keep))
+
+    def size_of(s):
+        n = C.c_size_t(0)
+        assert L.specgen_fork_decode_attn_workspace_size(C.byref(s), C.byref(n)) == 0, L.specgen_last_error().decode()
+        return n.value
+
+    serial = [size_of(s) for s, _ in structs]
+    errors = []
+
+    def worker(i):
+        try:
+            s, _ = structs[i]
+            bad, keep = _host_batch(num_q_heads=7)   # rejected: Hq % Hkv != 0
+            for k in range(150):
+                assert size_of(s) == serial[i]
+                n = C.c_size_t(0)
+                assert L.specgen_fork_decode_attn_workspace_size(C.byref(bad), C.byref(n)) == B.SPECGEN_ERR_INVALID_ARG
+                assert "num_q_heads" in L.specgen_last_error().decode() or "Hq" in L.specgen_last_error().decode()
+        except Exception as e:   # reported below: an assertion in a thread does not fail the test by itself
+            errors.append((i, repr(e)))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(8)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
