@@ -7,8 +7,8 @@
  * fork is conditioned on the trace's prefix and reuses its cached KV state,
  * then continues with a short private suffix (Sec. 1; Sec. 4.2 "Insight:
  * Speculative Generation"; Sec. 8.7, prefix caching paragraph).  A fork event
- * launches K forks (Algorithm 1, the line that sets K from the resource
- * capacity), and idle-triggered forking adds more forks on the same prefix
+ * launches K forks, K set from the resource capacity (Algorithm 1), and
+ * idle-triggered forking adds more forks on the same prefix
  * (Sec. 6.1.1), so one trace's prefix is shared by F forks.  Successive
  * trigger points of one trace fork from ever longer prefixes while the
  * reasoning generation continues (Algorithm 1), so forks of different
