@@ -164,6 +164,33 @@ def _stream(stream) -> C.c_void_p:
     return C.c_void_p(int(stream))
 
 
+def _need(*bufs) -> None:
+    """Each (tensor, name, bytes, dtypes or None) whose pointer goes to the
+    library must be a contiguous tensor of an accepted dtype holding the bytes
+    the call reads or writes, in device memory: the C ABI gets a bare pointer
+    and cannot check its extent, so a short buffer would become an
+    out-of-bounds access on the device.  None tensors are skipped."""
+    bufs = [b for b in bufs if b[0] is not None]
+    for t, what, nbytes, dtypes in bufs:
+        if dtypes is not None and t.dtype not in dtypes:
+            raise ValueError(f"{what}: dtype {t.dtype}, expected one of {dtypes}")
+        if not t.is_contiguous():
+            raise ValueError(f"{what} must be contiguous")
+        if t.numel() * t.element_size() < nbytes:
+            raise ValueError(f"{what} holds {t.numel() * t.element_size()} bytes; the call needs {nbytes}")
+    for t, what, _, _ in bufs:
+        if t.device.type != "cuda":
+            raise ValueError(f"{what} must be device memory, not {t.device}")
+
+
+def _need_outputs(s, rows: int, out: Optional[torch.Tensor], out_lse: Optional[torch.Tensor], workspace=None) -> None:
+    """out [rows][Hq][D] bf16 and out_lse [rows][Hq] fp32 of an attention call
+    (the library checks the workspace's size itself)."""
+    _need((out, "out", rows * s.num_q_heads * s.head_dim * 2, (torch.bfloat16,)),
+          (out_lse, "out_lse", rows * s.num_q_heads * 4, (torch.float32,)),
+          (workspace, "workspace", 0, None))
+
+
 @dataclasses.dataclass
 class ForkBatchTensors:
     """Device tensors + host mirrors of one fork batch (see specgen_fork_batch_t)."""
@@ -266,6 +293,7 @@ def alloc_workspace(batch, device="cuda") -> torch.Tensor:
 def specgen_fork_decode_attn(batch, out: torch.Tensor, out_lse: Optional[torch.Tensor], workspace: torch.Tensor,
                              stream=None) -> None:
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _need_outputs(s, s.num_forks, out, out_lse, workspace)
     _check(lib().specgen_fork_decode_attn(C.byref(s), _dptr(out), _dptr(out_lse), _dptr(workspace),
                                           workspace.numel() * workspace.element_size(), _stream(stream)))
 
@@ -277,12 +305,14 @@ def specgen_fork_decode_attn_noalloc(batch, out: torch.Tensor, out_lse: Optional
     """specgen_fork_decode_attn without a workspace: the partials live in the
     library's per-GPU scratch (calls that overlap on one GPU race)."""
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _need_outputs(s, s.num_forks, out, out_lse)
     _check(lib().specgen_fork_decode_attn_noalloc(C.byref(s), _dptr(out), _dptr(out_lse), _stream(stream)))
 
 
 def specgen_fork_decode_attn_phase(batch, phase: int, out: Optional[torch.Tensor], out_lse: Optional[torch.Tensor],
                                    workspace: torch.Tensor, stream=None) -> None:
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
+    _need_outputs(s, s.num_forks, out, out_lse, workspace)
     _check(lib().specgen_fork_decode_attn_phase(C.byref(s), int(phase), _dptr(out), _dptr(out_lse), _dptr(workspace),
                                                 workspace.numel() * workspace.element_size(), _stream(stream)))
 
@@ -309,6 +339,7 @@ def specgen_fork_prefill_attn(batch, q_len, out: torch.Tensor, out_lse: Optional
     """q_len: host int32 [N]; batch.q is [sum q_len][Hq][D]; out [sum q_len][Hq][D] bf16."""
     s = batch if isinstance(batch, ForkBatchC) else batch.c_struct()
     ql = _q_len(q_len)
+    _need_outputs(s, int(ql.astype(np.int64).sum()), out, out_lse, workspace)   # one row per query
     _check(lib().specgen_fork_prefill_attn(C.byref(s), ql.ctypes.data_as(C.c_void_p), _dptr(out), _dptr(out_lse),
                                            _dptr(workspace), workspace.numel() * workspace.element_size(),
                                            _stream(stream)))
@@ -318,6 +349,11 @@ def specgen_kv_import(tensors: Sequence[tuple], dst_block_ids: torch.Tensor, num
                       bad_id_count: Optional[torch.Tensor] = None, stream=None) -> None:
     """tensors: sequence of (dst_pool tensor, src_staging tensor, block_bytes)."""
     arr = (KvTensorC * max(1, len(tensors)))()
+    n = int(dst_block_ids.numel())
+    _need((dst_block_ids, "dst_block_ids", 4 * n, (torch.int32,)),
+          *[b for i, (dst, src, bb) in enumerate(tensors)
+            for b in ((dst, f"tensors[{i}] dst_pool", int(num_dst_blocks) * int(bb), None),
+                      (src, f"tensors[{i}] src_staging", n * int(bb), None))])
     for i, (dst, src, bb) in enumerate(tensors):
         arr[i].dst_pool = dst.data_ptr()
         arr[i].src_staging = src.data_ptr()
@@ -330,6 +366,11 @@ def specgen_kv_export(tensors: Sequence[tuple], src_block_ids: torch.Tensor, num
                       bad_id_count: Optional[torch.Tensor] = None, stream=None) -> None:
     """tensors: sequence of (dst_staging tensor, src_pool tensor, block_bytes)."""
     arr = (KvExportTensorC * max(1, len(tensors)))()
+    n = int(src_block_ids.numel())
+    _need((src_block_ids, "src_block_ids", 4 * n, (torch.int32,)),
+          *[b for i, (dst, src, bb) in enumerate(tensors)
+            for b in ((dst, f"tensors[{i}] dst_staging", n * int(bb), None),
+                      (src, f"tensors[{i}] src_pool", int(num_src_blocks) * int(bb), None))])
     for i, (dst, src, bb) in enumerate(tensors):
         arr[i].dst_staging = dst.data_ptr()
         arr[i].src_pool = src.data_ptr()
@@ -359,6 +400,9 @@ def specgen_lse_merge(o_parts: torch.Tensor, lse_parts: torch.Tensor, out: torch
                       out_lse: Optional[torch.Tensor] = None, stream=None) -> None:
     """o_parts [S][R][D] f32, lse_parts [S][R] f32, out [R][D] bf16 or f32."""
     S, R, D = o_parts.shape
+    _need((o_parts, "o_parts", S * R * D * 4, (torch.float32,)), (lse_parts, "lse_parts", S * R * 4, (torch.float32,)),
+          (out, "out", R * D * out.element_size(), (torch.bfloat16, torch.float32)),
+          (out_lse, "out_lse", R * 4, (torch.float32,)))
     dt = SPECGEN_BF16 if out.dtype == torch.bfloat16 else SPECGEN_FP32
     _check(lib().specgen_lse_merge(_dptr(o_parts), _dptr(lse_parts), S, R, D, _dptr(out), dt, _dptr(out_lse),
                                    _stream(stream)))
