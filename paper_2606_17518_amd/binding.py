@@ -388,6 +388,14 @@ def specgen_kv_append(k_pool: torch.Tensor, v_pool: torch.Tensor, k_new: torch.T
     es = 2 if kv_dtype == SPECGEN_BF16 else 1
     if num_blocks is None:
         num_blocks = k_pool.numel() * k_pool.element_size() // (num_kv_heads * 16 * head_dim * es)
+    n = int(pos.numel())
+    block = int(num_kv_heads) * 16 * int(head_dim) * es
+    i32 = (torch.int32,)
+    _need((k_pool, "k_pool", int(num_blocks) * block, None), (v_pool, "v_pool", int(num_blocks) * block, None),
+          (k_new, "k_new", n * int(num_kv_heads) * int(head_dim) * es, None),
+          (v_new, "v_new", n * int(num_kv_heads) * int(head_dim) * es, None),
+          (pos, "pos", 4 * n, i32), (suffix_table_off, "suffix_table_off", 4 * (n + 1), i32),
+          (suffix_table, "suffix_table", 0, i32), (bad_count, "bad_count", 4, i32))
     a = KvAppendC(num_forks=int(pos.numel()), num_kv_heads=int(num_kv_heads), head_dim=int(head_dim),
                   kv_dtype=int(kv_dtype), num_blocks=int(num_blocks), k_pool=k_pool.data_ptr(),
                   v_pool=v_pool.data_ptr(), k_new=k_new.data_ptr(), v_new=v_new.data_ptr(), pos=pos.data_ptr(),

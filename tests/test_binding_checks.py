@@ -86,3 +86,23 @@ def test_block_move_buffers_checked():
         sg.specgen_kv_export([(staging[:bb], pool, bb)], ids, nb)
     with pytest.raises(ValueError, match="src_pool holds"):
         sg.specgen_kv_export([(staging, pool, bb)], ids, nb + 1)
+
+
+def test_append_buffers_checked():
+    N, H, D, nb = 3, 2, 64, 8
+    blk = H * 16 * D
+    pools = [torch.zeros(nb * blk, dtype=torch.bfloat16) for _ in range(2)]
+    new = [torch.zeros((N, H, D), dtype=torch.bfloat16) for _ in range(2)]
+    pos = torch.zeros(N, dtype=torch.int32)
+    off = torch.arange(N + 1, dtype=torch.int32)
+    tab = torch.zeros(N, dtype=torch.int32)
+    with pytest.raises(ValueError, match="k_new holds"):
+        sg.specgen_kv_append(pools[0], pools[1], new[0][:-1], new[1], pos, off, tab, H, D)
+    with pytest.raises(ValueError, match="suffix_table_off holds"):
+        sg.specgen_kv_append(pools[0], pools[1], new[0], new[1], pos, off[:-1], tab, H, D)
+    with pytest.raises(ValueError, match="k_pool holds"):
+        sg.specgen_kv_append(pools[0], pools[1], new[0], new[1], pos, off, tab, H, D, num_blocks=nb + 1)
+    with pytest.raises(ValueError, match="pos: dtype"):
+        sg.specgen_kv_append(pools[0], pools[1], new[0], new[1], pos.long(), off, tab, H, D)
+    with pytest.raises(ValueError, match="device memory"):
+        sg.specgen_kv_append(pools[0], pools[1], new[0], new[1], pos, off, tab, H, D)
