@@ -1,6 +1,6 @@
 """Properties of the HIP path that hold exactly: determinism, independence of
 physical block placement, fork independence, no dependence on workspace
-contents."""
+contents, and no state shared by calls in flight together on two streams."""
 import copy
 
 import numpy as np
@@ -90,3 +90,41 @@ def test_two_phases_equal_one_call():
     sg.specgen_fork_decode_attn_phase(fb, sg.SPECGEN_PHASE_MERGE, o2, l2, ws)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_two_streams_at_once_give_the_serial_bits():
+    """Two calls with their own workspaces and outputs in flight together on
+    two streams (default priority) give the bits each gives alone: the calls
+    share no device state."""
+    say("two streams")
+    b1 = synth.make_fork_batch(prefix_lens=[3000], forks_per_trace=6, suffix_range=(0, 300), num_q_heads=32,
+                               num_kv_heads=4, head_dim=128, key_bias_std=0.5, seed=810)
+    b2 = synth.make_fork_batch(prefix_lens=[900, 2000], forks_per_trace=[3, 5], suffix_range=(0, 200), num_q_heads=16,
+                               num_kv_heads=2, head_dim=64, kv_dtype="fp8_e4m3", seed=811)
+    batches = [(b, sg.ForkBatchTensors.from_numpy(b, "cuda")) for b in (b1, b2)]
+
+    def buffers(b, fb):
+        out = torch.full((b.num_forks, b.num_q_heads, b.head_dim), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((b.num_forks, b.num_q_heads), float("nan"), dtype=torch.float32, device="cuda")
+        return out, lse, sg.alloc_workspace(fb)
+
+    alone = []
+    for b, fb in batches:
+        out, lse, ws = buffers(b, fb)
+        sg.specgen_fork_decode_attn(fb, out, lse, ws)
+        torch.cuda.synchronize()
+        alone.append((out.clone(), lse.clone()))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    bufs = [buffers(b, fb) for b, fb in batches]
+    torch.cuda.synchronize()
+    for rep in range(5):
+        for (b, fb), (out, lse, ws), st in zip(batches, bufs, streams):
+            out.fill_(float("nan"))
+            lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        for (b, fb), (out, lse, ws), st in zip(batches, bufs, streams):
+            sg.specgen_fork_decode_attn(fb, out, lse, ws, stream=st)
+        torch.cuda.synchronize()
+        for (out, lse, _), (ao, al) in zip(bufs, alone):
+            assert torch.equal(out.view(torch.int16), ao.view(torch.int16)), f"repeat {rep}"
+            assert torch.equal(lse.view(torch.int32), al.view(torch.int32)), f"repeat {rep}"
