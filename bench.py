@@ -615,6 +615,9 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, q_len, attn_bytes)
+        cb = res["cpu_baseline"]
+        if cb["value"] > 0:   # the GPU call's rate over the oracle's, both on this machine and in the same unit
+            cb["gpu_over_oracle"] = round(value / cb["value"], 1)
     print(json.dumps(res), flush=True)
 
 
