@@ -48,9 +48,12 @@
  * work queued on `stream` has finished.  The library keeps no pointer after a
  * call returns; host-side index mirrors are read only during the call.
  * Errors: every entry point returns a status; argument checks all run before
- * anything is queued, so a non-OK status means nothing was launched and no
- * output was written.  specgen_last_error() gives a message for the calling
- * thread's most recent non-OK status.
+ * anything is queued, so SPECGEN_ERR_INVALID_ARG, SPECGEN_ERR_UNSUPPORTED
+ * and SPECGEN_ERR_WORKSPACE mean nothing was launched and no output was
+ * written.  SPECGEN_ERR_DEVICE (a failed launch) may leave the call's earlier
+ * kernels queued: its outputs and workspace are then unspecified.
+ * specgen_last_error() gives a message for the calling thread's most recent
+ * non-OK status.
  * Streams: all work is asynchronous on `stream` (0 = the null stream) of the
  * current HIP device.  Results are deterministic: the work split depends only
  * on the lengths, and no floating-point atomics are used.  A call queues
